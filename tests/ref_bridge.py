@@ -1,0 +1,35 @@
+"""Turns seeded workload arrays into the fp64 reference's inputs (tests only)."""
+import numpy as np
+
+import oracle.decoder as D
+from paper_2508_10259_amd import workload as W
+
+
+class _Decoded:
+    """Layer-indexable fp32 view of an encoded stack."""
+
+    def __init__(self, stack, dtype):
+        self.stack, self.dtype = stack, dtype
+
+    def __getitem__(self, l):
+        return W.to_f32(self.stack[l], self.dtype)
+
+
+def oracle_config(spec):
+    return D.Config(spec.n_layers, spec.d_model, spec.n_heads, spec.head_dim, spec.d_ffn,
+                    spec.vocab, spec.n_bins, spec.rms_eps, spec.rope_theta)
+
+
+def oracle_params(w):
+    spec = w.spec
+    arrays = {n: _Decoded(getattr(w, n), spec.dtype) for n in W.MATRICES}
+    arrays.update(g_attn=w.g_attn, g_ffn=w.g_ffn, g_final=w.g_final,
+                  embed=W.to_f32(w.embed, spec.dtype), head_bins=W.to_f32(w.head_bins, spec.dtype))
+    return D.Params(oracle_config(spec), **arrays)
+
+
+def prefix_f64(p, spec, prefix):
+    """Prefix embeddings: patch rows, then embedding rows of the instruction ids."""
+    x = W.to_f32(prefix.patches, spec.dtype).astype(np.float64)
+    t = D.embed_ids(p, prefix.text_ids)
+    return np.concatenate([x, t], axis=0)

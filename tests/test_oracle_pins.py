@@ -1,0 +1,36 @@
+"""The fp64 reference against closed forms, invariants, special cases and brute force."""
+import numpy as np
+import pytest
+
+import oracle.decoder as D
+from oracle_pins import ALL_PINS, tiny_params, _ctx_vs_full, _rand
+
+
+@pytest.mark.parametrize("pin", ALL_PINS, ids=[p.__name__ for p in ALL_PINS])
+def test_pin(pin):
+    pin(D)
+
+
+def test_cached_equals_full_random_shapes():
+    """Cached == full on a spread of small shapes (heads, dims, lengths, bins)."""
+    shapes = [  # (layers, d, H, F, V, n_bins)
+        (1, 4, 1, 6, 8, 8), (2, 8, 4, 16, 30, 5), (3, 12, 3, 10, 16, 16), (1, 16, 2, 40, 64, 7),
+    ]
+    for i, (nl, d, H, F, V, nb) in enumerate(shapes):
+        p = tiny_params(D, key=100 + i, n_layers=nl, d=d, H=H, F=F, V=V, n_bins=nb)
+        B = 1 + i % 3
+        prefixes = [_rand((2 + 3 * b + i, d), 200 + i, b) for b in range(B)]
+        news = [None, [(_rand((1 + b, d), 300 + i, b) if (b + i) % 2 == 0 else None) for b in range(B)]]
+        _ctx_vs_full(D, p, prefixes, news, n_actions=3)
+
+
+def test_cached_equals_full_tiny_workload():
+    """The 2-layer d=256 fp32 workload shape with its seeded weights: cached == full to 1e-12."""
+    from paper_2508_10259_amd import workload as W
+    from ref_bridge import oracle_params
+    wl = W.WORKLOADS["tiny-b1"]
+    w = W.make_weights(wl.spec, seed=0)
+    p = oracle_params(w)
+    pre = [W.to_f32(W.make_prefix(wl, 0, 0, 0).patches, "f32")]
+    obs = [[W.to_f32(W.make_observation(wl.spec, 0, s, 0, 1), "f32")] for s in range(2)]
+    _ctx_vs_full(D, p, pre, [None] + obs, n_actions=7)
