@@ -1,0 +1,209 @@
+"""Cached-context action decoding throughput on one MI355X.
+
+Workload (default): the 12-layer d=1024 decoder (16 heads of 64, FFN 4096,
+256 action bins), 8 episodes, each with a cached prefix of 256 patch
+embeddings + 24 instruction tokens, 7 greedy action tokens per step.  The
+timed region is one episode window: ctx_build of the 8 prefixes followed by
+K ctx_steps (K = 500 by default), inputs resident in HBM beforehand.
+Each step = 7 bin-logit evaluations and 6 decode passes over all layers.
+
+Prints one JSON line: action steps/s (rows x steps / s), the roofline of the
+dominant kernel (timed live with HIP events on its own stream), and the fp64
+CPU reference timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16/bf16
+
+
+def step_bytes(spec, lens, n_actions, es=2):
+    """Algorithmic bytes of one ctx_step with no new tokens: every decode pass
+    reads all matmul weights once and each row's K/V up to its current
+    position, writes the new token's K/V; every action reads the bin head."""
+    d, L = spec.d_model, spec.n_layers
+    w = spec.matmul_params * es
+    kv_tok = L * 2 * d * es
+    total = 0
+    for j in range(1, n_actions):
+        total += w
+        total += sum(int(l) + j for l in lens) * kv_tok  # keys 0..L_b+j-1 incl. the new one
+        total += len(lens) * kv_tok  # append
+    total += n_actions * spec.n_bins * d * es
+    return total
+
+
+def build_flops(spec, lens):
+    """Matmul + attention FLOPs of ctx_build."""
+    d, L = spec.d_model, spec.n_layers
+    m = sum(int(l) for l in lens)
+    pairs = sum(int(l) * (int(l) + 1) // 2 for l in lens)
+    return 2 * spec.matmul_params * m + 4 * d * L * pairs
+
+
+def gu_launch_bytes(spec, B, es=2):
+    """Gate|up projection of one decode pass: weights [2F, d] once, u [B, d] in, a [B, F] out."""
+    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * es + B * spec.d_ffn * es
+
+
+def time_gate_up_kernel(model, B, iters=200):
+    """Average duration of the decode gate|up kernel (the largest weight stream of a
+    pass) in the bench's launch shape, timed with HIP events on its own stream."""
+    import torch
+    from paper_2508_10259_amd.build import PROBE_LIB
+    lib = C.CDLL(PROBE_LIB)
+    spec = model.spec
+    d, F = spec.d_model, spec.d_ffn
+    # packed layout of the model workspace: [wqkv | wo | wgu | ...], each region 256-byte aligned
+    es = 2
+    align = lambda x: (x + 255) // 256 * 256
+    w_ptr = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
+    u = torch.randn((B, d), device="cuda").half()
+    a = torch.empty((B, F), device="cuda", dtype=torch.float16)
+    s = torch.cuda.Stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        for _ in range(20):
+            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), C.c_void_p(w_ptr), B, 2 * F, d,
+                               C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+        ev0.record(s)
+        for l in range(iters):
+            lw = w_ptr + (l % spec.n_layers) * 2 * F * d * es
+            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), C.c_void_p(lw), B, 2 * F, d,
+                               C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+        ev1.record(s)
+    s.synchronize()
+    return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
+
+
+def cpu_baseline(wl, seed, sample_steps, window_steps):
+    """fp64 reference on row 0: build its prefix, then `sample_steps` steps;
+    row-steps/s with the build amortised over the workload's window."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import oracle.decoder as D
+    from ref_bridge import oracle_params, prefix_f64
+    from paper_2508_10259_amd import workload as W
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    w = W.make_weights(wl.spec, seed)
+    p = oracle_params(w)
+    pre = W.make_prefixes(wl, seed, 0)
+    x = prefix_f64(p, wl.spec, pre[0])
+    ctx = D.ActionContext(p, 1)
+    t0 = time.perf_counter()
+    ctx.build([x])
+    t1 = time.perf_counter()
+    for _ in range(sample_steps):
+        ctx.step(None, wl.n_actions)
+    t2 = time.perf_counter()
+    per_step = (t2 - t1) / sample_steps + (t1 - t0) / window_steps
+    return {"value": 1.0 / per_step, "unit": "action-steps/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"row 0 of {wl.name}: build of its {x.shape[0]}-token prefix ({t1 - t0:.2f} s) + "
+                      f"{sample_steps} steps ({t2 - t1:.2f} s), fp64 NumPy; build amortised over "
+                      f"{window_steps} steps as in the timed GPU window"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mid-b8")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=6)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decoder shards by episode, "
+              "one process per GPU, with no communication on the hot path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2508_10259_amd import workload as W
+    from paper_2508_10259_amd.runtime import DeviceContext, DeviceModel
+
+    wl = W.WORKLOADS[args.workload]
+    spec = wl.spec
+    torch.cuda.set_device(0)
+    print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
+    model = DeviceModel(W.make_weights(spec, args.seed), "cuda:0")
+    cap = wl.derived_capacity(steps_between_builds=0)
+    ctx = DeviceContext(model, wl.batch, cap)
+    prefix, lens = model.pack_prefixes(W.make_prefixes(wl, args.seed, 0))
+    B, A = wl.batch, wl.n_actions
+    tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
+    logits = torch.empty((B, A, spec.n_bins), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    ctx.build(prefix, lens)
+    for _ in range(args.warmup):
+        ctx.step(A, tokens=tokens, logits=logits)
+    torch.cuda.synchronize()
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    ctx.build(prefix, lens)
+    ev[1].record()
+    for _ in range(args.steps):
+        ctx.step(A, tokens=tokens, logits=logits)
+    ev[2].record()
+    torch.cuda.synchronize()
+    t_build = ev[0].elapsed_time(ev[1]) * 1e-3
+    t_steps = ev[1].elapsed_time(ev[2]) * 1e-3
+    total = t_build + t_steps
+    value = B * args.steps / total
+    sb = step_bytes(spec, lens, A)
+    print(f"[bench] build {t_build * 1e3:.3f} ms, {args.steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
+          flush=True)
+
+    t_gu = time_gate_up_kernel(model, B)
+    gb = gu_launch_bytes(spec, B)
+    achieved = gb / t_gu / 1e9
+    roof = {"kernel": "k_gemm_skinny<2,1,SWIGLU> (decode gate|up projection + SiLU gate)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "bytes_per_launch": gb, "avg_launch_us": round(t_gu * 1e6, 3)}
+
+    out = {
+        "metric": "action steps/s per GPU (cached-context decode)",
+        "value": round(value, 2), "unit": "action-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(total / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp16",
+        "data": "synthetic (seeded N(0,0.02) weights stored bf16, N(0,1) patch embeddings, uniform ids)",
+        "config": {"workload": wl.name, "n_layers": spec.n_layers, "d_model": spec.d_model,
+                   "n_heads": spec.n_heads, "head_dim": spec.head_dim, "d_ffn": spec.d_ffn,
+                   "vocab": spec.vocab, "n_bins": spec.n_bins, "batch": B, "prefix_tokens": int(lens[0]),
+                   "n_actions": A, "capacity": cap, "timed": f"1 build + {args.steps} steps"},
+        "roofline": roof,
+        "step": {"ms": round(t_steps / args.steps * 1e3, 4), "algorithmic_bytes": sb,
+                 "hbm_frac": round(sb / (t_steps / args.steps) / (HBM_PEAK_GBS * 1e9), 4)},
+        "build": {"ms": round(t_build * 1e3, 4), "flops": build_flops(spec, lens),
+                  "mfma_frac": round(build_flops(spec, lens) / t_build / (MFMA_F16_PEAK_TFLOPS * 1e12), 4)},
+    }
+    ctx.close()
+    model.close()
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_sample_steps, args.steps)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * ams.h -- C ABI of the cached-context action decoder on one AMD MI355X (gfx950).
+ *
+ * What the library computes
+ *   A decoder-only transformer (Llama-style: RMSNorm, rotary position
+ *   embedding, causal multi-head attention, SwiGLU feed-forward) that emits
+ *   discretised action tokens greedily over the last n_bins vocabulary ids.
+ *   The step-invariant prefix of each episode (instruction tokens and
+ *   unchanged observation tokens) stays resident in device memory as a
+ *   per-layer key/value cache -- the "action context" of the paper (section
+ *   3.2.1, Constructing the Action Context): cached intermediate state is
+ *   reused by the next inference so only new tokens are computed, and the
+ *   new tokens' K/V are added after the inference.  Discarding a context and
+ *   re-inferring from fresh environment data follows the common part of the
+ *   paper's exception handler (section 3.3, Handler).  Control logic stays on
+ *   the host; every arithmetic step runs in the library's HIP kernels
+ *   (section 4 places control on the CPU and context on the GPU).
+ *
+ * Conventions
+ *   - Device pointers come from the caller (e.g. torch tensors' data_ptr());
+ *     `stream` is a hipStream_t (NULL = the legacy default stream).
+ *   - The caller owns every device buffer: weights, workspaces, inputs and
+ *     outputs.  They must outlive the handles that use them.  The library
+ *     allocates no device memory; it owns host-side handles, metadata and
+ *     captured HIP graphs only.
+ *   - Calls are asynchronous: they return after enqueueing on `stream`;
+ *     outputs are valid once the caller synchronises that stream.
+ *   - Every argument, state and capacity check happens before anything is
+ *     enqueued.  A call that fails a check returns a negative status and
+ *     changes nothing.  A failed HIP enqueue returns AMS_EHIP and moves the
+ *     context to the INVALID state.  ams_last_error() gives a message
+ *     (thread-local, valid until the next call on the same thread).
+ *   - A model is read-only after creation and may be shared by contexts.
+ *     A context must be used by one host thread and one stream at a time.
+ *
+ * Data types and layouts (row-major throughout)
+ *   dtype AMS_F32: weights, embeddings and K/V in fp32; all arithmetic fp32.
+ *   dtype AMS_BF16: the caller's weights and embeddings are bf16.  The packed
+ *     weights, GEMM inputs (activations) and the K/V cache are fp16 (same
+ *     bytes and MFMA rate as bf16, three more mantissa bits); bf16 weights
+ *     convert exactly unless |w| < 2^-14, where the fp16 subnormal is within
+ *     2^-25.  fp16 values saturate at +-65504.  Accumulation, residual
+ *     stream, norm statistics, softmax and logits are fp32.
+ *   A weight matrix maps an input vector x to W x and is stored [out][in].
+ *
+ * Context state machine
+ *   create -> EMPTY;  build: EMPTY|READY|INVALID -> READY;
+ *   step: READY -> READY (EMPTY or INVALID: AMS_ESTATE);
+ *   invalidate: any -> INVALID.
+ */
+#ifndef AMS_H
+#define AMS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ams_model ams_model;
+typedef struct ams_ctx ams_ctx;
+
+typedef enum {
+  AMS_OK = 0,
+  AMS_EINVAL = -1,    /* bad argument (NULL, out of range, inconsistent sizes) */
+  AMS_ESTATE = -2,    /* context is not in a state that allows the call */
+  AMS_ECAPACITY = -3, /* a row would exceed the context's token capacity */
+  AMS_ENODEV = -4,    /* no usable gfx950 device */
+  AMS_EHIP = -5,      /* a HIP runtime call failed */
+  AMS_ENOMEM = -6     /* a workspace is smaller than required */
+} ams_status;
+
+typedef enum { AMS_F32 = 0, AMS_BF16 = 1 } ams_dtype;
+
+/* Decoder dimensions.  d_model = n_heads * head_dim; head_dim even and at
+ * most 128; d_model a multiple of 128; d_ffn a multiple of 128;
+ * 0 < n_bins <= vocab, n_bins <= 1024.  rms_eps > 0, rope_theta > 1. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, n_bins;
+  float rms_eps;    /* RMSNorm: x / sqrt(mean(x^2) + rms_eps) * gain */
+  float rope_theta; /* RoPE base: pair (i, i + head_dim/2) turns by t * theta^(-2i/head_dim) */
+  int32_t dtype;    /* ams_dtype */
+} ams_model_cfg;
+
+/* Device pointers to the model's parameters (dtype = cfg.dtype unless fp32 is stated).
+ * ams_model_create packs them into the model workspace -- each RMSNorm gain is
+ * folded into the columns of the matrices that read the normalised vector
+ * (W diag(g)) -- except `embed`, which ams_embed_ids reads and must outlive the
+ * model. */
+typedef struct {
+  const void *w_q, *w_k, *w_v, *w_o; /* [n_layers][d][d] */
+  const void *w_gate, *w_up;         /* [n_layers][d_ffn][d] */
+  const void *w_down;                /* [n_layers][d][d_ffn] */
+  const float *g_attn, *g_ffn;       /* [n_layers][d] fp32 RMSNorm gains */
+  const float *g_final;              /* [d] fp32 final RMSNorm gain */
+  const void *embed;                 /* [vocab][d] input embedding table */
+  const void *head_bins;             /* [n_bins][d]: rows vocab-n_bins..vocab-1 of the output head */
+} ams_weights;
+
+/* ---- library ---------------------------------------------------------- */
+
+/* Status name ("AMS_OK", ...); never NULL. */
+const char* ams_status_str(int32_t status);
+/* Message of the last failing call on this thread ("" if none); never NULL. */
+const char* ams_last_error(void);
+/* Number of visible gfx950 devices (0 when none or no HIP runtime). */
+int32_t ams_device_count(void);
+
+/* ---- model ------------------------------------------------------------ */
+
+/* Bytes of device workspace ams_model_create needs for `cfg` (0 if cfg is invalid). */
+size_t ams_model_workspace_bytes(const ams_model_cfg* cfg);
+
+/* Validates cfg and weights, then packs the weights into `ws` (device memory of
+ * at least ams_model_workspace_bytes(cfg) bytes, 256-byte aligned) with
+ * copies enqueued on `stream`.  The source weights may be freed once the
+ * stream has passed the copies; `ws` and `embed` must outlive the model.
+ * On success *out receives the handle.  Errors: AMS_EINVAL, AMS_ENOMEM,
+ * AMS_ENODEV, AMS_EHIP. */
+ams_status ams_model_create(const ams_model_cfg* cfg, const ams_weights* w, void* ws,
+                            size_t ws_bytes, void* stream, ams_model** out);
+void ams_model_destroy(ams_model* m); /* NULL is a no-op; destroy contexts first */
+
+/* ---- text embedding --------------------------------------------------- */
+
+/* out[i][:] = embed[ids[i]][:] for i < n (ids and out on the device, out of
+ * shape [n][d] in the model dtype).  Ids outside [0, vocab) are clamped into
+ * range by the kernel.  Prefix ingest for instruction tokens.
+ * Errors: AMS_EINVAL, AMS_EHIP. */
+ams_status ams_embed_ids(const ams_model* m, const int32_t* ids, int32_t n, void* out,
+                         void* stream);
+
+/* ---- context ---------------------------------------------------------- */
+
+/* Bytes of device workspace a context needs: the K/V slab for `batch` rows of
+ * `capacity` tokens (head-major [layer][K|V][row][head][capacity][head_dim])
+ * plus activations for `max_pass_tokens` tokens per forward pass
+ * (0 selects min(batch * capacity, 32768)).  0 if an argument is invalid. */
+size_t ams_ctx_workspace_bytes(const ams_model_cfg* cfg, int32_t batch, int32_t capacity,
+                               int32_t max_pass_tokens);
+
+/* Creates a context of `batch` rows, each holding up to `capacity` tokens
+ * (1 <= batch <= 1024, capacity a multiple of 64, capacity >= 64).  `ws` is
+ * device memory of at least ams_ctx_workspace_bytes(...) bytes, 256-byte
+ * aligned, owned by the caller.  State EMPTY.  Errors: AMS_EINVAL,
+ * AMS_ENOMEM, AMS_EHIP. */
+ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens,
+                          void* ws, size_t ws_bytes, ams_ctx** out);
+void ams_ctx_destroy(ams_ctx* c); /* NULL is a no-op */
+
+/* Builds the context from each row's prefix: `prefix` is a device array
+ * [sum_b lens[b]][d] in the model dtype, rows packed one after another
+ * (row b's tokens at positions 0..lens[b]-1); `lens` is a host array [batch]
+ * with 1 <= lens[b] <= capacity.  Computes and keeps every layer's K/V
+ * and the final hidden state of each row's last token.  Any previous
+ * content is discarded.  State -> READY.
+ * Errors: AMS_EINVAL, AMS_ECAPACITY, AMS_EHIP. */
+ams_status ams_ctx_build(ams_ctx* c, const void* prefix, const int32_t* lens, void* stream);
+
+/* One action step.
+ *   new_tokens: device [sum_b new_lens[b]][d] (model dtype) or NULL;
+ *   new_lens:   host [batch] (0 allowed per row) or NULL for no new tokens.
+ * The new tokens are appended to the rows' contexts first (their K/V kept:
+ * the paper's post-inference insert).  Then n_actions bins are decoded
+ * greedily per row: the first from the last committed token's hidden state,
+ * each later one after feeding back the previous bin's embedding (vocabulary
+ * id vocab - n_bins + bin).  The fed-back tokens occupy scratch positions
+ * that are dropped when the call ends, so committed lengths grow only by
+ * new_lens.  Ties between equal logits go to the lowest bin.
+ *   out_tokens: device int32 [batch][n_actions]: chosen bins.
+ *   out_logits: device fp32 [batch][n_actions][n_bins] or NULL.
+ *   forced:     device int32 [batch][n_actions] or NULL: when given, bin
+ *               forced[b][j] is fed back after action j instead of the
+ *               argmax (teacher forcing); out_tokens still reports the
+ *               argmax.  Forced bins are clamped into [0, n_bins).
+ * Requires READY (else AMS_ESTATE), 1 <= n_actions, and for every row
+ * len[b] + new_lens[b] + n_actions - 1 <= capacity (else AMS_ECAPACITY).
+ * Errors: AMS_EINVAL, AMS_ESTATE, AMS_ECAPACITY, AMS_EHIP. */
+ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_lens,
+                        int32_t n_actions, int32_t* out_tokens, float* out_logits,
+                        const int32_t* forced, void* stream);
+
+/* Discards the context (host-side only; enqueues nothing).  State -> INVALID;
+ * lengths read 0 until the next build. */
+ams_status ams_ctx_invalidate(ams_ctx* c);
+
+/* Committed length of every row into host array lens[batch]. */
+ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens);
+
+/* Current state: 0 EMPTY, 1 READY, 2 INVALID; negative status on error. */
+int32_t ams_ctx_state(const ams_ctx* c);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AMS_H */

@@ -1,0 +1,308 @@
+// C ABI (include/ams.h): argument, state and capacity checks, device-pointer
+// range checks, then the engine.  Nothing is enqueued before every check has
+// passed; a HIP failure after that invalidates the context.
+#include "ams.h"
+
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "engine.h"
+#include "kernels.h"
+
+struct ams_model {
+  ams::Model m;
+};
+struct ams_ctx {
+  ams::Ctx c;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+ams_status fail(int s, const std::string& msg) {
+  g_err = msg;
+  return (ams_status)s;
+}
+
+ams::Cfg to_cfg(const ams_model_cfg& c) {
+  return ams::Cfg{c.n_layers, c.d_model, c.n_heads, c.head_dim, c.d_ffn, c.vocab, c.n_bins,
+                  c.rms_eps, c.rope_theta, c.dtype};
+}
+
+bool is_gfx950(int dev) {
+  hipDeviceProp_t p;
+  if (hipGetDeviceProperties(&p, dev) != hipSuccess) return false;
+  return strncmp(p.gcnArchName, "gfx950", 6) == 0;
+}
+
+// Current device must be a gfx950.
+int current_device(int* dev, std::string& err) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+    err = "no HIP device";
+    return ams::S_ENODEV;
+  }
+  if (hipGetDevice(dev) != hipSuccess) {
+    err = "hipGetDevice failed";
+    return ams::S_ENODEV;
+  }
+  if (!is_gfx950(*dev)) {
+    err = "current device is not a gfx950";
+    return ams::S_ENODEV;
+  }
+  return ams::S_OK;
+}
+
+// [p, p + bytes) must lie inside one device allocation of `dev`.
+bool dev_range(const void* p, size_t bytes, int dev, const char* what, std::string& err) {
+  if (!p) {
+    err = std::string(what) + " is NULL";
+    return false;
+  }
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess || a.type != hipMemoryTypeDevice || a.device != dev) {
+    (void)hipGetLastError();
+    err = std::string(what) + " is not device memory of the current device";
+    return false;
+  }
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p) != hipSuccess) {
+    (void)hipGetLastError();
+    err = std::string(what) + ": allocation range unknown";
+    return false;
+  }
+  if ((const char*)p + bytes > (const char*)base + size) {
+    err = std::string(what) + " is smaller than " + std::to_string(bytes) + " bytes";
+    return false;
+  }
+  return true;
+}
+
+bool aligned256(const void* p) { return ((uintptr_t)p & 255) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* ams_status_str(int32_t s) {
+  switch (s) {
+    case AMS_OK: return "AMS_OK";
+    case AMS_EINVAL: return "AMS_EINVAL";
+    case AMS_ESTATE: return "AMS_ESTATE";
+    case AMS_ECAPACITY: return "AMS_ECAPACITY";
+    case AMS_ENODEV: return "AMS_ENODEV";
+    case AMS_EHIP: return "AMS_EHIP";
+    case AMS_ENOMEM: return "AMS_ENOMEM";
+    default: return "AMS_UNKNOWN";
+  }
+}
+
+const char* ams_last_error(void) { return g_err.c_str(); }
+
+int32_t ams_device_count(void) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int k = 0;
+  for (int i = 0; i < n; ++i) k += is_gfx950(i);
+  return k;
+}
+
+size_t ams_model_workspace_bytes(const ams_model_cfg* cfg) {
+  if (!cfg) return 0;
+  std::string e;
+  const ams::Cfg c = to_cfg(*cfg);
+  if (ams::check_cfg(c, e) != ams::S_OK) return 0;
+  return ams::model_layout(c).total;
+}
+
+ams_status ams_model_create(const ams_model_cfg* cfg, const ams_weights* w, void* ws, size_t ws_bytes, void* stream,
+                            ams_model** out) {
+  g_err.clear();
+  if (!cfg || !w || !out) return fail(AMS_EINVAL, "cfg, weights and out must not be NULL");
+  const ams::Cfg c = to_cfg(*cfg);
+  std::string e;
+  if (int s = ams::check_cfg(c, e)) return fail(s, e);
+  const ams::ModelLayout lay = ams::model_layout(c);
+  if (!ws) return fail(AMS_EINVAL, "workspace is NULL");
+  if (!aligned256(ws)) return fail(AMS_EINVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < lay.total) return fail(AMS_ENOMEM, "model workspace too small: need " + std::to_string(lay.total));
+  const void* ptrs[] = {w->w_q, w->w_k, w->w_v, w->w_o, w->w_gate, w->w_up, w->w_down,
+                        w->g_attn, w->g_ffn, w->g_final, w->embed, w->head_bins};
+  for (const void* p : ptrs)
+    if (!p) return fail(AMS_EINVAL, "a weight pointer is NULL");
+  int dev = 0;
+  if (int s = current_device(&dev, e)) return fail(s, e);
+  const size_t es = ams::elem_size(c), d = c.d_model, F = c.d_ffn, L = c.n_layers;
+  struct {
+    const void* p;
+    size_t bytes;
+    const char* what;
+  } chk[] = {
+      {w->w_q, L * d * d * es, "w_q"},         {w->w_k, L * d * d * es, "w_k"},
+      {w->w_v, L * d * d * es, "w_v"},         {w->w_o, L * d * d * es, "w_o"},
+      {w->w_gate, L * F * d * es, "w_gate"},   {w->w_up, L * F * d * es, "w_up"},
+      {w->w_down, L * d * F * es, "w_down"},   {w->g_attn, L * d * 4, "g_attn"},
+      {w->g_ffn, L * d * 4, "g_ffn"},          {w->g_final, d * 4, "g_final"},
+      {w->embed, (size_t)c.vocab * d * es, "embed"}, {w->head_bins, (size_t)c.n_bins * d * es, "head_bins"},
+      {ws, lay.total, "model workspace"},
+  };
+  for (auto& k : chk)
+    if (!dev_range(k.p, k.bytes, dev, k.what, e)) return fail(AMS_EINVAL, e);
+
+  ams_model* m = new ams_model();
+  m->m.cfg = c;
+  m->m.lay = lay;
+  m->m.device = dev;
+  m->m.ws = (char*)ws;
+  m->m.embed = w->embed;
+  m->m.st = c.dtype == AMS_F32 ? ams::DT_F32 : ams::DT_BF16;
+  m->m.ct = c.dtype == AMS_F32 ? ams::DT_F32 : ams::DT_F16;
+  const ams::ams_weights_view v{w->w_q,    w->w_k,  w->w_v,    w->w_o,     w->w_gate, w->w_up,
+                                w->w_down, w->g_attn, w->g_ffn, w->g_final, w->embed,  w->head_bins};
+  if (ams::model_pack(m->m, v, (hipStream_t)stream, e) != hipSuccess) {
+    delete m;
+    return fail(AMS_EHIP, e);
+  }
+  *out = m;
+  return AMS_OK;
+}
+
+void ams_model_destroy(ams_model* m) { delete m; }
+
+ams_status ams_embed_ids(const ams_model* m, const int32_t* ids, int32_t n, void* out, void* stream) {
+  g_err.clear();
+  if (!m) return fail(AMS_EINVAL, "model is NULL");
+  if (n < 0) return fail(AMS_EINVAL, "n must be >= 0");
+  if (n == 0) return AMS_OK;
+  const ams::Cfg& c = m->m.cfg;
+  std::string e;
+  if (!dev_range(ids, (size_t)n * 4, m->m.device, "ids", e)) return fail(AMS_EINVAL, e);
+  if (!dev_range(out, (size_t)n * c.d_model * ams::elem_size(c), m->m.device, "out", e)) return fail(AMS_EINVAL, e);
+  hipError_t r = ams::embed_rows(m->m.st, m->m.embed, ids, n, c.d_model, c.vocab, out, (hipStream_t)stream);
+  if (r != hipSuccess) return fail(AMS_EHIP, std::string("embed: ") + hipGetErrorString(r));
+  return AMS_OK;
+}
+
+size_t ams_ctx_workspace_bytes(const ams_model_cfg* cfg, int32_t batch, int32_t capacity, int32_t max_pass_tokens) {
+  if (!cfg) return 0;
+  std::string e;
+  const ams::Cfg c = to_cfg(*cfg);
+  if (ams::check_cfg(c, e) != ams::S_OK) return 0;
+  if (ams::check_ctx_args(c, batch, capacity, max_pass_tokens, e) != ams::S_OK) return 0;
+  return ams::ctx_layout(c, batch, capacity, max_pass_tokens).total;
+}
+
+ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens, void* ws,
+                          size_t ws_bytes, ams_ctx** out) {
+  g_err.clear();
+  if (!m || !out) return fail(AMS_EINVAL, "model and out must not be NULL");
+  std::string e;
+  if (int s = ams::check_ctx_args(m->m.cfg, batch, capacity, max_pass_tokens, e)) return fail(s, e);
+  const ams::CtxLayout lay = ams::ctx_layout(m->m.cfg, batch, capacity, max_pass_tokens);
+  if (!ws) return fail(AMS_EINVAL, "workspace is NULL");
+  if (!aligned256(ws)) return fail(AMS_EINVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < lay.total) return fail(AMS_ENOMEM, "context workspace too small: need " + std::to_string(lay.total));
+  if (!dev_range(ws, lay.total, m->m.device, "context workspace", e)) return fail(AMS_EINVAL, e);
+  ams_ctx* c = new ams_ctx();
+  c->c.model = &m->m;
+  c->c.lay = lay;
+  c->c.ws = (char*)ws;
+  c->c.book.init(batch, capacity);
+  if (ams::ctx_init(c->c, e) != hipSuccess) {
+    ams::ctx_release(c->c);
+    delete c;
+    return fail(AMS_EHIP, e);
+  }
+  m->m.live_ctx++;
+  *out = c;
+  return AMS_OK;
+}
+
+void ams_ctx_destroy(ams_ctx* c) {
+  if (!c) return;
+  ams::ctx_release(c->c);
+  c->c.model->live_ctx--;
+  delete c;
+}
+
+ams_status ams_ctx_build(ams_ctx* c, const void* prefix, const int32_t* lens, void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = x.book.check_build(lens, e)) return fail(s, e);
+  size_t tot = 0;
+  for (int b = 0; b < x.lay.batch; ++b) tot += (size_t)lens[b];
+  const ams::Cfg& m = x.model->cfg;
+  if (!dev_range(prefix, tot * m.d_model * ams::elem_size(m), x.model->device, "prefix", e))
+    return fail(AMS_EINVAL, e);
+  std::vector<int32_t> start(x.lay.batch, 0);
+  if (ams::ctx_forward_tokens(x, prefix, lens, start.data(), 1, (hipStream_t)stream, e) != hipSuccess) {
+    x.book.invalidate();
+    return fail(AMS_EHIP, e);
+  }
+  x.book.commit_build(lens);
+  return AMS_OK;
+}
+
+ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_lens, int32_t n_actions,
+                        int32_t* out_tokens, float* out_logits, const int32_t* forced, void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = x.book.check_step(new_lens, n_actions, e)) return fail(s, e);
+  const ams::Cfg& m = x.model->cfg;
+  const int B = x.lay.batch, dev = x.model->device;
+  const size_t BA = (size_t)B * n_actions;
+  if (!dev_range(out_tokens, BA * 4, dev, "out_tokens", e)) return fail(AMS_EINVAL, e);
+  if (out_logits && !dev_range(out_logits, BA * m.n_bins * 4, dev, "out_logits", e)) return fail(AMS_EINVAL, e);
+  if (forced && !dev_range(forced, BA * 4, dev, "forced", e)) return fail(AMS_EINVAL, e);
+  size_t n_new = 0;
+  if (new_lens)
+    for (int b = 0; b < B; ++b) n_new += (size_t)new_lens[b];
+  if (n_new > 0 && !dev_range(new_tokens, n_new * m.d_model * ams::elem_size(m), dev, "new_tokens", e))
+    return fail(AMS_EINVAL, e);
+
+  hipStream_t s = (hipStream_t)stream;
+  if (n_new > 0) {
+    if (ams::ctx_forward_tokens(x, new_tokens, new_lens, x.book.len.data(), 0, s, e) != hipSuccess) {
+      x.book.invalidate();
+      return fail(AMS_EHIP, e);
+    }
+    x.book.commit_new(new_lens);
+  }
+  if (ams::ctx_decode(x, n_actions, out_tokens, out_logits, forced, s, e) != hipSuccess) {
+    x.book.invalidate();
+    return fail(AMS_EHIP, e);
+  }
+  return AMS_OK;
+}
+
+ams_status ams_ctx_invalidate(ams_ctx* c) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  c->c.book.invalidate();
+  return AMS_OK;
+}
+
+ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens) {
+  g_err.clear();
+  if (!c || !lens) return fail(AMS_EINVAL, "context and lens must not be NULL");
+  for (int b = 0; b < c->c.lay.batch; ++b) lens[b] = c->c.book.len[b];
+  return AMS_OK;
+}
+
+int32_t ams_ctx_state(const ams_ctx* c) {
+  if (!c) return AMS_EINVAL;
+  return c->c.book.state;
+}
+
+}  // extern "C"

@@ -1,0 +1,224 @@
+// Engine: weight packing, context set-up, the token forward pass (prefix
+// build and observation extension) and the greedy decode loop, which is
+// captured once per (n_actions, output buffers) into a HIP graph and replayed.
+#include "engine.h"
+
+#include <stdlib.h>
+
+#include "../kernels/kernels.h"
+
+namespace ams {
+
+#define TRY(expr)                                                        \
+  do {                                                                   \
+    hipError_t e_ = (expr);                                              \
+    if (e_ != hipSuccess) {                                              \
+      err = std::string(#expr) + ": " + hipGetErrorString(e_);           \
+      return e_;                                                         \
+    }                                                                    \
+  } while (0)
+
+static const char* off(const void* p, size_t bytes) { return (const char*)p + bytes; }
+
+hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err) {
+  // bf16 weights become fp16 in the packed copy: exact for |w| >= 2^-14, an
+  // fp16 subnormal (absolute error <= 2^-25) below; fp32 models are copied.
+  // Each RMSNorm gain is folded into the columns of the matrices that read the
+  // normalised vector: W u = (W diag(g)) (h / rms(h)).
+  const Cfg& c = m.cfg;
+  const size_t es = elem_size(c), d = c.d_model, F = c.d_ffn;
+  const size_t dde = d * d * es;
+  const int st = m.st, ct = m.ct;
+  for (int l = 0; l < c.n_layers; ++l) {
+    char* qkv = (char*)m.wqkv(l);
+    const float* ga = w.g_attn + (size_t)l * d;
+    const float* gf = w.g_ffn + (size_t)l * d;
+    TRY(convert(st, ct, off(w.w_q, l * dde), d, (int)d, ga, qkv, s));
+    TRY(convert(st, ct, off(w.w_k, l * dde), d, (int)d, ga, qkv + dde, s));
+    TRY(convert(st, ct, off(w.w_v, l * dde), d, (int)d, ga, qkv + 2 * dde, s));
+    TRY(convert(st, ct, off(w.w_o, l * dde), d, (int)d, nullptr, (void*)m.wo(l), s));
+    TRY(pack_gate_up(st, ct, off(w.w_gate, l * F * d * es), off(w.w_up, l * F * d * es), gf, (int)F, (int)d,
+                     (void*)m.wgu(l), s));
+    TRY(convert(st, ct, off(w.w_down, l * d * F * es), d, (int)F, nullptr, (void*)m.wd(l), s));
+  }
+  TRY(hipMemsetAsync(m.ws + m.lay.head_bins, 0, (size_t)bins_padded(c) * d * es, s));
+  TRY(convert(st, ct, w.head_bins, c.n_bins, (int)d, w.g_final, m.ws + m.lay.head_bins, s));
+  TRY(convert(st, ct, off(w.embed, (size_t)(c.vocab - c.n_bins) * d * es), c.n_bins, (int)d, nullptr,
+              m.ws + m.lay.bin_embed, s));
+  return hipSuccess;
+}
+
+hipError_t ctx_init(Ctx& c, std::string& err) {
+  const Cfg& m = c.model->cfg;
+  TRY(hipStreamCreateWithFlags(&c.capture_stream, hipStreamNonBlocking));
+  hipStream_t s = c.capture_stream;
+  TRY(rope_table(c.rope(), c.lay.capacity, m.head_dim, m.rope_theta, s));
+  TRY(hipMemsetAsync(c.ws + c.lay.h_last, 0, c.lay.part - c.lay.h_last, s));
+  TRY(hipMemsetAsync(c.ws + c.lay.lens, 0, c.lay.total - c.lay.lens, s));
+  TRY(hipStreamSynchronize(s));
+  c.splits = decode_splits(c.lay.batch, m.n_heads, c.lay.capacity);
+  c.meta_host.assign(c.lay.meta_ints, 0);
+  return hipSuccess;
+}
+
+void ctx_release(Ctx& c) {
+  if (!c.graphs.empty()) hipDeviceSynchronize();
+  for (auto& kv : c.graphs) hipGraphExecDestroy(kv.second);
+  c.graphs.clear();
+  c.graph_lru.clear();
+  if (c.capture_stream) hipStreamDestroy(c.capture_stream);
+  c.capture_stream = nullptr;
+}
+
+// One decoder layer over the M tokens of a token pass.
+static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t s, std::string& err) {
+  const Model& md = *c.model;
+  const Cfg& m = md.cfg;
+  const int d = m.d_model, F = m.d_ffn, dt = md.ct;
+  TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
+  TRY(gemm(dt, EPI_STORE, c.u(), md.wqkv(l), M, 3 * d, d, c.qkv(), 3 * d, s));
+  TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), s));
+  TRY(attn_prefill(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), c.o(),
+                   s));
+  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), M, d, d, c.h(), d, s));
+  TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
+  TRY(gemm(dt, EPI_SWIGLU, c.u(), md.wgu(l), M, 2 * F, d, c.a(), F, s));
+  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), M, d, F, c.h(), d, s));
+  return hipSuccess;
+}
+
+hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, const int32_t* start, int set_lens,
+                              hipStream_t s, std::string& err) {
+  const Cfg& m = c.model->cfg;
+  const int B = c.lay.batch;
+  const size_t es = elem_size(m), d = m.d_model;
+  Plan p = plan_passes(B, counts, start, c.lay.pass_tokens);
+  // meta layout: row[B] pos[B] off[2B+1] lensv[B]
+  std::vector<int32_t>& h = c.meta_host;
+  std::fill(h.begin(), h.end(), 0);
+  std::copy(p.row.begin(), p.row.end(), h.begin());
+  std::copy(p.pos.begin(), p.pos.end(), h.begin() + B);
+  std::copy(p.off.begin(), p.off.end(), h.begin() + 2 * B);
+  for (int b = 0; b < B; ++b) h[4 * B + 1 + b] = counts[b];
+  int32_t* md = c.meta();
+  TRY(hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  for (size_t pi = 0; pi < p.passes.size(); ++pi) {
+    const Pass& ps = p.passes[pi];
+    Segs sg{md + ps.seg_begin, md + B + ps.seg_begin, md + 2 * B + ps.seg_begin + (int)pi, ps.n_seg, ps.n_tok,
+            ps.max_len, ps.max_end};
+    TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
+    for (int l = 0; l < m.n_layers; ++l)
+      if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
+    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s));
+  }
+  TRY(update_lens(c.lens(), md + 4 * B + 1, B, set_lens, s));
+  return hipSuccess;
+}
+
+// Projection of a normalised input in the decode pass: up to 16 fp16 rows run
+// the GEMV with the RMSNorm fused; otherwise rmsnorm writes u first.
+static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* W, int N, int K, void* out, int ldo,
+                            hipStream_t s, std::string& err) {
+  const Model& md = *c.model;
+  const int B = c.lay.batch;
+  const float eps = md.cfg.rms_eps;
+  if (md.ct == DT_F16 && B <= 16) {
+    TRY(gemv_rmsnorm(md.ct, epi, h, eps, W, B, N, K, out, ldo, s));
+  } else {
+    TRY(rmsnorm(md.ct, h, B, K, eps, c.u(), s));
+    TRY(gemm(md.ct, epi, c.u(), W, B, N, K, out, ldo, s));
+  }
+  return hipSuccess;
+}
+
+// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.
+static hipError_t layer_decode(Ctx& c, int l, int jpos, hipStream_t s, std::string& err) {
+  const Model& md = *c.model;
+  const Cfg& m = md.cfg;
+  const int d = m.d_model, F = m.d_ffn, dt = md.ct, B = c.lay.batch;
+  if (norm_proj(c, EPI_STORE, c.h(), md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, s, err) != hipSuccess)
+    return hipErrorLaunchFailure;
+  TRY(attn_decode(dt, c.qkv(), c.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
+                  c.kslab(l), c.vslab(l), c.part(), c.o(), s));
+  if (c.splits > 1) TRY(attn_merge(dt, c.part(), B, m.n_heads, m.head_dim, c.splits, c.o(), s));
+  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s));
+  if (norm_proj(c, EPI_SWIGLU, c.h(), md.wgu(l), 2 * F, d, c.a(), F, s, err) != hipSuccess)
+    return hipErrorLaunchFailure;
+  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s));
+  return hipSuccess;
+}
+
+// Action head for decode position j: final RMSNorm + bin logits (the
+// projection GEMV over the padded head rows), then argmax/outputs/feed.
+static hipError_t head(Ctx& c, const float* hin, int A, int j, int32_t* tok, float* logits, const int32_t* forced,
+                       hipStream_t s, std::string& err) {
+  const Model& md = *c.model;
+  const Cfg& m = md.cfg;
+  const int B = c.lay.batch, d = m.d_model, nbp = bins_padded(m);
+  if (norm_proj(c, EPI_STORE, hin, md.head_bins(), nbp, d, c.logits(), nbp, s, err) != hipSuccess)
+    return hipErrorLaunchFailure;
+  TRY(argmax_feed(md.ct, c.logits(), nbp, md.bin_embed(), B, d, m.n_bins, A, j, tok, logits, forced, c.h(),
+                  j + 1 < A, s));
+  return hipSuccess;
+}
+
+static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
+                                 std::string& err) {
+  const Cfg& m = c.model->cfg;
+  if (head(c, c.h_last(), A, 0, tok, logits, forced, s, err) != hipSuccess) return hipErrorLaunchFailure;
+  for (int j = 1; j < A; ++j) {
+    for (int l = 0; l < m.n_layers; ++l)
+      if (layer_decode(c, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
+    if (head(c, c.h(), A, j, tok, logits, forced, s, err) != hipSuccess) return hipErrorLaunchFailure;
+  }
+  return hipSuccess;
+}
+
+static bool graphs_enabled() {
+  const char* e = getenv("AMS_GRAPH");
+  return !(e && e[0] == '0');
+}
+
+hipError_t ctx_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
+                      std::string& err) {
+  if (!graphs_enabled()) return enqueue_decode(c, A, tok, logits, forced, s, err);
+  GraphKey key{A, tok, logits, forced};
+  auto it = c.graphs.find(key);
+  if (it == c.graphs.end()) {
+    hipStream_t cs = c.capture_stream;
+    TRY(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal));
+    hipError_t e = enqueue_decode(c, A, tok, logits, forced, cs, err);
+    hipGraph_t g = nullptr;
+    hipError_t e2 = hipStreamEndCapture(cs, &g);
+    if (e != hipSuccess) {
+      if (g) hipGraphDestroy(g);
+      return e;
+    }
+    if (e2 != hipSuccess) {
+      err = std::string("hipStreamEndCapture: ") + hipGetErrorString(e2);
+      return e2;
+    }
+    hipGraphExec_t ex = nullptr;
+    hipError_t e3 = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    hipGraphDestroy(g);
+    if (e3 != hipSuccess) {
+      err = std::string("hipGraphInstantiate: ") + hipGetErrorString(e3);
+      return e3;
+    }
+    if (c.graph_lru.size() >= 8) {
+      TRY(hipStreamSynchronize(s));  // the evicted graph may still be running on s
+      auto old = c.graphs.find(c.graph_lru.front());
+      if (old != c.graphs.end()) {
+        hipGraphExecDestroy(old->second);
+        c.graphs.erase(old);
+      }
+      c.graph_lru.erase(c.graph_lru.begin());
+    }
+    it = c.graphs.emplace(key, ex).first;
+    c.graph_lru.push_back(key);
+  }
+  TRY(hipGraphLaunch(it->second, s));
+  return hipSuccess;
+}
+
+}  // namespace ams

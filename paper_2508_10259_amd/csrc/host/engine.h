@@ -1,0 +1,86 @@
+// Engine: owns the host handles of a model and of a context and enqueues the
+// forward passes.  All checks happen in the C ABI layer before these run.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "state.h"
+
+namespace ams {
+
+struct ams_weights_view {
+  const void *w_q, *w_k, *w_v, *w_o, *w_gate, *w_up, *w_down;
+  const float *g_attn, *g_ffn, *g_final;
+  const void *embed, *head_bins;
+};
+
+struct Model {
+  Cfg cfg;
+  ModelLayout lay;
+  int st = 0;  // storage type of the caller's arrays (kernels.h DType)
+  int ct = 0;  // compute type of the packed weights, activations and K/V
+  int device = 0;
+  char* ws = nullptr;
+  const void* embed = nullptr;  // caller's full table (referenced)
+  int live_ctx = 0;
+
+  const void* wqkv(int l) const { return ws + lay.wqkv + l * lay.per_layer_qkv; }
+  const void* wo(int l) const { return ws + lay.wo + l * lay.per_layer_o; }
+  const void* wgu(int l) const { return ws + lay.wgu + l * lay.per_layer_gu; }
+  const void* wd(int l) const { return ws + lay.wd + l * lay.per_layer_d; }
+  const void* head_bins() const { return ws + lay.head_bins; }
+  const void* bin_embed() const { return ws + lay.bin_embed; }
+};
+
+struct GraphKey {
+  int n_actions;
+  void* tokens;
+  void* logits;
+  const void* forced;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(n_actions, tokens, logits, forced) < std::tie(o.n_actions, o.tokens, o.logits, o.forced);
+  }
+};
+
+struct Ctx {
+  Model* model = nullptr;
+  CtxLayout lay;
+  RowBook book;
+  char* ws = nullptr;
+  int splits = 1;
+  hipStream_t capture_stream = nullptr;
+  std::map<GraphKey, hipGraphExec_t> graphs;
+  std::vector<GraphKey> graph_lru;
+  std::vector<int32_t> meta_host;  // staging of one call's pass metadata (kept until the next call)
+
+  void* kslab(int l) const { return ws + lay.kv + (size_t)(2 * l) * lay.slab_layer; }
+  void* vslab(int l) const { return ws + lay.kv + (size_t)(2 * l + 1) * lay.slab_layer; }
+  float* h() const { return (float*)(ws + lay.h); }
+  void* u() const { return ws + lay.u; }
+  float* qkv() const { return (float*)(ws + lay.qkv); }
+  void* o() const { return ws + lay.o; }
+  void* a() const { return ws + lay.a; }
+  float* h_last() const { return (float*)(ws + lay.h_last); }
+  float* part() const { return (float*)(ws + lay.part); }
+  float* logits() const { return (float*)(ws + lay.logits); }
+  float2* rope() const { return (float2*)(ws + lay.rope); }
+  int32_t* lens() const { return (int32_t*)(ws + lay.lens); }
+  int32_t* meta() const { return (int32_t*)(ws + lay.meta); }
+};
+
+// Enqueue-level operations; each returns hipSuccess or the first failure and
+// fills `err`.
+hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err);
+hipError_t ctx_init(Ctx& c, std::string& err);
+hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, const int32_t* start, int set_lens,
+                              hipStream_t s, std::string& err);
+hipError_t ctx_decode(Ctx& c, int n_actions, int32_t* out_tokens, float* out_logits, const int32_t* forced,
+                      hipStream_t s, std::string& err);
+void ctx_release(Ctx& c);
+
+}  // namespace ams

@@ -1,0 +1,245 @@
+// Host-only bookkeeping of the cached-context decoder: configuration checks,
+// device workspace layouts, the per-row length book (commit / rollback /
+// invalidate) and the planner that packs ragged rows into forward passes.
+// No HIP dependency: the CPU tests compile this header with a plain C++
+// compiler and sanitizers.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <string>
+#include <vector>
+
+namespace ams {
+
+enum Status { S_OK = 0, S_EINVAL = -1, S_ESTATE = -2, S_ECAPACITY = -3, S_ENODEV = -4, S_EHIP = -5, S_ENOMEM = -6 };
+
+struct Cfg {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, n_bins;
+  float rms_eps, rope_theta;
+  int32_t dtype;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline int check_cfg(const Cfg& c, std::string& err) {
+  auto bad = [&](const char* m) { err = m; return (int)S_EINVAL; };
+  if (c.n_layers < 1 || c.n_layers > 1024) return bad("n_layers must be in [1, 1024]");
+  if (c.head_dim != 64 && c.head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c.n_heads < 1 || (int64_t)c.n_heads * c.head_dim != c.d_model) return bad("d_model must equal n_heads * head_dim");
+  if (c.d_model % 128 != 0 || c.d_model > 16384) return bad("d_model must be a multiple of 128 and <= 16384");
+  if (c.d_ffn < 128 || c.d_ffn % 128 != 0 || c.d_ffn > 65536) return bad("d_ffn must be a multiple of 128 in [128, 65536]");
+  if (c.n_bins < 1 || c.n_bins > 1024) return bad("n_bins must be in [1, 1024]");
+  if (c.vocab < c.n_bins || c.vocab > (1 << 24)) return bad("vocab must be in [n_bins, 2^24]");
+  if (!(c.rms_eps > 0.f) || !std::isfinite(c.rms_eps)) return bad("rms_eps must be finite and > 0");
+  if (!(c.rope_theta > 1.f) || !std::isfinite(c.rope_theta)) return bad("rope_theta must be finite and > 1");
+  if (c.dtype != 0 && c.dtype != 1) return bad("dtype must be AMS_F32 (0) or AMS_BF16 (1)");
+  return S_OK;
+}
+
+inline size_t elem_size(const Cfg& c) { return c.dtype == 0 ? 4 : 2; }
+
+// Rows of the packed action head, padded with zero rows to a multiple of 64
+// so the head runs through the same GEMV/GEMM kernels as the projections.
+inline int bins_padded(const Cfg& c) { return (c.n_bins + 63) / 64 * 64; }
+
+// Model workspace: packed weights (RMSNorm gains folded in), the bin rows of
+// the head and of the embedding table.  Offsets in bytes from the workspace base.
+struct ModelLayout {
+  size_t wqkv, wo, wgu, wd, head_bins, bin_embed, total;
+  size_t per_layer_qkv, per_layer_o, per_layer_gu, per_layer_d;  // bytes per layer
+};
+
+inline ModelLayout model_layout(const Cfg& c) {
+  const size_t es = elem_size(c), d = c.d_model, F = c.d_ffn, L = c.n_layers;
+  ModelLayout m{};
+  m.per_layer_qkv = 3 * d * d * es;
+  m.per_layer_o = d * d * es;
+  m.per_layer_gu = 2 * F * d * es;
+  m.per_layer_d = d * F * es;
+  size_t o = 0;
+  m.wqkv = o; o = align256(o + L * m.per_layer_qkv);
+  m.wo = o; o = align256(o + L * m.per_layer_o);
+  m.wgu = o; o = align256(o + L * m.per_layer_gu);
+  m.wd = o; o = align256(o + L * m.per_layer_d);
+  m.head_bins = o; o = align256(o + (size_t)bins_padded(c) * d * es);
+  m.bin_embed = o; o = align256(o + (size_t)c.n_bins * d * es);
+  m.total = o;
+  return m;
+}
+
+// Context workspace: the K/V slab, activations of one forward pass, and
+// small device-side tables.
+struct CtxLayout {
+  int batch, capacity, pass_tokens, max_splits;
+  size_t slab_layer;  // bytes of K (or V) for one layer
+  size_t kv, h, u, qkv, o, a, h_last, part, logits, rope, lens, meta, total;
+  size_t meta_ints;
+};
+
+inline int default_pass_tokens(int batch, int capacity) {
+  const int64_t bc = (int64_t)batch * capacity;
+  int t = (int)std::min<int64_t>(bc, 32768);
+  return std::max(t, capacity);
+}
+
+inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens, std::string& err) {
+  if (batch < 1 || batch > 1024) { err = "batch must be in [1, 1024]"; return S_EINVAL; }
+  if (capacity < 64 || capacity % 64 != 0 || capacity > (1 << 20)) {
+    err = "capacity must be a multiple of 64 in [64, 2^20]";
+    return S_EINVAL;
+  }
+  if (pass_tokens != 0 && (pass_tokens < capacity || pass_tokens > (1 << 22))) {
+    err = "max_pass_tokens must be 0 or in [capacity, 2^22]";
+    return S_EINVAL;
+  }
+  (void)c;
+  return S_OK;
+}
+
+inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_tokens) {
+  CtxLayout x{};
+  const size_t es = elem_size(c), d = c.d_model, F = c.d_ffn, L = c.n_layers, B = batch;
+  x.batch = batch;
+  x.capacity = capacity;
+  x.pass_tokens = pass_tokens ? pass_tokens : default_pass_tokens(batch, capacity);
+  x.max_splits = capacity / 64;
+  const size_t T = std::max<size_t>(x.pass_tokens, B);
+  x.slab_layer = B * (size_t)capacity * d * es;
+  size_t o = 0;
+  x.kv = o; o = align256(o + 2 * L * x.slab_layer);
+  x.h = o; o = align256(o + T * d * 4);
+  x.u = o; o = align256(o + T * d * es);
+  x.qkv = o; o = align256(o + T * 3 * d * 4);
+  x.o = o; o = align256(o + T * d * es);
+  x.a = o; o = align256(o + T * F * es);
+  x.h_last = o; o = align256(o + B * d * 4);
+  x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
+  x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
+  x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
+  x.lens = o; o = align256(o + B * 4);
+  // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B]
+  x.meta_ints = 5 * B + 1;
+  x.meta = o; o = align256(o + x.meta_ints * 4);
+  x.total = o;
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// length book: the host-side truth of each row's committed length
+
+enum CtxState { EMPTY = 0, READY = 1, INVALID = 2 };
+
+struct RowBook {
+  int batch = 0, capacity = 0;
+  int state = EMPTY;
+  std::vector<int32_t> len;
+
+  void init(int b, int cap) {
+    batch = b;
+    capacity = cap;
+    state = EMPTY;
+    len.assign(b, 0);
+  }
+
+  int check_build(const int32_t* lens, std::string& err) const {
+    if (!lens) { err = "lens is NULL"; return S_EINVAL; }
+    for (int b = 0; b < batch; ++b) {
+      if (lens[b] < 1) { err = "prefix length must be >= 1 (row " + std::to_string(b) + ")"; return S_EINVAL; }
+      if (lens[b] > capacity) { err = "prefix longer than capacity (row " + std::to_string(b) + ")"; return S_ECAPACITY; }
+    }
+    return S_OK;
+  }
+
+  int check_step(const int32_t* new_lens, int n_actions, std::string& err) const {
+    if (state != READY) { err = state == EMPTY ? "context was never built" : "context is invalidated"; return S_ESTATE; }
+    if (n_actions < 1 || n_actions > capacity) { err = "n_actions must be in [1, capacity]"; return S_EINVAL; }
+    for (int b = 0; b < batch; ++b) {
+      const int64_t n = new_lens ? new_lens[b] : 0;
+      if (n < 0) { err = "negative new length (row " + std::to_string(b) + ")"; return S_EINVAL; }
+      if ((int64_t)len[b] + n + n_actions - 1 > capacity) {
+        err = "row " + std::to_string(b) + " would exceed capacity";
+        return S_ECAPACITY;
+      }
+    }
+    return S_OK;
+  }
+
+  void commit_build(const int32_t* lens) {
+    for (int b = 0; b < batch; ++b) len[b] = lens[b];
+    state = READY;
+  }
+  void commit_new(const int32_t* new_lens) {
+    if (!new_lens) return;
+    for (int b = 0; b < batch; ++b) len[b] += new_lens[b];
+  }
+  void invalidate() {
+    std::fill(len.begin(), len.end(), 0);
+    state = INVALID;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// pass planner: rows with pending tokens, packed in row order into passes of
+// at most `pass_tokens` tokens (a row is never split: its count <= capacity
+// <= pass_tokens).
+
+struct Pass {
+  int seg_begin, n_seg;  // into the call's segment arrays
+  int tok_src;           // first token of the pass in the packed input
+  int n_tok, max_len, max_end;
+};
+
+struct Plan {
+  std::vector<int32_t> row, pos;  // per segment
+  std::vector<int32_t> off;       // per pass: n_seg + 1 local offsets, passes back to back
+  std::vector<Pass> passes;
+};
+
+// counts[b]: tokens to process for row b (0 = none); start[b]: first position.
+inline Plan plan_passes(int batch, const int32_t* counts, const int32_t* start, int pass_tokens) {
+  Plan p;
+  int src = 0;
+  Pass cur{0, 0, 0, 0, 0, 0};
+  std::vector<int32_t> cur_off{0};
+  auto flush = [&]() {
+    if (cur.n_seg == 0) return;
+    p.passes.push_back(cur);
+    p.off.insert(p.off.end(), cur_off.begin(), cur_off.end());
+    cur = Pass{(int)p.row.size(), 0, src, 0, 0, 0};
+    cur_off.assign(1, 0);
+  };
+  cur.tok_src = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int n = counts[b];
+    if (n <= 0) continue;
+    if (cur.n_tok + n > pass_tokens) flush();
+    if (cur.n_seg == 0) { cur.seg_begin = (int)p.row.size(); cur.tok_src = src; }
+    p.row.push_back(b);
+    p.pos.push_back(start[b]);
+    cur.n_seg++;
+    cur.n_tok += n;
+    cur.max_len = std::max(cur.max_len, n);
+    cur.max_end = std::max(cur.max_end, start[b] + n);
+    cur_off.push_back(cur.n_tok);
+    src += n;
+  }
+  flush();
+  return p;
+}
+
+// Key splits of the decode attention.  One workgroup per (row, head) covers
+// the whole context when there are >= 128 of them; fewer pairs with long
+// contexts split the keys (>= 256 positions per split) and merge by
+// log-sum-exp in a second kernel.
+inline int decode_splits(int batch, int n_heads, int capacity) {
+  const int pairs = batch * n_heads;
+  if (pairs >= 128) return 1;
+  const int s = (128 + pairs - 1) / pairs;
+  return std::max(1, std::min(s, capacity / 256));
+}
+
+}  // namespace ams

@@ -1,0 +1,429 @@
+// Attention over the cached context.
+//
+// K/V slab of one layer: K and V each [row][head][capacity][head_dim] in the
+// model dtype, so the keys of one (row, head) are one contiguous stream.
+//
+//  * k_kv_append:     new tokens of a pass -> rotate k (RoPE), write k and v
+//                     at their absolute positions.
+//  * k_attn_prefill:  causal attention of a pass's tokens (a row's new
+//                     segment at positions pos..pos+n-1) over keys
+//                     0..pos+n-1 of that row: Q tile of 64 queries in LDS,
+//                     K/V tiles of 32 keys staged in LDS, online softmax.
+//  * k_attn_decode:   one query per row at position p = lens[b] + jpos (a
+//                     fed-back action token).  Appends its own K/V, then
+//                     each workgroup covers one split of the keys: lane-per-key
+//                     scores, wavefront-shuffle online softmax, and a P.V
+//                     pass with lanes over (key subgroup, 8-dim chunk).  The
+//                     split partials (m, l, acc) are merged by k_attn_merge
+//                     with log-sum-exp weights.
+#include "common.h"
+#include "kernels.h"
+
+namespace ams {
+
+__device__ __forceinline__ int find_seg(const int32_t* off, int n_seg, int i) {
+  int lo = 0, hi = n_seg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// 8 consecutive elements as floats
+__device__ __forceinline__ void load8(const float* p, float* v) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void load8(const f16* p, float* v) {
+  const half8 a = __builtin_bit_cast(half8, *(const uint4*)p);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)a[i];
+}
+
+// ----------------------------------------------------------------------------
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_kv_append(const float* __restrict__ qkv, const int32_t* __restrict__ row,
+                                                   const int32_t* __restrict__ pos, const int32_t* __restrict__ off,
+                                                   int n_seg, int H, int dh, int cap, const float2* __restrict__ rope,
+                                                   T* __restrict__ kslab, T* __restrict__ vslab) {
+  const int i = blockIdx.x;
+  const int s = find_seg(off, n_seg, i);
+  const int b = row[s], p = pos[s] + (i - off[s]);
+  const int d = H * dh, half = dh / 2;
+  const float* k = qkv + (size_t)i * 3 * d + d;
+  const float* v = k + d;
+  for (int e = threadIdx.x; e < H * half; e += blockDim.x) {
+    const int h = e / half, ii = e % half;
+    const float2 cs = rope[(size_t)p * half + ii];
+    const float a = k[h * dh + ii], c = k[h * dh + ii + half];
+    T* dst = kslab + (((size_t)b * H + h) * cap + p) * dh;
+    st<T>(dst, ii, a * cs.x - c * cs.y);
+    st<T>(dst, ii + half, a * cs.y + c * cs.x);
+  }
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    const int h = e / dh, dd = e % dh;
+    st<T>(vslab + (((size_t)b * H + h) * cap + p) * dh, dd, v[e]);
+  }
+}
+
+hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+                     void* kslab, void* vslab, hipStream_t s) {
+  if (sg.n_tok <= 0) return hipSuccess;
+  if (ct == DT_F32)
+    hipLaunchKernelGGL(k_kv_append<float>, dim3(sg.n_tok), dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off,
+                       sg.n_seg, H, dh, cap, rope, (float*)kslab, (float*)vslab);
+  else
+    hipLaunchKernelGGL(k_kv_append<f16>, dim3(sg.n_tok), dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off,
+                       sg.n_seg, H, dh, cap, rope, (f16*)kslab, (f16*)vslab);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ qkv, const int32_t* __restrict__ row,
+                                                      const int32_t* __restrict__ pos,
+                                                      const int32_t* __restrict__ off, int H, int cap,
+                                                      const float2* __restrict__ rope, const T* __restrict__ kslab,
+                                                      const T* __restrict__ vslab, T* __restrict__ o, float scale) {
+  constexpr int QT = 64, KT = 32, HALF = DH / 2, DPT = DH / 4;
+  __shared__ float Qs[QT][DH + 1];
+  __shared__ float Ks[KT][DH + 1];
+  __shared__ float Vs[KT][DH];
+  __shared__ float Ps[QT][KT + 1];
+  const int s = blockIdx.z, h = blockIdx.y, tid = threadIdx.x;
+  const int b = row[s], p0 = pos[s], t0 = off[s], n = off[s + 1] - off[s];
+  const int q_lo = blockIdx.x * QT;
+  if (q_lo >= n) return;  // uniform across the workgroup
+  const int d = H * DH;
+
+  for (int e = tid; e < QT * HALF; e += blockDim.x) {
+    const int qi = e / HALF, ii = e % HALF;
+    float x0 = 0.f, x1 = 0.f;
+    if (q_lo + qi < n) {
+      const int tok = t0 + q_lo + qi, p = p0 + q_lo + qi;
+      const float* q = qkv + (size_t)tok * 3 * d + h * DH;
+      const float2 cs = rope[(size_t)p * HALF + ii];
+      const float a = q[ii], c = q[ii + HALF];
+      x0 = (a * cs.x - c * cs.y) * scale;
+      x1 = (a * cs.y + c * cs.x) * scale;
+    }
+    Qs[qi][ii] = x0;
+    Qs[qi][ii + HALF] = x1;
+  }
+
+  const int qi = tid >> 2, sub = tid & 3;
+  const bool valid = q_lo + qi < n;
+  const int qpos = valid ? p0 + q_lo + qi : -1;
+  const int kv_end = p0 + (n < q_lo + QT ? n : q_lo + QT);  // exclusive
+  const T* Kb = kslab + ((size_t)b * H + h) * cap * DH;
+  const T* Vb = vslab + ((size_t)b * H + h) * cap * DH;
+  float m = -INFINITY, l = 0.f, acc[DPT];
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) acc[i] = 0.f;
+
+  for (int k0 = 0; k0 < kv_end; k0 += KT) {
+    __syncthreads();  // Qs ready on the first pass; Ks/Vs/Ps free on later ones
+    for (int e = tid; e < KT * DH; e += blockDim.x) {
+      const int kk = e / DH, dd = e % DH;
+      const bool ok = k0 + kk < kv_end;
+      Ks[kk][dd] = ok ? ld<T>(Kb, (size_t)(k0 + kk) * DH + dd) : 0.f;
+      Vs[kk][dd] = ok ? ld<T>(Vb, (size_t)(k0 + kk) * DH + dd) : 0.f;
+    }
+    __syncthreads();
+    float sc[KT / 4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int jj = 0; jj < KT / 4; ++jj) {
+      const int kk = sub + 4 * jj, kp = k0 + kk;
+      float t = -INFINITY;
+      if (kp <= qpos && kp < kv_end) {
+        t = 0.f;
+#pragma unroll 16
+        for (int dd = 0; dd < DH; ++dd) t = fmaf(Qs[qi][dd], Ks[kk][dd], t);
+      }
+      sc[jj] = t;
+      mx = fmaxf(mx, t);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+    const float m_new = fmaxf(m, mx);
+    const float alpha = (m_new == -INFINITY) ? 1.f : __expf(m - m_new);
+    float ps = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < KT / 4; ++jj) {
+      const float pv = (sc[jj] == -INFINITY) ? 0.f : __expf(sc[jj] - m_new);
+      Ps[qi][sub + 4 * jj] = pv;
+      ps += pv;
+    }
+    ps += __shfl_xor(ps, 1, 64);
+    ps += __shfl_xor(ps, 2, 64);
+    l = l * alpha + ps;
+    m = m_new;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) acc[i] *= alpha;
+    __syncthreads();
+    for (int kk = 0; kk < KT; ++kk) {
+      const float pk = Ps[qi][kk];
+#pragma unroll
+      for (int i = 0; i < DPT; ++i) acc[i] = fmaf(pk, Vs[kk][sub * DPT + i], acc[i]);
+    }
+  }
+  if (valid) {
+    const float inv = 1.0f / l;
+    T* dst = o + (size_t)(t0 + q_lo + qi) * d + h * DH + sub * DPT;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) st<T>(dst, i, acc[i] * inv);
+  }
+}
+
+template <typename T>
+static hipError_t prefill_t(const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope, const void* k,
+                            const void* v, void* o, hipStream_t s) {
+  const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
+  const float scale = 1.0f / sqrtf((float)dh);
+  if (dh == 64)
+    hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+                       (const T*)k, (const T*)v, (T*)o, scale);
+  else
+    hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+                       (const T*)k, (const T*)v, (T*)o, scale);
+  return hipGetLastError();
+}
+
+hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+                        const void* kslab, const void* vslab, void* o, hipStream_t s) {
+  if (sg.n_tok <= 0) return hipSuccess;
+  if (ct == DT_F32) return prefill_t<float>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
+  return prefill_t<f16>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
+}
+
+// ----------------------------------------------------------------------------
+
+template <typename T> struct Raw;  // 16-byte chunks of T -> floats
+template <> struct Raw<f16> {
+  static constexpr int E = 8;
+  static __device__ __forceinline__ void cvt(const uint4& r, float* v) {
+    const half8 a = __builtin_bit_cast(half8, r);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (float)a[i];
+  }
+};
+template <> struct Raw<float> {
+  static constexpr int E = 4;
+  static __device__ __forceinline__ void cvt(const uint4& r, float* v) {
+    v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y); v[2] = __uint_as_float(r.z); v[3] = __uint_as_float(r.w);
+  }
+};
+
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ qkv, const int32_t* __restrict__ lens,
+                                                     int jpos, int H, int cap, int splits,
+                                                     const float2* __restrict__ rope, T* __restrict__ kslab,
+                                                     T* __restrict__ vslab, float* __restrict__ part,
+                                                     T* __restrict__ o, float scale) {
+  constexpr int HALF = DH / 2, NC = DH / 8, KS = 64 / NC;  // dim chunks of 8; key subgroups per wave
+  constexpr int E = Raw<T>::E, KR = DH / E, VI = 64 / KS, VR = 8 / E;
+  __shared__ float qs[DH], kn[DH], vn[DH];
+  __shared__ float wm[4], wl[4], wacc[4][DH];
+  const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = H * DH;
+  const int p = lens[b] + jpos;  // position of this pass's token
+  const int T_ = p + 1;          // keys 0..p
+  const int chunk = (cap + splits - 1) / splits;
+  const int k0 = sp * chunk;
+  const int k1 = (k0 + chunk < T_) ? k0 + chunk : T_;
+  const float* qrow = qkv + (size_t)b * 3 * d + h * DH;
+
+  const size_t bh = ((size_t)b * H + h) * cap;
+  const T* Kb = kslab + bh * DH;
+  const T* Vb = vslab + bh * DH;
+  const int ks = lane / NC, dc = lane % NC;
+  uint4 kraw[KR];
+  uint4 vraw[VI][VR];
+  // one block's K row (lane = key) and V chunks (lane = key subgroup x dim chunk)
+  auto load_block = [&](int kb) {
+    const int key = kb + lane;
+    if (key < k1 && key != p) {
+      const uint4* kr = (const uint4*)(Kb + (size_t)key * DH);
+#pragma unroll
+      for (int i = 0; i < KR; ++i) kraw[i] = kr[i];
+    }
+#pragma unroll
+    for (int it = 0; it < VI; ++it) {
+      const int kk = kb + it * KS + ks;
+      if (kk < k1 && kk != p) {
+        const uint4* vr = (const uint4*)(Vb + (size_t)kk * DH + dc * 8);
+#pragma unroll
+        for (int r = 0; r < VR; ++r) vraw[it][r] = vr[r];
+      }
+    }
+  };
+  // the first block's loads go out before the prologue, overlapping it
+  const int kb0 = k0 + wave * 64;
+  if (kb0 < k1) load_block(kb0);
+
+  if (tid < HALF) {
+    const float2 cs = rope[(size_t)p * HALF + tid];
+    float a = qrow[tid], c = qrow[tid + HALF];
+    qs[tid] = (a * cs.x - c * cs.y) * scale;
+    qs[tid + HALF] = (a * cs.y + c * cs.x) * scale;
+    a = qrow[d + tid];
+    c = qrow[d + tid + HALF];
+    // the stored (rounded) key is the one every later step reads; use it here too
+    T r0, r1;
+    st<T>(&r0, 0, a * cs.x - c * cs.y);
+    st<T>(&r1, 0, a * cs.y + c * cs.x);
+    kn[tid] = ld<T>(&r0, 0);
+    kn[tid + HALF] = ld<T>(&r1, 0);
+  }
+  if (tid < DH) {
+    T r;
+    st<T>(&r, 0, qrow[2 * d + tid]);
+    vn[tid] = ld<T>(&r, 0);
+  }
+  __syncthreads();
+  if (k0 <= p && p < k1 && tid < DH) {
+    st<T>(kslab + (bh + p) * DH, tid, kn[tid]);
+    st<T>(vslab + (bh + p) * DH, tid, vn[tid]);
+  }
+
+  float m = -INFINITY, l = 0.f, acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+
+  for (int kb = kb0; kb < k1; kb += 256) {
+    if (kb != kb0) load_block(kb);
+    const int key = kb + lane;
+    float sc = -INFINITY;
+    if (key < k1) {
+      sc = 0.f;
+      if (key == p) {
+#pragma unroll 8
+        for (int dd = 0; dd < DH; ++dd) sc = fmaf(qs[dd], kn[dd], sc);
+      } else {
+#pragma unroll
+        for (int i = 0; i < KR; ++i) {
+          float kv[E];
+          Raw<T>::cvt(kraw[i], kv);
+#pragma unroll
+          for (int e = 0; e < E; ++e) sc = fmaf(qs[i * E + e], kv[e], sc);
+        }
+      }
+    }
+    const float m_new = fmaxf(m, wave_max(sc));
+    const float alpha = __expf(m - m_new);  // m = -inf on the first block gives 0
+    const float pl = (key < k1) ? __expf(sc - m_new) : 0.f;
+    l = l * alpha + wave_sum(pl);
+    m = m_new;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] *= alpha;
+#pragma unroll
+    for (int it = 0; it < VI; ++it) {
+      const int kl = it * KS + ks;
+      const float pk = __shfl(pl, kl, 64);
+      const int kk = kb + kl;
+      if (kk < k1) {
+        float vv[8];
+        if (kk == p) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vv[e] = vn[dc * 8 + e];
+        } else {
+#pragma unroll
+          for (int r = 0; r < VR; ++r) Raw<T>::cvt(vraw[it][r], vv + r * E);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(pk, vv[e], acc[e]);
+      }
+    }
+  }
+  // sum the key subgroups: lanes that share a dim chunk differ in the high bits
+#pragma unroll
+  for (int off_ = NC; off_ < 64; off_ <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], off_, 64);
+  if (lane == 0) {
+    wm[wave] = m;
+    wl[wave] = l;
+  }
+  if (lane < NC)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) wacc[wave][lane * 8 + e] = acc[e];
+  __syncthreads();
+  if (tid < DH) {
+    const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    float L = 0.f, Acc = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float f = __expf(wm[w] - M);
+        L += wl[w] * f;
+        Acc += wacc[w][tid] * f;
+      }
+    }
+    if (splits == 1) {
+      st<T>(o, (size_t)b * d + h * DH + tid, Acc / L);
+    } else {
+      float* out = part + (((size_t)b * H + h) * splits + sp) * (DH + 2);
+      out[2 + tid] = Acc;
+      if (tid == 0) {
+        out[0] = M;
+        out[1] = L;
+      }
+    }
+  }
+}
+
+template <typename T, int DH>
+__global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, T* __restrict__ o) {
+  const int h = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+  const float* pp = part + ((size_t)b * H + h) * splits * (DH + 2);
+  float M = -INFINITY;
+  for (int s = 0; s < splits; ++s) M = fmaxf(M, pp[s * (DH + 2)]);
+  float L = 0.f, A = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    const float ms = pp[s * (DH + 2)];
+    if (ms == -INFINITY) continue;
+    const float f = __expf(ms - M);
+    L += pp[s * (DH + 2) + 1] * f;
+    A += pp[s * (DH + 2) + 2 + t] * f;
+  }
+  st<T>(o, (size_t)b * H * DH + h * DH + t, A / L);
+}
+
+template <typename T>
+static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, int splits,
+                           const float2* rope, void* k, void* v, float* part, void* o, hipStream_t s) {
+  const float scale = 1.0f / sqrtf((float)dh);
+  const dim3 grid(splits, H, B);
+  if (dh == 64)
+    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(256), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
+                       (T*)v, part, (T*)o, scale);
+  else
+    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(256), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
+                       (T*)v, part, (T*)o, scale);
+  return hipGetLastError();
+}
+
+hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
+                       int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s) {
+  if (ct == DT_F32) return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, s);
+  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, s);
+}
+
+hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s) {
+  const dim3 grid(H, B);
+  if (ct == DT_F32) {
+    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<float, 64>), grid, dim3(64), 0, s, part, H, splits, (float*)o);
+    else hipLaunchKernelGGL((k_attn_merge<float, 128>), grid, dim3(128), 0, s, part, H, splits, (float*)o);
+  } else {
+    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<f16, 64>), grid, dim3(64), 0, s, part, H, splits, (f16*)o);
+    else hipLaunchKernelGGL((k_attn_merge<f16, 128>), grid, dim3(128), 0, s, part, H, splits, (f16*)o);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ams

@@ -1,0 +1,105 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher only enqueues
+// on the given stream and returns the launch status; argument validation
+// happens in the C ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ams {
+
+// Storage types at the boundary: DT_F32, DT_BF16.  Compute types inside the
+// kernels (GEMM inputs, activations, K/V slab, packed weights): DT_F32 for
+// fp32 models, DT_F16 for bf16 models.
+enum DType { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// Packed-token pass metadata (device arrays).  Segment s covers tokens
+// off[s]..off[s+1]-1 of the pass, which belong to row `row[s]` at positions
+// pos[s], pos[s]+1, ...
+struct Segs {
+  const int32_t* row;
+  const int32_t* pos;
+  const int32_t* off;  // n_seg + 1 entries
+  int n_seg;
+  int n_tok;
+  int max_len;  // longest segment
+  int max_end;  // largest pos[s] + len(s)
+};
+
+// Gate/up rows are packed interleaved in blocks of 16: packed row 32i+j is
+// gate row 16i+j for j < 16 and up row 16i+j-16 otherwise.
+constexpr int GU_BLOCK = 16;
+
+// y[m][n] = sum_k u[m][k] * W[n][k] followed by the epilogue:
+//   EPI_STORE : out_f32[m*ldo + n] = y
+//   EPI_RESID : out_f32[m*ldo + n] += y          (residual stream)
+//   EPI_SWIGLU: out_T[m*ldo + c] = silu(gate_c) * up_c with W packed as above
+hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out,
+                int ldo, hipStream_t s);
+
+// Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16):
+// y[m] = (W fp16(h[m])) / sqrt(mean(h[m]^2) + eps), followed by the epilogue as
+// in gemm().  W carries the RMSNorm gain (folded at packing); fp16(h) saturates
+// at +-65504.
+hipError_t gemv_rmsnorm(int ct, int epi, const float* h, float eps, const void* W, int M, int N, int K, void* out,
+                        int ldo, hipStream_t s);
+
+// Per row b: argmax over logits[b][0..n_bins) (lowest index on ties) -> out_tok[b*A+j],
+// logits copied to out_logits[b][j] (if non-NULL); when feed, h[b] = bin_embed[t]
+// with t the argmax or the clamped forced[b*A+j].
+hipError_t argmax_feed(int ct, const float* logits, int ld_logits, const void* bin_embed, int B, int d, int n_bins,
+                       int A, int j, int32_t* out_tok, float* out_logits, const int32_t* forced, float* h, int feed,
+                       hipStream_t s);
+
+// u[m] = h[m] / sqrt(mean(h[m]^2) + eps), written in the compute type (the
+// gain is folded into the weights that consume u).
+hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s);
+
+// out[i] = E[clamp(ids[i])] in the storage type.
+hipError_t embed_rows(int st, const void* E, const int32_t* ids, int n, int d, int vocab, void* out,
+                      hipStream_t s);
+
+// h[i] = float(x[i]) for n rows of d (x in the storage type).
+hipError_t ingest(int st, const void* x, int n, int d, float* h, hipStream_t s);
+
+// Gate/up interleave of one layer: dst [2F][d] (compute type) from gate [F][d]
+// and up [F][d] (storage type), each column k scaled by gain[k] (the RMSNorm
+// gain folded into the weights).
+hipError_t pack_gate_up(int st, int ct, const void* gate, const void* up, const float* gain, int F, int d, void* dst,
+                        hipStream_t s);
+
+// dst[n][k] = ct(src[n][k] * gain[k]) for a [rows][cols] matrix (gain == NULL:
+// plain conversion; storage -> compute type; fp16 saturates).
+hipError_t convert(int st, int ct, const void* src, size_t rows, int cols, const float* gain, void* dst,
+                   hipStream_t s);
+
+// tab[t][i] = (cos, sin)(t * theta^(-2i/dh)) for t < cap, i < dh/2 (computed in fp64).
+hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s);
+
+// Rotates the new tokens' keys and writes K/V into the slab of one layer.
+hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+                     void* kslab, void* vslab, hipStream_t s);
+
+// Causal attention of the pass's tokens over each row's slab (cache + new).
+hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int cap,
+                        const float2* rope, const void* kslab, const void* vslab, void* o,
+                        hipStream_t s);
+
+// One query per row at position lens[b] + jpos: appends its K/V, attends over
+// positions 0..lens[b]+jpos.  splits == 1: the output goes straight to o;
+// otherwise the keys are cut into `splits` chunks whose partials (m, l, acc)
+// go to `part` for attn_merge.
+hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh,
+                       int cap, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
+                       hipStream_t s);
+hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
+                      hipStream_t s);
+
+// h_last[row[s]] = h[off[s+1]-1] for each segment.
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s);
+
+// lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
+hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
+
+}  // namespace ams

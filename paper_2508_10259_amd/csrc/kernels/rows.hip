@@ -1,0 +1,183 @@
+// Row-wise kernels: RMSNorm, embedding gathers, prefix ingest, weight
+// packing, the RoPE table, last-token gathers and length bookkeeping.
+#include "common.h"
+#include "kernels.h"
+
+namespace ams {
+
+// One workgroup per token row (256 threads up to d = 4096, else 1024);
+// statistics in fp32.  Each thread loads its EPT (<= 16) elements before
+// reducing, so a row costs one memory round trip.
+template <typename T, int EPT>
+__global__ __launch_bounds__(1024) void k_rmsnorm(const float* __restrict__ h, int d, float eps, T* __restrict__ u) {
+  __shared__ float red[16];
+  const size_t base = (size_t)blockIdx.x * d;
+  const int nt = blockDim.x;
+  float x[EPT];
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = threadIdx.x + e * nt;
+    x[e] = i < d ? h[base + i] : 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) ss = fmaf(x[e], x[e], ss);
+  const float tot = block_sum(ss, red);
+  const float rs = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = threadIdx.x + e * nt;
+    if (i < d) st<T>(u, base + i, x[e] * rs);
+  }
+}
+
+template <typename T>
+static hipError_t rmsnorm_t(const float* h, int M, int d, float eps, T* u, hipStream_t s) {
+  const int nt = d <= 4096 ? 256 : 1024;
+  const int ept = (d + nt - 1) / nt;  // <= 16 for d <= 16384
+#define AMS_RMS(E) hipLaunchKernelGGL((k_rmsnorm<T, E>), dim3(M), dim3(nt), 0, s, h, d, eps, u)
+  if (ept <= 1) AMS_RMS(1);
+  else if (ept <= 2) AMS_RMS(2);
+  else if (ept <= 4) AMS_RMS(4);
+  else if (ept <= 8) AMS_RMS(8);
+  else AMS_RMS(16);
+#undef AMS_RMS
+  return hipGetLastError();
+}
+
+hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (ct == DT_F32) return rmsnorm_t<float>(h, M, d, eps, (float*)u, s);
+  return rmsnorm_t<f16>(h, M, d, eps, (f16*)u, s);
+}
+
+// Copies rows as raw elements (8/16-byte chunks); `ids` selects source rows.
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed(const T* __restrict__ E, const int32_t* __restrict__ ids, int d,
+                                               int vocab, T* __restrict__ out) {
+  int id = ids[blockIdx.x];
+  id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
+  const T* src = E + (size_t)id * d;
+  T* dst = out + (size_t)blockIdx.x * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = src[i];
+}
+
+hipError_t embed_rows(int st, const void* E, const int32_t* ids, int n, int d, int vocab, void* out,
+                      hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (st == DT_F32)
+    hipLaunchKernelGGL(k_embed<float>, dim3(n), dim3(256), 0, s, (const float*)E, ids, d, vocab, (float*)out);
+  else
+    hipLaunchKernelGGL(k_embed<bf16>, dim3(n), dim3(256), 0, s, (const bf16*)E, ids, d, vocab, (bf16*)out);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_ingest(const T* __restrict__ x, size_t n, float* __restrict__ h) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    h[i] = ld<T>(x, i);
+}
+
+hipError_t ingest(int st, const void* x, int n, int d, float* h, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const size_t tot = (size_t)n * d;
+  const int blocks = (int)((tot + 255) / 256 < 65536 ? (tot + 255) / 256 : 65536);
+  if (st == DT_F32)
+    hipLaunchKernelGGL(k_ingest<float>, dim3(blocks), dim3(256), 0, s, (const float*)x, tot, h);
+  else
+    hipLaunchKernelGGL(k_ingest<bf16>, dim3(blocks), dim3(256), 0, s, (const bf16*)x, tot, h);
+  return hipGetLastError();
+}
+
+template <typename TS, typename TC>
+__global__ __launch_bounds__(256) void k_pack_gu(const TS* __restrict__ gate, const TS* __restrict__ up,
+                                                 const float* __restrict__ gain, int d, TC* __restrict__ dst) {
+  const int r = blockIdx.x;  // packed row
+  const int blk = r / (2 * GU_BLOCK), j = r % (2 * GU_BLOCK);
+  const TS* src = j < GU_BLOCK ? gate + (size_t)(blk * GU_BLOCK + j) * d
+                               : up + (size_t)(blk * GU_BLOCK + j - GU_BLOCK) * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) st<TC>(dst, (size_t)r * d + i, ld<TS>(src, i) * gain[i]);
+}
+
+hipError_t pack_gate_up(int st_, int ct, const void* gate, const void* up, const float* gain, int F, int d, void* dst,
+                        hipStream_t s) {
+  if (st_ == DT_F32 && ct == DT_F32)
+    hipLaunchKernelGGL((k_pack_gu<float, float>), dim3(2 * F), dim3(256), 0, s, (const float*)gate,
+                       (const float*)up, gain, d, (float*)dst);
+  else if (st_ == DT_BF16 && ct == DT_F16)
+    hipLaunchKernelGGL((k_pack_gu<bf16, f16>), dim3(2 * F), dim3(256), 0, s, (const bf16*)gate, (const bf16*)up,
+                       gain, d, (f16*)dst);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <typename TS, typename TC>
+__global__ __launch_bounds__(256) void k_convert(const TS* __restrict__ src, size_t rows, int cols,
+                                                 const float* __restrict__ gain, TC* __restrict__ dst) {
+  const size_t n = rows * (size_t)cols;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    st<TC>(dst, i, gain ? ld<TS>(src, i) * gain[i % cols] : ld<TS>(src, i));
+}
+
+hipError_t convert(int st_, int ct, const void* src, size_t rows, int cols, const float* gain, void* dst,
+                   hipStream_t s) {
+  const size_t n = rows * (size_t)cols;
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+  if (st_ == DT_F32 && ct == DT_F32)
+    hipLaunchKernelGGL((k_convert<float, float>), dim3(blocks), dim3(256), 0, s, (const float*)src, rows, cols, gain,
+                       (float*)dst);
+  else if (st_ == DT_BF16 && ct == DT_F16)
+    hipLaunchKernelGGL((k_convert<bf16, f16>), dim3(blocks), dim3(256), 0, s, (const bf16*)src, rows, cols, gain,
+                       (f16*)dst);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+__global__ void k_rope_table(float2* tab, int cap, int half, double log2_theta_over_dh2) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= cap * half) return;
+  const int t = idx / half, i = idx % half;
+  // theta^(-2i/dh) = 2^(-i * log2(theta) * 2/dh)
+  const double ang = (double)t * exp2(-(double)i * log2_theta_over_dh2);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  tab[idx] = make_float2((float)cs, (float)sn);
+}
+
+hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s) {
+  const int half = dh / 2;
+  const double l = 2.0 * log2((double)theta) / (double)dh;
+  hipLaunchKernelGGL(k_rope_table, dim3((cap * half + 255) / 256), dim3(256), 0, s, tab, cap, half, l);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_gather_last(const float* __restrict__ h, const int32_t* __restrict__ row,
+                                                     const int32_t* __restrict__ off, int d,
+                                                     float* __restrict__ h_last) {
+  const int sidx = blockIdx.x;
+  const int last = off[sidx + 1] - 1;
+  const float* src = h + (size_t)last * d;
+  float* dst = h_last + (size_t)row[sidx] * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = src[i];
+}
+
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s) {
+  if (sg.n_seg <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_last, dim3(sg.n_seg), dim3(256), 0, s, h, sg.row, sg.off, d, h_last);
+  return hipGetLastError();
+}
+
+__global__ void k_update_lens(int32_t* lens, const int32_t* add, int B, int set) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) lens[b] = set ? add[b] : lens[b] + add[b];
+}
+
+hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s) {
+  hipLaunchKernelGGL(k_update_lens, dim3((B + 255) / 256), dim3(256), 0, s, lens, add, B, set);
+  return hipGetLastError();
+}
+
+}  // namespace ams

@@ -1,0 +1,171 @@
+"""Torch-facing wrapper over the C ABI.
+
+PyTorch only provides device memory and the stream; every step of the
+decoder runs in ``libams.so``.  ``DeviceModel`` uploads encoded weights and
+creates the model handle; ``DeviceContext`` owns a context workspace and
+exposes build / step / invalidate.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import capi
+from .workload import MATRICES, ModelSpec, Prefix, Weights
+
+
+def torch_dtype(dtype: str) -> torch.dtype:
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+def to_device(values: np.ndarray, dtype: str, device="cuda") -> torch.Tensor:
+    """Encoded numpy array (fp32, or bf16 bit patterns) -> device tensor."""
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(values).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(values, dtype=np.float32))
+    return t.to(device)
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def model_cfg(spec: ModelSpec) -> capi.ModelCfg:
+    return capi.ModelCfg(spec.n_layers, spec.d_model, spec.n_heads, spec.head_dim, spec.d_ffn, spec.vocab,
+                         spec.n_bins, spec.rms_eps, spec.rope_theta,
+                         capi.AMS_F32 if spec.dtype == "f32" else capi.AMS_BF16)
+
+
+class DeviceModel:
+    """Weights on the device plus the library's packed copy."""
+
+    def __init__(self, w: Weights, device="cuda", keep_source: bool = False):
+        self.lib = capi.load()
+        self.spec = spec = w.spec
+        self.device = torch.device(device)
+        td = torch_dtype(spec.dtype)
+        src = {}
+        for name in MATRICES:
+            stack = getattr(w, name)
+            t = torch.empty((spec.n_layers,) + tuple(stack[0].shape), dtype=td, device=device)
+            for l in range(spec.n_layers):
+                t[l].copy_(to_device(stack[l], spec.dtype, device))
+            src[name] = t
+        src["g_attn"] = torch.from_numpy(w.g_attn).to(device)
+        src["g_ffn"] = torch.from_numpy(w.g_ffn).to(device)
+        src["g_final"] = torch.from_numpy(w.g_final).to(device)
+        self.embed = to_device(w.embed, spec.dtype, device)
+        src["embed"] = self.embed
+        src["head_bins"] = to_device(w.head_bins, spec.dtype, device)
+        self.cfg = model_cfg(spec)
+        wts = capi.Weights(**{k: v.data_ptr() for k, v in src.items()})
+        nbytes = self.lib.ams_model_workspace_bytes(C.byref(self.cfg))
+        if nbytes == 0:
+            raise ValueError("invalid model configuration")
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        h = C.c_void_p()
+        capi.check(self.lib.ams_model_create(C.byref(self.cfg), C.byref(wts), self.ws.data_ptr(), nbytes,
+                                             _stream(), C.byref(h)), "ams_model_create")
+        torch.cuda.current_stream().synchronize()
+        self.handle = h
+        # the packed copy is all the library reads afterwards, except `embed`
+        self.source = src if keep_source else {"embed": self.embed}
+
+    def embed_ids(self, ids: torch.Tensor, out: torch.Tensor) -> None:
+        assert ids.dtype == torch.int32 and ids.is_contiguous() and out.is_contiguous()
+        capi.check(self.lib.ams_embed_ids(self.handle, ids.data_ptr(), ids.numel(), out.data_ptr(), _stream()),
+                   "ams_embed_ids")
+
+    def pack_prefixes(self, prefixes: Sequence[Prefix]) -> Tuple[torch.Tensor, List[int]]:
+        """Packed prefix rows: each row's patch embeddings, then its instruction
+        ids embedded on the device by the library."""
+        spec = self.spec
+        lens = [p.length for p in prefixes]
+        out = torch.empty((sum(lens), spec.d_model), dtype=torch_dtype(spec.dtype), device=self.device)
+        o = 0
+        for p in prefixes:
+            n_p = p.patches.shape[0]
+            if n_p:
+                out[o:o + n_p].copy_(to_device(p.patches, spec.dtype, self.device))
+            if len(p.text_ids):
+                ids = torch.from_numpy(p.text_ids.astype(np.int32)).to(self.device)
+                self.embed_ids(ids, out[o + n_p:o + p.length])
+            o += p.length
+        return out, lens
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.ams_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class DeviceContext:
+    """Per-row cached context: K/V slab + activations in one workspace."""
+
+    def __init__(self, model: DeviceModel, batch: int, capacity: int, max_pass_tokens: int = 0):
+        self.lib, self.model, self.batch, self.capacity = model.lib, model, batch, capacity
+        nbytes = self.lib.ams_ctx_workspace_bytes(C.byref(model.cfg), batch, capacity, max_pass_tokens)
+        if nbytes == 0:
+            raise ValueError("invalid context arguments")
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=model.device)
+        h = C.c_void_p()
+        capi.check(self.lib.ams_ctx_create(model.handle, batch, capacity, max_pass_tokens, self.ws.data_ptr(),
+                                           nbytes, C.byref(h)), "ams_ctx_create")
+        self.handle = h
+        self._keep = []
+
+    def build(self, prefix: torch.Tensor, lens: Sequence[int]) -> None:
+        assert prefix.is_contiguous()
+        capi.check(self.lib.ams_ctx_build(self.handle, prefix.data_ptr(), capi.int_array(lens), _stream()),
+                   "ams_ctx_build")
+
+    def step(self, n_actions: int, new: Optional[torch.Tensor] = None, new_lens: Optional[Sequence[int]] = None,
+             tokens: Optional[torch.Tensor] = None, logits: Optional[torch.Tensor] = None, want_logits: bool = True,
+             forced: Optional[torch.Tensor] = None):
+        """Returns (tokens [B, A] int32, logits [B, A, n_bins] fp32 or None) on the device."""
+        B, nb = self.batch, self.model.spec.n_bins
+        dev = self.model.device
+        if tokens is None:
+            tokens = torch.empty((B, n_actions), dtype=torch.int32, device=dev)
+        if logits is None and want_logits:
+            logits = torch.empty((B, n_actions, nb), dtype=torch.float32, device=dev)
+        nl = capi.int_array(new_lens) if new_lens is not None else None
+        capi.check(self.lib.ams_ctx_step(self.handle, new.data_ptr() if new is not None else None, nl, n_actions,
+                                         tokens.data_ptr(), logits.data_ptr() if logits is not None else None,
+                                         forced.data_ptr() if forced is not None else None, _stream()),
+                   "ams_ctx_step")
+        return tokens, logits
+
+    def invalidate(self) -> None:
+        capi.check(self.lib.ams_ctx_invalidate(self.handle), "ams_ctx_invalidate")
+
+    def lengths(self) -> List[int]:
+        arr = (C.c_int32 * self.batch)()
+        capi.check(self.lib.ams_ctx_lengths(self.handle, arr), "ams_ctx_lengths")
+        return list(arr)
+
+    @property
+    def state(self) -> int:
+        return self.lib.ams_ctx_state(self.handle)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.ams_ctx_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

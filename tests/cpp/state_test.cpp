@@ -1,0 +1,130 @@
+// Host-only checks of the context bookkeeping (csrc/host/state.h), built with
+// g++ and sanitizers by tests/test_abi_cpu.py.
+#include <stdio.h>
+#include <stdlib.h>
+
+#include "state.h"
+
+using namespace ams;
+
+static int failures = 0;
+#define EXPECT(c)                                                  \
+  do {                                                             \
+    if (!(c)) {                                                    \
+      fprintf(stderr, "%s:%d: EXPECT(%s) failed\n", __FILE__, __LINE__, #c); \
+      ++failures;                                                  \
+    }                                                              \
+  } while (0)
+
+static void test_book() {
+  RowBook b;
+  b.init(3, 128);
+  std::string e;
+  int32_t nl[3] = {0, 0, 0};
+  EXPECT(b.check_step(nl, 7, e) == S_ESTATE);  // never built
+  int32_t bad[3] = {10, 0, 5};
+  EXPECT(b.check_build(bad, e) == S_EINVAL);
+  int32_t big[3] = {10, 129, 5};
+  EXPECT(b.check_build(big, e) == S_ECAPACITY);
+  int32_t lens[3] = {100, 1, 128};
+  EXPECT(b.check_build(lens, e) == S_OK);
+  b.commit_build(lens);
+  EXPECT(b.state == READY);
+  EXPECT(b.check_step(nullptr, 1, e) == S_OK);       // 128 + 0 + 1 - 1 = 128 fits
+  EXPECT(b.check_step(nullptr, 2, e) == S_ECAPACITY);
+  int32_t l2[3] = {90, 1, 100};
+  b.commit_build(l2);
+  int32_t n1[3] = {28, 0, 0};
+  EXPECT(b.check_step(n1, 11, e) == S_OK);          // 90 + 28 + 11 - 1 = 128: exact fit
+  EXPECT(b.check_step(n1, 12, e) == S_ECAPACITY);
+  int32_t neg[3] = {0, -1, 0};
+  EXPECT(b.check_step(neg, 1, e) == S_EINVAL);
+  EXPECT(b.check_step(nullptr, 0, e) == S_EINVAL);
+  b.commit_new(n1);
+  EXPECT(b.len[0] == 118 && b.len[1] == 1 && b.len[2] == 100);
+  b.invalidate();
+  EXPECT(b.state == INVALID && b.len[0] == 0 && b.len[2] == 0);
+  EXPECT(b.check_step(nullptr, 1, e) == S_ESTATE);
+  b.commit_build(l2);
+  EXPECT(b.state == READY && b.len[2] == 100);
+}
+
+static void test_plan() {
+  // rows 0..5 with ragged counts, one empty; pass budget 100
+  int32_t counts[6] = {40, 0, 70, 30, 100, 1};
+  int32_t start[6] = {0, 0, 5, 7, 0, 9};
+  Plan p = plan_passes(6, counts, start, 100);
+  // passes: [r0] (40, next 70 overflows) [r2, r3] (100) [r4] (100) [r5] (1)
+  EXPECT(p.passes.size() == 4);
+  EXPECT(p.row.size() == 5);
+  int tok = 0, seg = 0;
+  for (size_t i = 0; i < p.passes.size(); ++i) {
+    const Pass& ps = p.passes[i];
+    EXPECT(ps.seg_begin == seg);
+    EXPECT(ps.tok_src == tok);
+    const int32_t* off = p.off.data() + ps.seg_begin + i;
+    EXPECT(off[0] == 0);
+    int sum = 0, mx = 0, me = 0;
+    for (int s = 0; s < ps.n_seg; ++s) {
+      const int r = p.row[ps.seg_begin + s];
+      EXPECT(off[s + 1] - off[s] == counts[r]);
+      EXPECT(p.pos[ps.seg_begin + s] == start[r]);
+      sum += counts[r];
+      mx = std::max(mx, counts[r]);
+      me = std::max(me, start[r] + counts[r]);
+    }
+    EXPECT(sum == ps.n_tok && ps.n_tok <= 100);
+    EXPECT(mx == ps.max_len && me == ps.max_end);
+    tok += ps.n_tok;
+    seg += ps.n_seg;
+  }
+  EXPECT(tok == 241);
+  EXPECT(p.off.size() == p.row.size() + p.passes.size());
+  int32_t none[3] = {0, 0, 0};
+  EXPECT(plan_passes(3, none, none, 64).passes.empty());
+}
+
+static void test_layout() {
+  Cfg c{12, 1024, 16, 64, 4096, 256, 256, 1e-5f, 10000.f, 1};
+  std::string e;
+  EXPECT(check_cfg(c, e) == S_OK);
+  const ModelLayout m = model_layout(c);
+  EXPECT(m.per_layer_qkv == 3ull * 1024 * 1024 * 2);
+  EXPECT(m.total >= 12ull * (4 * 1024 * 1024 + 3 * 1024 * 4096) * 2);
+  const CtxLayout x = ctx_layout(c, 8, 320, 0);
+  EXPECT(x.slab_layer == 8ull * 320 * 1024 * 2);
+  EXPECT(x.kv == 0 && x.h >= 2ull * 12 * x.slab_layer);
+  EXPECT(x.pass_tokens == 2560 && x.total % 256 == 0);
+  size_t offs[] = {x.kv, x.h, x.u, x.qkv, x.o, x.a, x.h_last, x.part, x.logits, x.rope, x.lens, x.meta, x.total};
+  for (size_t i = 0; i + 1 < sizeof(offs) / sizeof(offs[0]); ++i) EXPECT(offs[i] < offs[i + 1] && offs[i] % 256 == 0);
+  Cfg bad = c;
+  bad.head_dim = 96; bad.n_heads = 1024 / 96;
+  EXPECT(check_cfg(bad, e) == S_EINVAL);
+  bad = c; bad.d_ffn = 4000;
+  EXPECT(check_cfg(bad, e) == S_EINVAL);
+  bad = c; bad.n_bins = 300;
+  EXPECT(check_cfg(bad, e) == S_EINVAL);
+  bad = c; bad.rms_eps = 0.f;
+  EXPECT(check_cfg(bad, e) == S_EINVAL);
+  EXPECT(check_ctx_args(c, 0, 320, 0, e) == S_EINVAL);
+  EXPECT(check_ctx_args(c, 8, 100, 0, e) == S_EINVAL);
+  EXPECT(check_ctx_args(c, 8, 320, 100, e) == S_EINVAL);
+  EXPECT(check_ctx_args(c, 8, 320, 320, e) == S_OK);
+  EXPECT(decode_splits(1, 32, 320) == 1);   // short context: one split
+  EXPECT(decode_splits(1, 32, 1024) == 4);  // 32 pairs, long context: 4 splits of 256
+  EXPECT(decode_splits(8, 16, 320) == 1);
+  EXPECT(decode_splits(64, 32, 768) == 1);
+  EXPECT(bins_padded(c) == 256);
+}
+
+int main() {
+  test_book();
+  test_plan();
+  test_layout();
+  if (failures) {
+    fprintf(stderr, "%d failures\n", failures);
+    return 1;
+  }
+  printf("state_test: ok\n");
+  return 0;
+}

@@ -1,0 +1,173 @@
+"""GPU path (through the C ABI) against the fp64 reference on the same seeded inputs.
+
+Tolerances: logits max-abs 1e-4 on the fp32 path and 3e-2 on the bf16 path;
+argmax agreement counted strictly (fp32) or within the logit tolerance of the
+reference maximum (bf16, where several bins can be correct when the top
+reference logits sit closer than the tolerance).  bf16 runs are
+teacher-forced with the reference's choices so one near-tie cannot cascade.
+"""
+import numpy as np
+import pytest
+
+from paper_2508_10259_amd import workload as W
+import oracle.decoder as D
+from gpu_util import Pair, compare, gpu_new_tokens, log, small_spec
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32, TOL_BF16 = 1e-4, 3e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(pair, wl_prefixes, news_per_step, n_actions, capacity, forced_from_ref, max_pass_tokens=0, seed_tag=""):
+    """Builds and steps both sides; returns per-step (ref logits, gpu logits, gpu tokens)."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec = pair.spec
+    B = len(wl_prefixes)
+    ref = D.ActionContext(pair.p, B)
+    ref.build(pair.prefixes_f64(wl_prefixes))
+    ctx = DeviceContext(pair.dev, B, capacity, max_pass_tokens)
+    prefix, lens = pair.dev.pack_prefixes(wl_prefixes)
+    ctx.build(prefix, lens)
+    out = []
+    for s, news in enumerate(news_per_step):
+        log(f"{seed_tag} step {s}")
+        rn = None if news is None else [None if x is None else pair.obs_f64(x) for x in news]
+        t_ref, z_ref = ref.step(rn, n_actions)
+        forced = torch.from_numpy(t_ref.astype(np.int32)).cuda() if forced_from_ref else None
+        new_t, new_lens = gpu_new_tokens(spec, news) if news is not None else (None, None)
+        t_gpu, z_gpu = ctx.step(n_actions, new_t, new_lens, forced=forced)
+        torch.cuda.synchronize()
+        out.append((z_ref, z_gpu.cpu().numpy(), t_gpu.cpu().numpy(), t_ref))
+        assert ctx.lengths() == list(ref.lengths())
+    ctx.close()
+    return out
+
+
+def test_tiny_fp32_free_running():
+    """2-layer d=256 fp32 decoder, 64-token prefix, 7 actions: tokens equal, logits <= 1e-4."""
+    wl = W.WORKLOADS["tiny-b1"]
+    pair = Pair(wl.spec, seed=0)
+    pre = W.make_prefixes(wl, 0, 0)
+    news = [None] + [[W.make_observation(wl.spec, 0, s, 0, 1)] for s in range(1, 6)]
+    res = _run(pair, pre, news, wl.n_actions, 128, forced_from_ref=False, seed_tag="tiny")
+    for z_ref, z_gpu, t_gpu, t_ref in res:
+        c = compare(z_ref, z_gpu, t_gpu, TOL_F32)
+        log(f"tiny max_abs={c.max_abs:.2e} strict={c.strict}")
+        assert c.max_abs <= TOL_F32
+        assert np.array_equal(t_gpu, t_ref)
+
+
+@pytest.mark.parametrize("n_layers,d,H,F", [(2, 256, 4, 512), (2, 256, 2, 512)])
+def test_small_bf16_ragged(n_layers, d, H, F):
+    """bf16, ragged rows (1..150 tokens, tile tails), per-row new tokens incl. empty rows."""
+    spec = small_spec("bf16", n_layers, d, H, F)
+    pair = Pair(spec, seed=3)
+    wl = W.Workload("small", "tiny", 4, 5, 3, ragged=(1, 150, 8))
+    lens = [1, 37, 150, 64]
+    pre = [W.Prefix(W.make_observation(spec, 5, 100, b, lens[b] - min(8, lens[b] - 1)),
+                    np.arange(min(8, lens[b] - 1), dtype=np.int32) * 7 % 44) for b in range(4)]
+    news = [None,
+            [W.make_observation(spec, 5, 1, b, n) if n else None for b, n in enumerate([3, 0, 1, 70])],
+            [W.make_observation(spec, 5, 2, b, 1) for b in range(4)]]
+    res = _run(pair, pre, news, 5, 320, forced_from_ref=True, seed_tag="small")
+    for z_ref, z_gpu, t_gpu, _ in res:
+        c = compare(z_ref, z_gpu, t_gpu, TOL_BF16)
+        log(f"small bf16 max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16
+        assert c.band == 1.0
+
+
+def test_small_bf16_nonunit_gains():
+    """RMSNorm gains drawn around 1 (folded into the packed weights by the library)."""
+    spec = small_spec("bf16", 2, 256, 4, 512)
+    pair = Pair(spec, seed=8, gains=True)
+    pre = [W.Prefix(W.make_observation(spec, 9, 0, b, 30 + 20 * b), np.zeros(0, np.int32)) for b in range(3)]
+    news = [None, [W.make_observation(spec, 9, 1, b, 2) for b in range(3)]]
+    res = _run(pair, pre, news, 4, 128, forced_from_ref=True, seed_tag="gains")
+    for z_ref, z_gpu, t_gpu, _ in res:
+        c = compare(z_ref, z_gpu, t_gpu, TOL_BF16)
+        log(f"gains max_abs={c.max_abs:.2e} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16 and c.band == 1.0
+
+
+def test_multi_pass_build():
+    """A build split over several passes (max_pass_tokens = capacity: passes [60] [57] [10, 33] [41])
+    matches the reference; the single-pass build uses other GEMM kernels, so the two agree
+    to rounding, not bitwise."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec = small_spec("bf16")
+    pair = Pair(spec, seed=4)
+    lens = [60, 57, 10, 33, 41]
+    pre = [W.Prefix(W.make_observation(spec, 6, 0, b, n), np.zeros(0, np.int32)) for b, n in enumerate(lens)]
+    z_by_mpt = {}
+    for mpt in (0, 64):
+        res = _run(pair, pre, [None], 4, 64, forced_from_ref=True, max_pass_tokens=mpt, seed_tag=f"mpt={mpt}")
+        z_ref, z_gpu, t_gpu, _ = res[0]
+        c = compare(z_ref, z_gpu, t_gpu, TOL_BF16)
+        log(f"multi-pass mpt={mpt} max_abs={c.max_abs:.2e} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16 and c.band == 1.0
+        z_by_mpt[mpt] = z_gpu
+    assert np.max(np.abs(z_by_mpt[0] - z_by_mpt[64])) <= TOL_BF16
+
+
+def test_mid_bf16_full_size():
+    """12-layer d=1024 bf16 decoder, 8 rows of 256 patches + 24 ids, 7 actions;
+    parity variant with one fresh observation token per step, teacher-forced."""
+    wl = W.WORKLOADS["mid-b8"]
+    pair = Pair(wl.spec, seed=0)
+    pre = W.make_prefixes(wl, 0, 0)
+    news = [None] + [[W.make_observation(wl.spec, 0, s, b, 1) for b in range(wl.batch)] for s in (1, 2)]
+    res = _run(pair, pre, news, wl.n_actions, 320, forced_from_ref=True, seed_tag="mid")
+    worst = 0.0
+    bands = []
+    for z_ref, z_gpu, t_gpu, _ in res:
+        c = compare(z_ref, z_gpu, t_gpu, TOL_BF16)
+        log(f"mid max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+        worst = max(worst, c.max_abs)
+        bands.append(c.band)
+    assert worst <= TOL_BF16
+    assert min(bands) == 1.0
+
+
+def test_determinism_and_lifecycle():
+    """Same inputs twice -> bitwise equal; invalidate -> AMS_ESTATE; rebuild == fresh build."""
+    import torch
+    from paper_2508_10259_amd import capi
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec = small_spec("bf16")
+    pair = Pair(spec, seed=5)
+    pre = [W.Prefix(W.make_observation(spec, 7, 0, b, 40 + 9 * b), np.zeros(0, np.int32)) for b in range(3)]
+    prefix, lens = pair.dev.pack_prefixes(pre)
+    ctx = DeviceContext(pair.dev, 3, 128)
+    ctx.build(prefix, lens)
+    t1, z1 = ctx.step(6)
+    t2, z2 = ctx.step(6)
+    torch.cuda.synchronize()
+    assert torch.equal(t1, t2) and torch.equal(z1, z2)
+    ctx.invalidate()
+    assert ctx.state == capi.STATE_INVALID and ctx.lengths() == [0, 0, 0]
+    with pytest.raises(capi.AmsError) as e:
+        ctx.step(6)
+    assert e.value.status == capi.AMS_ESTATE
+    ctx.build(prefix, lens)
+    t3, z3 = ctx.step(6)
+    torch.cuda.synchronize()
+    assert torch.equal(t1, t3) and torch.equal(z1, z3)
+    # capacity: 40+9*2 = 58 tokens + n_actions - 1 must fit 128
+    with pytest.raises(capi.AmsError) as e:
+        ctx.step(72)
+    assert e.value.status == capi.AMS_ECAPACITY
+    assert ctx.lengths() == lens
+    t4, _ = ctx.step(71)  # exact fit: 58 + 71 - 1 = 128
+    torch.cuda.synchronize()
+    assert torch.equal(t4[:, :6], t1)
+    ctx.close()
