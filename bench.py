@@ -54,38 +54,65 @@ def build_flops(spec, lens):
 
 
 def gu_launch_bytes(spec, B, es=2):
-    """Gate|up projection of one decode pass: weights [2F, d] once, u [B, d] in, a [B, F] out."""
-    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * es + B * spec.d_ffn * es
+    """Decode gate|up projection with fused RMSNorm: weights [2F, d] once, h [B, d] fp32 in,
+    a [B, F] out."""
+    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4 + B * spec.d_ffn * es
 
 
-def time_gate_up_kernel(model, B, iters=200):
-    """Average duration of the decode gate|up kernel (the largest weight stream of a
-    pass) in the bench's launch shape, timed with HIP events on its own stream."""
+def time_gate_up_kernel(model, B, iters=240):
+    """Average duration of the decode gate|up kernel (RMSNorm + gate|up GEMV + SiLU gate,
+    the largest weight stream of a decode pass) in the decode step's launch shape,
+    cycling through the layers' packed weights, timed with HIP events on its own stream."""
     import torch
     from paper_2508_10259_amd.build import PROBE_LIB
     lib = C.CDLL(PROBE_LIB)
     spec = model.spec
-    d, F = spec.d_model, spec.d_ffn
+    d, F, es = spec.d_model, spec.d_ffn, 2
     # packed layout of the model workspace: [wqkv | wo | wgu | ...], each region 256-byte aligned
-    es = 2
     align = lambda x: (x + 255) // 256 * 256
-    w_ptr = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
-    u = torch.randn((B, d), device="cuda").half()
+    w_gu = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
+    h = torch.randn((B, d), device="cuda") * 30.0
     a = torch.empty((B, F), device="cuda", dtype=torch.float16)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def launch(l):
+        lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(h.data_ptr()), C.c_float(spec.rms_eps),
+                                   C.c_void_p(w_gu + (l % spec.n_layers) * 2 * F * d * es), B, 2 * F, d,
+                                   C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
     with torch.cuda.stream(s):
-        for _ in range(20):
-            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), C.c_void_p(w_ptr), B, 2 * F, d,
-                               C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+        for l in range(24):
+            launch(l)
         ev0.record(s)
         for l in range(iters):
-            lw = w_ptr + (l % spec.n_layers) * 2 * F * d * es
-            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), C.c_void_p(lw), B, 2 * F, d,
-                               C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+            launch(l)
         ev1.record(s)
     s.synchronize()
     return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
+
+
+def profiled_traffic(path=os.path.join(ROOT, "profiles", "decode_gate_up_mid-b8_pmc.txt")):
+    """HBM bytes per launch of the roofline kernel from the committed PMC summary,
+    or None when the kernel's source has changed since the counters were taken."""
+    import hashlib
+    try:
+        kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
+        src = open(os.path.join(ROOT, kv["kernel_source"]), "rb").read()
+        if hashlib.sha256(src).hexdigest() != kv["kernel_source_sha256"]:
+            return None
+        return int(kv["traffic_bytes"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration(nbytes=256 << 20):
+    """A device-to-device copy of known size, for scaling the FETCH_SIZE/WRITE_SIZE counters."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    return nbytes
 
 
 def cpu_baseline(wl, seed, sample_steps, window_steps):
@@ -176,9 +203,10 @@ def main():
     t_gu = time_gate_up_kernel(model, B)
     gb = gu_launch_bytes(spec, B)
     achieved = gb / t_gu / 1e9
-    roof = {"kernel": "k_gemm_skinny<2,1,SWIGLU> (decode gate|up projection + SiLU gate)",
+    copy_calibration()
+    roof = {"kernel": "k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(),
             "bytes_per_launch": gb, "avg_launch_us": round(t_gu * 1e6, 3)}
 
     out = {

@@ -218,16 +218,21 @@ template <> struct Raw<float> {
   }
 };
 
+// Waves per decode workgroup: 8 for 64-wide heads (one round covers 512
+// positions), 4 for 128-wide heads (their K/V fragments need twice the registers).
+template <int DH> constexpr int decode_waves() { return DH == 64 ? 8 : 4; }
+
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ qkv, const int32_t* __restrict__ lens,
+__global__ __launch_bounds__(64 * decode_waves<DH>()) void k_attn_decode(const float* __restrict__ qkv, const int32_t* __restrict__ lens,
                                                      int jpos, int H, int cap, int splits,
                                                      const float2* __restrict__ rope, T* __restrict__ kslab,
                                                      T* __restrict__ vslab, float* __restrict__ part,
                                                      T* __restrict__ o, float scale) {
   constexpr int HALF = DH / 2, NC = DH / 8, KS = 64 / NC;  // dim chunks of 8; key subgroups per wave
   constexpr int E = Raw<T>::E, KR = DH / E, VI = 64 / KS, VR = 8 / E;
+  constexpr int NWV = decode_waves<DH>();
   __shared__ float qs[DH], kn[DH], vn[DH];
-  __shared__ float wm[4], wl[4], wacc[4][DH];
+  __shared__ float wm[NWV], wl[NWV], wacc[NWV][DH];
   const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = H * DH;
@@ -295,7 +300,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
 
-  for (int kb = kb0; kb < k1; kb += 256) {
+  for (int kb = kb0; kb < k1; kb += NWV * 64) {
     if (kb != kb0) load_block(kb);
     const int key = kb + lane;
     float sc = -INFINITY;
@@ -354,11 +359,13 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
     for (int e = 0; e < 8; ++e) wacc[wave][lane * 8 + e] = acc[e];
   __syncthreads();
   if (tid < DH) {
-    const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    float M = wm[0];
+#pragma unroll
+    for (int w = 1; w < NWV; ++w) M = fmaxf(M, wm[w]);
     float L = 0.f, Acc = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < NWV; ++w) {
         const float f = __expf(wm[w] - M);
         L += wl[w] * f;
         Acc += wacc[w][tid] * f;
@@ -400,10 +407,10 @@ static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int 
   const float scale = 1.0f / sqrtf((float)dh);
   const dim3 grid(splits, H, B);
   if (dh == 64)
-    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(256), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
+    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * decode_waves<64>()), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
                        (T*)v, part, (T*)o, scale);
   else
-    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(256), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
+    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * decode_waves<128>()), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
                        (T*)v, part, (T*)o, scale);
   return hipGetLastError();
 }

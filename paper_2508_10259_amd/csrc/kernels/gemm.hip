@@ -25,9 +25,10 @@ __device__ __forceinline__ half8 as_half8(uint4 v) { return __builtin_bit_cast(h
 // ----------------------------------------------------------------------------
 // skinny: M <= 64
 //
-// Each wave walks its K chunks software-pipelined: the weight and activation
-// fragments of chunk c+1 are requested before chunk c's MFMAs, so a wave has
-// two chunks in flight.
+// Each wave requests the weight and activation fragments of up to CPW of its
+// K chunks before the first MFMA, so its loads overlap in one round trip; a
+// residual epilogue's h values are requested at kernel entry for the same
+// reason.
 //
 // NRM (M <= 16): the input is the fp32 residual stream h [M][K] and the
 // kernel applies RMSNorm itself.  The MFMA consumes fp16(h); the sum of
@@ -125,13 +126,32 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
     }
   };
 
-  Frag<RB, MB, NRM> fa, fb;
-  if (c0 < c1) load(fa, c0);
-  for (int c = c0; c < c1; c += 2) {
-    if (c + 1 < c1) load(fb, c + 1);
-    consume(fa);
-    if (c + 2 < c1) load(fa, c + 2);
-    if (c + 1 < c1) consume(fb);
+  // the residual epilogue's h values do not depend on this kernel: request them first
+  constexpr int EPT = (MB * 256 + 63) / 64;  // epilogue values per thread at the smallest workgroup
+  float hres[EPI == EPI_RESID ? RB * EPT : 1];
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int idx = threadIdx.x + e * blockDim.x;
+      const int mb = idx >> 8, ln = (idx >> 2) & 63, i = idx & 3;
+      const int tok = mb * 16 + (ln & 15), row = 4 * (ln >> 4) + i;
+      const bool ok = idx < MB * 256 && tok < M;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        hres[rb * EPT + e] = ok ? ((const float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] : 0.f;
+    }
+  }
+
+  // chunks in flight per wave: up to CPW loads are issued before the first MFMA
+  constexpr int CPW = (!NRM && RB + MB <= 2) ? 4 : 2;
+  Frag<RB, MB, NRM> fr[CPW];
+  for (int cb = c0; cb < c1; cb += CPW) {
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+      if (cb + j < c1) load(fr[j], cb + j);
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+      if (cb + j < c1) consume(fr[j]);
   }
 
 #pragma unroll
@@ -156,7 +176,10 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
   __syncthreads();
 
   // value (rb, mb, ln, i) is packed row n0 + rb*16 + 4*(ln>>4) + i, token mb*16 + (ln&15)
-  for (int idx = threadIdx.x; idx < MB * 256; idx += blockDim.x) {
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int idx = threadIdx.x + e * blockDim.x;
+    if (idx >= MB * 256) break;
     const int mb = idx >> 8, ln = (idx >> 2) & 63, i = idx & 3;
     const int tok = mb * 16 + (ln & 15);
     if (tok >= M) continue;
@@ -174,7 +197,8 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
       for (int rb = 0; rb < RB; ++rb) ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] = v[rb];
     } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] += v[rb];
+      for (int rb = 0; rb < RB; ++rb)
+        ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] = hres[rb * EPT + e] + v[rb];
     } else {
       st<f16>((f16*)out, (size_t)tok * ldo + (n0 >> 1) + row, silu(v[0]) * v[RB - 1]);
     }
