@@ -54,9 +54,9 @@ def build_flops(spec, lens):
 
 
 def gu_launch_bytes(spec, B, es=2):
-    """Decode gate|up projection with fused RMSNorm: weights [2F, d] once, h [B, d] fp32 in,
-    a [B, F] out."""
-    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4 + B * spec.d_ffn * es
+    """Decode gate|up projection: weights [2F, d] once, the input rows (fp32 h with the
+    RMSNorm fused up to 16 rows, fp16 u beyond) and a [B, F] out."""
+    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * (4 if B <= 16 else es) + B * spec.d_ffn * es
 
 
 def time_gate_up_kernel(model, B, iters=240):
@@ -72,14 +72,19 @@ def time_gate_up_kernel(model, B, iters=240):
     align = lambda x: (x + 255) // 256 * 256
     w_gu = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
     h = torch.randn((B, d), device="cuda") * 30.0
+    u = torch.randn((B, d), device="cuda").half()
     a = torch.empty((B, F), device="cuda", dtype=torch.float16)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def launch(l):
-        lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(h.data_ptr()), C.c_float(spec.rms_eps),
-                                   C.c_void_p(w_gu + (l % spec.n_layers) * 2 * F * d * es), B, 2 * F, d,
-                                   C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+        w = C.c_void_p(w_gu + (l % spec.n_layers) * 2 * F * d * es)
+        if B <= 16:  # the decode pass fuses the RMSNorm up to 16 rows
+            lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(h.data_ptr()), C.c_float(spec.rms_eps), w, B, 2 * F, d,
+                                       C.c_void_p(a.data_ptr()), F, C.c_void_p(s.cuda_stream))
+        else:
+            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
+                               C.c_void_p(s.cuda_stream))
     with torch.cuda.stream(s):
         for l in range(24):
             launch(l)
@@ -91,12 +96,14 @@ def time_gate_up_kernel(model, B, iters=240):
     return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
 
 
-def profiled_traffic(path=os.path.join(ROOT, "profiles", "decode_gate_up_mid-b8_pmc.txt")):
-    """HBM bytes per launch of the roofline kernel from the committed PMC summary,
-    or None when the kernel's source has changed since the counters were taken."""
+def profiled_traffic(workload, path=os.path.join(ROOT, "profiles", "decode_gate_up_mid-b8_pmc.txt")):
+    """HBM bytes per launch of the roofline kernel from the committed PMC summary, or None
+    for another workload or when the kernel's source has changed since the counters were taken."""
     import hashlib
     try:
         kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
+        if kv.get("workload") != workload:
+            return None
         src = open(os.path.join(ROOT, kv["kernel_source"]), "rb").read()
         if hashlib.sha256(src).hexdigest() != kv["kernel_source_sha256"]:
             return None
@@ -115,9 +122,9 @@ def copy_calibration(nbytes=256 << 20):
     return nbytes
 
 
-def cpu_baseline(wl, seed, sample_steps, window_steps):
-    """fp64 reference on row 0: build its prefix, then `sample_steps` steps;
-    row-steps/s with the build amortised over the workload's window."""
+def cpu_baseline(wl, w, seed, sample_steps, window_steps):
+    """fp64 reference on row 0 (same weights `w` as the GPU run): build its prefix, then
+    `sample_steps` steps; row-steps/s with the build amortised over the workload's window."""
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     import oracle.decoder as D
     from ref_bridge import oracle_params, prefix_f64
@@ -127,16 +134,19 @@ def cpu_baseline(wl, seed, sample_steps, window_steps):
         cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:
         cores = len(os.sched_getaffinity(0))
-    w = W.make_weights(wl.spec, seed)
     p = oracle_params(w)
-    pre = W.make_prefixes(wl, seed, 0)
-    x = prefix_f64(p, wl.spec, pre[0])
+    x = prefix_f64(p, wl.spec, W.make_prefix(wl, seed, 0, 0))
+    new = [W.to_f32(W.make_observation(wl.spec, seed, 0, 0, wl.new_per_step), wl.spec.dtype).astype(np.float64)] \
+        if wl.new_per_step else None
+    for l in range(wl.spec.n_layers):  # decode every weight once before timing
+        for n in W.MATRICES:
+            p.layer(n, l)
     ctx = D.ActionContext(p, 1)
     t0 = time.perf_counter()
     ctx.build([x])
     t1 = time.perf_counter()
     for _ in range(sample_steps):
-        ctx.step(None, wl.n_actions)
+        ctx.step(new, wl.n_actions)
     t2 = time.perf_counter()
     per_step = (t2 - t1) / sample_steps + (t1 - t0) / window_steps
     return {"value": 1.0 / per_step, "unit": "action-steps/s", "cores": int(cores), "kind": "oracle",
@@ -145,15 +155,40 @@ def cpu_baseline(wl, seed, sample_steps, window_steps):
                       f"{window_steps} steps as in the timed GPU window"}
 
 
+def make_inputs(model, wl, seed, steps, device_draws):
+    """Every input of the timed window, resident in HBM: one packed prefix set per build
+    epoch and a pool of per-step observation tokens (one invalidation window's worth)."""
+    import torch
+    from paper_2508_10259_amd import workload as W
+    inv = wl.invalidate_every
+    n_epochs = 1 + (steps - 1) // inv if inv else 1
+    epochs = []
+    for e in range(n_epochs):
+        lens = W.prefix_lengths(wl, seed, e)
+        if device_draws:
+            pre = [W.make_prefix_device(wl, seed, e, b, int(lens[b])) for b in range(wl.batch)]
+        else:
+            pre = [W.make_prefix(wl, seed, e, b, int(lens[b])) for b in range(wl.batch)]
+        epochs.append(model.pack_prefixes(pre))
+    pool = []
+    if wl.new_per_step:
+        for s in range(min(steps, inv or steps)):
+            pool.append(W.make_observation_device(wl.spec, seed, s, wl.batch, wl.new_per_step))
+    torch.cuda.synchronize()
+    return epochs, pool
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--steps", type=int, default=None, help="default: the workload's step count")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mid-b8")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=6)
+    ap.add_argument("--recompute", action="store_true",
+                    help="invalidate + rebuild the prefix before every step (the no-reuse comparison)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decoder shards by episode, "
@@ -166,70 +201,86 @@ def main():
 
     wl = W.WORKLOADS[args.workload]
     spec = wl.spec
+    steps = args.steps if args.steps is not None else wl.steps
+    big = spec.matmul_params > 1e9
     torch.cuda.set_device(0)
-    print(f"[bench] {wl.name}: generating weights", file=sys.stderr, flush=True)
-    model = DeviceModel(W.make_weights(spec, args.seed), "cuda:0")
-    cap = wl.derived_capacity(steps_between_builds=0)
+    print(f"[bench] {wl.name}: weights", file=sys.stderr, flush=True)
+    weights = W.make_device_weights(spec, args.seed) if big else W.make_weights(spec, args.seed)
+    model = DeviceModel(weights, "cuda:0")
+    cap = wl.derived_capacity()
     ctx = DeviceContext(model, wl.batch, cap)
-    prefix, lens = model.pack_prefixes(W.make_prefixes(wl, args.seed, 0))
+    print(f"[bench] inputs (capacity {cap})", file=sys.stderr, flush=True)
+    epochs, pool = make_inputs(model, wl, args.seed, steps, big)
     B, A = wl.batch, wl.n_actions
     tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
     logits = torch.empty((B, A, spec.n_bins), dtype=torch.float32, device="cuda")
-    torch.cuda.synchronize()
+    new_lens = [wl.new_per_step] * B if wl.new_per_step else None
+    inv = wl.invalidate_every
+
+    def window(n_steps):
+        """One build then n_steps steps, with the workload's rebuilds; returns (t_build, t_steps)."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record()
+        ctx.build(*epochs[0])
+        ev[1].record()
+        for s_ in range(n_steps):
+            if inv and s_ and s_ % inv == 0:
+                ctx.invalidate()
+                ctx.build(*epochs[(s_ // inv) % len(epochs)])
+            if args.recompute and s_:
+                ctx.invalidate()
+                ctx.build(*epochs[0])
+            new = pool[s_ % len(pool)] if pool else None
+            ctx.step(A, new, new_lens, tokens=tokens, logits=logits)
+        ev[2].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) * 1e-3, ev[1].elapsed_time(ev[2]) * 1e-3
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    ctx.build(prefix, lens)
-    for _ in range(args.warmup):
-        ctx.step(A, tokens=tokens, logits=logits)
-    torch.cuda.synchronize()
-
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    torch.cuda.synchronize()
-    ev[0].record()
-    ctx.build(prefix, lens)
-    ev[1].record()
-    for _ in range(args.steps):
-        ctx.step(A, tokens=tokens, logits=logits)
-    ev[2].record()
-    torch.cuda.synchronize()
-    t_build = ev[0].elapsed_time(ev[1]) * 1e-3
-    t_steps = ev[1].elapsed_time(ev[2]) * 1e-3
+    window(min(args.warmup, inv or args.warmup))
+    t_build, t_steps = window(steps)
     total = t_build + t_steps
-    value = B * args.steps / total
+    value = B * steps / total
+    lens = epochs[0][1]
     sb = step_bytes(spec, lens, A)
-    print(f"[bench] build {t_build * 1e3:.3f} ms, {args.steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
+    print(f"[bench] build {t_build * 1e3:.3f} ms, {steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
           flush=True)
 
     t_gu = time_gate_up_kernel(model, B)
     gb = gu_launch_bytes(spec, B)
     achieved = gb / t_gu / 1e9
     copy_calibration()
-    roof = {"kernel": "k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)",
+    roof = {"kernel": ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 16
+                       else f"k_gemm_skinny<2,{(B + 15) // 16},SWIGLU> (decode gate|up projection + SiLU gate)"),
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(),
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
             "bytes_per_launch": gb, "avg_launch_us": round(t_gu * 1e6, 3)}
 
     out = {
         "metric": "action steps/s per GPU (cached-context decode)",
-        "value": round(value, 2), "unit": "action-steps/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(total / args.steps * 1e3, 4), "higher_is_better": True,
+        "value": round(value, 2), "unit": "action-steps/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(total / steps * 1e3, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "fp16",
         "data": "synthetic (seeded N(0,0.02) weights stored bf16, N(0,1) patch embeddings, uniform ids)",
         "config": {"workload": wl.name, "n_layers": spec.n_layers, "d_model": spec.d_model,
                    "n_heads": spec.n_heads, "head_dim": spec.head_dim, "d_ffn": spec.d_ffn,
                    "vocab": spec.vocab, "n_bins": spec.n_bins, "batch": B, "prefix_tokens": int(lens[0]),
-                   "n_actions": A, "capacity": cap, "timed": f"1 build + {args.steps} steps"},
+                   "n_actions": A, "capacity": cap, "new_tokens_per_step": wl.new_per_step,
+                   "invalidate_every": inv, "recompute_each_step": bool(args.recompute),
+                   "timed": f"1 build + {steps} steps" + (f" (rebuild every {inv})" if inv else "")
+                            + (" (rebuild before every step)" if args.recompute else "")},
         "roofline": roof,
-        "step": {"ms": round(t_steps / args.steps * 1e3, 4), "algorithmic_bytes": sb,
-                 "hbm_frac": round(sb / (t_steps / args.steps) / (HBM_PEAK_GBS * 1e9), 4)},
+        "step": {"ms": round(t_steps / steps * 1e3, 4), "algorithmic_bytes_no_new_tokens": sb,
+                 "hbm_frac": round(sb / (t_steps / steps) / (HBM_PEAK_GBS * 1e9), 4)},
         "build": {"ms": round(t_build * 1e3, 4), "flops": build_flops(spec, lens),
                   "mfma_frac": round(build_flops(spec, lens) / t_build / (MFMA_F16_PEAK_TFLOPS * 1e12), 4)},
     }
     ctx.close()
     model.close()
+    del epochs, pool
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_sample_steps, args.steps)
+        out["cpu_baseline"] = cpu_baseline(wl, weights, args.seed, args.cpu_sample_steps if not big else 1, steps)
     print(json.dumps(out), flush=True)
 
 

@@ -5,10 +5,11 @@
 //
 //  * k_kv_append:     new tokens of a pass -> rotate k (RoPE), write k and v
 //                     at their absolute positions.
-//  * k_attn_prefill:  causal attention of a pass's tokens (a row's new
-//                     segment at positions pos..pos+n-1) over keys
-//                     0..pos+n-1 of that row: Q tile of 64 queries in LDS,
-//                     K/V tiles of 32 keys staged in LDS, online softmax.
+//  * k_attn_prefill_mfma (fp16) / k_attn_prefill (fp32): causal attention of
+//                     a pass's tokens (a row's new segment at positions
+//                     pos..pos+n-1) over keys 0..pos+n-1 of that row, K/V
+//                     tiles staged in LDS, online softmax; the fp16 kernel
+//                     runs both products on MFMA.
 //  * k_attn_decode:   one query per row at position p = lens[b] + jpos (a
 //                     fed-back action token).  Appends its own K/V, then
 //                     each workgroup covers one split of the keys: lane-per-key
@@ -179,6 +180,166 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   }
 }
 
+// ----------------------------------------------------------------------------
+// fp16 prefill attention on MFMA (flash-attention style).
+//
+// Workgroup: 64 queries of one segment and head, 4 waves x 16 queries.
+// Per 64-key tile: K [key][dh] and V^T [dh][key] staged in LDS (fp16);
+// S = Q K^T with v_mfma_f32_16x16x32_f16 (A = Q fragments held in registers,
+// rotated and scaled at load; B = K rows), online softmax in fp32 over the
+// 16-lane groups that share a query, P written to LDS and read back in the
+// A-operand layout, O += P V with B = V^T rows.  MFMA layouts (16x16x32):
+// A lane (r, g) = A[r][8g..8g+7], B lane (r, g) = B[8g..8g+7][r],
+// C lane (r, g) = C[4g+i][r], with r = lane & 15, g = lane >> 4.
+
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv,
+                                                           const int32_t* __restrict__ row,
+                                                           const int32_t* __restrict__ pos,
+                                                           const int32_t* __restrict__ off, int H, int cap,
+                                                           const float2* __restrict__ rope,
+                                                           const f16* __restrict__ kslab,
+                                                           const f16* __restrict__ vslab, f16* __restrict__ o,
+                                                           float scale) {
+  constexpr int QT = 64, KT = 64, HALF = DH / 2, KPAD = DH + 8, VPAD = KT + 8, PPAD = KT + 8;
+  constexpr int NQI = DH / 32;  // 32-wide dim blocks of a head (MFMA k-steps of S)
+  constexpr int NDJ = DH / 16;  // 16-wide dim blocks of O
+  __shared__ __attribute__((aligned(16))) f16 Ks[KT * KPAD];
+  __shared__ __attribute__((aligned(16))) f16 VT[DH * VPAD];
+  __shared__ __attribute__((aligned(16))) f16 Ps[4 * 16 * PPAD];
+  const int sg = blockIdx.z, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int b = row[sg], p0 = pos[sg], t0 = off[sg], n = off[sg + 1] - off[sg];
+  const int q_lo = blockIdx.x * QT;
+  if (q_lo >= n) return;  // uniform across the workgroup
+  const int d = H * DH;
+  const int kv_end = p0 + (n < q_lo + QT ? n : q_lo + QT);  // exclusive
+
+  // Q fragments: this lane's query row r of the wave, dims 32i + 8g + e
+  half8 qf[NQI];
+  {
+    const int qi = q_lo + wave * 16 + r;
+    const bool ok = qi < n;
+    const float* q = qkv + (size_t)(t0 + (ok ? qi : 0)) * 3 * d + h * DH;
+    const float2* rp = rope + (size_t)(p0 + (ok ? qi : 0)) * HALF;
+#pragma unroll
+    for (int i = 0; i < NQI / 2; ++i) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int dd = 32 * i + 8 * g + e;  // < HALF; its partner is dd + HALF
+        const float a = ok ? q[dd] : 0.f, c = ok ? q[dd + HALF] : 0.f;
+        const float2 cs = rp[dd];
+        qf[i][e] = (f16)((a * cs.x - c * cs.y) * scale);
+        qf[i + NQI / 2][e] = (f16)((a * cs.y + c * cs.x) * scale);
+      }
+    }
+  }
+  // query positions of this lane's C rows (4g + i)
+  int qp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qi = q_lo + wave * 16 + 4 * g + i;
+    qp[i] = qi < n ? p0 + qi : -1;
+  }
+
+  float m[4], l[4];
+  f32x4 acc[NDJ];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; l[i] = 0.f; }
+#pragma unroll
+  for (int j = 0; j < NDJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const f16* Kb = kslab + ((size_t)b * H + h) * cap * DH;
+  const f16* Vb = vslab + ((size_t)b * H + h) * cap * DH;
+  f16* Pw = Ps + wave * 16 * PPAD;
+  constexpr int CH = DH / 8;  // 16-byte chunks per key row
+
+  for (int kt = 0; kt < kv_end; kt += KT) {
+    __syncthreads();  // previous tile's Ks / VT / Ps reads are done
+    for (int c = tid; c < KT * CH; c += 256) {
+      const int kk = c / CH, ch = c % CH;
+      const bool ok = kt + kk < kv_end;
+      uint4 kv = ok ? *(const uint4*)(Kb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+      uint4 vv = ok ? *(const uint4*)(Vb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+      *(uint4*)(Ks + kk * KPAD + ch * 8) = kv;
+      const half8 vh = __builtin_bit_cast(half8, vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) VT[(ch * 8 + e) * VPAD + kk] = vh[e];
+    }
+    __syncthreads();
+
+    // S for 4 blocks of 16 keys
+    f32x4 sc[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < NQI; ++i) {
+        const half8 kf = *(const half8*)(Ks + (kb * 16 + r) * KPAD + 32 * i + 8 * g);
+        sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qf[i], kf, sc[kb], 0, 0, 0);
+      }
+    }
+    // mask, online softmax per query row 4g+i (its 64 keys sit in the 16 lanes sharing g)
+    float mx[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int key = kt + kb * 16 + r;
+        if (key > qp[i] || key >= kv_end) sc[kb][i] = -INFINITY;
+        v = fmaxf(v, sc[kb][i]);
+      }
+#pragma unroll
+      for (int o_ = 1; o_ < 16; o_ <<= 1) v = fmaxf(v, __shfl_xor(v, o_, 64));
+      mx[i] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float m_new = fmaxf(m[i], mx[i]);
+      const float alpha = (m_new == -INFINITY) ? 1.f : __expf(m[i] - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const float pv = (sc[kb][i] == -INFINITY) ? 0.f : __expf(sc[kb][i] - m_new);
+        sc[kb][i] = pv;
+        rs += pv;
+      }
+#pragma unroll
+      for (int o_ = 1; o_ < 16; o_ <<= 1) rs += __shfl_xor(rs, o_, 64);
+      l[i] = l[i] * alpha + rs;
+      m[i] = m_new;
+#pragma unroll
+      for (int j = 0; j < NDJ; ++j) acc[j][i] *= alpha;
+    }
+    // P (C layout) -> LDS [q][key] -> A layout
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Pw[(4 * g + i) * PPAD + kb * 16 + r] = (f16)sc[kb][i];
+    __syncthreads();
+#pragma unroll
+    for (int s2 = 0; s2 < KT / 32; ++s2) {
+      const half8 pf = *(const half8*)(Pw + r * PPAD + 32 * s2 + 8 * g);
+#pragma unroll
+      for (int j = 0; j < NDJ; ++j) {
+        const half8 vf = *(const half8*)(VT + (16 * j + r) * VPAD + 32 * s2 + 8 * g);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf, vf, acc[j], 0, 0, 0);
+      }
+    }
+  }
+  // O / l -> o[token][h*DH + dh]
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qi = q_lo + wave * 16 + 4 * g + i;
+    if (qi >= n) continue;
+    const float inv = 1.0f / l[i];
+    f16* dst = o + (size_t)(t0 + qi) * d + h * DH;
+#pragma unroll
+    for (int j = 0; j < NDJ; ++j) st<f16>(dst, 16 * j + r, acc[j][i] * inv);
+  }
+}
+
 template <typename T>
 static hipError_t prefill_t(const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope, const void* k,
                             const void* v, void* o, hipStream_t s) {
@@ -197,7 +358,15 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int ca
                         const void* kslab, const void* vslab, void* o, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;
   if (ct == DT_F32) return prefill_t<float>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
-  return prefill_t<f16>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
+  const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
+  const float scale = 1.0f / sqrtf((float)dh);
+  if (dh == 64)
+    hipLaunchKernelGGL((k_attn_prefill_mfma<64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+                       (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+  else
+    hipLaunchKernelGGL((k_attn_prefill_mfma<128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+                       (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------

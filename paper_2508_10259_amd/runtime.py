@@ -52,6 +52,9 @@ class DeviceModel:
         src = {}
         for name in MATRICES:
             stack = getattr(w, name)
+            if hasattr(stack, "t"):  # drawn on the device already
+                src[name] = stack.t
+                continue
             t = torch.empty((spec.n_layers,) + tuple(stack[0].shape), dtype=td, device=device)
             for l in range(spec.n_layers):
                 t[l].copy_(to_device(stack[l], spec.dtype, device))
@@ -91,7 +94,8 @@ class DeviceModel:
         for p in prefixes:
             n_p = p.patches.shape[0]
             if n_p:
-                out[o:o + n_p].copy_(to_device(p.patches, spec.dtype, self.device))
+                src = p.patches if isinstance(p.patches, torch.Tensor) else to_device(p.patches, spec.dtype, self.device)
+                out[o:o + n_p].copy_(src)
             if len(p.text_ids):
                 ids = torch.from_numpy(p.text_ids.astype(np.int32)).to(self.device)
                 self.embed_ids(ids, out[o + n_p:o + p.length])

@@ -225,6 +225,72 @@ def make_weights(spec: ModelSpec, seed: int = 0, lazy: Optional[bool] = None) ->
 
 
 # ----------------------------------------------------------------------------
+# device-side draws for the 7B-parameter model (numpy draws ~30 M normals/s,
+# minutes for 6.5 G weights): torch's CUDA Philox generator, one stream per
+# (seed, purpose, indices) key, same N(0, std) recipe, rounded to bf16 by
+# torch (round to nearest even).  The CPU reference receives host copies.
+
+
+def _key_seed(*key: int) -> int:
+    return int(np.random.SeedSequence([int(k) for k in key]).generate_state(1, dtype=np.uint64)[0] >> 1)
+
+
+def device_normal(shape, std, dtype: str, device, *key: int):
+    """torch tensor on `device`: N(0, std) drawn in fp32 from the stream `key`, in `dtype`."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(_key_seed(*key))
+    x = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
+    if std != 1.0:
+        x.mul_(std)
+    return x.to(torch.bfloat16) if dtype == "bf16" else x
+
+
+class DeviceStack:
+    """``[n_layers, out, in]`` device tensor of one matrix kind; ``stack[l]`` gives a host
+    fp32 numpy copy of layer l (for the CPU reference)."""
+
+    def __init__(self, t):
+        self.t = t
+        self.shape = tuple(t.shape)
+
+    def __len__(self):
+        return self.shape[0]
+
+    def __getitem__(self, layer: int) -> np.ndarray:
+        return self.t[layer].float().cpu().numpy()
+
+
+def make_device_weights(spec: ModelSpec, seed: int = 0, device="cuda") -> Weights:
+    """All weights of ``spec`` drawn on the device (matrices N(0, 0.02), gains 1.0).
+    Matrix fields are DeviceStack; tables are host arrays in the model dtype encoding."""
+    import torch
+    d = spec.d_model
+    mats = {}
+    for idx, name in enumerate(MATRICES):
+        out_, in_ = matrix_shape(spec, name)
+        t = torch.empty((spec.n_layers, out_, in_), device=device,
+                        dtype=torch.bfloat16 if spec.dtype == "bf16" else torch.float32)
+        for l in range(spec.n_layers):
+            t[l].copy_(device_normal((out_, in_), spec.init_std, spec.dtype, device, seed, _T_MAT, l, idx))
+        mats[name] = DeviceStack(t)
+
+    def table(tag, rows):
+        x = device_normal((rows, d), spec.init_std, spec.dtype, device, seed, tag)
+        if spec.dtype == "bf16":
+            return x.view(torch.int16).cpu().numpy().view(np.uint16)
+        return x.cpu().numpy()
+    return Weights(
+        spec=spec, seed=seed, **mats,
+        g_attn=np.ones((spec.n_layers, d), np.float32),
+        g_ffn=np.ones((spec.n_layers, d), np.float32),
+        g_final=np.ones((d,), np.float32),
+        embed=table(_T_EMB, spec.vocab),
+        head_bins=table(_T_HEAD, spec.n_bins),
+    )
+
+
+# ----------------------------------------------------------------------------
 # episodes: prefixes, per-step observation tokens, ragged lengths
 
 
@@ -330,6 +396,24 @@ def make_prefix(wl: Workload, seed: int, epoch: int, row: int, length: Optional[
 def make_prefixes(wl: Workload, seed: int, epoch: int) -> List[Prefix]:
     lens = prefix_lengths(wl, seed, epoch)
     return [make_prefix(wl, seed, epoch, b, int(lens[b])) for b in range(wl.batch)]
+
+
+def make_prefix_device(wl: Workload, seed: int, epoch: int, row: int, length: Optional[int] = None,
+                       device="cuda") -> Prefix:
+    """As make_prefix, with the patch embeddings drawn on the device (a torch tensor)."""
+    spec = wl.spec
+    if length is None:
+        length = int(prefix_lengths(wl, seed, epoch)[row])
+    n_text = min(_n_text(wl), length)
+    x = device_normal((length - n_text, spec.d_model), 1.0, spec.dtype, device, seed, _T_PATCH, epoch, row)
+    lo, hi = text_id_range(spec)
+    ids = _rng(seed, _T_IDS, epoch, row).integers(lo, hi, size=n_text).astype(np.int32)
+    return Prefix(x, ids)
+
+
+def make_observation_device(spec: ModelSpec, seed: int, step: int, n_rows: int, n: int, device="cuda"):
+    """[n_rows * n, d] fresh N(0,1) observation embeddings for all rows of one step, on the device."""
+    return device_normal((n_rows * n, spec.d_model), 1.0, spec.dtype, device, seed, _T_OBS, step, 1 << 20)
 
 
 def make_observation(spec: ModelSpec, seed: int, step: int, row: int, n: int) -> np.ndarray:

@@ -6,13 +6,20 @@ from paper_2508_10259_amd import workload as W
 
 
 class _Decoded:
-    """Layer-indexable fp32 view of an encoded stack."""
+    """Layer-indexable fp64 view of an encoded stack (host numpy or device-drawn),
+    each layer decoded once and kept."""
 
     def __init__(self, stack, dtype):
         self.stack, self.dtype = stack, dtype
+        self.cache = {}
 
     def __getitem__(self, l):
-        return W.to_f32(self.stack[l], self.dtype)
+        if l not in self.cache:
+            x = self.stack[l]
+            if not isinstance(self.stack, W.DeviceStack):  # device stacks hand out fp32 already
+                x = W.to_f32(x, self.dtype)
+            self.cache[l] = np.asarray(x, dtype=np.float64)
+        return self.cache[l]
 
 
 def oracle_config(spec):

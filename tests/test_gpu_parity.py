@@ -65,7 +65,7 @@ def test_tiny_fp32_free_running():
         assert np.array_equal(t_gpu, t_ref)
 
 
-@pytest.mark.parametrize("n_layers,d,H,F", [(2, 256, 4, 512), (2, 256, 2, 512)])
+@pytest.mark.parametrize("n_layers,d,H,F", [(2, 256, 4, 512), (2, 256, 2, 512), (2, 512, 4, 1408)])
 def test_small_bf16_ragged(n_layers, d, H, F):
     """bf16, ragged rows (1..150 tokens, tile tails), per-row new tokens incl. empty rows."""
     spec = small_spec("bf16", n_layers, d, H, F)
@@ -170,4 +170,126 @@ def test_determinism_and_lifecycle():
     t4, _ = ctx.step(71)  # exact fit: 58 + 71 - 1 = 128
     torch.cuda.synchronize()
     assert torch.equal(t4[:, :6], t1)
+    ctx.close()
+
+
+def test_7b_single_row_full_size():
+    """7B decoder (32 layers, d=4096, 32 heads of 128, FFN 11008, vocab 32000, bins = last 256 ids),
+    1 row of 256 patches + 32 instruction ids, 7 actions, plus one step with a fresh observation
+    token; weights drawn on the device, reference on host copies; teacher-forced."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext, DeviceModel
+    from ref_bridge import oracle_params, prefix_f64
+    wl = W.WORKLOADS["7b-b1"]
+    spec = wl.spec
+    log("7b: drawing weights on the device")
+    w = W.make_device_weights(spec, seed=0)
+    dev = DeviceModel(w)
+    p = oracle_params(w)
+    pre = W.make_prefixes(wl, 0, 0)
+    ref = D.ActionContext(p, 1)
+    log("7b: reference build")
+    ref.build([prefix_f64(p, spec, pre[0])])
+    ctx = DeviceContext(dev, 1, 320)
+    prefix, lens = dev.pack_prefixes(pre)
+    ctx.build(prefix, lens)
+    obs = W.make_observation(spec, 0, 1, 0, 1)
+    for s_, news in enumerate([None, [obs]]):
+        log(f"7b: step {s_}")
+        t_ref, z_ref = ref.step(None if news is None else [W.to_f32(obs, "bf16").astype(np.float64)], wl.n_actions)
+        forced = torch.from_numpy(t_ref.astype(np.int32)).cuda()
+        new_t, new_lens = gpu_new_tokens(spec, news) if news is not None else (None, None)
+        t_gpu, z_gpu = ctx.step(wl.n_actions, new_t, new_lens, forced=forced)
+        torch.cuda.synchronize()
+        c = compare(z_ref, z_gpu.cpu().numpy(), t_gpu.cpu().numpy(), TOL_BF16)
+        log(f"7b max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16 and c.band == 1.0
+    ctx.close()
+
+
+@pytest.fixture(scope="module")
+def model_7b():
+    from paper_2508_10259_amd.runtime import DeviceModel
+    from ref_bridge import oracle_params
+    spec = W.MODELS["7b"]
+    w = W.make_device_weights(spec, seed=0)
+    return spec, DeviceModel(w), oracle_params(w)
+
+
+def _rows_ref(p, spec, prefixes, rows):
+    ref = D.ActionContext(p, len(rows))
+    ref.build([prefix_f64_of(p, spec, prefixes[b]) for b in rows])
+    return ref
+
+
+def prefix_f64_of(p, spec, prefix):
+    from ref_bridge import prefix_f64
+    return prefix_f64(p, spec, prefix)
+
+
+def test_7b_ragged_batch64_extension_and_rebuild(model_7b):
+    """64 rows with prefixes U{200..400} (capacity 768); a step that appends 16 fresh observation
+    tokens to every row, then invalidate + rebuild on the next epoch's prefixes and step again.
+    The reference checks rows 0, 37 and 63 (one by one, teacher-forced); the other rows are fed
+    bin 0."""
+    import torch
+    from paper_2508_10259_amd import capi
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec, dev, p = model_7b
+    wl = W.WORKLOADS["7b-b64-ragged"]
+    rows = [0, 37, 63]
+    ctx = DeviceContext(dev, wl.batch, wl.capacity)
+    for epoch in (0, 1):
+        pre = W.make_prefixes(wl, 0, epoch)
+        log(f"7b-b64 epoch {epoch}: lens {[p_.length for p_ in pre[:4]]}...")
+        if epoch:
+            ctx.invalidate()
+            with pytest.raises(capi.AmsError):
+                ctx.step(wl.n_actions)
+        prefix, lens = dev.pack_prefixes(pre)
+        ctx.build(prefix, lens)
+        ref = _rows_ref(p, spec, pre, rows)
+        news = [W.make_observation(spec, 0, 100 * epoch + 1, b, wl.new_per_step) for b in range(wl.batch)]
+        t_ref, z_ref = ref.step([W.to_f32(news[b], "bf16").astype(np.float64) for b in rows], wl.n_actions)
+        forced = np.zeros((wl.batch, wl.n_actions), np.int32)
+        forced[rows] = t_ref
+        new_t, new_lens = gpu_new_tokens(spec, news)
+        t_gpu, z_gpu = ctx.step(wl.n_actions, new_t, new_lens, forced=torch.from_numpy(forced).cuda())
+        torch.cuda.synchronize()
+        assert ctx.lengths() == [l + wl.new_per_step for l in lens]
+        c = compare(z_ref, z_gpu.cpu().numpy()[rows], t_gpu.cpu().numpy()[rows], TOL_BF16)
+        log(f"7b-b64 epoch {epoch} max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16 and c.band == 1.0
+    ctx.close()
+
+
+def test_7b_chunk56_batch16_and_recompute(model_7b):
+    """16 rows of 568 patches + 32 ids, 56 greedy tokens per step (8 actions x 7 tokens):
+    row 0 against the reference over all 56 positions (teacher-forced); then the
+    recompute mode (invalidate + build + step) reproduces the cached step bit for bit."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec, dev, p = model_7b
+    wl = W.WORKLOADS["7b-chunk56-b16"]
+    cap = wl.derived_capacity()
+    pre = W.make_prefixes(wl, 0, 0)
+    ctx = DeviceContext(dev, wl.batch, cap)
+    prefix, lens = dev.pack_prefixes(pre)
+    ctx.build(prefix, lens)
+    log("7b-chunk56: reference row 0")
+    ref = _rows_ref(p, spec, pre, [0])
+    t_ref, z_ref = ref.step(None, wl.n_actions)
+    forced = np.zeros((wl.batch, wl.n_actions), np.int32)
+    forced[0] = t_ref[0]
+    forced_d = torch.from_numpy(forced).cuda()
+    t_gpu, z_gpu = ctx.step(wl.n_actions, forced=forced_d)
+    torch.cuda.synchronize()
+    c = compare(z_ref, z_gpu.cpu().numpy()[:1], t_gpu.cpu().numpy()[:1], TOL_BF16)
+    log(f"7b-chunk56 max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+    assert c.max_abs <= TOL_BF16 and c.band == 1.0
+    ctx.invalidate()
+    ctx.build(prefix, lens)
+    t2, z2 = ctx.step(wl.n_actions, forced=forced_d)
+    torch.cuda.synchronize()
+    assert torch.equal(t2, t_gpu) and torch.equal(z2, z_gpu)
     ctx.close()
