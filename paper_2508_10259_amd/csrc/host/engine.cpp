@@ -20,6 +20,10 @@ namespace ams {
 
 static const char* off(const void* p, size_t bytes) { return (const char*)p + bytes; }
 
+// Decode runs its RMSNorms inside the projection GEMVs for fp16 compute and up
+// to 16 rows (see norm_proj).
+static bool fused_norm(const Ctx& c) { return c.model->ct == DT_F16 && c.lay.batch <= 16; }
+
 hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err) {
   // bf16 weights become fp16 in the packed copy: exact for |w| >= 2^-14, an
   // fp16 subnormal (absolute error <= 2^-25) below; fp32 models are copied.
@@ -109,21 +113,23 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
     TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s));
+    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, fused_norm(c) ? c.h_last16() : nullptr));
   }
   TRY(update_lens(c.lens(), md + 4 * B + 1, B, set_lens, s));
   return hipSuccess;
 }
 
-// Projection of a normalised input in the decode pass: up to 16 fp16 rows run
-// the GEMV with the RMSNorm fused; otherwise rmsnorm writes u first.
-static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* W, int N, int K, void* out, int ldo,
-                            hipStream_t s, std::string& err) {
+// Projection of a normalised input in the decode pass.  Up to 16 fp16 rows run
+// the GEMV with the RMSNorm fused, reading h16, the fp16 copy of the residual
+// rows that their producers (residual GEMV epilogue, feed, gather of the last
+// prefix token) write beside h; otherwise rmsnorm writes u from h first.
+static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* h16, const void* W, int N, int K, void* out,
+                            int ldo, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const int B = c.lay.batch;
   const float eps = md.cfg.rms_eps;
-  if (md.ct == DT_F16 && B <= 16) {
-    TRY(gemv_rmsnorm(md.ct, epi, h, eps, W, B, N, K, out, ldo, s));
+  if (fused_norm(c)) {
+    TRY(gemv_rmsnorm(md.ct, epi, h16, eps, W, B, N, K, out, ldo, s));
   } else {
     TRY(rmsnorm(md.ct, h, B, K, eps, c.u(), s));
     TRY(gemm(md.ct, epi, c.u(), W, B, N, K, out, ldo, s));
@@ -131,45 +137,50 @@ static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* W, int 
   return hipSuccess;
 }
 
-// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.
+// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.  In
+// the fused-RMSNorm path u holds the fp16 copy of h during decode.
 static hipError_t layer_decode(Ctx& c, int l, int jpos, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   const int d = m.d_model, F = m.d_ffn, dt = md.ct, B = c.lay.batch;
-  if (norm_proj(c, EPI_STORE, c.h(), md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, s, err) != hipSuccess)
+  void* h16 = fused_norm(c) ? c.u() : nullptr;
+  if (norm_proj(c, EPI_STORE, c.h(), h16, md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, c.qkv(), c.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
                   c.kslab(l), c.vslab(l), c.part(), c.o(), s));
   if (c.splits > 1) TRY(attn_merge(dt, c.part(), B, m.n_heads, m.head_dim, c.splits, c.o(), s));
-  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s));
-  if (norm_proj(c, EPI_SWIGLU, c.h(), md.wgu(l), 2 * F, d, c.a(), F, s, err) != hipSuccess)
+  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s, h16));
+  if (norm_proj(c, EPI_SWIGLU, c.h(), h16, md.wgu(l), 2 * F, d, c.a(), F, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s));
+  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s, h16));
   return hipSuccess;
 }
 
 // Action head for decode position j: final RMSNorm + bin logits (the
 // projection GEMV over the padded head rows), then argmax/outputs/feed.
-static hipError_t head(Ctx& c, const float* hin, int A, int j, int32_t* tok, float* logits, const int32_t* forced,
-                       hipStream_t s, std::string& err) {
+static hipError_t head(Ctx& c, const float* hin, const void* hin16, int A, int j, int32_t* tok, float* logits,
+                       const int32_t* forced, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   const int B = c.lay.batch, d = m.d_model, nbp = bins_padded(m);
-  if (norm_proj(c, EPI_STORE, hin, md.head_bins(), nbp, d, c.logits(), nbp, s, err) != hipSuccess)
+  if (norm_proj(c, EPI_STORE, hin, hin16, md.head_bins(), nbp, d, c.logits(), nbp, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(argmax_feed(md.ct, c.logits(), nbp, md.bin_embed(), B, d, m.n_bins, A, j, tok, logits, forced, c.h(),
-                  j + 1 < A, s));
+                  j + 1 < A, s, fused_norm(c) ? c.u() : nullptr));
   return hipSuccess;
 }
 
 static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
                                  std::string& err) {
   const Cfg& m = c.model->cfg;
-  if (head(c, c.h_last(), A, 0, tok, logits, forced, s, err) != hipSuccess) return hipErrorLaunchFailure;
+  const bool fused = fused_norm(c);
+  if (head(c, c.h_last(), fused ? c.h_last16() : nullptr, A, 0, tok, logits, forced, s, err) != hipSuccess)
+    return hipErrorLaunchFailure;
   for (int j = 1; j < A; ++j) {
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_decode(c, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    if (head(c, c.h(), A, j, tok, logits, forced, s, err) != hipSuccess) return hipErrorLaunchFailure;
+    if (head(c, c.h(), fused ? c.u() : nullptr, A, j, tok, logits, forced, s, err) != hipSuccess)
+      return hipErrorLaunchFailure;
   }
   return hipSuccess;
 }

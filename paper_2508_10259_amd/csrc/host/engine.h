@@ -66,6 +66,7 @@ struct Ctx {
   void* o() const { return ws + lay.o; }
   void* a() const { return ws + lay.a; }
   float* h_last() const { return (float*)(ws + lay.h_last); }
+  void* h_last16() const { return ws + lay.h_last16; }
   float* part() const { return (float*)(ws + lay.part); }
   float* logits() const { return (float*)(ws + lay.logits); }
   float2* rope() const { return (float2*)(ws + lay.rope); }

@@ -76,7 +76,7 @@ inline ModelLayout model_layout(const Cfg& c) {
 struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
   size_t slab_layer;  // bytes of K (or V) for one layer
-  size_t kv, h, u, qkv, o, a, h_last, part, logits, rope, lens, meta, total;
+  size_t kv, h, u, qkv, o, a, h_last, h_last16, part, logits, rope, lens, meta, total;
   size_t meta_ints;
 };
 
@@ -117,6 +117,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.o = o; o = align256(o + T * d * es);
   x.a = o; o = align256(o + T * F * es);
   x.h_last = o; o = align256(o + B * d * 4);
+  x.h_last16 = o; o = align256(o + B * d * 2);  // fp16 copy for the fused-RMSNorm head
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);

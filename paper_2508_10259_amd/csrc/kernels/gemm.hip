@@ -28,35 +28,30 @@ __device__ __forceinline__ half8 as_half8(uint4 v) { return __builtin_bit_cast(h
 // Each wave requests the weight and activation fragments of up to CPW of its
 // K chunks before the first MFMA, so its loads overlap in one round trip; a
 // residual epilogue's h values are requested at kernel entry for the same
-// reason.
+// reason.  The K range a wave covers is rotated by the workgroup index, so
+// concurrent workgroups read different parts of the shared activations.
 //
-// NRM (M <= 16): the input is the fp32 residual stream h [M][K] and the
-// kernel applies RMSNorm itself.  The MFMA consumes fp16(h); the sum of
-// squares of each token row comes from the same fragments (reduced across the
-// waves, which together cover all of K) and the 1/rms scale multiplies the
-// result in the epilogue.  The RMSNorm gain is folded into W at packing.
-
-template <int RB, int MB, bool NRM> struct Frag;
-template <int RB, int MB> struct Frag<RB, MB, false> {
-  uint4 w[RB][4];
-  uint4 u[MB][4];
-};
-template <int RB> struct Frag<RB, 1, true> {
-  uint4 w[RB][4];
-  float4 h[8];
-};
+// NRM (M <= 16): the input is the fp16 copy of the residual stream h [M][K]
+// and the kernel applies RMSNorm itself: the MFMA consumes it as is, the sum
+// of squares of each token row comes from the same fragments (reduced across
+// the waves, which together cover all of K), and the 1/rms scale multiplies
+// the result in the epilogue.  The RMSNorm gain is folded into W at packing.
+//
+// RESID may also write an fp16 copy of the updated residual rows (out16, same
+// leading dimension), the input of the next fused-RMSNorm GEMV.
 
 template <int RB, int MB, int EPI, bool NRM>
-__global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xin, float eps,
+__global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin, float eps,
                                                      const f16* __restrict__ W, int M, int K,
-                                                     void* __restrict__ out, int ldo) {
+                                                     void* __restrict__ out, int ldo, f16* __restrict__ out16) {
   static_assert(!NRM || MB == 1, "the fused RMSNorm handles up to 16 tokens");
   extern __shared__ float red[];  // [nw][RB][MB][64 lanes][4], then (NRM) wsum[<=16 waves][16] + rstd[16]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * (RB * 16);
   const int nchunks = K >> 7;
-  const int c0 = wave * nchunks / nw, c1 = (wave + 1) * nchunks / nw;
+  const int wk = (wave + blockIdx.x) % nw;
+  const int c0 = wk * nchunks / nw, c1 = (wk + 1) * nchunks / nw;
 
   f32x4 acc[RB][MB];
 #pragma unroll
@@ -68,63 +63,14 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) wrow[rb] = W + (size_t)(n0 + rb * 16 + r) * K + g * 8;
   bool uok[MB];
-  size_t uoff[MB];
+  const f16* urow[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int tok = mb * 16 + r;
     uok[mb] = tok < M;
-    uoff[mb] = (size_t)(uok[mb] ? tok : 0) * K + g * 8;
+    urow[mb] = xin + (size_t)(uok[mb] ? tok : 0) * K + g * 8;
   }
   float ss = 0.f;  // NRM: this lane's share of sum(h^2) of token r
-
-  auto load = [&](Frag<RB, MB, NRM>& f, int c) {
-    const int kb = c << 7;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) f.w[rb][i] = *(const uint4*)(wrow[rb] + kb + 32 * i);
-    if constexpr (NRM) {
-      const float* hp = (const float*)xin + uoff[0] + kb;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f.h[2 * i] = uok[0] ? *(const float4*)(hp + 32 * i) : float4{0.f, 0.f, 0.f, 0.f};
-        f.h[2 * i + 1] = uok[0] ? *(const float4*)(hp + 32 * i + 4) : float4{0.f, 0.f, 0.f, 0.f};
-      }
-    } else {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          f.u[mb][i] = uok[mb] ? *(const uint4*)((const f16*)xin + uoff[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
-    }
-  };
-  auto consume = [&](const Frag<RB, MB, NRM>& f) {
-    if constexpr (NRM) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 a = f.h[2 * i], b = f.h[2 * i + 1];
-        ss = fmaf(a.x, a.x, ss); ss = fmaf(a.y, a.y, ss); ss = fmaf(a.z, a.z, ss); ss = fmaf(a.w, a.w, ss);
-        ss = fmaf(b.x, b.x, ss); ss = fmaf(b.y, b.y, ss); ss = fmaf(b.z, b.z, ss); ss = fmaf(b.w, b.w, ss);
-        half8 v;
-        v[0] = (f16)fminf(fmaxf(a.x, -F16_MAX), F16_MAX); v[1] = (f16)fminf(fmaxf(a.y, -F16_MAX), F16_MAX);
-        v[2] = (f16)fminf(fmaxf(a.z, -F16_MAX), F16_MAX); v[3] = (f16)fminf(fmaxf(a.w, -F16_MAX), F16_MAX);
-        v[4] = (f16)fminf(fmaxf(b.x, -F16_MAX), F16_MAX); v[5] = (f16)fminf(fmaxf(b.y, -F16_MAX), F16_MAX);
-        v[6] = (f16)fminf(fmaxf(b.z, -F16_MAX), F16_MAX); v[7] = (f16)fminf(fmaxf(b.w, -F16_MAX), F16_MAX);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          acc[rb][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(f.w[rb][i]), v, acc[rb][0], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(f.w[rb][i]), as_half8(f.u[mb][i]),
-                                                                  acc[rb][mb], 0, 0, 0);
-    }
-  };
 
   // the residual epilogue's h values do not depend on this kernel: request them first
   constexpr int EPT = (MB * 256 + 63) / 64;  // epilogue values per thread at the smallest workgroup
@@ -143,15 +89,42 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
   }
 
   // chunks in flight per wave: up to CPW loads are issued before the first MFMA
-  constexpr int CPW = (!NRM && RB + MB <= 2) ? 4 : 2;
-  Frag<RB, MB, NRM> fr[CPW];
+  constexpr int CPW = RB + MB <= 2 ? 4 : 2;
+  uint4 fw[CPW][RB][4], fu[CPW][MB][4];
   for (int cb = c0; cb < c1; cb += CPW) {
 #pragma unroll
-    for (int j = 0; j < CPW; ++j)
-      if (cb + j < c1) load(fr[j], cb + j);
+    for (int j = 0; j < CPW; ++j) {
+      if (cb + j < c1) {
+        const int kb = (cb + j) << 7;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j)
-      if (cb + j < c1) consume(fr[j]);
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) fw[j][rb][i] = *(const uint4*)(wrow[rb] + kb + 32 * i);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            fu[j][mb][i] = uok[mb] ? *(const uint4*)(urow[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      if (cb + j < c1) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const half8 v = as_half8(fu[j][mb][i]);
+            if constexpr (NRM) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) ss = fmaf((float)v[e], (float)v[e], ss);
+            }
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+              acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(fw[j][rb][i]), v, acc[rb][mb], 0, 0, 0);
+          }
+      }
+    }
   }
 
 #pragma unroll
@@ -197,8 +170,12 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
       for (int rb = 0; rb < RB; ++rb) ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] = v[rb];
     } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] = hres[rb * EPT + e] + v[rb];
+      for (int rb = 0; rb < RB; ++rb) {
+        const size_t o = (size_t)tok * ldo + n0 + rb * 16 + row;
+        const float hn = hres[rb * EPT + e] + v[rb];
+        ((float*)out)[o] = hn;
+        if (out16) st<f16>(out16, o, hn);
+      }
     } else {
       st<f16>((f16*)out, (size_t)tok * ldo + (n0 >> 1) + row, silu(v[0]) * v[RB - 1]);
     }
@@ -206,25 +183,26 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const void* __restrict__ xi
 }
 
 template <int RB, int MB, int EPI, bool NRM>
-static hipError_t launch_skinny(const void* x, float eps, const f16* W, int M, int N, int K, void* out, int ldo,
-                                hipStream_t s) {
+static hipError_t launch_skinny(const f16* x, float eps, const f16* W, int M, int N, int K, void* out, int ldo,
+                                f16* out16, hipStream_t s) {
   const int nchunks = K >> 7;
-  int nw = 8;  // <= 512 threads: leaves 256 VGPRs for the two chunks in flight
+  int nw = 8;  // <= 512 threads: leaves 256 VGPRs for the chunks in flight
   while (nw > 1 && nw * RB * MB * 1024 > 65536) nw >>= 1;
   while (nw > 1 && nw > nchunks) nw >>= 1;
   const size_t lds = (size_t)nw * RB * MB * 1024 + (NRM ? (256 + 16) * 4 : 0);
   hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM>), dim3(N / (RB * 16)), dim3(64 * nw), lds, s, x, eps, W, M,
-                     K, out, ldo);
+                     K, out, ldo, out16);
   return hipGetLastError();
 }
 
 template <int EPI>
-static hipError_t skinny_mb(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {
+static hipError_t skinny_mb(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, f16* out16,
+                            hipStream_t s) {
   constexpr int RB = EPI == EPI_SWIGLU ? 2 : 1;
-  if (M <= 16) return launch_skinny<RB, 1, EPI, false>(u, 0.f, W, M, N, K, out, ldo, s);
-  if (M <= 32) return launch_skinny<RB, 2, EPI, false>(u, 0.f, W, M, N, K, out, ldo, s);
-  if (M <= 48) return launch_skinny<RB, 3, EPI, false>(u, 0.f, W, M, N, K, out, ldo, s);
-  return launch_skinny<RB, 4, EPI, false>(u, 0.f, W, M, N, K, out, ldo, s);
+  if (M <= 16) return launch_skinny<RB, 1, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
+  if (M <= 32) return launch_skinny<RB, 2, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
+  if (M <= 48) return launch_skinny<RB, 3, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
+  return launch_skinny<RB, 4, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
 }
 
 // ----------------------------------------------------------------------------
@@ -395,36 +373,41 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 
 template <int EPI>
 static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, int K, void* out, int ldo,
-                           hipStream_t s) {
+                           void* out16, hipStream_t s) {
+  // the fp16 residual copy is produced by the decode GEMV only
+  if (out16 && (EPI != EPI_RESID || ct != DT_F16 || M > 64)) return hipErrorInvalidValue;
   if (ct == DT_F32) {
     hipLaunchKernelGGL((k_gemm_f32<EPI>), dim3(N / FBN, (M + FBM - 1) / FBM), dim3(256), 0, s,
                        (const float*)u, (const float*)W, M, K, out, ldo);
     return hipGetLastError();
   }
-  if (M <= 64) return skinny_mb<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+  if (M <= 64) return skinny_mb<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, (f16*)out16, s);
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
 }
 
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo,
-                hipStream_t s) {
+                hipStream_t s, void* out16) {
   if (M <= 0) return hipSuccess;
   switch (epi) {
-    case EPI_STORE: return gemm_epi<EPI_STORE>(ct, u, W, M, N, K, out, ldo, s);
-    case EPI_RESID: return gemm_epi<EPI_RESID>(ct, u, W, M, N, K, out, ldo, s);
-    default: return gemm_epi<EPI_SWIGLU>(ct, u, W, M, N, K, out, ldo, s);
+    case EPI_STORE: return gemm_epi<EPI_STORE>(ct, u, W, M, N, K, out, ldo, out16, s);
+    case EPI_RESID: return gemm_epi<EPI_RESID>(ct, u, W, M, N, K, out, ldo, out16, s);
+    default: return gemm_epi<EPI_SWIGLU>(ct, u, W, M, N, K, out, ldo, out16, s);
   }
 }
 
-hipError_t gemv_rmsnorm(int ct, int epi, const float* h, float eps, const void* W, int M, int N, int K, void* out,
-                        int ldo, hipStream_t s) {
+hipError_t gemv_rmsnorm(int ct, int epi, const void* h16, float eps, const void* W, int M, int N, int K, void* out,
+                        int ldo, hipStream_t s, void* out16) {
   if (M <= 0) return hipSuccess;
   if (ct != DT_F16 || M > 16) return hipErrorInvalidValue;
+  if (out16 && epi != EPI_RESID) return hipErrorInvalidValue;
+  const f16* x = (const f16*)h16;
+  const f16* w = (const f16*)W;
   switch (epi) {
-    case EPI_STORE: return launch_skinny<1, 1, EPI_STORE, true>(h, eps, (const f16*)W, M, N, K, out, ldo, s);
-    case EPI_RESID: return launch_skinny<1, 1, EPI_RESID, true>(h, eps, (const f16*)W, M, N, K, out, ldo, s);
-    default: return launch_skinny<2, 1, EPI_SWIGLU, true>(h, eps, (const f16*)W, M, N, K, out, ldo, s);
+    case EPI_STORE: return launch_skinny<1, 1, EPI_STORE, true>(x, eps, w, M, N, K, out, ldo, nullptr, s);
+    case EPI_RESID: return launch_skinny<1, 1, EPI_RESID, true>(x, eps, w, M, N, K, out, ldo, (f16*)out16, s);
+    default: return launch_skinny<2, 1, EPI_SWIGLU, true>(x, eps, w, M, N, K, out, ldo, nullptr, s);
   }
 }
 

@@ -35,22 +35,26 @@ constexpr int GU_BLOCK = 16;
 //   EPI_STORE : out_f32[m*ldo + n] = y
 //   EPI_RESID : out_f32[m*ldo + n] += y          (residual stream)
 //   EPI_SWIGLU: out_T[m*ldo + c] = silu(gate_c) * up_c with W packed as above
+// out16 (fp16 compute, EPI_RESID, M <= 64 only; NULL otherwise): the updated
+// residual rows are also written there as fp16 (saturating), same ldo.
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out,
-                int ldo, hipStream_t s);
+                int ldo, hipStream_t s, void* out16 = nullptr);
 
-// Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16):
-// y[m] = (W fp16(h[m])) / sqrt(mean(h[m]^2) + eps), followed by the epilogue as
-// in gemm().  W carries the RMSNorm gain (folded at packing); fp16(h) saturates
-// at +-65504.
-hipError_t gemv_rmsnorm(int ct, int epi, const float* h, float eps, const void* W, int M, int N, int K, void* out,
-                        int ldo, hipStream_t s);
+// Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16), on the fp16
+// copy x = fp16(h) of the residual rows:
+// y[m] = (W x[m]) / sqrt(mean(x[m]^2) + eps), followed by the epilogue as in
+// gemm() (out16 as there, EPI_RESID only).  W carries the RMSNorm gain (folded
+// at packing).
+hipError_t gemv_rmsnorm(int ct, int epi, const void* h16, float eps, const void* W, int M, int N, int K, void* out,
+                        int ldo, hipStream_t s, void* out16 = nullptr);
 
 // Per row b: argmax over logits[b][0..n_bins) (lowest index on ties) -> out_tok[b*A+j],
 // logits copied to out_logits[b][j] (if non-NULL); when feed, h[b] = bin_embed[t]
-// with t the argmax or the clamped forced[b*A+j].
+// with t the argmax or the clamped forced[b*A+j], and (if h16 is non-NULL, fp16
+// compute only) h16[b] = the same row in fp16.
 hipError_t argmax_feed(int ct, const float* logits, int ld_logits, const void* bin_embed, int B, int d, int n_bins,
                        int A, int j, int32_t* out_tok, float* out_logits, const int32_t* forced, float* h, int feed,
-                       hipStream_t s);
+                       hipStream_t s, void* h16 = nullptr);
 
 // u[m] = h[m] / sqrt(mean(h[m]^2) + eps), written in the compute type (the
 // gain is folded into the weights that consume u).
@@ -96,8 +100,9 @@ hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, 
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
                       hipStream_t s);
 
-// h_last[row[s]] = h[off[s+1]-1] for each segment.
-hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s);
+// h_last[row[s]] = h[off[s+1]-1] for each segment, and the same rows as fp16
+// (saturating) into h_last16 when it is non-NULL.
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16 = nullptr);
 
 // lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);

@@ -156,17 +156,21 @@ hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s) 
 
 __global__ __launch_bounds__(256) void k_gather_last(const float* __restrict__ h, const int32_t* __restrict__ row,
                                                      const int32_t* __restrict__ off, int d,
-                                                     float* __restrict__ h_last) {
+                                                     float* __restrict__ h_last, f16* __restrict__ h_last16) {
   const int sidx = blockIdx.x;
   const int last = off[sidx + 1] - 1;
   const float* src = h + (size_t)last * d;
-  float* dst = h_last + (size_t)row[sidx] * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = src[i];
+  const size_t o = (size_t)row[sidx] * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = src[i];
+    h_last[o + i] = v;
+    if (h_last16) st<f16>(h_last16, o + i, v);
+  }
 }
 
-hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s) {
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16) {
   if (sg.n_seg <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather_last, dim3(sg.n_seg), dim3(256), 0, s, h, sg.row, sg.off, d, h_last);
+  hipLaunchKernelGGL(k_gather_last, dim3(sg.n_seg), dim3(256), 0, s, h, sg.row, sg.off, d, h_last, (f16*)h_last16);
   return hipGetLastError();
 }
 

@@ -88,11 +88,22 @@ def test_gemm(probe, dtype, epi, M, K):
         h0 = W.random_gaussian((M, N), 3, M, dtype="f32")
         out = torch.from_numpy(h0.copy() if epi == EPI_RESID else np.zeros_like(h0)).cuda()
         ldo = N
+    # the decode GEMV (fp16, M <= 64) can also write the fp16 copy of updated residual rows
+    with16 = epi == EPI_RESID and dtype == "f16" and M <= 64
+    out16 = torch.full((M, N), 7.0, dtype=torch.float16, device="cuda") if with16 else None
     rc = probe.ams_probe_gemm(CT[dtype], epi, C.c_void_p(ud.data_ptr()), C.c_void_p(Wd.data_ptr()),
-                              M, N, K, C.c_void_p(out.data_ptr()), ldo, _stream())
+                              M, N, K, C.c_void_p(out.data_ptr()), ldo,
+                              C.c_void_p(out16.data_ptr() if with16 else None), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().astype(np.float64)
+    if with16:
+        assert torch.equal(out16, out.half()), "fp16 residual copy differs from the fp32 rows"
+    elif dtype == "f32" or epi != EPI_RESID or M > 64:
+        # any other configuration rejects the fp16 copy before launching
+        spare = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        assert probe.ams_probe_gemm(CT[dtype], epi, C.c_void_p(ud.data_ptr()), C.c_void_p(Wd.data_ptr()), M, N, K,
+                                    C.c_void_p(out.data_ptr()), ldo, C.c_void_p(spare.data_ptr()), _stream()) != 0
     if epi == EPI_STORE:
         ref = y
     elif epi == EPI_RESID:
@@ -144,55 +155,64 @@ def test_argmax_feed_ties(probe, dtype, n_bins):
     out = torch.zeros((B, A, n_bins), dtype=torch.float32, device="cuda")
     forced = torch.tensor([[0, 5, 0], [0, n_bins + 7, 0], [0, -3, 0], [0, 2, 0]], dtype=torch.int32, device="cuda")
     h = torch.zeros((B, d), dtype=torch.float32, device="cuda")
+    h16 = torch.zeros((B, d), dtype=torch.float16, device="cuda") if dtype == "f16" else None
     ref = np.argmax(lg[:, :n_bins], axis=-1)
     assert list(ref[:3]) == [3, n_bins - 2, 0]
     for use_forced in (False, True):
         rc = probe.ams_probe_argmax_feed(CT[dtype], C.c_void_p(lgd.data_ptr()), ldl, C.c_void_p(embd.data_ptr()), B, d,
                                          n_bins, A, j, C.c_void_p(tok.data_ptr()), C.c_void_p(out.data_ptr()),
                                          C.c_void_p(forced.data_ptr() if use_forced else None),
-                                         C.c_void_p(h.data_ptr()), 1, _stream())
+                                         C.c_void_p(h.data_ptr()), 1,
+                                         C.c_void_p(h16.data_ptr() if h16 is not None else None), _stream())
         assert rc == 0
         torch.cuda.synchronize()
         assert np.array_equal(tok[:, j].cpu().numpy(), ref)
         assert np.array_equal(out[:, j].cpu().numpy(), lg[:, :n_bins])
         feed = forced[:, j].cpu().numpy().clip(0, n_bins - 1) if use_forced else ref
         assert np.array_equal(h.cpu().numpy(), _f(emb, dtype)[feed].astype(np.float32))
+        if h16 is not None:
+            assert np.array_equal(h16.cpu().numpy(), emb[feed])
 
 
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
 @pytest.mark.parametrize("M", [1, 5, 16])
 @pytest.mark.parametrize("K", [256, 1024, 4096])
 def test_gemv_rmsnorm(probe, epi, M, K):
-    """Fused RMSNorm GEMV: y = W (h / rms(h)) computed as (W fp16(h)) / rms(h); checked against
-    the exact product with a bound built from the fp16 rounding of h (2^-11 relative)."""
+    """Fused RMSNorm GEMV on the fp16 residual copy x: y = W (x / rms(x)) with the statistic
+    from the same fp16 values; fp16 products are exact in the fp32 accumulator, so the bound
+    is the accumulation (and, for SwiGLU, the fp16 output rounding)."""
     import torch
     N, eps = 256, 1e-5
-    h = W.random_gaussian((M, K), 21, M, K, dtype="f32") * 4.0
+    log(f"gemv_rmsnorm epi={epi} M={M} K={K}")
+    x = (W.random_gaussian((M, K), 21, M, K, dtype="f32") * 4.0).astype(np.float16)
     Wt = _rand((N, K), 23, K, dtype="f16", std=0.05)
-    h64 = h.astype(np.float64)
-    rs = 1.0 / np.sqrt(np.mean(h64 * h64, axis=-1, keepdims=True) + eps)
-    W64 = _f(Wt, "f16")
-    y = (h64 * rs) @ W64.T
-    # per-output scale of the rounding error: 2^-11 * sqrt(sum_k (W u)^2)
-    scale = 2.0 ** -11 * np.sqrt(((h64 * rs) ** 2) @ (W64 ** 2).T)
+    x64 = x.astype(np.float64)
+    rs = 1.0 / np.sqrt(np.mean(x64 * x64, axis=-1, keepdims=True) + eps)
+    y = (x64 * rs) @ _f(Wt, "f16").T
+    with16 = epi == EPI_RESID
     if epi == EPI_SWIGLU:
         out = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
         ldo = N // 2
         gg, up = _unpack_gu(y.T, N // 2)
-        sg, su = _unpack_gu(scale.T, N // 2)
         ref = (_silu(gg) * up).T
-        # d(silu(g) u) = silu'(g) u dg + silu(g) du, with |silu'| <= 1.1
-        scale = (1.1 * np.abs(up) * sg + np.abs(_silu(gg)) * su).T + 2.0 ** -11 * np.abs(ref)
     else:
         h0 = W.random_gaussian((M, N), 24, M, dtype="f32")
         out = torch.from_numpy(h0.copy() if epi == EPI_RESID else np.zeros_like(h0)).cuda()
         ldo = N
         ref = y + (h0 if epi == EPI_RESID else 0.0)
-    hd, wd = torch.from_numpy(h).cuda(), _dev(Wt, "f16")  # keep both alive across the launch
-    rc = probe.ams_probe_gemv_rmsnorm(2, epi, C.c_void_p(hd.data_ptr()), C.c_float(eps), C.c_void_p(wd.data_ptr()),
-                                      M, N, K, C.c_void_p(out.data_ptr()), ldo, _stream())
+    out16 = torch.zeros((M, N), dtype=torch.float16, device="cuda") if with16 else None
+    xd, wd = torch.from_numpy(x).cuda(), _dev(Wt, "f16")  # keep both alive across the launch
+    rc = probe.ams_probe_gemv_rmsnorm(2, epi, C.c_void_p(xd.data_ptr()), C.c_float(eps), C.c_void_p(wd.data_ptr()),
+                                      M, N, K, C.c_void_p(out.data_ptr()), ldo,
+                                      C.c_void_p(out16.data_ptr() if with16 else None), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().astype(np.float64)
-    err = np.abs(got - ref)
-    assert np.all(err <= 6.0 * scale + 1e-5), float(np.max(err / (scale + 1e-12)))
+    scale = max(1.0, float(np.max(np.abs(ref))))
+    tol = 2e-5 * scale * np.sqrt(K / 128)
+    if epi == EPI_SWIGLU:
+        tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
+    err = float(np.max(np.abs(got - ref)))
+    assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
+    if with16:
+        assert torch.equal(out16, out.half())
