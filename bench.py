@@ -71,20 +71,28 @@ def time_gate_up_kernel(model, B, iters=240):
     # packed layout of the model workspace: [wqkv | wo | wgu | ...], each region 256-byte aligned
     align = lambda x: (x + 255) // 256 * 256
     w_gu = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
-    h16 = (torch.randn((B, d), device="cuda") * 30.0).half()  # fp16 copy of the residual rows
-    u = torch.randn((B, d), device="cuda").half()
+    # the decode pass's form: inputs and SwiGLU output as fp16 pairs (hi + rounding error)
+    h = torch.randn((B, d), device="cuda") * 30.0
+    hhi = h.half()
+    hlo = (h - hhi.float()).half()
+    u = torch.randn((B, d), device="cuda")
+    uhi = u.half()
+    ulo = (u - uhi.float()).half()
     a = torch.empty((B, F), device="cuda", dtype=torch.float16)
+    alo = torch.empty((B, F), device="cuda", dtype=torch.float16)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def launch(l):
         w = C.c_void_p(w_gu + (l % spec.n_layers) * 2 * F * d * es)
         if B <= 16:  # the decode pass fuses the RMSNorm up to 16 rows
-            lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(h16.data_ptr()), C.c_float(spec.rms_eps), w, B, 2 * F, d,
-                                       C.c_void_p(a.data_ptr()), F, C.c_void_p(None), C.c_void_p(s.cuda_stream))
+            lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(hhi.data_ptr()), C.c_void_p(hlo.data_ptr()),
+                                       C.c_float(spec.rms_eps), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
+                                       C.c_void_p(None), C.c_void_p(alo.data_ptr()), C.c_void_p(s.cuda_stream))
         else:
-            lib.ams_probe_gemm(2, 2, C.c_void_p(u.data_ptr()), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
-                               C.c_void_p(None), C.c_void_p(s.cuda_stream))
+            lib.ams_probe_gemm(2, 2, C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
+                               C.c_void_p(a.data_ptr()), F, C.c_void_p(None), C.c_void_p(alo.data_ptr()),
+                               C.c_void_p(s.cuda_stream))
     with torch.cuda.stream(s):
         for l in range(24):
             launch(l)

@@ -113,60 +113,72 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
     TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, fused_norm(c) ? c.h_last16() : nullptr));
+    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, fused_norm(c) ? c.h_last16() : nullptr,
+                    fused_norm(c) ? c.h_last16lo() : nullptr));
   }
   TRY(update_lens(c.lens(), md + 4 * B + 1, B, set_lens, s));
   return hipSuccess;
 }
 
-// Projection of a normalised input in the decode pass.  Up to 16 fp16 rows run
-// the GEMV with the RMSNorm fused, reading h16, the fp16 copy of the residual
-// rows that their producers (residual GEMV epilogue, feed, gather of the last
-// prefix token) write beside h; otherwise rmsnorm writes u from h first.
-static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* h16, const void* W, int N, int K, void* out,
-                            int ldo, hipStream_t s, std::string& err) {
+// Decode-pass GEMV inputs are fp16 pairs (hi + lo, lo the rounding error of
+// hi) in fp16 compute, so the action tokens' own products see their inputs to
+// about 22 significant bits; the MFMA count doubles at most, the weight stream
+// (the bound) does not change.
+//
+// Projection of a normalised input.  Up to 16 fp16 rows run the GEMV with the
+// RMSNorm fused, reading the fp16 pair of the residual rows (hhi, hlo) that
+// their producers (residual GEMV epilogue, feed, gather of the last prefix
+// token) write beside h; otherwise rmsnorm writes the pair u + hlo from h
+// first (the fused copies are unused then, so hlo serves as u's lo part).
+static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* hhi, const void* hlo, const void* W, int N,
+                            int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const int B = c.lay.batch;
   const float eps = md.cfg.rms_eps;
   if (fused_norm(c)) {
-    TRY(gemv_rmsnorm(md.ct, epi, h16, eps, W, B, N, K, out, ldo, s));
+    TRY(gemv_rmsnorm(md.ct, epi, hhi, eps, W, B, N, K, out, ldo, s, hlo, nullptr, olo));
   } else {
-    TRY(rmsnorm(md.ct, h, B, K, eps, c.u(), s));
-    TRY(gemm(md.ct, epi, c.u(), W, B, N, K, out, ldo, s));
+    void* ulo = md.ct == DT_F16 ? c.hlo() : nullptr;
+    TRY(rmsnorm(md.ct, h, B, K, eps, c.u(), s, ulo));
+    TRY(gemm(md.ct, epi, c.u(), W, B, N, K, out, ldo, s, ulo, nullptr, olo));
   }
   return hipSuccess;
 }
 
-// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.  In
-// the fused-RMSNorm path u holds the fp16 copy of h during decode.
+// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.
 static hipError_t layer_decode(Ctx& c, int l, int jpos, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   const int d = m.d_model, F = m.d_ffn, dt = md.ct, B = c.lay.batch;
-  void* h16 = fused_norm(c) ? c.u() : nullptr;
-  if (norm_proj(c, EPI_STORE, c.h(), h16, md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, s, err) != hipSuccess)
+  const bool f16 = dt == DT_F16, fused = fused_norm(c);
+  void* hhi = fused ? c.u() : nullptr;   // fp16 pair of h (fused path)
+  void* hlo = fused ? c.hlo() : nullptr;
+  void* olo = f16 ? c.olo() : nullptr;   // lo parts of the attention and SwiGLU outputs
+  void* alo = f16 ? c.alo() : nullptr;
+  if (norm_proj(c, EPI_STORE, c.h(), hhi, hlo, md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, nullptr, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, c.qkv(), c.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
-                  c.kslab(l), c.vslab(l), c.part(), c.o(), s));
-  if (c.splits > 1) TRY(attn_merge(dt, c.part(), B, m.n_heads, m.head_dim, c.splits, c.o(), s));
-  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s, h16));
-  if (norm_proj(c, EPI_SWIGLU, c.h(), h16, md.wgu(l), 2 * F, d, c.a(), F, s, err) != hipSuccess)
+                  c.kslab(l), c.vslab(l), c.part(), c.o(), s, olo));
+  if (c.splits > 1) TRY(attn_merge(dt, c.part(), B, m.n_heads, m.head_dim, c.splits, c.o(), s, olo));
+  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s, olo, hhi, hlo));
+  if (norm_proj(c, EPI_SWIGLU, c.h(), hhi, hlo, md.wgu(l), 2 * F, d, c.a(), F, alo, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s, h16));
+  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s, alo, hhi, hlo));
   return hipSuccess;
 }
 
 // Action head for decode position j: final RMSNorm + bin logits (the
 // projection GEMV over the padded head rows), then argmax/outputs/feed.
-static hipError_t head(Ctx& c, const float* hin, const void* hin16, int A, int j, int32_t* tok, float* logits,
-                       const int32_t* forced, hipStream_t s, std::string& err) {
+static hipError_t head(Ctx& c, const float* hin, const void* hhi, const void* hlo, int A, int j, int32_t* tok,
+                       float* logits, const int32_t* forced, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   const int B = c.lay.batch, d = m.d_model, nbp = bins_padded(m);
-  if (norm_proj(c, EPI_STORE, hin, hin16, md.head_bins(), nbp, d, c.logits(), nbp, s, err) != hipSuccess)
+  const bool fused = fused_norm(c);
+  if (norm_proj(c, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, c.logits(), nbp, nullptr, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(argmax_feed(md.ct, c.logits(), nbp, md.bin_embed(), B, d, m.n_bins, A, j, tok, logits, forced, c.h(),
-                  j + 1 < A, s, fused_norm(c) ? c.u() : nullptr));
+                  j + 1 < A, s, fused ? c.u() : nullptr, fused ? c.hlo() : nullptr));
   return hipSuccess;
 }
 
@@ -174,12 +186,14 @@ static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, con
                                  std::string& err) {
   const Cfg& m = c.model->cfg;
   const bool fused = fused_norm(c);
-  if (head(c, c.h_last(), fused ? c.h_last16() : nullptr, A, 0, tok, logits, forced, s, err) != hipSuccess)
+  if (head(c, c.h_last(), fused ? c.h_last16() : nullptr, fused ? c.h_last16lo() : nullptr, A, 0, tok, logits,
+           forced, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
   for (int j = 1; j < A; ++j) {
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_decode(c, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    if (head(c, c.h(), fused ? c.u() : nullptr, A, j, tok, logits, forced, s, err) != hipSuccess)
+    if (head(c, c.h(), fused ? c.u() : nullptr, fused ? c.hlo() : nullptr, A, j, tok, logits, forced, s, err) !=
+        hipSuccess)
       return hipErrorLaunchFailure;
   }
   return hipSuccess;

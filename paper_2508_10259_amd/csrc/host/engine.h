@@ -67,6 +67,10 @@ struct Ctx {
   void* a() const { return ws + lay.a; }
   float* h_last() const { return (float*)(ws + lay.h_last); }
   void* h_last16() const { return ws + lay.h_last16; }
+  void* h_last16lo() const { return ws + lay.h_last16lo; }
+  void* hlo() const { return ws + lay.hlo; }
+  void* olo() const { return ws + lay.olo; }
+  void* alo() const { return ws + lay.alo; }
   float* part() const { return (float*)(ws + lay.part); }
   float* logits() const { return (float*)(ws + lay.logits); }
   float2* rope() const { return (float2*)(ws + lay.rope); }

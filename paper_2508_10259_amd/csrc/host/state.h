@@ -76,7 +76,7 @@ inline ModelLayout model_layout(const Cfg& c) {
 struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
   size_t slab_layer;  // bytes of K (or V) for one layer
-  size_t kv, h, u, qkv, o, a, h_last, h_last16, part, logits, rope, lens, meta, total;
+  size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, part, logits, rope, lens, meta, total;
   size_t meta_ints;
 };
 
@@ -117,7 +117,13 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.o = o; o = align256(o + T * d * es);
   x.a = o; o = align256(o + T * F * es);
   x.h_last = o; o = align256(o + B * d * 4);
-  x.h_last16 = o; o = align256(o + B * d * 2);  // fp16 copy for the fused-RMSNorm head
+  // decode-pass fp16 pairs (hi, lo = rounding error of hi): hi of h lives in u,
+  // hi of the attention / SwiGLU outputs in o / a; the lo parts here
+  x.h_last16 = o; o = align256(o + B * d * 2);
+  x.h_last16lo = o; o = align256(o + B * d * 2);
+  x.hlo = o; o = align256(o + B * d * 2);
+  x.olo = o; o = align256(o + B * d * 2);
+  x.alo = o; o = align256(o + B * F * 2);
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
@@ -233,14 +239,16 @@ inline Plan plan_passes(int batch, const int32_t* counts, const int32_t* start, 
 }
 
 // Key splits of the decode attention.  One workgroup per (row, head) covers
-// the whole context when there are >= 128 of them; fewer pairs with long
-// contexts split the keys (>= 256 positions per split) and merge by
-// log-sum-exp in a second kernel.
+// the row's keys in rounds of up to 8 waves x one key block; a split costs a
+// second (merge) kernel of a few microseconds, which only pays when there are
+// few (row, head) pairs and each would need many rounds: fewer than 128 pairs
+// and a capacity above 2048 positions split into parts of at least 1024, for
+// about 256 workgroups in all.
 inline int decode_splits(int batch, int n_heads, int capacity) {
   const int pairs = batch * n_heads;
-  if (pairs >= 128) return 1;
-  const int s = (128 + pairs - 1) / pairs;
-  return std::max(1, std::min(s, capacity / 256));
+  if (pairs >= 128 || capacity <= 2048) return 1;
+  const int s = (256 + pairs - 1) / pairs;
+  return std::max(1, std::min(s, capacity / 1024));
 }
 
 }  // namespace ams

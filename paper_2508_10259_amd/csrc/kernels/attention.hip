@@ -12,11 +12,17 @@
 //                     runs both products on MFMA.
 //  * k_attn_decode:   one query per row at position p = lens[b] + jpos (a
 //                     fed-back action token).  Appends its own K/V, then
-//                     each workgroup covers one split of the keys: lane-per-key
-//                     scores, wavefront-shuffle online softmax, and a P.V
-//                     pass with lanes over (key subgroup, 8-dim chunk).  The
-//                     split partials (m, l, acc) are merged by k_attn_merge
-//                     with log-sum-exp weights.
+//                     each workgroup covers one split of the row's keys 0..p
+//                     (split by the actual length, so no workgroup idles on
+//                     unused capacity) and each of its waves a block of keys
+//                     at a time.  Lanes are laid over (key, 16-byte chunk of
+//                     the head dimension) for both K and V, so every load is
+//                     row-contiguous; a score is a chunk dot product summed
+//                     over the key's lanes with DPP, the online softmax runs
+//                     on wavefront shuffles, and each lane keeps the weights
+//                     of its own keys for P.V.  The split partials (m, l,
+//                     acc) are merged by k_attn_merge with log-sum-exp
+//                     weights.
 #include "common.h"
 #include "kernels.h"
 
@@ -387,161 +393,182 @@ template <> struct Raw<float> {
   }
 };
 
-// Waves per decode workgroup: 8 for 64-wide heads (one round covers 512
-// positions), 4 for 128-wide heads (their K/V fragments need twice the registers).
-template <int DH> constexpr int decode_waves() { return DH == 64 ? 8 : 4; }
+// Output element of the decode kernels: fp16 outputs also give their rounding
+// error to olo when it is non-NULL.
+template <typename T> __device__ __forceinline__ void st_out(T* o, T* olo, size_t i, float v) {
+  if constexpr (sizeof(T) == 2) split16(v, o, olo, i);
+  else o[i] = v;
+}
+
+// Decode lane geometry.  A lane holds one 16-byte chunk (CH elements) of the
+// head dimension for one key: NC lanes cover a key, a wave covers KS keys per
+// iteration and BK keys per block (IT iterations), so K and V loads are both
+// row-contiguous across each group of NC lanes.
+template <typename T, int DH> struct DecGeo {
+  static constexpr int CH = Raw<T>::E;
+  static constexpr int NC = DH / CH;
+  static constexpr int KS = 64 / NC;
+  static constexpr int BK = 8 * KS;
+  static constexpr int IT = BK / KS;
+};
+// at most 8 waves (512 threads) per decode workgroup; a launch may use fewer
+constexpr int DECODE_MAX_WAVES = 8;
+
+// Sum over each aligned group of N lanes (N <= 32), every lane of a group
+// receiving its total: DPP quad permutes for distances 1 and 2, half-row and
+// row mirrors for 4 and 8 (their partner lanes hold equal partial sums by
+// then), a lane shuffle for 16.
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int N> __device__ __forceinline__ float group_sum(float v) {
+  if constexpr (N >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+  if constexpr (N >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+  if constexpr (N >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror
+  if constexpr (N >= 16) v += dpp_mov<0x140>(v); // row_mirror
+  if constexpr (N >= 32) v += __shfl_xor(v, 16, 64);
+  return v;
+}
+
+// Max / sum across the lane groups of size N (values uniform within a group).
+template <int N> __device__ __forceinline__ float cross_max(float v) {
+#pragma unroll
+  for (int o = N; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+template <int N> __device__ __forceinline__ float cross_sum(float v) {
+#pragma unroll
+  for (int o = N; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
 
 template <typename T, int DH>
-__global__ __launch_bounds__(64 * decode_waves<DH>()) void k_attn_decode(const float* __restrict__ qkv, const int32_t* __restrict__ lens,
-                                                     int jpos, int H, int cap, int splits,
-                                                     const float2* __restrict__ rope, T* __restrict__ kslab,
-                                                     T* __restrict__ vslab, float* __restrict__ part,
-                                                     T* __restrict__ o, float scale) {
-  constexpr int HALF = DH / 2, NC = DH / 8, KS = 64 / NC;  // dim chunks of 8; key subgroups per wave
-  constexpr int E = Raw<T>::E, KR = DH / E, VI = 64 / KS, VR = 8 / E;
-  constexpr int NWV = decode_waves<DH>();
-  __shared__ float qs[DH], kn[DH], vn[DH];
-  __shared__ float wm[NWV], wl[NWV], wacc[NWV][DH];
+__global__ __launch_bounds__(64 * DECODE_MAX_WAVES) void k_attn_decode(
+    const float* __restrict__ qkv, const int32_t* __restrict__ lens, int jpos, int H, int cap, int splits,
+    const float2* __restrict__ rope, T* __restrict__ kslab, T* __restrict__ vslab, float* __restrict__ part,
+    T* __restrict__ o, T* __restrict__ olo, float scale) {
+  using G = DecGeo<T, DH>;
+  constexpr int CH = G::CH, NC = G::NC, KS = G::KS, BK = G::BK, IT = G::IT, HALF = DH / 2;
+  __shared__ float wm[DECODE_MAX_WAVES], wl[DECODE_MAX_WAVES], wacc[DECODE_MAX_WAVES][DH];
   const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int ks = lane / NC, dc = lane % NC, i0 = dc * CH;  // this lane: key subgroup, first dimension
   const int d = H * DH;
   const int p = lens[b] + jpos;  // position of this pass's token
   const int T_ = p + 1;          // keys 0..p
-  const int chunk = (cap + splits - 1) / splits;
-  const int k0 = sp * chunk;
+  const int chunk = (T_ + splits - 1) / splits;
+  const int k0 = sp * chunk < T_ ? sp * chunk : T_;
   const int k1 = (k0 + chunk < T_) ? k0 + chunk : T_;
-  const float* qrow = qkv + (size_t)b * 3 * d + h * DH;
 
   const size_t bh = ((size_t)b * H + h) * cap;
-  const T* Kb = kslab + bh * DH;
-  const T* Vb = vslab + bh * DH;
-  const int ks = lane / NC, dc = lane % NC;
-  uint4 kraw[KR];
-  uint4 vraw[VI][VR];
-  // one block's K row (lane = key) and V chunks (lane = key subgroup x dim chunk)
+  const T* Kb = kslab + bh * DH + i0;
+  const T* Vb = vslab + bh * DH + i0;
+  uint4 kr[IT], vr[IT];
+  // one block: key kb + it*KS + ks of each iteration; slot p is not read (its K/V come from registers)
   auto load_block = [&](int kb) {
-    const int key = kb + lane;
-    if (key < k1 && key != p) {
-      const uint4* kr = (const uint4*)(Kb + (size_t)key * DH);
 #pragma unroll
-      for (int i = 0; i < KR; ++i) kraw[i] = kr[i];
-    }
-#pragma unroll
-    for (int it = 0; it < VI; ++it) {
-      const int kk = kb + it * KS + ks;
-      if (kk < k1 && kk != p) {
-        const uint4* vr = (const uint4*)(Vb + (size_t)kk * DH + dc * 8);
-#pragma unroll
-        for (int r = 0; r < VR; ++r) vraw[it][r] = vr[r];
-      }
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
+      const bool ok = key < k1 && key != p;
+      kr[it] = ok ? *(const uint4*)(Kb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
+      vr[it] = ok ? *(const uint4*)(Vb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
     }
   };
-  // the first block's loads go out before the prologue, overlapping it
-  const int kb0 = k0 + wave * 64;
-  if (kb0 < k1) load_block(kb0);
+  const int kb0 = k0 + wave * BK;
+  if (kb0 < k1) load_block(kb0);  // in flight during the prologue
 
-  if (tid < HALF) {
-    const float2 cs = rope[(size_t)p * HALF + tid];
-    float a = qrow[tid], c = qrow[tid + HALF];
-    qs[tid] = (a * cs.x - c * cs.y) * scale;
-    qs[tid + HALF] = (a * cs.y + c * cs.x) * scale;
-    a = qrow[d + tid];
-    c = qrow[d + tid + HALF];
-    // the stored (rounded) key is the one every later step reads; use it here too
-    T r0, r1;
-    st<T>(&r0, 0, a * cs.x - c * cs.y);
-    st<T>(&r1, 0, a * cs.y + c * cs.x);
-    kn[tid] = ld<T>(&r0, 0);
-    kn[tid + HALF] = ld<T>(&r1, 0);
-  }
-  if (tid < DH) {
-    T r;
-    st<T>(&r, 0, qrow[2 * d + tid]);
-    vn[tid] = ld<T>(&r, 0);
-  }
-  __syncthreads();
-  if (k0 <= p && p < k1 && tid < DH) {
-    st<T>(kslab + (bh + p) * DH, tid, kn[tid]);
-    st<T>(vslab + (bh + p) * DH, tid, vn[tid]);
-  }
-
-  float m = -INFINITY, l = 0.f, acc[8];
+  // this lane's CH dimensions of the rotated, scaled query and of the new
+  // token's key and value, rounded to the slab type as every later step reads them
+  float q[CH], kn[CH], vn[CH];
+  {
+    const float* qrow = qkv + (size_t)b * 3 * d + h * DH;
+    const bool lo = i0 < HALF;  // chunks never straddle the rotation halves
+    const int j0 = lo ? i0 : i0 - HALF;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    for (int e = 0; e < CH; ++e) {
+      const float2 cs = rope[(size_t)p * HALF + j0 + e];
+      const float qa = qrow[j0 + e], qc = qrow[j0 + e + HALF];
+      const float ka = qrow[d + j0 + e], kc = qrow[d + j0 + e + HALF];
+      const float qr = lo ? qa * cs.x - qc * cs.y : qa * cs.y + qc * cs.x;
+      const float kr_ = lo ? ka * cs.x - kc * cs.y : ka * cs.y + kc * cs.x;
+      q[e] = qr * scale;
+      T t;
+      st<T>(&t, 0, kr_);
+      kn[e] = ld<T>(&t, 0);
+      st<T>(&t, 0, qrow[2 * d + i0 + e]);
+      vn[e] = ld<T>(&t, 0);
+    }
+  }
+  if (k0 <= p && p < k1 && wave == 0 && ks == 0) {  // the split holding p appends the token
+#pragma unroll
+    for (int e = 0; e < CH; ++e) {
+      st<T>(kslab + (bh + p) * DH + i0, e, kn[e]);
+      st<T>(vslab + (bh + p) * DH + i0, e, vn[e]);
+    }
+  }
 
-  for (int kb = kb0; kb < k1; kb += NWV * 64) {
+  float m = -INFINITY, l = 0.f, acc[CH];
+#pragma unroll
+  for (int e = 0; e < CH; ++e) acc[e] = 0.f;
+
+  for (int kb = kb0; kb < k1; kb += nw * BK) {
     if (kb != kb0) load_block(kb);
-    const int key = kb + lane;
-    float sc = -INFINITY;
-    if (key < k1) {
-      sc = 0.f;
-      if (key == p) {
-#pragma unroll 8
-        for (int dd = 0; dd < DH; ++dd) sc = fmaf(qs[dd], kn[dd], sc);
-      } else {
+    float sc[IT];
+    float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < KR; ++i) {
-          float kv[E];
-          Raw<T>::cvt(kraw[i], kv);
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
+      float kv[CH];
+      Raw<T>::cvt(kr[it], kv);
+      float s = 0.f;
 #pragma unroll
-          for (int e = 0; e < E; ++e) sc = fmaf(qs[i * E + e], kv[e], sc);
-        }
-      }
+      for (int e = 0; e < CH; ++e) s = fmaf(q[e], key == p ? kn[e] : kv[e], s);
+      s = group_sum<NC>(s);
+      sc[it] = key < k1 ? s : -INFINITY;
+      mx = fmaxf(mx, sc[it]);
     }
-    const float m_new = fmaxf(m, wave_max(sc));
-    const float alpha = __expf(m - m_new);  // m = -inf on the first block gives 0
-    const float pl = (key < k1) ? __expf(sc - m_new) : 0.f;
-    l = l * alpha + wave_sum(pl);
+    const float m_new = fmaxf(m, cross_max<NC>(mx));  // finite: key kb is valid
+    const float alpha = __expf(m - m_new);           // m = -inf on the first block gives 0
+    float ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < CH; ++e) acc[e] *= alpha;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
+      const float pe = __expf(sc[it] - m_new);  // 0 for masked keys
+      ps += pe;
+      float vv[CH];
+      Raw<T>::cvt(vr[it], vv);
+#pragma unroll
+      for (int e = 0; e < CH; ++e) acc[e] = fmaf(pe, key == p ? vn[e] : vv[e], acc[e]);
+    }
+    l = l * alpha + cross_sum<NC>(ps);
     m = m_new;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] *= alpha;
-#pragma unroll
-    for (int it = 0; it < VI; ++it) {
-      const int kl = it * KS + ks;
-      const float pk = __shfl(pl, kl, 64);
-      const int kk = kb + kl;
-      if (kk < k1) {
-        float vv[8];
-        if (kk == p) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) vv[e] = vn[dc * 8 + e];
-        } else {
-#pragma unroll
-          for (int r = 0; r < VR; ++r) Raw<T>::cvt(vraw[it][r], vv + r * E);
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = fmaf(pk, vv[e], acc[e]);
-      }
-    }
   }
-  // sum the key subgroups: lanes that share a dim chunk differ in the high bits
+  // sum the key subgroups; lanes of subgroup 0 then hold the wave's partial output
 #pragma unroll
-  for (int off_ = NC; off_ < 64; off_ <<= 1)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], off_, 64);
+  for (int e = 0; e < CH; ++e) acc[e] = cross_sum<NC>(acc[e]);
   if (lane == 0) {
     wm[wave] = m;
     wl[wave] = l;
   }
-  if (lane < NC)
+  if (ks == 0)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) wacc[wave][lane * 8 + e] = acc[e];
+    for (int e = 0; e < CH; ++e) wacc[wave][i0 + e] = acc[e];
   __syncthreads();
   if (tid < DH) {
     float M = wm[0];
-#pragma unroll
-    for (int w = 1; w < NWV; ++w) M = fmaxf(M, wm[w]);
+    for (int w = 1; w < nw; ++w) M = fmaxf(M, wm[w]);
     float L = 0.f, Acc = 0.f;
     if (M != -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < NWV; ++w) {
+      for (int w = 0; w < nw; ++w) {
         const float f = __expf(wm[w] - M);
         L += wl[w] * f;
         Acc += wacc[w][tid] * f;
       }
     }
     if (splits == 1) {
-      st<T>(o, (size_t)b * d + h * DH + tid, Acc / L);
+      st_out<T>(o, olo, (size_t)b * d + h * DH + tid, Acc / L);
     } else {
       float* out = part + (((size_t)b * H + h) * splits + sp) * (DH + 2);
       out[2 + tid] = Acc;
@@ -554,7 +581,8 @@ __global__ __launch_bounds__(64 * decode_waves<DH>()) void k_attn_decode(const f
 }
 
 template <typename T, int DH>
-__global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, T* __restrict__ o) {
+__global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, T* __restrict__ o,
+                             T* __restrict__ olo) {
   const int h = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
   const float* pp = part + ((size_t)b * H + h) * splits * (DH + 2);
   float M = -INFINITY;
@@ -567,37 +595,53 @@ __global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, 
     L += pp[s * (DH + 2) + 1] * f;
     A += pp[s * (DH + 2) + 2 + t] * f;
   }
-  st<T>(o, (size_t)b * H * DH + h * DH + t, A / L);
+  st_out<T>(o, olo, (size_t)b * H * DH + h * DH + t, A / L);
 }
 
 template <typename T>
 static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, int splits,
-                           const float2* rope, void* k, void* v, float* part, void* o, hipStream_t s) {
+                           const float2* rope, void* k, void* v, float* part, void* o, void* olo, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)dh);
   const dim3 grid(splits, H, B);
+  // waves: enough for the longest split (ceil(cap / splits) keys) at one block
+  // each, and at least DH threads for the output merge
+  const int keys = (cap + splits - 1) / splits;
+  const int bk = dh == 64 ? DecGeo<T, 64>::BK : DecGeo<T, 128>::BK;
+  int nw = (keys + bk - 1) / bk;
+  nw = nw < dh / 64 ? dh / 64 : (nw > DECODE_MAX_WAVES ? DECODE_MAX_WAVES : nw);
   if (dh == 64)
-    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * decode_waves<64>()), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
-                       (T*)v, part, (T*)o, scale);
+    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, cap, splits, rope,
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
   else
-    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * decode_waves<128>()), 0, s, qkv, lens, jpos, H, cap, splits, rope, (T*)k,
-                       (T*)v, part, (T*)o, scale);
+    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, cap, splits, rope,
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
   return hipGetLastError();
 }
 
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
-                       int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s) {
-  if (ct == DT_F32) return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, s);
-  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, s);
+                       int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s,
+                       void* olo) {
+  if (ct == DT_F32) {
+    if (olo) return hipErrorInvalidValue;
+    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, nullptr, s);
+  }
+  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, olo, s);
 }
 
-hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s) {
+hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s,
+                      void* olo) {
   const dim3 grid(H, B);
   if (ct == DT_F32) {
-    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<float, 64>), grid, dim3(64), 0, s, part, H, splits, (float*)o);
-    else hipLaunchKernelGGL((k_attn_merge<float, 128>), grid, dim3(128), 0, s, part, H, splits, (float*)o);
+    if (olo) return hipErrorInvalidValue;
+    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<float, 64>), grid, dim3(64), 0, s, part, H, splits, (float*)o,
+                                     (float*)nullptr);
+    else hipLaunchKernelGGL((k_attn_merge<float, 128>), grid, dim3(128), 0, s, part, H, splits, (float*)o,
+                            (float*)nullptr);
   } else {
-    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<f16, 64>), grid, dim3(64), 0, s, part, H, splits, (f16*)o);
-    else hipLaunchKernelGGL((k_attn_merge<f16, 128>), grid, dim3(128), 0, s, part, H, splits, (f16*)o);
+    if (dh == 64) hipLaunchKernelGGL((k_attn_merge<f16, 64>), grid, dim3(64), 0, s, part, H, splits, (f16*)o,
+                                     (f16*)olo);
+    else hipLaunchKernelGGL((k_attn_merge<f16, 128>), grid, dim3(128), 0, s, part, H, splits, (f16*)o,
+                            (f16*)olo);
   }
   return hipGetLastError();
 }

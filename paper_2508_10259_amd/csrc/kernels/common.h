@@ -45,6 +45,15 @@ template <> struct Elem<f16> {
 template <typename T> __device__ __forceinline__ float ld(const T* p, size_t i) { return Elem<T>::load(p, i); }
 template <typename T> __device__ __forceinline__ void st(T* p, size_t i, float v) { Elem<T>::store(p, i, v); }
 
+// fp16 pair of v: hi[i] = fp16(v) (saturating), lo[i] = fp16(v - hi[i]) when lo
+// is non-NULL; hi + lo carries about 22 significant bits of v.
+__device__ __forceinline__ f16 sat16(float v) { return (f16)fminf(fmaxf(v, -F16_MAX), F16_MAX); }
+__device__ __forceinline__ void split16(float v, f16* hi, f16* lo, size_t i) {
+  const f16 h = sat16(v);
+  hi[i] = h;
+  if (lo) lo[i] = sat16(v - (float)h);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

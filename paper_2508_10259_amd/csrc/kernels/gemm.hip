@@ -31,46 +31,79 @@ __device__ __forceinline__ half8 as_half8(uint4 v) { return __builtin_bit_cast(h
 // reason.  The K range a wave covers is rotated by the workgroup index, so
 // concurrent workgroups read different parts of the shared activations.
 //
-// NRM (M <= 16): the input is the fp16 copy of the residual stream h [M][K]
-// and the kernel applies RMSNorm itself: the MFMA consumes it as is, the sum
-// of squares of each token row comes from the same fragments (reduced across
-// the waves, which together cover all of K), and the 1/rms scale multiplies
-// the result in the epilogue.  The RMSNorm gain is folded into W at packing.
+// Compensated input (LO != 0): the activations arrive as an fp16 pair
+// x = hi + lo (lo = the rounding error of hi), and W x = W hi + W lo, so the
+// product carries about 22 significant bits of x instead of 11.  With up to 8
+// tokens (LO == 1) the pair shares one MFMA: B columns 0..7 take hi, columns
+// 8..15 take lo of the same tokens, and the epilogue adds the two halves;
+// otherwise (LO == 2) lo has its own fragments and MFMAs.
 //
-// RESID may also write an fp16 copy of the updated residual rows (out16, same
-// leading dimension), the input of the next fused-RMSNorm GEMV.
+// NRM (M <= 16): the input is the (fp16 or fp16-pair) copy of the residual
+// stream h [M][K] and the kernel applies RMSNorm itself: the MFMA consumes it
+// as is, the sum of squares of each token row comes from the hi fragments
+// (reduced across the waves, which together cover all of K), and the 1/rms
+// scale multiplies the result in the epilogue.  The RMSNorm gain is folded
+// into W at packing.  Taking the statistic from hi alone changes it by about
+// 2^-11 / sqrt(K) relative for rounding errors of random sign (the product,
+// where one term's error does not average out, takes hi + lo).
+//
+// RESID may also write the updated residual rows as fp16 (ohi, and olo for
+// the pair), the input of the next fused-RMSNorm GEMV; SWIGLU may write the
+// rounding error of its fp16 output to olo.
 
-template <int RB, int MB, int EPI, bool NRM>
-__global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin, float eps,
-                                                     const f16* __restrict__ W, int M, int K,
-                                                     void* __restrict__ out, int ldo, f16* __restrict__ out16) {
+struct SkinnyArgs {
+  const f16* xhi;  // [M][K]
+  const f16* xlo;  // [M][K] or NULL
+  float eps;
+  const f16* W;    // [N][K]
+  int M, K;
+  void* out;
+  int ldo;
+  f16* ohi;  // RESID only, or NULL
+  f16* olo;  // RESID / SWIGLU, or NULL
+};
+
+template <int RB, int MB, int LO>
+constexpr int skinny_cpw() {
+  return (RB + MB * (LO == 2 ? 2 : 1)) <= 2 ? 4 : ((RB + MB * (LO == 2 ? 2 : 1)) <= 4 ? 2 : 1);
+}
+
+template <int RB, int MB, int EPI, bool NRM, int LO>
+__global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
   static_assert(!NRM || MB == 1, "the fused RMSNorm handles up to 16 tokens");
+  static_assert(LO != 1 || MB == 1, "the packed pair handles up to 8 tokens");
+  constexpr int LB = LO == 2 ? MB : 1;  // lo fragment blocks (unused unless LO == 2)
   extern __shared__ float red[];  // [nw][RB][MB][64 lanes][4], then (NRM) wsum[<=16 waves][16] + rstd[16]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * (RB * 16);
+  const int M = a.M, K = a.K, ldo = a.ldo;
   const int nchunks = K >> 7;
   const int wk = (wave + blockIdx.x) % nw;
   const int c0 = wk * nchunks / nw, c1 = (wk + 1) * nchunks / nw;
 
   f32x4 acc[RB][MB];
 #pragma unroll
-  for (int a = 0; a < RB; ++a)
+  for (int q = 0; q < RB; ++q)
 #pragma unroll
-    for (int b = 0; b < MB; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < MB; ++b) acc[q][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const f16* wrow[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) wrow[rb] = W + (size_t)(n0 + rb * 16 + r) * K + g * 8;
+  for (int rb = 0; rb < RB; ++rb) wrow[rb] = a.W + (size_t)(n0 + rb * 16 + r) * K + g * 8;
+  // B-operand rows of this lane: token mb*16 + r (LO == 1: token r & 7, hi for r < 8, lo above)
   bool uok[MB];
   const f16* urow[MB];
+  const f16* lrow[LB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
-    const int tok = mb * 16 + r;
+    const int tok = LO == 1 ? (r & 7) : mb * 16 + r;
     uok[mb] = tok < M;
-    urow[mb] = xin + (size_t)(uok[mb] ? tok : 0) * K + g * 8;
+    const size_t off = (size_t)(uok[mb] ? tok : 0) * K + g * 8;
+    urow[mb] = (LO == 1 && r >= 8 ? a.xlo : a.xhi) + off;
+    if constexpr (LO == 2) lrow[mb] = a.xlo + off;
   }
-  float ss = 0.f;  // NRM: this lane's share of sum(h^2) of token r
+  float ss = 0.f;  // NRM: this lane's share of sum(x^2) of its token
 
   // the residual epilogue's h values do not depend on this kernel: request them first
   constexpr int EPT = (MB * 256 + 63) / 64;  // epilogue values per thread at the smallest workgroup
@@ -81,16 +114,16 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin
       const int idx = threadIdx.x + e * blockDim.x;
       const int mb = idx >> 8, ln = (idx >> 2) & 63, i = idx & 3;
       const int tok = mb * 16 + (ln & 15), row = 4 * (ln >> 4) + i;
-      const bool ok = idx < MB * 256 && tok < M;
+      const bool ok = idx < MB * 256 && tok < M && (LO != 1 || (ln & 15) < 8);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
-        hres[rb * EPT + e] = ok ? ((const float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] : 0.f;
+        hres[rb * EPT + e] = ok ? ((const float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] : 0.f;
     }
   }
 
   // chunks in flight per wave: up to CPW loads are issued before the first MFMA
-  constexpr int CPW = RB + MB <= 2 ? 4 : 2;
-  uint4 fw[CPW][RB][4], fu[CPW][MB][4];
+  constexpr int CPW = skinny_cpw<RB, MB, LO>();
+  uint4 fw[CPW][RB][4], fu[CPW][MB][4], fl[CPW][LB][4];
   for (int cb = c0; cb < c1; cb += CPW) {
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
@@ -103,8 +136,11 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i) {
             fu[j][mb][i] = uok[mb] ? *(const uint4*)(urow[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
+            if constexpr (LO == 2)
+              fl[j][mb][i] = uok[mb] ? *(const uint4*)(lrow[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
+          }
       }
     }
 #pragma unroll
@@ -116,12 +152,18 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin
           for (int i = 0; i < 4; ++i) {
             const half8 v = as_half8(fu[j][mb][i]);
             if constexpr (NRM) {
+              if (LO != 1 || r < 8) {  // the statistic reads hi only
 #pragma unroll
-              for (int e = 0; e < 8; ++e) ss = fmaf((float)v[e], (float)v[e], ss);
+                for (int e = 0; e < 8; ++e) ss = fmaf((float)v[e], (float)v[e], ss);
+              }
             }
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
+            for (int rb = 0; rb < RB; ++rb) {
               acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(fw[j][rb][i]), v, acc[rb][mb], 0, 0, 0);
+              if constexpr (LO == 2)
+                acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(fw[j][rb][i]), as_half8(fl[j][mb][i]),
+                                                                      acc[rb][mb], 0, 0, 0);
+            }
           }
       }
     }
@@ -143,66 +185,81 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(const f16* __restrict__ xin
     if (threadIdx.x < 16) {
       float t = 0.f;
       for (int w = 0; w < nw; ++w) t += wsum[w * 16 + threadIdx.x];
-      rstd[threadIdx.x] = 1.0f / sqrtf(t / (float)K + eps);
+      rstd[threadIdx.x] = 1.0f / sqrtf(t / (float)K + a.eps);
     }
   }
   __syncthreads();
 
-  // value (rb, mb, ln, i) is packed row n0 + rb*16 + 4*(ln>>4) + i, token mb*16 + (ln&15)
+  // value (rb, mb, ln, i) is packed row n0 + rb*16 + 4*(ln>>4) + i, B column mb*16 + (ln&15)
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int idx = threadIdx.x + e * blockDim.x;
     if (idx >= MB * 256) break;
     const int mb = idx >> 8, ln = (idx >> 2) & 63, i = idx & 3;
     const int tok = mb * 16 + (ln & 15);
-    if (tok >= M) continue;
+    if (tok >= M || (LO == 1 && (ln & 15) >= 8)) continue;
     const int row = 4 * (ln >> 4) + i;
     float v[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       float t = 0.f;
-      for (int w = 0; w < nw; ++w) t += red[(((w * RB + rb) * MB + mb) * 64 + ln) * 4 + i];
+      for (int w = 0; w < nw; ++w) {
+        t += red[(((w * RB + rb) * MB + mb) * 64 + ln) * 4 + i];
+        if constexpr (LO == 1) t += red[(((w * RB + rb) * MB + mb) * 64 + ln + 8) * 4 + i];
+      }
       if constexpr (NRM) t *= rstd[tok];
       v[rb] = t;
     }
     if constexpr (EPI == EPI_STORE) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) ((float*)out)[(size_t)tok * ldo + n0 + rb * 16 + row] = v[rb];
+      for (int rb = 0; rb < RB; ++rb) ((float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] = v[rb];
     } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const size_t o = (size_t)tok * ldo + n0 + rb * 16 + row;
         const float hn = hres[rb * EPT + e] + v[rb];
-        ((float*)out)[o] = hn;
-        if (out16) st<f16>(out16, o, hn);
+        ((float*)a.out)[o] = hn;
+        if (a.ohi) split16(hn, a.ohi, a.olo, o);
       }
     } else {
-      st<f16>((f16*)out, (size_t)tok * ldo + (n0 >> 1) + row, silu(v[0]) * v[RB - 1]);
+      split16(silu(v[0]) * v[RB - 1], (f16*)a.out, a.olo, (size_t)tok * ldo + (n0 >> 1) + row);
     }
   }
 }
 
-template <int RB, int MB, int EPI, bool NRM>
-static hipError_t launch_skinny(const f16* x, float eps, const f16* W, int M, int N, int K, void* out, int ldo,
-                                f16* out16, hipStream_t s) {
-  const int nchunks = K >> 7;
+template <int RB, int MB, int EPI, bool NRM, int LO>
+static hipError_t launch_skinny(const SkinnyArgs& a, int N, hipStream_t s) {
+  const int nchunks = a.K >> 7;
   int nw = 8;  // <= 512 threads: leaves 256 VGPRs for the chunks in flight
   while (nw > 1 && nw * RB * MB * 1024 > 65536) nw >>= 1;
   while (nw > 1 && nw > nchunks) nw >>= 1;
   const size_t lds = (size_t)nw * RB * MB * 1024 + (NRM ? (256 + 16) * 4 : 0);
-  hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM>), dim3(N / (RB * 16)), dim3(64 * nw), lds, s, x, eps, W, M,
-                     K, out, ldo, out16);
+  hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM, LO>), dim3(N / (RB * 16)), dim3(64 * nw), lds, s, a);
   return hipGetLastError();
 }
 
-template <int EPI>
-static hipError_t skinny_mb(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, f16* out16,
-                            hipStream_t s) {
+// token blocks and input form of one skinny launch
+template <int EPI, bool NRM>
+static hipError_t skinny_dispatch(const SkinnyArgs& a, int N, hipStream_t s) {
   constexpr int RB = EPI == EPI_SWIGLU ? 2 : 1;
-  if (M <= 16) return launch_skinny<RB, 1, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
-  if (M <= 32) return launch_skinny<RB, 2, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
-  if (M <= 48) return launch_skinny<RB, 3, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
-  return launch_skinny<RB, 4, EPI, false>(u, 0.f, W, M, N, K, out, ldo, out16, s);
+  const int M = a.M;
+  if (!a.xlo) {
+    if (M <= 16) return launch_skinny<RB, 1, EPI, NRM, 0>(a, N, s);
+    if constexpr (!NRM) {
+      if (M <= 32) return launch_skinny<RB, 2, EPI, false, 0>(a, N, s);
+      if (M <= 48) return launch_skinny<RB, 3, EPI, false, 0>(a, N, s);
+      return launch_skinny<RB, 4, EPI, false, 0>(a, N, s);
+    }
+  } else {
+    if (M <= 8) return launch_skinny<RB, 1, EPI, NRM, 1>(a, N, s);
+    if (M <= 16) return launch_skinny<RB, 1, EPI, NRM, 2>(a, N, s);
+    if constexpr (!NRM) {
+      if (M <= 32) return launch_skinny<RB, 2, EPI, false, 2>(a, N, s);
+      if (M <= 48) return launch_skinny<RB, 3, EPI, false, 2>(a, N, s);
+      return launch_skinny<RB, 4, EPI, false, 2>(a, N, s);
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 // ----------------------------------------------------------------------------
@@ -373,41 +430,49 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 
 template <int EPI>
 static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, int K, void* out, int ldo,
-                           void* out16, hipStream_t s) {
-  // the fp16 residual copy is produced by the decode GEMV only
-  if (out16 && (EPI != EPI_RESID || ct != DT_F16 || M > 64)) return hipErrorInvalidValue;
+                           hipStream_t s, const void* ulo, void* o16, void* olo) {
+  const bool pair = ulo || o16 || olo;
+  if (pair) {  // the fp16-pair forms belong to the decode GEMV only
+    if (ct != DT_F16 || M > 64) return hipErrorInvalidValue;
+    if (o16 && EPI != EPI_RESID) return hipErrorInvalidValue;
+    if (olo && EPI == EPI_STORE) return hipErrorInvalidValue;
+    if (olo && EPI == EPI_RESID && !o16) return hipErrorInvalidValue;
+  }
   if (ct == DT_F32) {
     hipLaunchKernelGGL((k_gemm_f32<EPI>), dim3(N / FBN, (M + FBM - 1) / FBM), dim3(256), 0, s,
                        (const float*)u, (const float*)W, M, K, out, ldo);
     return hipGetLastError();
   }
-  if (M <= 64) return skinny_mb<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, (f16*)out16, s);
+  if (M <= 64) {
+    const SkinnyArgs a{(const f16*)u, (const f16*)ulo, 0.f, (const f16*)W, M, K, out, ldo, (f16*)o16, (f16*)olo};
+    return skinny_dispatch<EPI, false>(a, N, s);
+  }
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
 }
 
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo,
-                hipStream_t s, void* out16) {
+                hipStream_t s, const void* ulo, void* o16, void* olo) {
   if (M <= 0) return hipSuccess;
   switch (epi) {
-    case EPI_STORE: return gemm_epi<EPI_STORE>(ct, u, W, M, N, K, out, ldo, out16, s);
-    case EPI_RESID: return gemm_epi<EPI_RESID>(ct, u, W, M, N, K, out, ldo, out16, s);
-    default: return gemm_epi<EPI_SWIGLU>(ct, u, W, M, N, K, out, ldo, out16, s);
+    case EPI_STORE: return gemm_epi<EPI_STORE>(ct, u, W, M, N, K, out, ldo, s, ulo, o16, olo);
+    case EPI_RESID: return gemm_epi<EPI_RESID>(ct, u, W, M, N, K, out, ldo, s, ulo, o16, olo);
+    default: return gemm_epi<EPI_SWIGLU>(ct, u, W, M, N, K, out, ldo, s, ulo, o16, olo);
   }
 }
 
-hipError_t gemv_rmsnorm(int ct, int epi, const void* h16, float eps, const void* W, int M, int N, int K, void* out,
-                        int ldo, hipStream_t s, void* out16) {
+hipError_t gemv_rmsnorm(int ct, int epi, const void* hhi, float eps, const void* W, int M, int N, int K, void* out,
+                        int ldo, hipStream_t s, const void* hlo, void* o16, void* olo) {
   if (M <= 0) return hipSuccess;
   if (ct != DT_F16 || M > 16) return hipErrorInvalidValue;
-  if (out16 && epi != EPI_RESID) return hipErrorInvalidValue;
-  const f16* x = (const f16*)h16;
-  const f16* w = (const f16*)W;
+  if (o16 && epi != EPI_RESID) return hipErrorInvalidValue;
+  if (olo && (epi == EPI_STORE || (epi == EPI_RESID && !o16))) return hipErrorInvalidValue;
+  const SkinnyArgs a{(const f16*)hhi, (const f16*)hlo, eps, (const f16*)W, M, K, out, ldo, (f16*)o16, (f16*)olo};
   switch (epi) {
-    case EPI_STORE: return launch_skinny<1, 1, EPI_STORE, true>(x, eps, w, M, N, K, out, ldo, nullptr, s);
-    case EPI_RESID: return launch_skinny<1, 1, EPI_RESID, true>(x, eps, w, M, N, K, out, ldo, (f16*)out16, s);
-    default: return launch_skinny<2, 1, EPI_SWIGLU, true>(x, eps, w, M, N, K, out, ldo, nullptr, s);
+    case EPI_STORE: return skinny_dispatch<EPI_STORE, true>(a, N, s);
+    case EPI_RESID: return skinny_dispatch<EPI_RESID, true>(a, N, s);
+    default: return skinny_dispatch<EPI_SWIGLU, true>(a, N, s);
   }
 }
 

@@ -35,30 +35,35 @@ constexpr int GU_BLOCK = 16;
 //   EPI_STORE : out_f32[m*ldo + n] = y
 //   EPI_RESID : out_f32[m*ldo + n] += y          (residual stream)
 //   EPI_SWIGLU: out_T[m*ldo + c] = silu(gate_c) * up_c with W packed as above
-// out16 (fp16 compute, EPI_RESID, M <= 64 only; NULL otherwise): the updated
-// residual rows are also written there as fp16 (saturating), same ldo.
+// fp16-pair forms (fp16 compute, M <= 64 only; NULL otherwise):
+//   ulo : the input is u + ulo (ulo = the rounding error of u, same shape)
+//   o16 : EPI_RESID also writes the updated rows as fp16 (saturating), same ldo
+//   olo : the rounding error of o16 (EPI_RESID) or of the fp16 out (EPI_SWIGLU)
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out,
-                int ldo, hipStream_t s, void* out16 = nullptr);
+                int ldo, hipStream_t s, const void* ulo = nullptr, void* o16 = nullptr, void* olo = nullptr);
 
 // Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16), on the fp16
-// copy x = fp16(h) of the residual rows:
-// y[m] = (W x[m]) / sqrt(mean(x[m]^2) + eps), followed by the epilogue as in
-// gemm() (out16 as there, EPI_RESID only).  W carries the RMSNorm gain (folded
-// at packing).
-hipError_t gemv_rmsnorm(int ct, int epi, const void* h16, float eps, const void* W, int M, int N, int K, void* out,
-                        int ldo, hipStream_t s, void* out16 = nullptr);
+// copy x = hhi (+ hlo, its rounding error, when non-NULL) of the residual rows:
+// y[m] = (W x[m]) / sqrt(mean(hhi[m]^2) + eps), followed by the epilogue as in
+// gemm() (o16 / olo as there).  W carries the RMSNorm gain (folded at packing).
+hipError_t gemv_rmsnorm(int ct, int epi, const void* hhi, float eps, const void* W, int M, int N, int K, void* out,
+                        int ldo, hipStream_t s, const void* hlo = nullptr, void* o16 = nullptr,
+                        void* olo = nullptr);
 
 // Per row b: argmax over logits[b][0..n_bins) (lowest index on ties) -> out_tok[b*A+j],
 // logits copied to out_logits[b][j] (if non-NULL); when feed, h[b] = bin_embed[t]
 // with t the argmax or the clamped forced[b*A+j], and (if h16 is non-NULL, fp16
-// compute only) h16[b] = the same row in fp16.
+// compute only) h16[b] = the same row in fp16 and h16lo[b] (if non-NULL) = 0,
+// its rounding error.
 hipError_t argmax_feed(int ct, const float* logits, int ld_logits, const void* bin_embed, int B, int d, int n_bins,
                        int A, int j, int32_t* out_tok, float* out_logits, const int32_t* forced, float* h, int feed,
-                       hipStream_t s, void* h16 = nullptr);
+                       hipStream_t s, void* h16 = nullptr, void* h16lo = nullptr);
 
 // u[m] = h[m] / sqrt(mean(h[m]^2) + eps), written in the compute type (the
 // gain is folded into the weights that consume u).
-hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s);
+// ulo (fp16 only, or NULL): the rounding error of u, so that u + ulo is the
+// normalised row to about 22 significant bits.
+hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s, void* ulo = nullptr);
 
 // out[i] = E[clamp(ids[i])] in the storage type.
 hipError_t embed_rows(int st, const void* E, const int32_t* ids, int n, int d, int vocab, void* out,
@@ -93,16 +98,19 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int ca
 // One query per row at position lens[b] + jpos: appends its K/V, attends over
 // positions 0..lens[b]+jpos.  splits == 1: the output goes straight to o;
 // otherwise the keys are cut into `splits` chunks whose partials (m, l, acc)
-// go to `part` for attn_merge.
+// go to `part` for attn_merge.  olo (fp16 only, or NULL): the rounding error of
+// the fp16 output o, written by whichever of the two kernels writes o.
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh,
                        int cap, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
-                       hipStream_t s);
+                       hipStream_t s, void* olo = nullptr);
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
-                      hipStream_t s);
+                      hipStream_t s, void* olo = nullptr);
 
 // h_last[row[s]] = h[off[s+1]-1] for each segment, and the same rows as fp16
-// (saturating) into h_last16 when it is non-NULL.
-hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16 = nullptr);
+// (saturating) into h_last16 when it is non-NULL, with their rounding error
+// into h_last16lo when that is non-NULL too.
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16 = nullptr,
+                       void* h_last16lo = nullptr);
 
 // lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);

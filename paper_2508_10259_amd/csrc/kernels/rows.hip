@@ -9,7 +9,8 @@ namespace ams {
 // statistics in fp32.  Each thread loads its EPT (<= 16) elements before
 // reducing, so a row costs one memory round trip.
 template <typename T, int EPT>
-__global__ __launch_bounds__(1024) void k_rmsnorm(const float* __restrict__ h, int d, float eps, T* __restrict__ u) {
+__global__ __launch_bounds__(1024) void k_rmsnorm(const float* __restrict__ h, int d, float eps, T* __restrict__ u,
+                                                  T* __restrict__ ulo) {
   __shared__ float red[16];
   const size_t base = (size_t)blockIdx.x * d;
   const int nt = blockDim.x;
@@ -27,15 +28,18 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(const float* __restrict__ h, i
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int i = threadIdx.x + e * nt;
-    if (i < d) st<T>(u, base + i, x[e] * rs);
+    if (i < d) {
+      if constexpr (sizeof(T) == 2) split16(x[e] * rs, u, ulo, base + i);
+      else st<T>(u, base + i, x[e] * rs);
+    }
   }
 }
 
 template <typename T>
-static hipError_t rmsnorm_t(const float* h, int M, int d, float eps, T* u, hipStream_t s) {
+static hipError_t rmsnorm_t(const float* h, int M, int d, float eps, T* u, T* ulo, hipStream_t s) {
   const int nt = d <= 4096 ? 256 : 1024;
   const int ept = (d + nt - 1) / nt;  // <= 16 for d <= 16384
-#define AMS_RMS(E) hipLaunchKernelGGL((k_rmsnorm<T, E>), dim3(M), dim3(nt), 0, s, h, d, eps, u)
+#define AMS_RMS(E) hipLaunchKernelGGL((k_rmsnorm<T, E>), dim3(M), dim3(nt), 0, s, h, d, eps, u, ulo)
   if (ept <= 1) AMS_RMS(1);
   else if (ept <= 2) AMS_RMS(2);
   else if (ept <= 4) AMS_RMS(4);
@@ -45,10 +49,13 @@ static hipError_t rmsnorm_t(const float* h, int M, int d, float eps, T* u, hipSt
   return hipGetLastError();
 }
 
-hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s) {
+hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s, void* ulo) {
   if (M <= 0) return hipSuccess;
-  if (ct == DT_F32) return rmsnorm_t<float>(h, M, d, eps, (float*)u, s);
-  return rmsnorm_t<f16>(h, M, d, eps, (f16*)u, s);
+  if (ct == DT_F32) {
+    if (ulo) return hipErrorInvalidValue;
+    return rmsnorm_t<float>(h, M, d, eps, (float*)u, nullptr, s);
+  }
+  return rmsnorm_t<f16>(h, M, d, eps, (f16*)u, (f16*)ulo, s);
 }
 
 // Copies rows as raw elements (8/16-byte chunks); `ids` selects source rows.
@@ -156,7 +163,8 @@ hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s) 
 
 __global__ __launch_bounds__(256) void k_gather_last(const float* __restrict__ h, const int32_t* __restrict__ row,
                                                      const int32_t* __restrict__ off, int d,
-                                                     float* __restrict__ h_last, f16* __restrict__ h_last16) {
+                                                     float* __restrict__ h_last, f16* __restrict__ h_last16,
+                                                     f16* __restrict__ h_last16lo) {
   const int sidx = blockIdx.x;
   const int last = off[sidx + 1] - 1;
   const float* src = h + (size_t)last * d;
@@ -164,13 +172,16 @@ __global__ __launch_bounds__(256) void k_gather_last(const float* __restrict__ h
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     const float v = src[i];
     h_last[o + i] = v;
-    if (h_last16) st<f16>(h_last16, o + i, v);
+    if (h_last16) split16(v, h_last16, h_last16lo, o + i);
   }
 }
 
-hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16) {
+hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16,
+                       void* h_last16lo) {
   if (sg.n_seg <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather_last, dim3(sg.n_seg), dim3(256), 0, s, h, sg.row, sg.off, d, h_last, (f16*)h_last16);
+  if (h_last16lo && !h_last16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gather_last, dim3(sg.n_seg), dim3(256), 0, s, h, sg.row, sg.off, d, h_last, (f16*)h_last16,
+                     (f16*)h_last16lo);
   return hipGetLastError();
 }
 

@@ -8,25 +8,36 @@
 
 extern "C" {
 
-int ams_probe_gemm(int dtype, int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo,
-                   void* out16, void* stream) {
-  return (int)ams::gemm(dtype, epi, u, W, M, N, K, out, ldo, (hipStream_t)stream, out16);
+int ams_probe_gemm(int dtype, int epi, const void* u, const void* ulo, const void* W, int M, int N, int K, void* out,
+                   int ldo, void* o16, void* olo, void* stream) {
+  return (int)ams::gemm(dtype, epi, u, W, M, N, K, out, ldo, (hipStream_t)stream, ulo, o16, olo);
 }
 
-int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* stream) {
-  return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream);
+int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* ulo, void* stream) {
+  return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream, ulo);
 }
 
 int ams_probe_argmax_feed(int ct, const float* logits, int ld, const void* bin_embed, int B, int d, int n_bins,
                           int A, int j, int32_t* out_tok, float* out_logits, const int32_t* forced, float* h, int feed,
-                          void* h16, void* stream) {
+                          void* h16, void* h16lo, void* stream) {
   return (int)ams::argmax_feed(ct, logits, ld, bin_embed, B, d, n_bins, A, j, out_tok, out_logits, forced, h, feed,
-                               (hipStream_t)stream, h16);
+                               (hipStream_t)stream, h16, h16lo);
 }
 
-int ams_probe_gemv_rmsnorm(int ct, int epi, const void* h16, float eps, const void* W, int M, int N, int K, void* out,
-                           int ldo, void* out16, void* stream) {
-  return (int)ams::gemv_rmsnorm(ct, epi, h16, eps, W, M, N, K, out, ldo, (hipStream_t)stream, out16);
+int ams_probe_gemv_rmsnorm(int ct, int epi, const void* hhi, const void* hlo, float eps, const void* W, int M, int N,
+                           int K, void* out, int ldo, void* o16, void* olo, void* stream) {
+  return (int)ams::gemv_rmsnorm(ct, epi, hhi, eps, W, M, N, K, out, ldo, (hipStream_t)stream, hlo, o16, olo);
+}
+
+// decode attention of one pass (jpos) for B rows, merged when splits > 1
+int ams_probe_attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
+                          int splits, const void* rope, void* kslab, void* vslab, float* part, void* o, void* olo,
+                          void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = ams::attn_decode(ct, qkv, lens, jpos, B, H, dh, cap, splits, (const float2*)rope, kslab, vslab,
+                                  part, o, s, olo);
+  if (e == hipSuccess && splits > 1) e = ams::attn_merge(ct, part, B, H, dh, splits, o, s, olo);
+  return (int)e;
 }
 
 }  // extern "C"

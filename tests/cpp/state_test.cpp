@@ -110,10 +110,13 @@ static void test_layout() {
   EXPECT(check_ctx_args(c, 8, 100, 0, e) == S_EINVAL);
   EXPECT(check_ctx_args(c, 8, 320, 100, e) == S_EINVAL);
   EXPECT(check_ctx_args(c, 8, 320, 320, e) == S_OK);
-  EXPECT(decode_splits(1, 32, 320) == 1);   // short context: one split
-  EXPECT(decode_splits(1, 32, 1024) == 4);  // 32 pairs, long context: 4 splits of 256
-  EXPECT(decode_splits(8, 16, 320) == 1);
+  EXPECT(decode_splits(1, 32, 320) == 1);    // short context: one workgroup per pair
+  EXPECT(decode_splits(1, 32, 2048) == 1);
+  EXPECT(decode_splits(1, 32, 4096) == 4);   // long context, 32 pairs: parts of >= 1024
+  EXPECT(decode_splits(1, 32, 16384) == 8);  // 32 pairs x 8 = 256 workgroups
+  EXPECT(decode_splits(8, 16, 8192) == 1);   // 128 pairs: no split
   EXPECT(decode_splits(64, 32, 768) == 1);
+  EXPECT(decode_splits(1, 1, 64) == 1);
   EXPECT(bins_padded(c) == 256);
 }
 

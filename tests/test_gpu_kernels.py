@@ -69,18 +69,41 @@ def _unpack_gu(Wp, F):
     return gate, up
 
 
+def _pair(x):
+    """fp16 pair of x: hi = fp16(x), lo = fp16(x - hi)."""
+    hi = x.astype(np.float16)
+    return hi, (x.astype(np.float64) - hi.astype(np.float64)).astype(np.float16)
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr() if t is not None else None)
+
+
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
-@pytest.mark.parametrize("M", [1, 3, 16, 17, 40, 64, 65, 130, 257])
+@pytest.mark.parametrize("M", [1, 3, 8, 9, 16, 17, 40, 64, 65, 130, 257])
 @pytest.mark.parametrize("K", [384, 1024])
-def test_gemm(probe, dtype, epi, M, K):
+@pytest.mark.parametrize("pair", [False, True])
+def test_gemm(probe, dtype, epi, M, K, pair):
+    """GEMM with each epilogue against the exact product of its inputs.  `pair`: the fp16 decode
+    GEMV form, whose input is hi + lo (lo = the rounding error of hi) and whose residual / SwiGLU
+    outputs also come as fp16 pairs."""
     import torch
+    if pair and (dtype != "f16" or M > 64):
+        pytest.skip("fp16 pairs belong to the fp16 decode GEMV (M <= 64)")
     N = 256
-    log(f"gemm dtype={dtype} epi={epi} M={M} N={N} K={K}")
-    u = _rand((M, K), 1, M, K, dtype=dtype)
+    log(f"gemm dtype={dtype} epi={epi} M={M} N={N} K={K} pair={pair}")
+    x = W.random_gaussian((M, K), 1, M, K, dtype="f32")
+    if pair:
+        u, ulo = _pair(x)
+        xin = u.astype(np.float64) + ulo.astype(np.float64)
+    else:
+        u, ulo = (x.astype(np.float16) if dtype == "f16" else x), None
+        xin = _f(u, dtype)
     Wt = _rand((N, K), 2, N, K, dtype=dtype, std=0.05)
     ud, Wd = _dev(u, dtype), _dev(Wt, dtype)
-    y = _f(u, dtype) @ _f(Wt, dtype).T
+    ulod = _dev(ulo, dtype) if pair else None
+    y = xin @ _f(Wt, dtype).T
     if epi == EPI_SWIGLU:
         out = torch.zeros((M, N // 2), dtype=torch.float32 if dtype == "f32" else torch.float16, device="cuda")
         ldo = N // 2
@@ -88,22 +111,28 @@ def test_gemm(probe, dtype, epi, M, K):
         h0 = W.random_gaussian((M, N), 3, M, dtype="f32")
         out = torch.from_numpy(h0.copy() if epi == EPI_RESID else np.zeros_like(h0)).cuda()
         ldo = N
-    # the decode GEMV (fp16, M <= 64) can also write the fp16 copy of updated residual rows
+    # fp16 outputs beside the residual rows (and the rounding error of SwiGLU's fp16 output)
     with16 = epi == EPI_RESID and dtype == "f16" and M <= 64
-    out16 = torch.full((M, N), 7.0, dtype=torch.float16, device="cuda") if with16 else None
-    rc = probe.ams_probe_gemm(CT[dtype], epi, C.c_void_p(ud.data_ptr()), C.c_void_p(Wd.data_ptr()),
-                              M, N, K, C.c_void_p(out.data_ptr()), ldo,
-                              C.c_void_p(out16.data_ptr() if with16 else None), _stream())
+    o16 = torch.full((M, N), 7.0, dtype=torch.float16, device="cuda") if with16 else None
+    olo = None
+    if pair and epi == EPI_RESID:
+        olo = torch.full((M, N), 7.0, dtype=torch.float16, device="cuda")
+    elif pair and epi == EPI_SWIGLU:
+        olo = torch.full((M, N // 2), 7.0, dtype=torch.float16, device="cuda")
+    rc = probe.ams_probe_gemm(CT[dtype], epi, _ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, _ptr(out), ldo, _ptr(o16),
+                              _ptr(olo), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().astype(np.float64)
     if with16:
-        assert torch.equal(out16, out.half()), "fp16 residual copy differs from the fp32 rows"
-    elif dtype == "f32" or epi != EPI_RESID or M > 64:
+        assert torch.equal(o16, out.half()), "fp16 residual copy differs from the fp32 rows"
+        if pair:
+            assert torch.equal(olo, (out - out.half().float()).half()), "lo part is not the rounding error"
+    elif not pair and (dtype == "f32" or epi != EPI_RESID or M > 64):
         # any other configuration rejects the fp16 copy before launching
         spare = torch.empty((M, N), dtype=torch.float16, device="cuda")
-        assert probe.ams_probe_gemm(CT[dtype], epi, C.c_void_p(ud.data_ptr()), C.c_void_p(Wd.data_ptr()), M, N, K,
-                                    C.c_void_p(out.data_ptr()), ldo, C.c_void_p(spare.data_ptr()), _stream()) != 0
+        assert probe.ams_probe_gemm(CT[dtype], epi, _ptr(ud), C.c_void_p(None), _ptr(Wd), M, N, K, _ptr(out), ldo,
+                                    _ptr(spare), C.c_void_p(None), _stream()) != 0
     if epi == EPI_STORE:
         ref = y
     elif epi == EPI_RESID:
@@ -111,9 +140,11 @@ def test_gemm(probe, dtype, epi, M, K):
     else:
         g, up = _unpack_gu(y.T, N // 2)
         ref = (_silu(g) * up).T
+        if pair:  # the SwiGLU value as the fp16 pair carries it
+            got = got + olo.float().cpu().numpy().astype(np.float64)
     scale = max(1.0, float(np.max(np.abs(ref))))
     tol = (1e-5 if dtype == "f32" else 2e-5) * scale * np.sqrt(K / 128)
-    if epi == EPI_SWIGLU and dtype == "f16":
+    if epi == EPI_SWIGLU and dtype == "f16" and not pair:
         tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
     err = float(np.max(np.abs(got - ref)))
     assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
@@ -121,20 +152,28 @@ def test_gemm(probe, dtype, epi, M, K):
 
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 @pytest.mark.parametrize("d", [384, 4096])
-def test_rmsnorm(probe, dtype, d):
+@pytest.mark.parametrize("pair", [False, True])
+def test_rmsnorm(probe, dtype, d, pair):
     import torch
+    if pair and dtype != "f16":
+        pytest.skip("fp16 pairs only")
     M, eps = 5, 1e-5
     h = W.random_gaussian((M, d), 4, d, dtype="f32") * 3.0
     hd = torch.from_numpy(h).cuda()
     out = torch.empty((M, d), dtype=torch.float32 if dtype == "f32" else torch.float16, device="cuda")
+    lo = torch.empty((M, d), dtype=torch.float16, device="cuda") if pair else None
     rc = probe.ams_probe_rmsnorm(CT[dtype], C.c_void_p(hd.data_ptr()), M, d, C.c_float(eps),
-                                 C.c_void_p(out.data_ptr()), _stream())
+                                 C.c_void_p(out.data_ptr()), _ptr(lo), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     h64 = h.astype(np.float64)
     ref = h64 / np.sqrt(np.mean(h64 * h64, axis=-1, keepdims=True) + eps)
-    got = out.float().cpu().numpy()
-    tol = 1e-5 * np.max(np.abs(ref)) if dtype == "f32" else 2 ** -11 * np.max(np.abs(ref))
+    got = out.float().cpu().numpy().astype(np.float64)
+    if pair:
+        got = got + lo.float().cpu().numpy()
+        tol = 2e-6 * np.max(np.abs(ref))
+    else:
+        tol = 1e-5 * np.max(np.abs(ref)) if dtype == "f32" else 2 ** -11 * np.max(np.abs(ref))
     assert np.max(np.abs(got - ref)) <= tol
 
 
@@ -156,6 +195,7 @@ def test_argmax_feed_ties(probe, dtype, n_bins):
     forced = torch.tensor([[0, 5, 0], [0, n_bins + 7, 0], [0, -3, 0], [0, 2, 0]], dtype=torch.int32, device="cuda")
     h = torch.zeros((B, d), dtype=torch.float32, device="cuda")
     h16 = torch.zeros((B, d), dtype=torch.float16, device="cuda") if dtype == "f16" else None
+    h16lo = torch.full((B, d), 5.0, dtype=torch.float16, device="cuda") if dtype == "f16" else None
     ref = np.argmax(lg[:, :n_bins], axis=-1)
     assert list(ref[:3]) == [3, n_bins - 2, 0]
     for use_forced in (False, True):
@@ -163,31 +203,40 @@ def test_argmax_feed_ties(probe, dtype, n_bins):
                                          n_bins, A, j, C.c_void_p(tok.data_ptr()), C.c_void_p(out.data_ptr()),
                                          C.c_void_p(forced.data_ptr() if use_forced else None),
                                          C.c_void_p(h.data_ptr()), 1,
-                                         C.c_void_p(h16.data_ptr() if h16 is not None else None), _stream())
+                                         _ptr(h16), _ptr(h16lo), _stream())
         assert rc == 0
         torch.cuda.synchronize()
         assert np.array_equal(tok[:, j].cpu().numpy(), ref)
         assert np.array_equal(out[:, j].cpu().numpy(), lg[:, :n_bins])
         feed = forced[:, j].cpu().numpy().clip(0, n_bins - 1) if use_forced else ref
         assert np.array_equal(h.cpu().numpy(), _f(emb, dtype)[feed].astype(np.float32))
-        if h16 is not None:
+        if h16 is not None:  # fp16 pair of the fed row: (embedding, 0)
             assert np.array_equal(h16.cpu().numpy(), emb[feed])
+            assert not h16lo.float().abs().sum().item()
 
 
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
-@pytest.mark.parametrize("M", [1, 5, 16])
+@pytest.mark.parametrize("M", [1, 5, 8, 9, 16])
 @pytest.mark.parametrize("K", [256, 1024, 4096])
-def test_gemv_rmsnorm(probe, epi, M, K):
-    """Fused RMSNorm GEMV on the fp16 residual copy x: y = W (x / rms(x)) with the statistic
-    from the same fp16 values; fp16 products are exact in the fp32 accumulator, so the bound
-    is the accumulation (and, for SwiGLU, the fp16 output rounding)."""
+@pytest.mark.parametrize("pair", [False, True])
+def test_gemv_rmsnorm(probe, epi, M, K, pair):
+    """Fused RMSNorm GEMV on the fp16 copy x = hi of the residual rows (or the pair x = hi + lo):
+    y = W x / rms(hi), the statistic taken from hi; fp16 products are exact in the fp32
+    accumulator, so the bound is the accumulation (and, for plain SwiGLU, the fp16 output
+    rounding)."""
     import torch
     N, eps = 256, 1e-5
-    log(f"gemv_rmsnorm epi={epi} M={M} K={K}")
-    x = (W.random_gaussian((M, K), 21, M, K, dtype="f32") * 4.0).astype(np.float16)
+    log(f"gemv_rmsnorm epi={epi} M={M} K={K} pair={pair}")
+    h = W.random_gaussian((M, K), 21, M, K, dtype="f32") * 4.0
+    if pair:
+        hi, lo = _pair(h)
+        x64 = hi.astype(np.float64) + lo.astype(np.float64)
+    else:
+        hi, lo = h.astype(np.float16), None
+        x64 = hi.astype(np.float64)
     Wt = _rand((N, K), 23, K, dtype="f16", std=0.05)
-    x64 = x.astype(np.float64)
-    rs = 1.0 / np.sqrt(np.mean(x64 * x64, axis=-1, keepdims=True) + eps)
+    h64 = hi.astype(np.float64)
+    rs = 1.0 / np.sqrt(np.mean(h64 * h64, axis=-1, keepdims=True) + eps)
     y = (x64 * rs) @ _f(Wt, "f16").T
     with16 = epi == EPI_RESID
     if epi == EPI_SWIGLU:
@@ -200,19 +249,107 @@ def test_gemv_rmsnorm(probe, epi, M, K):
         out = torch.from_numpy(h0.copy() if epi == EPI_RESID else np.zeros_like(h0)).cuda()
         ldo = N
         ref = y + (h0 if epi == EPI_RESID else 0.0)
-    out16 = torch.zeros((M, N), dtype=torch.float16, device="cuda") if with16 else None
-    xd, wd = torch.from_numpy(x).cuda(), _dev(Wt, "f16")  # keep both alive across the launch
-    rc = probe.ams_probe_gemv_rmsnorm(2, epi, C.c_void_p(xd.data_ptr()), C.c_float(eps), C.c_void_p(wd.data_ptr()),
-                                      M, N, K, C.c_void_p(out.data_ptr()), ldo,
-                                      C.c_void_p(out16.data_ptr() if with16 else None), _stream())
+    o16 = torch.zeros((M, N), dtype=torch.float16, device="cuda") if with16 else None
+    olo = None
+    if pair and epi != EPI_STORE:
+        olo = torch.zeros(tuple(out.shape), dtype=torch.float16, device="cuda")
+    hd, wd = torch.from_numpy(hi).cuda(), _dev(Wt, "f16")  # keep every input alive across the launch
+    lod = torch.from_numpy(lo).cuda() if pair else None
+    rc = probe.ams_probe_gemv_rmsnorm(2, epi, _ptr(hd), _ptr(lod), C.c_float(eps), _ptr(wd), M, N, K, _ptr(out), ldo,
+                                      _ptr(o16), _ptr(olo), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().astype(np.float64)
+    if pair and epi == EPI_SWIGLU:
+        got = got + olo.float().cpu().numpy()
     scale = max(1.0, float(np.max(np.abs(ref))))
     tol = 2e-5 * scale * np.sqrt(K / 128)
-    if epi == EPI_SWIGLU:
+    if epi == EPI_SWIGLU and not pair:
         tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
     err = float(np.max(np.abs(got - ref)))
     assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
     if with16:
-        assert torch.equal(out16, out.half())
+        assert torch.equal(o16, out.half())
+        if pair:
+            assert torch.equal(olo, (out - out.half().float()).half())
+
+
+def _rope_tab(cap, dh, theta=10000.0):
+    half = dh // 2
+    ang = np.arange(cap)[:, None] * theta ** (-2.0 * np.arange(half)[None, :] / dh)
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)  # [cap][half][2]
+
+
+def _round(x, dtype):
+    return x.astype(np.float16).astype(np.float64) if dtype == "f16" else x.astype(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype,dh,cap,lens,jpos,splits", [
+    ("f32", 64, 512, [300, 17], 0, 1),        # two block rounds per wave
+    ("f32", 128, 512, [301, 0, 128], 2, 1),   # three rounds; an empty cached prefix
+    ("f16", 64, 1024, [700, 5], 1, 1),        # two rounds of 512 keys
+    ("f16", 128, 1024, [600, 63, 64, 65], 0, 1),
+    ("f16", 128, 320, [294], 0, 5),           # split keys, merged
+    ("f16", 64, 256, [2, 130], 0, 4),         # splits beyond a short row stay empty
+    ("f32", 64, 512, [260, 3], 5, 8),
+])
+def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
+    """Decode attention of one fed-back token per row against the plain definition: the
+    query and the new key rotated (rotate-half RoPE), the new key and value rounded to the
+    slab type and appended at p = lens[b] + jpos, softmax(K q / sqrt(dh)) V over keys 0..p."""
+    import torch
+    B, H = len(lens), 2
+    d, half = H * dh, dh // 2
+    log(f"attn_decode {dtype} dh={dh} cap={cap} lens={lens} jpos={jpos} splits={splits}")
+    np_t = np.float16 if dtype == "f16" else np.float32
+    qkv = W.random_gaussian((B, 3 * d), 31, dh, cap, dtype="f32")
+    K = W.random_gaussian((B, H, cap, dh), 32, dh, cap, dtype="f32").astype(np_t)
+    V = W.random_gaussian((B, H, cap, dh), 33, dh, cap, dtype="f32").astype(np_t)
+    tab = _rope_tab(cap, dh)
+    qkv_d, K_d, V_d = _dev(qkv, dtype), _dev(K, dtype), _dev(V, dtype)
+    tab_d = _dev(tab, "f32")
+    lens_d = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    part = torch.zeros((B * H * (cap // 64) * (dh + 2),), dtype=torch.float32, device="cuda")
+    o = torch.zeros((B, d), dtype=torch.float16 if dtype == "f16" else torch.float32, device="cuda")
+    olo = torch.zeros((B, d), dtype=torch.float16, device="cuda") if dtype == "f16" else None  # rounding error of o
+    rc = probe.ams_probe_attn_decode(CT[dtype], C.c_void_p(qkv_d.data_ptr()), C.c_void_p(lens_d.data_ptr()), jpos,
+                                     B, H, dh, cap, splits, C.c_void_p(tab_d.data_ptr()), C.c_void_p(K_d.data_ptr()),
+                                     C.c_void_p(V_d.data_ptr()), C.c_void_p(part.data_ptr()),
+                                     C.c_void_p(o.data_ptr()), _ptr(olo), _stream())
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy().astype(np.float64)
+    if olo is not None:  # the output as the fp16 pair carries it
+        got = got + olo.float().cpu().numpy()
+    K_after, V_after = K_d.cpu().numpy(), V_d.cpu().numpy()
+    for b in range(B):
+        p = lens[b] + jpos
+        cs = tab[p].astype(np.float64)  # [half][2]
+        for h in range(H):
+            x = qkv[b].astype(np.float64)
+            q, k, v = (x[j * d + h * dh:j * d + (h + 1) * dh] for j in range(3))
+            rot = lambda z: np.concatenate([z[:half] * cs[:, 0] - z[half:] * cs[:, 1],
+                                            z[:half] * cs[:, 1] + z[half:] * cs[:, 0]])
+            # the kernel appended the new token's K/V at p; it rotates in fp32, so the stored key
+            # is the rounded exact rotation up to fp32 rounding of the two products (bounded by
+            # their magnitudes, as they may cancel) plus one unit of the slab type
+            ulp = 2.0 ** -10 if dtype == "f16" else 2.0 ** -23
+            k_st, v_st = K_after[b, h, p].astype(np.float64), V_after[b, h, p].astype(np.float64)
+            k_def = rot(k)
+            ak, ac, asn = np.abs(k), np.abs(cs[:, 0]), np.abs(cs[:, 1])
+            terms = np.concatenate([ak[:half] * ac + ak[half:] * asn, ak[:half] * asn + ak[half:] * ac])
+            assert np.all(np.abs(k_st - k_def) <= ulp * np.abs(k_def) + 2.0 ** -22 * terms)
+            assert np.array_equal(v_st, _round(v, dtype))
+            k_new, v_new = k_st, v_st
+            Kc = np.concatenate([K[b, h, :p].astype(np.float64), k_new[None]])
+            Vc = np.concatenate([V[b, h, :p].astype(np.float64), v_new[None]])
+            s = Kc @ (rot(q) / np.sqrt(dh))
+            w = np.exp(s - s.max())
+            ref = (w / w.sum()) @ Vc
+            g = got[b, h * dh:(h + 1) * dh]
+            tol = 5e-6 * np.max(np.abs(ref)) + 1e-6
+            assert np.all(np.abs(g - ref) <= tol), (b, h, float(np.max(np.abs(g - ref))))
+    mask = np.ones(K.shape[:3], bool)
+    for b in range(B):
+        mask[b, :, lens[b] + jpos] = False
+    assert np.array_equal(K_after[mask], K[mask]) and np.array_equal(V_after[mask], V[mask])
