@@ -384,6 +384,137 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const f16* __restrict__ u, c
 }
 
 // ----------------------------------------------------------------------------
+// big f16 MFMA tiles: large prefix builds (enough 256 x 256 tiles to fill the chip)
+//
+// 256 (tokens) x 256 (weight rows) per workgroup, eight waves of 64 x 128
+// (4 x 2), K steps of 64 double-buffered in LDS.  The tiles move from global
+// memory straight into LDS (global_load_lds_dwordx4: each wave instruction
+// fills 1 KB of LDS, lane i the i-th 16 bytes), so no registers stage them.
+// A tile row is 128 bytes (8 chunks of 16); chunk c of row R sits in slot
+// c ^ (R & 7), which the DMA realises by choosing each lane's source chunk,
+// and which keeps the 16-byte fragment reads of 8 consecutive rows on 8
+// distinct bank groups.  A wave reuses each A fragment for 8 B fragments and
+// each B fragment for 4 A fragments.  The epilogue runs from registers: a lane
+// holds 4 consecutive tokens of one weight row per 16 x 16 block, and the gate
+// and up blocks of a SwiGLU pair sit side by side in the same lane.
+
+constexpr int GBM = 256, GBN = 256, GBK = 64;
+constexpr int G_TILE = 256 * 128;         // bytes of one A or B tile (256 rows of 64 fp16)
+constexpr int G_LDS = 2 * 2 * G_TILE;      // double-buffered A and B
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// DMA of one K step: wave w moves 1 KB blocks 4w..4w+3 of the A tile and of
+// the B tile (8 rows each).  Lane i of a block: row R0 + i/8, slot i%8, source
+// chunk (i%8) ^ (row & 7).  A rows past the last valid one (alast) read it
+// again: they only feed outputs that are never stored.
+__device__ __forceinline__ void big_dma(unsigned char* stage, const f16* A, const f16* B, int K, int k0, int alast,
+                                        int wave, int lane) {
+  const int slot = lane & 7;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int blk = wave * 4 + q;
+    const int row = blk * 8 + (lane >> 3);
+    const int c = slot ^ (row & 7);
+    const int ar = row <= alast ? row : alast;
+    __builtin_amdgcn_global_load_lds((const void*)(A + (size_t)ar * K + k0 + c * 8), (lds_ptr)(stage + blk * 1024),
+                                     16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(B + (size_t)row * K + k0 + c * 8),
+                                     (lds_ptr)(stage + G_TILE + blk * 1024), 16, 0, 0);
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, const f16* __restrict__ W, int M,
+                                                  int N, int K, void* __restrict__ out, int ldo) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char gsm[];  // [2 stages][A tile | B tile]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;  // wave tile: tokens wm*64.., weight rows wn*128..
+  // tile order: workgroups are dispatched round-robin over the 8 XCDs, so XCD x
+  // (ids = x mod 8) takes a contiguous range of the tile sequence, which walks
+  // groups of 8 token tiles down each weight tile: tiles that share a weight
+  // (or token) tile run close together on one XCD's L2
+  const int tm_n = (M + GBM - 1) / GBM, tn_n = N / GBN, T = tm_n * tn_n;
+  const int L = blockIdx.x, xcd = L & 7, per = T >> 3, rem = T & 7;
+  const int Lx = xcd * per + (xcd < rem ? xcd : rem) + (L >> 3);
+  const int grp = Lx / (8 * tn_n), first_m = grp * 8;
+  const int gm = tm_n - first_m < 8 ? tm_n - first_m : 8;
+  const int in_grp = Lx - grp * 8 * tn_n;
+  const int m0 = (first_m + in_grp % gm) * GBM, n0 = (in_grp / gm) * GBN;
+  const int alast = M - 1 - m0;  // last valid A row of this tile (>= 0)
+  const f16* A = u + (size_t)m0 * K;
+  const f16* B = W + (size_t)n0 * K;
+
+  f32x4 acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // fragment rows of this lane: A rows wm*64 + 16 i + r, B rows wn*128 + 16 j + r (all = r mod 8)
+  const int sw = r & 7;
+  const int KT = K / GBK;
+  big_dma(gsm, A, B, K, 0, alast, wave, lane);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    unsigned char* cur = gsm + (kt & 1) * 2 * G_TILE;
+    if (kt + 1 < KT) big_dma(gsm + ((kt + 1) & 1) * 2 * G_TILE, A, B, K, (kt + 1) * GBK, alast, wave, lane);
+    const unsigned char* Ab = cur + (wm * 64 + r) * 128;
+    const unsigned char* Bb = cur + G_TILE + (wn * 128 + r) * 128;
+#pragma unroll
+    for (int ks = 0; ks < GBK / 32; ++ks) {
+      const int off = (((4 * ks + g) ^ sw) << 4);
+      half8 af[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *(const half8*)(Ab + i * 16 * 128 + off);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const half8 bf = *(const half8*)(Bb + j * 16 * 128 + off);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf, acc[i][j], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA into the other stage has landed
+    __syncthreads();
+  }
+
+  // block (i, j): lane holds tokens tm + 4g + e of weight row tn + r
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tm = m0 + wm * 64 + i * 16 + 4 * g;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int tok = tm + e;
+      if (tok >= M) continue;
+      if constexpr (EPI == EPI_SWIGLU) {
+        // blocks 2p (gate) and 2p+1 (up) of the packed interleave; output column (n >> 1) + r
+#pragma unroll
+        for (int pr = 0; pr < 4; ++pr) {
+          const int col = ((n0 + wn * 128) >> 1) + pr * 16 + r;
+          st<f16>((f16*)out, (size_t)tok * ldo + col, silu(acc[i][2 * pr][e]) * acc[i][2 * pr + 1][e]);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float* p = (float*)out + (size_t)tok * ldo + n0 + wn * 128 + j * 16 + r;
+          if constexpr (EPI == EPI_STORE) *p = acc[i][j][e];
+          else *p += acc[i][j][e];
+        }
+      }
+    }
+  }
+}
+
+template <int EPI>
+static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {
+  hipLaunchKernelGGL((k_gemm_big<EPI>), dim3((N / GBN) * ((M + GBM - 1) / GBM)), dim3(512), G_LDS, s, u, W, M, N,
+                     K, out, ldo);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
 // fp32 model dtype
 
 constexpr int FBM = 64, FBN = 64, FBK = 16;
@@ -447,9 +578,22 @@ static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, i
     const SkinnyArgs a{(const f16*)u, (const f16*)ulo, 0.f, (const f16*)W, M, K, out, ldo, (f16*)o16, (f16*)olo};
     return skinny_dispatch<EPI, false>(a, N, s);
   }
+  // 256 x 256 tiles when they alone fill the chip (one workgroup per CU), 128 x 128 otherwise
+  if (N % GBN == 0 && (size_t)(N / GBN) * ((M + GBM - 1) / GBM) >= 256)
+    return launch_big<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
+}
+
+hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (N % GBN != 0 || K % GBK != 0) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_STORE: return launch_big<EPI_STORE>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+    case EPI_RESID: return launch_big<EPI_RESID>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+    default: return launch_big<EPI_SWIGLU>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+  }
 }
 
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo,

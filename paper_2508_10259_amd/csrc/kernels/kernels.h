@@ -42,6 +42,10 @@ constexpr int GU_BLOCK = 16;
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out,
                 int ldo, hipStream_t s, const void* ulo = nullptr, void* o16 = nullptr, void* olo = nullptr);
 
+// The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
+// callable for any M (N a multiple of 256, K of 64); same epilogues.
+hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s);
+
 // Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16), on the fp16
 // copy x = hhi (+ hlo, its rounding error, when non-NULL) of the residual rows:
 // y[m] = (W x[m]) / sqrt(mean(hhi[m]^2) + eps), followed by the epilogue as in

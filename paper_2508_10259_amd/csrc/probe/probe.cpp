@@ -13,6 +13,10 @@ int ams_probe_gemm(int dtype, int epi, const void* u, const void* ulo, const voi
   return (int)ams::gemm(dtype, epi, u, W, M, N, K, out, ldo, (hipStream_t)stream, ulo, o16, olo);
 }
 
+int ams_probe_gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, void* stream) {
+  return (int)ams::gemm_big(epi, u, W, M, N, K, out, ldo, (hipStream_t)stream);
+}
+
 int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* ulo, void* stream) {
   return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream, ulo);
 }

@@ -353,3 +353,37 @@ def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     for b in range(B):
         mask[b, :, lens[b] + jpos] = False
     assert np.array_equal(K_after[mask], K[mask]) and np.array_equal(V_after[mask], V[mask])
+
+
+@pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
+@pytest.mark.parametrize("M,N,K", [(1, 256, 64), (100, 256, 384), (256, 512, 1024), (300, 256, 384),
+                                   (513, 768, 1024)])
+def test_gemm_big(probe, epi, M, N, K):
+    """The 256 x 256-tile prefill GEMM (direct-to-LDS tiles, swizzled rows) on ragged token
+    counts, against the exact product of its fp16 inputs."""
+    import torch
+    log(f"gemm_big epi={epi} M={M} N={N} K={K}")
+    u = _rand((M, K), 41, M, K)
+    Wt = _rand((N, K), 42, N, K, std=0.05)
+    y = _f(u, "f16") @ _f(Wt, "f16").T
+    if epi == EPI_SWIGLU:
+        out = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
+        ldo = N // 2
+        g, up = _unpack_gu(y.T, N // 2)
+        ref = (_silu(g) * up).T
+    else:
+        h0 = W.random_gaussian((M, N), 43, M, dtype="f32")
+        out = torch.from_numpy(h0.copy() if epi == EPI_RESID else np.zeros_like(h0)).cuda()
+        ldo = N
+        ref = y + (h0.astype(np.float64) if epi == EPI_RESID else 0.0)
+    ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
+    rc = probe.ams_probe_gemm_big(epi, _ptr(ud), _ptr(Wd), M, N, K, _ptr(out), ldo, _stream())
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().astype(np.float64)
+    scale = max(1.0, float(np.max(np.abs(ref))))
+    tol = 2e-5 * scale * np.sqrt(K / 128)
+    if epi == EPI_SWIGLU:
+        tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
+    err = float(np.max(np.abs(got - ref)))
+    assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
