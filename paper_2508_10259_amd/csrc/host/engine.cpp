@@ -22,7 +22,7 @@ static const char* off(const void* p, size_t bytes) { return (const char*)p + by
 
 // Decode runs its RMSNorms inside the projection GEMVs for fp16 compute and up
 // to 16 rows (see norm_proj).
-static bool fused_norm(const Ctx& c) { return c.model->ct == DT_F16 && c.lay.batch <= 16; }
+static bool fused_norm(const Ctx& c, int rows) { return c.model->ct == DT_F16 && rows <= 16; }
 
 hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err) {
   // bf16 weights become fp16 in the packed copy: exact for |w| >= 2^-14, an
@@ -113,8 +113,8 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
     TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, fused_norm(c) ? c.h_last16() : nullptr,
-                    fused_norm(c) ? c.h_last16lo() : nullptr));
+    const bool f16 = c.model->ct == DT_F16;  // the fp16 pair of h_last feeds fused-RMSNorm heads
+    TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, f16 ? c.h_last16() : nullptr, f16 ? c.h_last16lo() : nullptr));
   }
   TRY(update_lens(c.lens(), md + 4 * B + 1, B, set_lens, s));
   return hipSuccess;
@@ -125,78 +125,122 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
 // about 22 significant bits; the MFMA count doubles at most, the weight stream
 // (the bound) does not change.
 //
+// Rows is a view of the per-row buffers from row r0 on (n rows): every decode
+// kernel addresses rows relative to the pointers it is given.
+struct Rows {
+  int r0, n;
+  size_t ces;  // bytes of a compute-type element
+  const Ctx* c;
+  char* at(size_t off, size_t row_bytes) const { return c->ws + off + (size_t)r0 * row_bytes; }
+  float* h() const { return (float*)at(c->lay.h, c->model->cfg.d_model * 4); }
+  void* u() const { return at(c->lay.u, c->model->cfg.d_model * ces); }
+  float* qkv() const { return (float*)at(c->lay.qkv, 3 * c->model->cfg.d_model * 4); }
+  void* o() const { return at(c->lay.o, c->model->cfg.d_model * ces); }
+  void* a() const { return at(c->lay.a, c->model->cfg.d_ffn * ces); }
+  float* h_last() const { return (float*)at(c->lay.h_last, c->model->cfg.d_model * 4); }
+  void* h_last16() const { return at(c->lay.h_last16, c->model->cfg.d_model * 2); }
+  void* h_last16lo() const { return at(c->lay.h_last16lo, c->model->cfg.d_model * 2); }
+  void* hlo() const { return at(c->lay.hlo, c->model->cfg.d_model * 2); }
+  void* olo() const { return at(c->lay.olo, c->model->cfg.d_model * 2); }
+  void* alo() const { return at(c->lay.alo, c->model->cfg.d_ffn * 2); }
+  float* logits() const { return (float*)at(c->lay.logits, bins_padded(c->model->cfg) * 4); }
+  int32_t* lens() const { return (int32_t*)at(c->lay.lens, 4); }
+  float* part() const {
+    const Cfg& m = c->model->cfg;
+    return (float*)at(c->lay.part, (size_t)m.n_heads * c->splits * (m.head_dim + 2) * 4);
+  }
+  void* kslab(int l) const {
+    const Cfg& m = c->model->cfg;
+    return (char*)c->kslab(l) + (size_t)r0 * m.n_heads * c->lay.capacity * m.head_dim * ces;
+  }
+  void* vslab(int l) const {
+    const Cfg& m = c->model->cfg;
+    return (char*)c->vslab(l) + (size_t)r0 * m.n_heads * c->lay.capacity * m.head_dim * ces;
+  }
+};
+
 // Projection of a normalised input.  Up to 16 fp16 rows run the GEMV with the
 // RMSNorm fused, reading the fp16 pair of the residual rows (hhi, hlo) that
 // their producers (residual GEMV epilogue, feed, gather of the last prefix
 // token) write beside h; otherwise rmsnorm writes the pair u + hlo from h
 // first (the fused copies are unused then, so hlo serves as u's lo part).
-static hipError_t norm_proj(Ctx& c, int epi, const float* h, const void* hhi, const void* hlo, const void* W, int N,
-                            int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err) {
-  const Model& md = *c.model;
-  const int B = c.lay.batch;
+static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* hhi, const void* hlo, const void* W,
+                            int N, int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err) {
+  const Model& md = *g.c->model;
   const float eps = md.cfg.rms_eps;
-  if (fused_norm(c)) {
-    TRY(gemv_rmsnorm(md.ct, epi, hhi, eps, W, B, N, K, out, ldo, s, hlo, nullptr, olo));
+  if (fused_norm(*g.c, g.n)) {
+    TRY(gemv_rmsnorm(md.ct, epi, hhi, eps, W, g.n, N, K, out, ldo, s, hlo, nullptr, olo));
   } else {
-    void* ulo = md.ct == DT_F16 ? c.hlo() : nullptr;
-    TRY(rmsnorm(md.ct, h, B, K, eps, c.u(), s, ulo));
-    TRY(gemm(md.ct, epi, c.u(), W, B, N, K, out, ldo, s, ulo, nullptr, olo));
+    void* ulo = md.ct == DT_F16 ? g.hlo() : nullptr;
+    TRY(rmsnorm(md.ct, h, g.n, K, eps, g.u(), s, ulo));
+    TRY(gemm(md.ct, epi, g.u(), W, g.n, N, K, out, ldo, s, ulo, nullptr, olo));
   }
   return hipSuccess;
 }
 
-// One decoder layer for the B fed-back tokens at positions lens[b] + jpos.
-static hipError_t layer_decode(Ctx& c, int l, int jpos, hipStream_t s, std::string& err) {
+// One decoder layer for a group's fed-back tokens at positions lens[b] + jpos.
+static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, std::string& err) {
+  const Ctx& c = *g.c;
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
-  const int d = m.d_model, F = m.d_ffn, dt = md.ct, B = c.lay.batch;
-  const bool f16 = dt == DT_F16, fused = fused_norm(c);
-  void* hhi = fused ? c.u() : nullptr;   // fp16 pair of h (fused path)
-  void* hlo = fused ? c.hlo() : nullptr;
-  void* olo = f16 ? c.olo() : nullptr;   // lo parts of the attention and SwiGLU outputs
-  void* alo = f16 ? c.alo() : nullptr;
-  if (norm_proj(c, EPI_STORE, c.h(), hhi, hlo, md.wqkv(l), 3 * d, d, c.qkv(), 3 * d, nullptr, s, err) != hipSuccess)
+  const int d = m.d_model, F = m.d_ffn, dt = md.ct, B = g.n;
+  const bool f16 = dt == DT_F16, fused = fused_norm(c, B);
+  void* hhi = fused ? g.u() : nullptr;   // fp16 pair of h (fused path)
+  void* hlo = fused ? g.hlo() : nullptr;
+  void* olo = f16 ? g.olo() : nullptr;   // lo parts of the attention and SwiGLU outputs
+  void* alo = f16 ? g.alo() : nullptr;
+  if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(attn_decode(dt, c.qkv(), c.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
-                  c.kslab(l), c.vslab(l), c.part(), c.o(), s, olo));
-  if (c.splits > 1) TRY(attn_merge(dt, c.part(), B, m.n_heads, m.head_dim, c.splits, c.o(), s, olo));
-  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), B, d, d, c.h(), d, s, olo, hhi, hlo));
-  if (norm_proj(c, EPI_SWIGLU, c.h(), hhi, hlo, md.wgu(l), 2 * F, d, c.a(), F, alo, s, err) != hipSuccess)
+  TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
+                  g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo));
+  if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
+  TRY(gemm(dt, EPI_RESID, g.o(), md.wo(l), B, d, d, g.h(), d, s, olo, hhi, hlo));
+  if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), B, d, F, c.h(), d, s, alo, hhi, hlo));
+  TRY(gemm(dt, EPI_RESID, g.a(), md.wd(l), B, d, F, g.h(), d, s, alo, hhi, hlo));
   return hipSuccess;
 }
 
 // Action head for decode position j: final RMSNorm + bin logits (the
 // projection GEMV over the padded head rows), then argmax/outputs/feed.
-static hipError_t head(Ctx& c, const float* hin, const void* hhi, const void* hlo, int A, int j, int32_t* tok,
+// tok / logits / forced point at the group's first row.
+static hipError_t head(const Rows& g, const float* hin, const void* hhi, const void* hlo, int A, int j, int32_t* tok,
                        float* logits, const int32_t* forced, hipStream_t s, std::string& err) {
-  const Model& md = *c.model;
+  const Model& md = *g.c->model;
   const Cfg& m = md.cfg;
-  const int B = c.lay.batch, d = m.d_model, nbp = bins_padded(m);
-  const bool fused = fused_norm(c);
-  if (norm_proj(c, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, c.logits(), nbp, nullptr, s, err) != hipSuccess)
+  const int d = m.d_model, nbp = bins_padded(m);
+  const bool fused = fused_norm(*g.c, g.n);
+  if (norm_proj(g, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, g.logits(), nbp, nullptr, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(argmax_feed(md.ct, c.logits(), nbp, md.bin_embed(), B, d, m.n_bins, A, j, tok, logits, forced, c.h(),
-                  j + 1 < A, s, fused ? c.u() : nullptr, fused ? c.hlo() : nullptr));
+  TRY(argmax_feed(md.ct, g.logits(), nbp, md.bin_embed(), g.n, d, m.n_bins, A, j, tok, logits, forced, g.h(),
+                  j + 1 < A, s, fused ? g.u() : nullptr, fused ? g.hlo() : nullptr));
   return hipSuccess;
 }
 
-static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
-                                 std::string& err) {
-  const Cfg& m = c.model->cfg;
-  const bool fused = fused_norm(c);
-  if (head(c, c.h_last(), fused ? c.h_last16() : nullptr, fused ? c.h_last16lo() : nullptr, A, 0, tok, logits,
-           forced, s, err) != hipSuccess)
+static hipError_t decode_rows(const Rows& g, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
+                              std::string& err) {
+  const Cfg& m = g.c->model->cfg;
+  const bool fused = fused_norm(*g.c, g.n);
+  int32_t* gt = tok + (size_t)g.r0 * A;
+  float* gl = logits ? logits + (size_t)g.r0 * A * m.n_bins : nullptr;
+  const int32_t* gf = forced ? forced + (size_t)g.r0 * A : nullptr;
+  if (head(g, g.h_last(), fused ? g.h_last16() : nullptr, fused ? g.h_last16lo() : nullptr, A, 0, gt, gl, gf, s,
+           err) != hipSuccess)
     return hipErrorLaunchFailure;
   for (int j = 1; j < A; ++j) {
     for (int l = 0; l < m.n_layers; ++l)
-      if (layer_decode(c, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    if (head(c, c.h(), fused ? c.u() : nullptr, fused ? c.hlo() : nullptr, A, j, tok, logits, forced, s, err) !=
-        hipSuccess)
+      if (layer_decode(g, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
+    if (head(g, g.h(), fused ? g.u() : nullptr, fused ? g.hlo() : nullptr, A, j, gt, gl, gf, s, err) != hipSuccess)
       return hipErrorLaunchFailure;
   }
   return hipSuccess;
+}
+
+// The greedy loop of a step over all rows.
+static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
+                                 std::string& err) {
+  const size_t ces = c.model->ct == DT_F16 ? 2 : 4;
+  return decode_rows(Rows{0, c.lay.batch, ces, &c}, A, tok, logits, forced, s, err);
 }
 
 static bool graphs_enabled() {

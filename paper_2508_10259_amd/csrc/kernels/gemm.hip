@@ -2,7 +2,7 @@
 //
 //  * k_gemm_skinny  (fp16, M <= 64 tokens: the per-action decode pass).  HBM
 //    bound on the weights: every weight byte is read exactly once.  A
-//    workgroup owns a strip of 16 (or 32 for SwiGLU) packed weight rows; its
+//    workgroup owns a strip of 16 (or 32 for SwiGLU: 16 gate + 16 up) packed weight rows; its
 //    waves split K in chunks of 128 and run v_mfma_f32_16x16x32_f16 with the
 //    weight rows on the M side and up to 64 tokens as 1..4 column blocks, so a
 //    weight fragment is loaded once and reused for every token block.  The
@@ -21,6 +21,7 @@
 namespace ams {
 
 __device__ __forceinline__ half8 as_half8(uint4 v) { return __builtin_bit_cast(half8, v); }
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
 // ----------------------------------------------------------------------------
 // skinny: M <= 64
@@ -63,18 +64,26 @@ struct SkinnyArgs {
   f16* olo;  // RESID / SWIGLU, or NULL
 };
 
+// most waves per workgroup: 16 for the SwiGLU strip with one token block (its
+// two chunks in flight fit 128 VGPRs), 8 otherwise (256 VGPRs)
+template <int RB, int MB, int LO>
+constexpr int skinny_max_waves() {
+  return RB == 2 && MB == 1 && LO != 2 ? 16 : 8;
+}
+
 template <int RB, int MB, int LO>
 constexpr int skinny_cpw() {
   return (RB + MB * (LO == 2 ? 2 : 1)) <= 2 ? 4 : ((RB + MB * (LO == 2 ? 2 : 1)) <= 4 ? 2 : 1);
 }
 
 template <int RB, int MB, int EPI, bool NRM, int LO>
-__global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
+__global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_skinny(SkinnyArgs a) {
   static_assert(!NRM || MB == 1, "the fused RMSNorm handles up to 16 tokens");
   static_assert(LO != 1 || MB == 1, "the packed pair handles up to 8 tokens");
   constexpr int LB = LO == 2 ? MB : 1;  // lo fragment blocks (unused unless LO == 2)
   extern __shared__ float red[];  // [nw][RB][MB][64 lanes][4], then (NRM) wsum[<=16 waves][16] + rstd[16]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: chunk loops branch on scalars
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * (RB * 16);
   const int M = a.M, K = a.K, ldo = a.ldo;
@@ -91,19 +100,20 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
   const f16* wrow[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) wrow[rb] = a.W + (size_t)(n0 + rb * 16 + r) * K + g * 8;
-  // B-operand rows of this lane: token mb*16 + r (LO == 1: token r & 7, hi for r < 8, lo above)
-  bool uok[MB];
+  // B-operand rows of this lane: token mb*16 + r (LO == 1: token r & 7, hi for r < 8, lo above).
+  // Columns of tokens >= M read token 0 instead of being masked (a masked load
+  // costs a branch per load): they only feed output columns that are never
+  // stored, and statistics that are never read.
   const f16* urow[MB];
   const f16* lrow[LB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int tok = LO == 1 ? (r & 7) : mb * 16 + r;
-    uok[mb] = tok < M;
-    const size_t off = (size_t)(uok[mb] ? tok : 0) * K + g * 8;
+    const size_t off = (size_t)(tok < M ? tok : 0) * K + g * 8;
     urow[mb] = (LO == 1 && r >= 8 ? a.xlo : a.xhi) + off;
     if constexpr (LO == 2) lrow[mb] = a.xlo + off;
   }
-  float ss = 0.f;  // NRM: this lane's share of sum(x^2) of its token
+  float ss0 = 0.f, ss1 = 0.f;  // NRM: this lane's share of sum(x^2) of its token (two chains)
 
   // the residual epilogue's h values do not depend on this kernel: request them first
   constexpr int EPT = (MB * 256 + 63) / 64;  // epilogue values per thread at the smallest workgroup
@@ -115,9 +125,9 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
       const int mb = idx >> 8, ln = (idx >> 2) & 63, i = idx & 3;
       const int tok = mb * 16 + (ln & 15), row = 4 * (ln >> 4) + i;
       const bool ok = idx < MB * 256 && tok < M && (LO != 1 || (ln & 15) < 8);
+      const size_t at = (size_t)(ok ? tok : 0) * ldo + n0 + row;  // unused values read row 0
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        hres[rb * EPT + e] = ok ? ((const float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] : 0.f;
+      for (int rb = 0; rb < RB; ++rb) hres[rb * EPT + e] = ((const float*)a.out)[at + rb * 16];
     }
   }
 
@@ -137,9 +147,8 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            fu[j][mb][i] = uok[mb] ? *(const uint4*)(urow[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
-            if constexpr (LO == 2)
-              fl[j][mb][i] = uok[mb] ? *(const uint4*)(lrow[mb] + kb + 32 * i) : uint4{0u, 0u, 0u, 0u};
+            fu[j][mb][i] = *(const uint4*)(urow[mb] + kb + 32 * i);
+            if constexpr (LO == 2) fl[j][mb][i] = *(const uint4*)(lrow[mb] + kb + 32 * i);
           }
       }
     }
@@ -151,11 +160,12 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const half8 v = as_half8(fu[j][mb][i]);
-            if constexpr (NRM) {
-              if (LO != 1 || r < 8) {  // the statistic reads hi only
-#pragma unroll
-                for (int e = 0; e < 8; ++e) ss = fmaf((float)v[e], (float)v[e], ss);
-              }
+            if constexpr (NRM) {  // the statistic reads hi only (LO == 1: lanes r >= 8 are unused)
+              const half2v* p2 = (const half2v*)&fu[j][mb][i];
+              ss0 = __builtin_amdgcn_fdot2(p2[0], p2[0], ss0, false);
+              ss1 = __builtin_amdgcn_fdot2(p2[1], p2[1], ss1, false);
+              ss0 = __builtin_amdgcn_fdot2(p2[2], p2[2], ss0, false);
+              ss1 = __builtin_amdgcn_fdot2(p2[3], p2[3], ss1, false);
             }
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) {
@@ -178,6 +188,7 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
   float* rstd = red + (size_t)nw * RB * MB * 256 + 256;
   if constexpr (NRM) {
     float* wsum = rstd - 256;  // [16 waves][16 tokens]
+    float ss = ss0 + ss1;
     ss += __shfl_xor(ss, 16, 64);
     ss += __shfl_xor(ss, 32, 64);
     if (lane < 16) wsum[wave * 16 + lane] = ss;
@@ -190,7 +201,16 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
   }
   __syncthreads();
 
-  // value (rb, mb, ln, i) is packed row n0 + rb*16 + 4*(ln>>4) + i, B column mb*16 + (ln&15)
+  // value (rb, mb, ln, i) is packed row n0 + rb*16 + 4*(ln>>4) + i, B column mb*16 + (ln&15);
+  // summed over the waves (and, LO == 1, over the hi and lo columns ln and ln+8)
+  auto reduced = [&](int rb, int mb, int ln, int i) {
+    float t = 0.f;
+    for (int w = 0; w < nw; ++w) {
+      t += red[(((w * RB + rb) * MB + mb) * 64 + ln) * 4 + i];
+      if constexpr (LO == 1) t += red[(((w * RB + rb) * MB + mb) * 64 + ln + 8) * 4 + i];
+    }
+    return t;
+  };
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int idx = threadIdx.x + e * blockDim.x;
@@ -199,40 +219,37 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(SkinnyArgs a) {
     const int tok = mb * 16 + (ln & 15);
     if (tok >= M || (LO == 1 && (ln & 15) >= 8)) continue;
     const int row = 4 * (ln >> 4) + i;
-    float v[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float t = 0.f;
-      for (int w = 0; w < nw; ++w) {
-        t += red[(((w * RB + rb) * MB + mb) * 64 + ln) * 4 + i];
-        if constexpr (LO == 1) t += red[(((w * RB + rb) * MB + mb) * 64 + ln + 8) * 4 + i];
-      }
-      if constexpr (NRM) t *= rstd[tok];
-      v[rb] = t;
-    }
+    const float sc = NRM ? rstd[tok] : 1.f;
     if constexpr (EPI == EPI_STORE) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) ((float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] = v[rb];
+      for (int rb = 0; rb < RB; ++rb)
+        ((float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] = reduced(rb, mb, ln, i) * sc;
     } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const size_t o = (size_t)tok * ldo + n0 + rb * 16 + row;
-        const float hn = hres[rb * EPT + e] + v[rb];
+        const float hn = hres[rb * EPT + e] + reduced(rb, mb, ln, i) * sc;
         ((float*)a.out)[o] = hn;
         if (a.ohi) split16(hn, a.ohi, a.olo, o);
       }
-    } else {
-      split16(silu(v[0]) * v[RB - 1], (f16*)a.out, a.olo, (size_t)tok * ldo + (n0 >> 1) + row);
+    } else {  // the strip's first 16 rows are gate rows, the next 16 the up rows of the same outputs
+      const float gt = reduced(0, mb, ln, i) * sc, up = reduced(RB - 1, mb, ln, i) * sc;
+      split16(silu(gt) * up, (f16*)a.out, a.olo, (size_t)tok * ldo + (n0 >> 1) + row);
     }
   }
 }
 
 template <int RB, int MB, int EPI, bool NRM, int LO>
 static hipError_t launch_skinny(const SkinnyArgs& a, int N, hipStream_t s) {
+  // waves per workgroup: up to the variant's maximum, at most 64 KB of
+  // reduction LDS, and at least one chunk per wave; the 16-wave variant keeps
+  // a full batch of CPW chunks per wave (its chunks then go out in one round)
   const int nchunks = a.K >> 7;
-  int nw = 8;  // <= 512 threads: leaves 256 VGPRs for the chunks in flight
+  constexpr int MW = skinny_max_waves<RB, MB, LO>();
+  constexpr int PER = MW == 16 ? skinny_cpw<RB, MB, LO>() : 1;
+  int nw = MW;
   while (nw > 1 && nw * RB * MB * 1024 > 65536) nw >>= 1;
-  while (nw > 1 && nw > nchunks) nw >>= 1;
+  while (nw > 1 && nw * PER > nchunks) nw >>= 1;
   const size_t lds = (size_t)nw * RB * MB * 1024 + (NRM ? (256 + 16) * 4 : 0);
   hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM, LO>), dim3(N / (RB * 16)), dim3(64 * nw), lds, s, a);
   return hipGetLastError();

@@ -28,7 +28,8 @@ struct Segs {
 };
 
 // Gate/up rows are packed interleaved in blocks of 16: packed row 32i+j is
-// gate row 16i+j for j < 16 and up row 16i+j-16 otherwise.
+// gate row 16i+j for j < 16 and up row 16i+j-16 otherwise, so a 32-row strip
+// holds the gate and up rows of the same 16 SwiGLU outputs.
 constexpr int GU_BLOCK = 16;
 
 // y[m][n] = sum_k u[m][k] * W[n][k] followed by the epilogue:
