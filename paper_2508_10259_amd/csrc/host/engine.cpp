@@ -178,7 +178,24 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
   return hipSuccess;
 }
 
-// One decoder layer for a group's fed-back tokens at positions lens[b] + jpos.
+// h += W x for the decode rows (x = the pair x + xlo in fp16 compute), writing
+// the fp16 pair of the new rows to (hhi, hlo) when given.  Narrow projections
+// split K over more workgroups and add the partial sums in a reduction kernel.
+static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, const void* W, int K, void* hhi, void* hlo,
+                             hipStream_t s) {
+  const Ctx& c = *g.c;
+  const Model& md = *c.model;
+  const int d = md.cfg.d_model;
+  const int splits = md.ct == DT_F16 ? decode_ksplit(d, K) : 1;
+  if (splits > 1) {
+    hipError_t e = gemm_part(x, xlo, W, g.n, d, K, splits, c.kpart(), s);
+    if (e == hipSuccess) e = part_resid(c.kpart(), splits, g.n, d, g.h(), hhi, hlo, s);
+    return e;
+  }
+  return gemm(md.ct, EPI_RESID, x, W, g.n, d, K, g.h(), d, s, xlo, hhi, hlo);
+}
+
+// One decoder layer for the rows' fed-back tokens at positions lens[b] + jpos.
 static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, std::string& err) {
   const Ctx& c = *g.c;
   const Model& md = *c.model;
@@ -194,10 +211,10 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
   TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
                   g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
-  TRY(gemm(dt, EPI_RESID, g.o(), md.wo(l), B, d, d, g.h(), d, s, olo, hhi, hlo));
+  TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s));
   if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(gemm(dt, EPI_RESID, g.a(), md.wd(l), B, d, F, g.h(), d, s, alo, hhi, hlo));
+  TRY(resid_proj(g, g.a(), alo, md.wd(l), F, hhi, hlo, s));
   return hipSuccess;
 }
 

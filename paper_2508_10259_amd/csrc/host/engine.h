@@ -71,6 +71,7 @@ struct Ctx {
   void* hlo() const { return ws + lay.hlo; }
   void* olo() const { return ws + lay.olo; }
   void* alo() const { return ws + lay.alo; }
+  float* kpart() const { return (float*)(ws + lay.kpart); }
   float* part() const { return (float*)(ws + lay.part); }
   float* logits() const { return (float*)(ws + lay.logits); }
   float2* rope() const { return (float2*)(ws + lay.rope); }

@@ -76,7 +76,7 @@ inline ModelLayout model_layout(const Cfg& c) {
 struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
   size_t slab_layer;  // bytes of K (or V) for one layer
-  size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, part, logits, rope, lens, meta, total;
+  size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
   size_t meta_ints;
 };
 
@@ -84,6 +84,18 @@ inline int default_pass_tokens(int batch, int capacity) {
   const int64_t bc = (int64_t)batch * capacity;
   int t = (int)std::min<int64_t>(bc, 32768);
   return std::max(t, capacity);
+}
+
+// K splits of a residual decode GEMV with N output rows and K inputs: when its
+// 16-row strips are fewer than one per CU (256), the K range is cut so that
+// strips x splits reaches about 256 workgroups, keeping at least 8 chunks of
+// 128 per split (a reduction kernel, ~3 us, then adds the partial sums into h,
+// which shorter ranges do not repay).
+inline int decode_ksplit(int N, int K) {
+  const int strips = N / 16;
+  if (strips >= 256) return 1;
+  const int s = std::min(256 / std::max(strips, 1), (K / 128) / 8);
+  return std::max(1, s);
 }
 
 inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens, std::string& err) {
@@ -124,6 +136,9 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.hlo = o; o = align256(o + B * d * 2);
   x.olo = o; o = align256(o + B * d * 2);
   x.alo = o; o = align256(o + B * F * 2);
+  // split-K partial sums of the residual decode GEMVs (fp16 compute)
+  const size_t ks = std::max(decode_ksplit((int)d, (int)d), decode_ksplit((int)d, (int)F));
+  x.kpart = o; o = align256(o + (ks > 1 ? ks * B * d * 4 : 0));
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);

@@ -79,6 +79,7 @@ constexpr int skinny_cpw() {
 template <int RB, int MB, int EPI, bool NRM, int LO>
 __global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_skinny(SkinnyArgs a) {
   static_assert(!NRM || MB == 1, "the fused RMSNorm handles up to 16 tokens");
+  static_assert(!NRM || EPI != EPI_PART, "the RMS statistic needs all of K");
   static_assert(LO != 1 || MB == 1, "the packed pair handles up to 8 tokens");
   constexpr int LB = LO == 2 ? MB : 1;  // lo fragment blocks (unused unless LO == 2)
   extern __shared__ float red[];  // [nw][RB][MB][64 lanes][4], then (NRM) wsum[<=16 waves][16] + rstd[16]
@@ -87,9 +88,11 @@ __global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * (RB * 16);
   const int M = a.M, K = a.K, ldo = a.ldo;
-  const int nchunks = K >> 7;
+  // K chunks of this workgroup: split blockIdx.y of gridDim.y (EPI_PART), shared by the waves
+  const int nchunks = K >> 7, S = gridDim.y, sp = blockIdx.y;
+  const int s0 = sp * nchunks / S, s1 = (sp + 1) * nchunks / S;
   const int wk = (wave + blockIdx.x) % nw;
-  const int c0 = wk * nchunks / nw, c1 = (wk + 1) * nchunks / nw;
+  const int c0 = s0 + wk * (s1 - s0) / nw, c1 = s0 + (wk + 1) * (s1 - s0) / nw;
 
   f32x4 acc[RB][MB];
 #pragma unroll
@@ -224,6 +227,10 @@ __global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
         ((float*)a.out)[(size_t)tok * ldo + n0 + rb * 16 + row] = reduced(rb, mb, ln, i) * sc;
+    } else if constexpr (EPI == EPI_PART) {  // this split's partial sums: out[sp][tok][n]
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        ((float*)a.out)[((size_t)sp * M + tok) * ldo + n0 + rb * 16 + row] = reduced(rb, mb, ln, i);
     } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -240,18 +247,17 @@ __global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_
 }
 
 template <int RB, int MB, int EPI, bool NRM, int LO>
-static hipError_t launch_skinny(const SkinnyArgs& a, int N, hipStream_t s) {
-  // waves per workgroup: up to the variant's maximum, at most 64 KB of
-  // reduction LDS, and at least one chunk per wave; the 16-wave variant keeps
-  // a full batch of CPW chunks per wave (its chunks then go out in one round)
-  const int nchunks = a.K >> 7;
+static hipError_t launch_skinny(const SkinnyArgs& a, int N, hipStream_t s, int splits = 1) {
+  // waves per workgroup: at most 64 KB of reduction LDS and at least one chunk
+  // per wave; the 16-wave variant takes 16 only when every wave then gets a
+  // full batch of CPW chunks (all chunks go out in one round), 8 otherwise
+  const int nchunks = (a.K >> 7) / splits;
   constexpr int MW = skinny_max_waves<RB, MB, LO>();
-  constexpr int PER = MW == 16 ? skinny_cpw<RB, MB, LO>() : 1;
-  int nw = MW;
+  int nw = MW == 16 && nchunks < 16 * skinny_cpw<RB, MB, LO>() ? 8 : MW;
   while (nw > 1 && nw * RB * MB * 1024 > 65536) nw >>= 1;
-  while (nw > 1 && nw * PER > nchunks) nw >>= 1;
+  while (nw > 1 && nw > nchunks) nw >>= 1;
   const size_t lds = (size_t)nw * RB * MB * 1024 + (NRM ? (256 + 16) * 4 : 0);
-  hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM, LO>), dim3(N / (RB * 16)), dim3(64 * nw), lds, s, a);
+  hipLaunchKernelGGL((k_gemm_skinny<RB, MB, EPI, NRM, LO>), dim3(N / (RB * 16), splits), dim3(64 * nw), lds, s, a);
   return hipGetLastError();
 }
 
@@ -575,6 +581,51 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 }
 
 // ----------------------------------------------------------------------------
+
+// ----------------------------------------------------------------------------
+// split-K decode GEMV: partial sums of `splits` K ranges, then a reduction
+
+hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                     hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M > 64 || splits < 1 || (K >> 7) < splits) return hipErrorInvalidValue;
+  const SkinnyArgs a{(const f16*)u, (const f16*)ulo, 0.f, (const f16*)W, M, K, part, N, nullptr, nullptr};
+  if (!ulo) {
+    if (M <= 16) return launch_skinny<1, 1, EPI_PART, false, 0>(a, N, s, splits);
+    if (M <= 32) return launch_skinny<1, 2, EPI_PART, false, 0>(a, N, s, splits);
+    if (M <= 48) return launch_skinny<1, 3, EPI_PART, false, 0>(a, N, s, splits);
+    return launch_skinny<1, 4, EPI_PART, false, 0>(a, N, s, splits);
+  }
+  if (M <= 8) return launch_skinny<1, 1, EPI_PART, false, 1>(a, N, s, splits);
+  if (M <= 16) return launch_skinny<1, 1, EPI_PART, false, 2>(a, N, s, splits);
+  if (M <= 32) return launch_skinny<1, 2, EPI_PART, false, 2>(a, N, s, splits);
+  if (M <= 48) return launch_skinny<1, 3, EPI_PART, false, 2>(a, N, s, splits);
+  return launch_skinny<1, 4, EPI_PART, false, 2>(a, N, s, splits);
+}
+
+// h[m][n] += sum_s part[s][m][n] (splits in order), and the fp16 pair of the
+// updated row when o16 is non-NULL
+__global__ __launch_bounds__(256) void k_part_resid(const float* __restrict__ part, int splits, int M, int N,
+                                                    float* __restrict__ h, f16* __restrict__ o16,
+                                                    f16* __restrict__ olo) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t MN = (size_t)M * N;
+  if (i >= MN) return;
+  float v = 0.f;
+  for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
+  const float hn = h[i] + v;
+  h[i] = hn;
+  if (o16) split16(hn, o16, olo, i);
+}
+
+hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (olo && !o16) return hipErrorInvalidValue;
+  const size_t MN = (size_t)M * N;
+  hipLaunchKernelGGL(k_part_resid, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, M, N, h,
+                     (f16*)o16, (f16*)olo);
+  return hipGetLastError();
+}
 
 template <int EPI>
 static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, int K, void* out, int ldo,

@@ -12,7 +12,7 @@ namespace ams {
 // kernels (GEMM inputs, activations, K/V slab, packed weights): DT_F32 for
 // fp32 models, DT_F16 for bf16 models.
 enum DType { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 /* internal: split-K partial sums */ };
 
 // Packed-token pass metadata (device arrays).  Segment s covers tokens
 // off[s]..off[s+1]-1 of the pass, which belong to row `row[s]` at positions
@@ -42,6 +42,15 @@ constexpr int GU_BLOCK = 16;
 //   olo : the rounding error of o16 (EPI_RESID) or of the fp16 out (EPI_SWIGLU)
 hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int K, void* out,
                 int ldo, hipStream_t s, const void* ulo = nullptr, void* o16 = nullptr, void* olo = nullptr);
+
+// Split-K decode GEMV (fp16, M <= 64): part[s][m][n] = sum over the s-th of
+// `splits` equal K ranges (in 128-wide chunks) of u[m][k] W[n][k], with u the
+// fp16 input or the pair u + ulo as in gemm().  part holds splits * M * N floats.
+hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                     hipStream_t s);
+// h[m][n] += sum_s part[s][m][n], the splits added in order; with o16 (and
+// olo) also the fp16 pair of the updated rows, as gemm()'s EPI_RESID.
+hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s);
 
 // The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
 // callable for any M (N a multiple of 256, K of 64); same epilogues.

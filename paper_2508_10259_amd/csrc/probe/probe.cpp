@@ -17,6 +17,15 @@ int ams_probe_gemm_big(int epi, const void* u, const void* W, int M, int N, int 
   return (int)ams::gemm_big(epi, u, W, M, N, K, out, ldo, (hipStream_t)stream);
 }
 
+int ams_probe_gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                        void* stream) {
+  return (int)ams::gemm_part(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);
+}
+
+int ams_probe_part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, void* stream) {
+  return (int)ams::part_resid(part, splits, M, N, h, o16, olo, (hipStream_t)stream);
+}
+
 int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* ulo, void* stream) {
   return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream, ulo);
 }

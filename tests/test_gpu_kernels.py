@@ -387,3 +387,42 @@ def test_gemm_big(probe, epi, M, N, K):
         tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
     err = float(np.max(np.abs(got - ref)))
     assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
+
+
+@pytest.mark.parametrize("M", [1, 8, 16, 40, 64])
+@pytest.mark.parametrize("K,splits", [(1024, 2), (4096, 4), (4096, 8), (1152, 3)])
+@pytest.mark.parametrize("pair", [False, True])
+def test_gemm_split_resid(probe, M, K, splits, pair):
+    """Split-K decode GEMV: per-split partial sums reduced into the residual rows (splits added in
+    order), against h + x W^T; the fp16 pair of the new rows as the unsplit residual epilogue."""
+    import torch
+    N = 256
+    log(f"gemm_part M={M} K={K} splits={splits} pair={pair}")
+    x = W.random_gaussian((M, K), 51, M, K, dtype="f32")
+    if pair:
+        u, ulo = _pair(x)
+        xin = u.astype(np.float64) + ulo.astype(np.float64)
+    else:
+        u, ulo = x.astype(np.float16), None
+        xin = u.astype(np.float64)
+    Wt = _rand((N, K), 52, N, K, std=0.05)
+    h0 = W.random_gaussian((M, N), 53, M, dtype="f32")
+    ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
+    ulod = _dev(ulo, "f16") if pair else None
+    part = torch.full((splits * M * N,), float("nan"), dtype=torch.float32, device="cuda")
+    h = torch.from_numpy(h0.copy()).cuda()
+    o16 = torch.zeros((M, N), dtype=torch.float16, device="cuda")
+    olo = torch.zeros((M, N), dtype=torch.float16, device="cuda") if pair else None
+    assert probe.ams_probe_gemm_part(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
+    assert probe.ams_probe_part_resid(_ptr(part), splits, M, N, _ptr(h), _ptr(o16), _ptr(olo), _stream()) == 0
+    torch.cuda.synchronize()
+    ref = h0.astype(np.float64) + xin @ _f(Wt, "f16").T
+    got = h.cpu().numpy().astype(np.float64)
+    tol = 2e-5 * max(1.0, float(np.max(np.abs(ref)))) * np.sqrt(K / 128)
+    assert float(np.max(np.abs(got - ref))) <= tol
+    # each split covers its own K range: the partials add up to the product
+    psum = part.view(splits, M, N).sum(0).cpu().numpy().astype(np.float64)
+    assert float(np.max(np.abs(psum - (ref - h0)))) <= tol
+    assert torch.equal(o16, h.half())
+    if pair:
+        assert torch.equal(olo, (h - h.half().float()).half())
