@@ -54,9 +54,11 @@ def build_flops(spec, lens):
 
 
 def gu_launch_bytes(spec, B, es=2):
-    """Decode gate|up projection: weights [2F, d] once, the input rows (fp32 h with the
-    RMSNorm fused up to 16 rows, fp16 u beyond) and a [B, F] out."""
-    return 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * (4 if B <= 16 else es) + B * spec.d_ffn * es
+    """Decode gate|up projection: weights [2F, d] once and the input rows as fp16 pairs
+    (hi + lo, 4 bytes a value); up to 16 rows the kernel also writes the [B, F] gated out,
+    from 17 to 64 rows the wide kernel leaves that to its split-K reduction."""
+    w = 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4
+    return w + (B * spec.d_ffn * es if B <= 16 or B > 64 else 0)
 
 
 def time_gate_up_kernel(model, B, iters=240):
@@ -80,6 +82,9 @@ def time_gate_up_kernel(model, B, iters=240):
     ulo = (u - uhi.float()).half()
     a = torch.empty((B, F), device="cuda", dtype=torch.float16)
     alo = torch.empty((B, F), device="cuda", dtype=torch.float16)
+    # split count of the wide kernel: about 256 workgroups over 128-row tiles, >= 4 chunks of 128 each
+    wsplit = max(1, min(-(-256 // max(2 * F // 128, 1)), d // 128 // 4))
+    part = torch.empty((wsplit, B, 2 * F) if 16 < B <= 64 else (1,), device="cuda", dtype=torch.float32)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
@@ -89,6 +94,9 @@ def time_gate_up_kernel(model, B, iters=240):
             lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(hhi.data_ptr()), C.c_void_p(hlo.data_ptr()),
                                        C.c_float(spec.rms_eps), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
                                        C.c_void_p(None), C.c_void_p(alo.data_ptr()), C.c_void_p(s.cuda_stream))
+        elif B <= 64:  # the wide kernel writes split-K partial sums; the reduction is timed apart
+            lib.ams_probe_gemm_wide(C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
+                                    wsplit, C.c_void_p(part.data_ptr()), C.c_void_p(s.cuda_stream))
         else:
             lib.ams_probe_gemm(2, 2, C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
                                C.c_void_p(a.data_ptr()), F, C.c_void_p(None), C.c_void_p(alo.data_ptr()),
@@ -259,7 +267,8 @@ def main():
     achieved = gb / t_gu / 1e9
     copy_calibration()
     roof = {"kernel": ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 16
-                       else f"k_gemm_skinny<2,{(B + 15) // 16},SWIGLU> (decode gate|up projection + SiLU gate)"),
+                       else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
+                       if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)"),
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
             "bytes_per_launch": gb, "avg_launch_us": round(t_gu * 1e6, 3)}

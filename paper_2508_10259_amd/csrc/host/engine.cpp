@@ -24,6 +24,12 @@ static const char* off(const void* p, size_t bytes) { return (const char*)p + by
 // to 16 rows (see norm_proj).
 static bool fused_norm(const Ctx& c, int rows) { return c.model->ct == DT_F16 && rows <= 16; }
 
+// Above 16 rows the fp16 decode GEMVs use the wide GEMM (128 weight rows per
+// workgroup, activations staged in LDS) with split-K partial sums.
+static bool wide_decode(const Ctx& c, int rows, int N) {
+  return c.model->ct == DT_F16 && rows > 16 && rows <= 64 && N % 128 == 0;
+}
+
 hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err) {
   // bf16 weights become fp16 in the packed copy: exact for |w| >= 2^-14, an
   // fp16 subnormal (absolute error <= 2^-25) below; fp32 models are copied.
@@ -173,7 +179,14 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
   } else {
     void* ulo = md.ct == DT_F16 ? g.hlo() : nullptr;
     TRY(rmsnorm(md.ct, h, g.n, K, eps, g.u(), s, ulo));
-    TRY(gemm(md.ct, epi, g.u(), W, g.n, N, K, out, ldo, s, ulo, nullptr, olo));
+    if (wide_decode(*g.c, g.n, N)) {  // partial sums of 128-row tiles, then the epilogue
+      const int splits = decode_wsplit(N, K);
+      TRY(gemm_wide(g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), s));
+      if (epi == EPI_SWIGLU) TRY(part_swiglu(g.c->kpart(), splits, g.n, N, out, olo, s));
+      else TRY(part_store(g.c->kpart(), splits, g.n, N, (float*)out, s));
+    } else {
+      TRY(gemm(md.ct, epi, g.u(), W, g.n, N, K, out, ldo, s, ulo, nullptr, olo));
+    }
   }
   return hipSuccess;
 }
@@ -186,6 +199,12 @@ static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, cons
   const Ctx& c = *g.c;
   const Model& md = *c.model;
   const int d = md.cfg.d_model;
+  if (wide_decode(c, g.n, d)) {
+    const int splits = decode_wsplit(d, K);
+    hipError_t e = gemm_wide(x, xlo, W, g.n, d, K, splits, c.kpart(), s);
+    if (e == hipSuccess) e = part_resid(c.kpart(), splits, g.n, d, g.h(), hhi, hlo, s);
+    return e;
+  }
   const int splits = md.ct == DT_F16 ? decode_ksplit(d, K) : 1;
   if (splits > 1) {
     hipError_t e = gemm_part(x, xlo, W, g.n, d, K, splits, c.kpart(), s);

@@ -98,6 +98,14 @@ inline int decode_ksplit(int N, int K) {
   return std::max(1, s);
 }
 
+// K splits of a wide decode GEMM (more than 16 rows; 128 weight rows per
+// workgroup): about 256 workgroups in all, at least 4 chunks of 128 per split.
+inline int decode_wsplit(int N, int K) {
+  const int tiles = std::max(N / 128, 1);
+  const int s = std::min((256 + tiles - 1) / tiles, (K / 128) / 4);
+  return std::max(1, s);
+}
+
 inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens, std::string& err) {
   if (batch < 1 || batch > 1024) { err = "batch must be in [1, 1024]"; return S_EINVAL; }
   if (capacity < 64 || capacity % 64 != 0 || capacity > (1 << 20)) {
@@ -136,9 +144,18 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.hlo = o; o = align256(o + B * d * 2);
   x.olo = o; o = align256(o + B * d * 2);
   x.alo = o; o = align256(o + B * F * 2);
-  // split-K partial sums of the residual decode GEMVs (fp16 compute)
+  // split-K partial sums of the decode GEMVs (fp16 compute): the narrow
+  // residual projections at up to 16 rows, every projection above 16 rows
+  size_t kp = 0;
   const size_t ks = std::max(decode_ksplit((int)d, (int)d), decode_ksplit((int)d, (int)F));
-  x.kpart = o; o = align256(o + (ks > 1 ? ks * B * d * 4 : 0));
+  if (ks > 1) kp = ks * B * d;
+  if (batch > 16 && batch <= 64) {
+    const size_t NB = bins_padded(c);
+    kp = std::max({kp, decode_wsplit(3 * (int)d, (int)d) * B * 3 * d, decode_wsplit((int)d, (int)d) * B * d,
+                   decode_wsplit(2 * (int)F, (int)d) * B * 2 * F, decode_wsplit((int)d, (int)F) * B * d,
+                   decode_wsplit((int)NB, (int)d) * B * NB});
+  }
+  x.kpart = o; o = align256(o + kp * 4);
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);

@@ -583,6 +583,190 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 // ----------------------------------------------------------------------------
 
 // ----------------------------------------------------------------------------
+// wide decode GEMM: 16 < M <= 64 tokens (batched decode), split-K partial sums
+//
+// A workgroup owns 128 weight rows (8 waves x 16) and one K split.  Every
+// 128-wide K chunk of the activations (hi, and lo for the fp16 pair; all M
+// tokens) is loaded once per workgroup into double-buffered LDS and read by
+// all 8 waves as MFMA B fragments, so activation traffic is about the weight
+// traffic instead of M/8 times it; each wave streams its own weight rows into
+// registers, WP chunks ahead.  Waves own disjoint rows, so no reduction runs
+// at the end: each writes its partial sums, and a reduction kernel applies
+// the epilogue (part_store / part_resid / part_swiglu).
+
+constexpr int WIDE_ROWS = 128, WIDE_WP = 4, WIDE_LDK = 128 + 8;
+
+// weight fragments of one chunk of a wave's 16 rows
+__device__ __forceinline__ void wide_wload(uint4 (&w)[4], const f16* wrow, int c) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = *(const uint4*)(wrow + (c << 7) + 32 * i);
+}
+template <int MB, int LO>
+__global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, const f16* __restrict__ xlo,
+                                                   const f16* __restrict__ W, int M, int K,
+                                                   float* __restrict__ part, int N) {
+  constexpr int NX = LO == 2 ? 2 : 1;               // activation arrays (hi, lo)
+  constexpr int XCH = NX * MB * 16 * 16;             // 16-byte pieces of one staged chunk
+  constexpr int XPT = (XCH + 511) / 512;             // pieces per thread
+  extern __shared__ __attribute__((aligned(16))) f16 xs[];  // [2 stages][NX][MB*16][WIDE_LDK]
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, g = lane >> 4;
+  const int n0 = blockIdx.x * WIDE_ROWS + wave * 16;
+  const int nch = K >> 7, S = gridDim.y, sp = blockIdx.y;
+  const int s0 = sp * nch / S, s1 = (sp + 1) * nch / S, n = s1 - s0;
+
+  const f16* wrow = W + (size_t)(n0 + r) * K + g * 8;
+  uint4 wr[WIDE_WP][4];
+  // activation staging, up to 4 pieces of 16 bytes per thread (named registers:
+  // an array here ends up on the stack).  Piece e = tid + 512 q: array
+  // e / (MB*256), token row (e / 16) % (MB*16) (rows past M read row M-1: they
+  // only feed token columns that are never stored), 16-byte column e % 16.
+  static_assert(XPT <= 4, "at most 4 staging pieces per thread");
+  uint4 x0 = {0u, 0u, 0u, 0u}, x1 = x0, x2 = x0, x3 = x0;
+#define AMS_WIDE_XLOAD1(q, xq, c)                                                                  \
+  do {                                                                                             \
+    const int e_ = tid + 512 * (q);                                                                \
+    if ((q) < XPT && (XCH % 512 == 0 || e_ < XCH)) {                                               \
+      const int arr_ = e_ / (MB * 256), row_ = (e_ >> 4) % (MB * 16), col_ = e_ & 15;              \
+      xq = *(const uint4*)((arr_ ? xlo : xhi) + (size_t)(row_ < M ? row_ : M - 1) * K + ((c) << 7) + col_ * 8); \
+    }                                                                                              \
+  } while (0)
+#define AMS_WIDE_XSTORE1(q, xq, stage)                                                             \
+  do {                                                                                             \
+    const int e_ = tid + 512 * (q);                                                                \
+    if ((q) < XPT && (XCH % 512 == 0 || e_ < XCH)) {                                               \
+      const int arr_ = e_ / (MB * 256), row_ = (e_ >> 4) % (MB * 16), col_ = e_ & 15;              \
+      *(uint4*)(xs + ((size_t)((stage) * NX + arr_) * MB * 16 + row_) * WIDE_LDK + col_ * 8) = xq; \
+    }                                                                                              \
+  } while (0)
+#define AMS_WIDE_XLOAD(c) \
+  do { AMS_WIDE_XLOAD1(0, x0, c); AMS_WIDE_XLOAD1(1, x1, c); AMS_WIDE_XLOAD1(2, x2, c); AMS_WIDE_XLOAD1(3, x3, c); } while (0)
+#define AMS_WIDE_XSTORE(stage) \
+  do { AMS_WIDE_XSTORE1(0, x0, stage); AMS_WIDE_XSTORE1(1, x1, stage); AMS_WIDE_XSTORE1(2, x2, stage); AMS_WIDE_XSTORE1(3, x3, stage); } while (0)
+
+  f32x4 acc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int p = 0; p < WIDE_WP; ++p)
+    if (p < n) wide_wload(wr[p], wrow, s0 + p);
+  AMS_WIDE_XLOAD(s0);
+  AMS_WIDE_XSTORE(0);
+  if (n > 1) AMS_WIDE_XLOAD(s0 + 1);
+  __syncthreads();
+
+  for (int tb = 0; tb < n; tb += WIDE_WP) {
+#pragma unroll
+    for (int p = 0; p < WIDE_WP; ++p) {
+      const int t = tb + p;
+      if (t < n) {  // uniform across the workgroup (n is)
+        const f16* xb = xs + (size_t)((t & 1) * NX) * MB * 16 * WIDE_LDK;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const half8 wf = as_half8(wr[p][i]);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const f16* bp = xb + (size_t)(mb * 16 + r) * WIDE_LDK + 32 * i + 8 * g;
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, *(const half8*)bp, acc[mb], 0, 0, 0);
+            if constexpr (LO == 2)
+              acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  wf, *(const half8*)(bp + (size_t)MB * 16 * WIDE_LDK), acc[mb], 0, 0, 0);
+          }
+        }
+        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, s0 + t + WIDE_WP);
+        if (t + 1 < n) AMS_WIDE_XSTORE((t + 1) & 1);
+        if (t + 2 < n) AMS_WIDE_XLOAD(s0 + t + 2);
+        __syncthreads();
+      }
+    }
+  }
+
+#undef AMS_WIDE_XLOAD1
+#undef AMS_WIDE_XSTORE1
+#undef AMS_WIDE_XLOAD
+#undef AMS_WIDE_XSTORE
+
+  // lane (r, g) holds rows n0 + 4g + i for token mb*16 + r
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int tok = mb * 16 + r;
+    if (tok >= M) continue;
+    float* dst = part + ((size_t)sp * M + tok) * N + n0 + 4 * g;
+    *(float4*)dst = float4{acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]};
+  }
+}
+
+template <int MB, int LO>
+static hipError_t launch_wide(const f16* x, const f16* xlo, const f16* W, int M, int N, int K, int splits,
+                              float* part, hipStream_t s) {
+  const size_t lds = (size_t)2 * (LO == 2 ? 2 : 1) * MB * 16 * WIDE_LDK * sizeof(f16);
+  hipLaunchKernelGGL((k_gemm_wide<MB, LO>), dim3(N / WIDE_ROWS, splits), dim3(512), lds, s, x, xlo, W, M, K, part, N);
+  return hipGetLastError();
+}
+
+hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                     hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M > 64 || N % WIDE_ROWS != 0 || splits < 1 || (K >> 7) < splits) return hipErrorInvalidValue;
+  const f16 *x = (const f16*)u, *xl = (const f16*)ulo, *w = (const f16*)W;
+  if (!ulo) {
+    if (M <= 16) return launch_wide<1, 0>(x, xl, w, M, N, K, splits, part, s);
+    if (M <= 32) return launch_wide<2, 0>(x, xl, w, M, N, K, splits, part, s);
+    if (M <= 48) return launch_wide<3, 0>(x, xl, w, M, N, K, splits, part, s);
+    return launch_wide<4, 0>(x, xl, w, M, N, K, splits, part, s);
+  }
+  if (M <= 16) return launch_wide<1, 2>(x, xl, w, M, N, K, splits, part, s);
+  if (M <= 32) return launch_wide<2, 2>(x, xl, w, M, N, K, splits, part, s);
+  if (M <= 48) return launch_wide<3, 2>(x, xl, w, M, N, K, splits, part, s);
+  return launch_wide<4, 2>(x, xl, w, M, N, K, splits, part, s);
+}
+
+// out[m][n] = sum_s part[s][m][n] (splits added in order)
+__global__ __launch_bounds__(256) void k_part_store(const float* __restrict__ part, int splits, size_t MN,
+                                                    float* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= MN) return;
+  float v = 0.f;
+  for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
+  out[i] = v;
+}
+
+// a[m][c] = silu(gate) * up for the packed gate/up rows of output column c
+// (16-row interleave), as an fp16 pair (out, olo)
+__global__ __launch_bounds__(256) void k_part_swiglu(const float* __restrict__ part, int splits, int M, int N,
+                                                     f16* __restrict__ out, f16* __restrict__ olo) {
+  const int F = N / 2;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)M * F) return;
+  const int m = (int)(i / F), c = (int)(i % F);
+  const size_t gi = (size_t)m * N + (size_t)(c / GU_BLOCK) * 2 * GU_BLOCK + c % GU_BLOCK, MN = (size_t)M * N;
+  float gt = 0.f, up = 0.f;
+  for (int sp = 0; sp < splits; ++sp) {
+    gt += part[sp * MN + gi];
+    up += part[sp * MN + gi + GU_BLOCK];
+  }
+  split16(silu(gt) * up, out, olo, i);
+}
+
+hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  const size_t MN = (size_t)M * N;
+  hipLaunchKernelGGL(k_part_store, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, MN, out);
+  return hipGetLastError();
+}
+
+hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (N % (2 * GU_BLOCK) != 0) return hipErrorInvalidValue;
+  const size_t MF = (size_t)M * (N / 2);
+  hipLaunchKernelGGL(k_part_swiglu, dim3((unsigned)((MF + 255) / 256)), dim3(256), 0, s, part, splits, M, N,
+                     (f16*)out, (f16*)olo);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
 // split-K decode GEMV: partial sums of `splits` K ranges, then a reduction
 
 hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,

@@ -48,6 +48,16 @@ hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int
 // fp16 input or the pair u + ulo as in gemm().  part holds splits * M * N floats.
 hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
+// Wide decode GEMM (fp16, 16 < M <= 64 typical, N a multiple of 128): the
+// same partial sums as gemm_part, with 128 weight rows per workgroup sharing
+// LDS-staged activations.  The epilogue is one of the part_* reductions.
+hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                     hipStream_t s);
+// out[m][n] = sum_s part[s][m][n] (fp32 out).
+hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s);
+// out[m][c] = silu(gate) * up of the summed packed gate/up rows of column c
+// (N = 2F packed rows), fp16 with its rounding error in olo (or NULL).
+hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s);
 // h[m][n] += sum_s part[s][m][n], the splits added in order; with o16 (and
 // olo) also the fp16 pair of the updated rows, as gemm()'s EPI_RESID.
 hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s);

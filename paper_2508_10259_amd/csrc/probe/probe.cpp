@@ -26,6 +26,19 @@ int ams_probe_part_resid(const float* part, int splits, int M, int N, float* h, 
   return (int)ams::part_resid(part, splits, M, N, h, o16, olo, (hipStream_t)stream);
 }
 
+int ams_probe_gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                        void* stream) {
+  return (int)ams::gemm_wide(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);
+}
+
+int ams_probe_part_store(const float* part, int splits, int M, int N, float* out, void* stream) {
+  return (int)ams::part_store(part, splits, M, N, out, (hipStream_t)stream);
+}
+
+int ams_probe_part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, void* stream) {
+  return (int)ams::part_swiglu(part, splits, M, N, out, olo, (hipStream_t)stream);
+}
+
 int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* ulo, void* stream) {
   return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream, ulo);
 }

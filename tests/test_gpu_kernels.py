@@ -426,3 +426,51 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
     assert torch.equal(o16, h.half())
     if pair:
         assert torch.equal(olo, (h - h.half().float()).half())
+
+
+@pytest.mark.parametrize("M", [5, 17, 33, 64])
+@pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (384, 4096, 8), (256, 1152, 3)])
+@pytest.mark.parametrize("pair", [False, True])
+def test_gemm_wide(probe, M, N, K, splits, pair):
+    """Wide decode GEMM (128 weight rows per workgroup, LDS-staged activations) and its
+    reductions: partial sums per K split, store / residual / SwiGLU epilogues, against the
+    exact products of the fp16 (pair) inputs."""
+    import torch
+    log(f"gemm_wide M={M} N={N} K={K} splits={splits} pair={pair}")
+    x = W.random_gaussian((M, K), 61, M, K, dtype="f32")
+    if pair:
+        u, ulo = _pair(x)
+        xin = u.astype(np.float64) + ulo.astype(np.float64)
+    else:
+        u, ulo = x.astype(np.float16), None
+        xin = u.astype(np.float64)
+    Wt = _rand((N, K), 62, N, K, std=0.05)
+    y = xin @ _f(Wt, "f16").T
+    ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
+    ulod = _dev(ulo, "f16") if pair else None
+    part = torch.full((splits * M * N,), float("nan"), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_gemm_wide(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
+    tol = 2e-5 * max(1.0, float(np.max(np.abs(y)))) * np.sqrt(K / 128)
+    # store
+    out = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_part_store(_ptr(part), splits, M, N, _ptr(out), _stream()) == 0
+    torch.cuda.synchronize()
+    assert float(np.max(np.abs(out.cpu().numpy() - y))) <= tol
+    # residual, with the fp16 pair of the new rows
+    h0 = W.random_gaussian((M, N), 63, M, dtype="f32")
+    h = torch.from_numpy(h0.copy()).cuda()
+    o16 = torch.zeros((M, N), dtype=torch.float16, device="cuda")
+    olo = torch.zeros((M, N), dtype=torch.float16, device="cuda")
+    assert probe.ams_probe_part_resid(_ptr(part), splits, M, N, _ptr(h), _ptr(o16), _ptr(olo), _stream()) == 0
+    torch.cuda.synchronize()
+    assert float(np.max(np.abs(h.cpu().numpy() - (h0 + y)))) <= tol
+    assert torch.equal(o16, h.half()) and torch.equal(olo, (h - h.half().float()).half())
+    # SwiGLU over the packed gate/up rows, fp16 pair out
+    a = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
+    alo = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
+    assert probe.ams_probe_part_swiglu(_ptr(part), splits, M, N, _ptr(a), _ptr(alo), _stream()) == 0
+    torch.cuda.synchronize()
+    gg, up = _unpack_gu(y.T, N // 2)
+    ref = (_silu(gg) * up).T
+    got = a.float().cpu().numpy().astype(np.float64) + alo.float().cpu().numpy()
+    assert float(np.max(np.abs(got - ref))) <= max(tol, 4e-6 * float(np.max(np.abs(ref))))
