@@ -54,17 +54,19 @@ def build_flops(spec, lens):
 
 
 def gu_launch_bytes(spec, B, es=2):
-    """Decode gate|up projection: weights [2F, d] once and the input rows as fp16 pairs
-    (hi + lo, 4 bytes a value); up to 16 rows the kernel also writes the [B, F] gated out,
-    from 17 to 64 rows the wide kernel leaves that to its split-K reduction."""
+    """Decode gate|up projection: weights [2F, d] once, the input rows and the [B, F] gated
+    out, both as fp16 pairs (hi + lo, 4 bytes a value); from 17 to 64 rows the wide kernel
+    leaves the out to its split-K reduction."""
     w = 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4
-    return w + (B * spec.d_ffn * es if B <= 16 or B > 64 else 0)
+    return w + (B * spec.d_ffn * 4 if B <= 16 or B > 64 else 0)
 
 
 def time_gate_up_kernel(model, B, iters=240):
     """Average duration of the decode gate|up kernel (RMSNorm + gate|up GEMV + SiLU gate,
-    the largest weight stream of a decode pass) in the decode step's launch shape,
-    cycling through the layers' packed weights, timed with HIP events on its own stream."""
+    the largest weight stream of a decode pass) in the decode step's launch shape, timed with
+    HIP events on its own stream.  Each launch reads a different copy of a layer's packed
+    weights out of a buffer of at least 1 GiB, four times the 256 MB memory-side cache, so
+    that every launch streams its weights from HBM as it does inside a decode pass."""
     import torch
     from paper_2508_10259_amd.build import PROBE_LIB
     lib = C.CDLL(PROBE_LIB)
@@ -72,7 +74,13 @@ def time_gate_up_kernel(model, B, iters=240):
     d, F, es = spec.d_model, spec.d_ffn, 2
     # packed layout of the model workspace: [wqkv | wo | wgu | ...], each region 256-byte aligned
     align = lambda x: (x + 255) // 256 * 256
-    w_gu = model.ws.data_ptr() + align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
+    off_gu = align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
+    slice_b = 2 * F * d * es
+    n_copy = max(4, -(-(1 << 30) // slice_b))
+    wbuf = torch.empty((n_copy, slice_b), dtype=torch.uint8, device="cuda")
+    for i in range(n_copy):
+        l = i % spec.n_layers
+        wbuf[i].copy_(model.ws[off_gu + l * slice_b: off_gu + (l + 1) * slice_b])
     # the decode pass's form: inputs and SwiGLU output as fp16 pairs (hi + rounding error)
     h = torch.randn((B, d), device="cuda") * 30.0
     hhi = h.half()
@@ -89,7 +97,7 @@ def time_gate_up_kernel(model, B, iters=240):
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def launch(l):
-        w = C.c_void_p(w_gu + (l % spec.n_layers) * 2 * F * d * es)
+        w = C.c_void_p(wbuf[l % n_copy].data_ptr())
         if B <= 16:  # the decode pass fuses the RMSNorm up to 16 rows
             lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(hhi.data_ptr()), C.c_void_p(hlo.data_ptr()),
                                        C.c_float(spec.rms_eps), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
@@ -101,14 +109,17 @@ def time_gate_up_kernel(model, B, iters=240):
             lib.ams_probe_gemm(2, 2, C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
                                C.c_void_p(a.data_ptr()), F, C.c_void_p(None), C.c_void_p(alo.data_ptr()),
                                C.c_void_p(s.cuda_stream))
+    torch.cuda.synchronize()
+    iters = max(iters, 2 * n_copy)
     with torch.cuda.stream(s):
-        for l in range(24):
+        for l in range(n_copy):
             launch(l)
         ev0.record(s)
         for l in range(iters):
             launch(l)
         ev1.record(s)
     s.synchronize()
+    del wbuf
     return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
 
 

@@ -30,6 +30,21 @@ static bool wide_decode(const Ctx& c, int rows, int N) {
   return c.model->ct == DT_F16 && rows > 16 && rows <= 64 && N % 128 == 0;
 }
 
+// The persistent decode (decode_fused) serves fp16 compute up to 8 rows when
+// the shapes fit its tiling and its 32-bit buffer offsets; AMS_FUSED=0 turns it
+// off (the per-kernel decode then runs).
+static bool fused_applies(const Ctx& c) {
+  const char* e = getenv("AMS_FUSED");
+  if (e && e[0] == '0') return false;
+  const Cfg& m = c.model->cfg;
+  const int B = c.lay.batch;
+  if (c.model->ct != DT_F16 || B > FUSED_MAX_ROWS) return false;
+  if (m.head_dim != 64 && m.head_dim != 128) return false;
+  if (m.d_model % 128 != 0 || m.d_ffn % 128 != 0 || bins_padded(m) % 16 != 0) return false;
+  return c.lay.slab_layer < ((size_t)1 << 31) && (size_t)B * 3 * m.d_model * 4 < ((size_t)1 << 31) &&
+         (size_t)B * m.d_ffn * 4 < ((size_t)1 << 31);
+}
+
 hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err) {
   // bf16 weights become fp16 in the packed copy: exact for |w| >= 2^-14, an
   // fp16 subnormal (absolute error <= 2^-25) below; fp32 models are copied.
@@ -68,6 +83,12 @@ hipError_t ctx_init(Ctx& c, std::string& err) {
   TRY(hipStreamSynchronize(s));
   c.splits = decode_splits(c.lay.batch, m.n_heads, c.lay.capacity);
   c.meta_host.assign(c.lay.meta_ints, 0);
+  c.fused_grid = fused_applies(c) ? decode_fused_grid(c.model->device, m.head_dim) : 0;
+  if (c.fused_grid > 0) {
+    c.split_o = fused_split(m, m.d_model, c.fused_grid);
+    c.split_d = fused_split(m, m.d_ffn, c.fused_grid);
+    c.split_a = fused_split_attn(m, c.lay.batch, c.lay.capacity, c.fused_grid);
+  }
   return hipSuccess;
 }
 
@@ -272,9 +293,37 @@ static hipError_t decode_rows(const Rows& g, int A, int32_t* tok, float* logits,
   return hipSuccess;
 }
 
+// The greedy loop of a step as one persistent launch.
+static hipError_t enqueue_fused(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
+                                std::string& err) {
+  const Model& md = *c.model;
+  const Cfg& m = md.cfg;
+  FusedDecode f{};
+  f.wqkv = md.wqkv(0); f.s_qkv = md.lay.per_layer_qkv;
+  f.wo = md.wo(0); f.s_o = md.lay.per_layer_o;
+  f.wgu = md.wgu(0); f.s_gu = md.lay.per_layer_gu;
+  f.wd = md.wd(0); f.s_d = md.lay.per_layer_d;
+  f.whead = md.head_bins();
+  f.bin_embed = md.bin_embed();
+  f.L = m.n_layers; f.d = m.d_model; f.H = m.n_heads; f.dh = m.head_dim; f.F = m.d_ffn;
+  f.nbp = bins_padded(m); f.n_bins = m.n_bins; f.eps = m.rms_eps;
+  f.M = c.lay.batch; f.cap = c.lay.capacity; f.A = A;
+  f.split_o = c.split_o; f.split_d = c.split_d; f.split_a = c.split_a;
+  f.lens = c.lens(); f.rope = c.rope();
+  f.kv = c.ws + c.lay.kv; f.slab_elems = c.lay.slab_layer / 2;
+  f.h = c.h(); f.hp = c.ws + c.lay.fx_hp;
+  f.hl = c.h_last16(); f.hl_lo = c.h_last16lo();
+  f.qkv = c.qkv(); f.op = c.ws + c.lay.fx_op; f.ap = c.ws + c.lay.fx_ap;
+  f.logits = c.logits(); f.part = (float*)(c.ws + c.lay.fx_part); f.sync = (unsigned*)(c.ws + c.lay.fx_sync);
+  f.out_tok = tok; f.out_logits = logits; f.forced = forced;
+  TRY(decode_fused(f, c.fused_grid, s));
+  return hipSuccess;
+}
+
 // The greedy loop of a step over all rows.
 static hipError_t enqueue_decode(Ctx& c, int A, int32_t* tok, float* logits, const int32_t* forced, hipStream_t s,
                                  std::string& err) {
+  if (c.fused_grid > 0) return enqueue_fused(c, A, tok, logits, forced, s, err);
   const size_t ces = c.model->ct == DT_F16 ? 2 : 4;
   return decode_rows(Rows{0, c.lay.batch, ces, &c}, A, tok, logits, forced, s, err);
 }

@@ -53,6 +53,8 @@ struct Ctx {
   RowBook book;
   char* ws = nullptr;
   int splits = 1;
+  int fused_grid = 0;  // workgroups of the persistent decode, 0 when it does not apply
+  int split_o = 1, split_d = 1, split_a = 1;
   hipStream_t capture_stream = nullptr;
   std::map<GraphKey, hipGraphExec_t> graphs;
   std::vector<GraphKey> graph_lru;

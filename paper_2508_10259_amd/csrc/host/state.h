@@ -13,6 +13,8 @@
 #include <string>
 #include <vector>
 
+#include "fused_limits.h"
+
 namespace ams {
 
 enum Status { S_OK = 0, S_EINVAL = -1, S_ESTATE = -2, S_ECAPACITY = -3, S_ENODEV = -4, S_EHIP = -5, S_ENOMEM = -6 };
@@ -77,6 +79,9 @@ struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
   size_t slab_layer;  // bytes of K (or V) for one layer
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
+  // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
+  // attention output and the SwiGLU output, split-K partials, sync words
+  size_t fx_hp, fx_op, fx_ap, fx_part, fx_sync;
   size_t meta_ints;
 };
 
@@ -104,6 +109,39 @@ inline int decode_wsplit(int N, int K) {
   const int tiles = std::max(N / 128, 1);
   const int s = std::min((256 + tiles - 1) / tiles, (K / 128) / 4);
   return std::max(1, s);
+}
+
+// Persistent decode (one launch per step) applies up to this many rows.
+constexpr int FUSED_MAX_ROWS = 8;
+// Split-K units of its O and down projections: at most this many.
+inline size_t fused_part_units(const Cfg& c) { return std::max<size_t>(c.d_model / 16, 1024); }
+// K splits of a residual projection (d/16 strips over K/128 chunks) in the
+// persistent decode on `grid` workgroups: a unit's weights should fit the 64 KB
+// a workgroup loads while it waits at the barrier before the phase, as long as
+// there are workgroups to spare.
+inline int fused_split(const Cfg& c, int K, int grid) {
+  const int strips = c.d_model / 16, nch = K / 128;
+  if (strips >= grid) return 1;
+  const size_t unit_bytes = (size_t)16 * K * 2;
+  int s = (int)std::min<size_t>((unit_bytes + 65535) / 65536, (size_t)(grid / std::max(strips, 1)));
+  s = std::max(1, std::min({s, nch, FUSED_MAX_SPLIT}));
+  while (s > 1 && (size_t)strips * s > fused_part_units(c)) --s;
+  return s;
+}
+
+// Key splits of its attention.  A split's keys take one round of its 8 waves
+// when they number at most 8 x 5 x (64 / (head_dim / 8)) (320 at head_dim 64,
+// 160 at 128).  Merging splits costs a memory round trip, so more splits than
+// that are taken only when (row, head) items would leave at least 3 in 4
+// workgroups idle (then up to 8).  Partials stay within the split-K buffer.
+inline int fused_split_attn(const Cfg& c, int rows, int capacity, int grid) {
+  const int items = rows * c.n_heads, round = 8 * 5 * (64 / (c.head_dim / 8));
+  const int need = (capacity + round - 1) / round;  // splits for one round each
+  const int spare = grid / std::max(items, 1);      // splits the idle workgroups allow
+  int s = std::max(need, spare >= 4 ? std::min(spare, 8) : 1);
+  s = std::max(1, std::min(s, FUSED_MAX_ATTN_SPLIT));
+  while (s > 1 && (size_t)items * s * (c.head_dim + 2) > fused_part_units(c) * 8 * 16) --s;
+  return s;
 }
 
 inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens, std::string& err) {
@@ -163,6 +201,12 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B]
   x.meta_ints = 5 * B + 1;
   x.meta = o; o = align256(o + x.meta_ints * 4);
+  const bool fx = batch <= FUSED_MAX_ROWS && es == 2;
+  x.fx_hp = o; o = align256(o + (fx ? 2 * B * d * 2 : 0));
+  x.fx_op = o; o = align256(o + (fx ? 2 * B * d * 2 : 0));
+  x.fx_ap = o; o = align256(o + (fx ? 2 * B * F * 2 : 0));
+  x.fx_part = o; o = align256(o + (fx ? fused_part_units(c) * 8 * 16 * 4 : 0));
+  x.fx_sync = o; o = align256(o + (fx ? (size_t)(32 * 64 + std::max<size_t>(d / 16, 8 * c.n_heads)) * 4 : 0));
   x.total = o;
   return x;
 }

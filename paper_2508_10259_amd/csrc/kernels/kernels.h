@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fused_limits.h"
+
 namespace ams {
 
 // Storage types at the boundary: DT_F32, DT_BF16.  Compute types inside the
@@ -135,6 +137,42 @@ hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int split
 // into h_last16lo when that is non-NULL too.
 hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_t s, void* h_last16 = nullptr,
                        void* h_last16lo = nullptr);
+
+// The whole greedy decode of a step in one persistent launch (fp16 compute,
+// M <= 8 rows; see decode_fused.hip): head on the last committed position, then
+// A - 1 times feed + all layers + head, with the outputs of argmax_feed.
+// Pointers into the packed model (per-layer byte strides) and the context
+// workspace; hp / op / ap are fp16 pairs laid out hi block then lo block
+// ([2][M][width]); hl / hl_lo the pair of the last committed position (hl_lo
+// after hl); part holds max(d/16, 1024) * 8 * 16 floats (enough for the
+// split-K sums and for M*H*split_a attention partials of dh + 2 floats) and
+// sync fused_sync_words(d, H) words.  The launch first clears sync with a kernel.
+struct FusedDecode {
+  const void *wqkv, *wo, *wgu, *wd, *whead, *bin_embed;
+  size_t s_qkv, s_o, s_gu, s_d;
+  int L, d, H, dh, F, nbp, n_bins;
+  float eps;
+  int M, cap, A, split_o, split_d, split_a;
+  const int32_t* lens;
+  const float2* rope;
+  void* kv;
+  size_t slab_elems;
+  float* h;
+  void* hp;
+  const void *hl, *hl_lo;
+  float* qkv;
+  void *op, *ap;
+  float *logits, *part;
+  unsigned* sync;
+  int32_t* out_tok;
+  float* out_logits;
+  const int32_t* forced;
+};
+hipError_t decode_fused(const FusedDecode& f, int grid, hipStream_t s);
+// Workgroups of the persistent decode on `device` (one per compute unit), 0 if
+// it cannot be resident there.
+int decode_fused_grid(int device, int dh);
+int fused_sync_words(int d, int H);
 
 // lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
