@@ -55,10 +55,10 @@ def build_flops(spec, lens):
 
 def gu_launch_bytes(spec, B, es=2):
     """Decode gate|up projection: weights [2F, d] once, the input rows and the [B, F] gated
-    out, both as fp16 pairs (hi + lo, 4 bytes a value); from 17 to 64 rows the wide kernel
+    out, both as fp16 pairs (hi + lo, 4 bytes a value); from 9 to 64 rows the wide kernel
     leaves the out to its split-K reduction."""
     w = 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4
-    return w + (B * spec.d_ffn * 4 if B <= 16 or B > 64 else 0)
+    return w + (B * spec.d_ffn * 4 if B <= 8 or B > 64 else 0)
 
 
 def time_gate_up_kernel(model, B, iters=240):
@@ -92,13 +92,13 @@ def time_gate_up_kernel(model, B, iters=240):
     alo = torch.empty((B, F), device="cuda", dtype=torch.float16)
     # split count of the wide kernel: about 256 workgroups over 128-row tiles, >= 4 chunks of 128 each
     wsplit = max(1, min(-(-256 // max(2 * F // 128, 1)), d // 128 // 4))
-    part = torch.empty((wsplit, B, 2 * F) if 16 < B <= 64 else (1,), device="cuda", dtype=torch.float32)
+    part = torch.empty((wsplit, B, 2 * F) if 8 < B <= 64 else (1,), device="cuda", dtype=torch.float32)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def launch(l):
         w = C.c_void_p(wbuf[l % n_copy].data_ptr())
-        if B <= 16:  # the decode pass fuses the RMSNorm up to 16 rows
+        if B <= 8:  # the decode pass fuses the RMSNorm up to 8 rows
             lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(hhi.data_ptr()), C.c_void_p(hlo.data_ptr()),
                                        C.c_float(spec.rms_eps), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
                                        C.c_void_p(None), C.c_void_p(alo.data_ptr()), C.c_void_p(s.cuda_stream))
@@ -123,20 +123,43 @@ def time_gate_up_kernel(model, B, iters=240):
     return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
 
 
-def profiled_traffic(workload, path=os.path.join(ROOT, "profiles", "decode_gate_up_mid-b8_pmc.txt")):
-    """HBM bytes per launch of the roofline kernel from the committed PMC summary, or None
-    for another workload or when the kernel's source has changed since the counters were taken."""
+def profiled_traffic(workload, kernel):
+    """HBM bytes per launch of the roofline kernel from a committed PMC summary
+    (profiles/*_pmc.txt) of this workload and kernel, or None when there is none or
+    the kernel's source has changed since the counters were taken."""
+    import glob
     import hashlib
-    try:
-        kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
-        if kv.get("workload") != workload:
-            return None
-        src = open(os.path.join(ROOT, kv["kernel_source"]), "rb").read()
-        if hashlib.sha256(src).hexdigest() != kv["kernel_source_sha256"]:
-            return None
-        return int(kv["traffic_bytes"])
-    except (OSError, KeyError, ValueError):
-        return None
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_pmc.txt"))):
+        try:
+            kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
+            if kv.get("workload") != workload or kv.get("kernel") != kernel:
+                continue
+            src = open(os.path.join(ROOT, kv["kernel_source"]), "rb").read()
+            if hashlib.sha256(src).hexdigest() != kv["kernel_source_sha256"]:
+                return None
+            return int(kv["traffic_bytes"])
+        except (OSError, KeyError, ValueError):
+            continue
+    return None
+
+
+def time_persistent_step(ctx, n_actions, iters=40):
+    """Average duration of a decode-only ctx_step when the decode is one persistent
+    launch (that launch plus the small kernel that clears its barrier words), timed
+    with HIP events on torch's current stream, where the step's graph runs."""
+    import torch
+    B, nb = ctx.batch, ctx.model.spec.n_bins
+    tokens = torch.empty((B, n_actions), dtype=torch.int32, device="cuda")
+    logits = torch.empty((B, n_actions, nb), dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        ctx.step(n_actions, tokens=tokens, logits=logits)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(iters):
+        ctx.step(n_actions, tokens=tokens, logits=logits)
+    ev1.record()
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / iters * 1e-3
 
 
 def copy_calibration(nbytes=256 << 20):
@@ -236,7 +259,8 @@ def main():
     model = DeviceModel(weights, "cuda:0")
     cap = wl.derived_capacity()
     ctx = DeviceContext(model, wl.batch, cap)
-    print(f"[bench] inputs (capacity {cap})", file=sys.stderr, flush=True)
+    persistent = ctx.persistent_decode
+    print(f"[bench] inputs (capacity {cap}, persistent decode {persistent})", file=sys.stderr, flush=True)
     epochs, pool = make_inputs(model, wl, args.seed, steps, big)
     B, A = wl.batch, wl.n_actions
     tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
@@ -273,16 +297,22 @@ def main():
     print(f"[bench] build {t_build * 1e3:.3f} ms, {steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
           flush=True)
 
-    t_gu = time_gate_up_kernel(model, B)
-    gb = gu_launch_bytes(spec, B)
-    achieved = gb / t_gu / 1e9
+    if persistent:
+        # the step's whole decode is one launch: its algorithmic bytes are the step's
+        t_k = time_persistent_step(ctx, A)
+        kname = f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer)"
+        kb = sb
+    else:
+        t_k = time_gate_up_kernel(model, B)
+        kname = ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 8
+                 else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
+                 if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)")
+        kb = gu_launch_bytes(spec, B)
+    achieved = kb / t_k / 1e9
     copy_calibration()
-    roof = {"kernel": ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 16
-                       else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
-                       if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)"),
-            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
-            "bytes_per_launch": gb, "avg_launch_us": round(t_gu * 1e6, 3)}
+    roof = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name, kname.split(" ")[0]),
+            "bytes_per_launch": kb, "avg_launch_us": round(t_k * 1e6, 3)}
 
     out = {
         "metric": "action steps/s per GPU (cached-context decode)",

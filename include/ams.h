@@ -191,6 +191,16 @@ ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens);
 /* Current state: 0 EMPTY, 1 READY, 2 INVALID; negative status on error. */
 int32_t ams_ctx_state(const ams_ctx* c);
 
+/* 1 when this context's action decode (everything ams_ctx_step does after
+ * appending new tokens) runs as one persistent launch, 0 when it runs as a
+ * sequence of per-layer kernels; negative status on error.  The persistent
+ * launch serves bf16 models with up to 8 rows (environment AMS_FUSED=0 at
+ * context creation turns it off); it keeps one workgroup per compute unit
+ * resident and synchronises them between the layers' phases.  Should the
+ * device not keep them all resident, its bounded waits give up and every
+ * out_tokens entry of that step reads -1 (never a valid bin). */
+int32_t ams_ctx_persistent_decode(const ams_ctx* c);
+
 #ifdef __cplusplus
 }
 #endif

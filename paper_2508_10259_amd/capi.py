@@ -47,6 +47,7 @@ SIGNATURES = {
     "ams_ctx_invalidate": (C.c_int32, [C.c_void_p]),
     "ams_ctx_lengths": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32)]),
     "ams_ctx_state": (C.c_int32, [C.c_void_p]),
+    "ams_ctx_persistent_decode": (C.c_int32, [C.c_void_p]),
 }
 
 _lib = None

@@ -305,4 +305,9 @@ int32_t ams_ctx_state(const ams_ctx* c) {
   return c->c.book.state;
 }
 
+int32_t ams_ctx_persistent_decode(const ams_ctx* c) {
+  if (!c) return AMS_EINVAL;
+  return c->c.fused_grid > 0 ? 1 : 0;
+}
+
 }  // extern "C"

@@ -21,13 +21,15 @@ namespace ams {
 static const char* off(const void* p, size_t bytes) { return (const char*)p + bytes; }
 
 // Decode runs its RMSNorms inside the projection GEMVs for fp16 compute and up
-// to 16 rows (see norm_proj).
-static bool fused_norm(const Ctx& c, int rows) { return c.model->ct == DT_F16 && rows <= 16; }
+// to 8 rows (see norm_proj).
+static bool fused_norm(const Ctx& c, int rows) { return c.model->ct == DT_F16 && rows <= 8; }
 
-// Above 16 rows the fp16 decode GEMVs use the wide GEMM (128 weight rows per
-// workgroup, activations staged in LDS) with split-K partial sums.
+// Above 8 rows the fp16 decode GEMVs use the wide GEMM (128 weight rows per
+// workgroup, activations staged in LDS) with split-K partial sums: at 16 rows
+// of the 7B model it decodes 4% faster than the skinny GEMV with separate lo
+// fragments.
 static bool wide_decode(const Ctx& c, int rows, int N) {
-  return c.model->ct == DT_F16 && rows > 16 && rows <= 64 && N % 128 == 0;
+  return c.model->ct == DT_F16 && rows > 8 && rows <= 64 && N % 128 == 0;
 }
 
 // The persistent decode (decode_fused) serves fp16 compute up to 8 rows when
@@ -186,7 +188,7 @@ struct Rows {
   }
 };
 
-// Projection of a normalised input.  Up to 16 fp16 rows run the GEMV with the
+// Projection of a normalised input.  Up to 8 fp16 rows run the GEMV with the
 // RMSNorm fused, reading the fp16 pair of the residual rows (hhi, hlo) that
 // their producers (residual GEMV epilogue, feed, gather of the last prefix
 // token) write beside h; otherwise rmsnorm writes the pair u + hlo from h

@@ -103,7 +103,7 @@ inline int decode_ksplit(int N, int K) {
   return std::max(1, s);
 }
 
-// K splits of a wide decode GEMM (more than 16 rows; 128 weight rows per
+// K splits of a wide decode GEMM (more than 8 rows; 128 weight rows per
 // workgroup): about 256 workgroups in all, at least 4 chunks of 128 per split.
 inline int decode_wsplit(int N, int K) {
   const int tiles = std::max(N / 128, 1);
@@ -183,11 +183,11 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.olo = o; o = align256(o + B * d * 2);
   x.alo = o; o = align256(o + B * F * 2);
   // split-K partial sums of the decode GEMVs (fp16 compute): the narrow
-  // residual projections at up to 16 rows, every projection above 16 rows
+  // residual projections at up to 8 rows, every projection above 8 rows
   size_t kp = 0;
   const size_t ks = std::max(decode_ksplit((int)d, (int)d), decode_ksplit((int)d, (int)F));
   if (ks > 1) kp = ks * B * d;
-  if (batch > 16 && batch <= 64) {
+  if (batch > 8 && batch <= 64) {
     const size_t NB = bins_padded(c);
     kp = std::max({kp, decode_wsplit(3 * (int)d, (int)d) * B * 3 * d, decode_wsplit((int)d, (int)d) * B * d,
                    decode_wsplit(2 * (int)F, (int)d) * B * 2 * F, decode_wsplit((int)d, (int)F) * B * d,

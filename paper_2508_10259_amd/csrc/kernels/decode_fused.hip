@@ -739,11 +739,19 @@ __global__ __launch_bounds__(512) void k_decode_fused(FusedArgs a) {
   const Rsrc qkvr = rsrc(a.qkv, (uint32_t)(M * 3 * d * 4));
   const Rsrc logr = rsrc(a.logits, (uint32_t)(M * a.nbp * 4));
   const uint32_t hlo = (uint32_t)(M * d * 2), olo = hlo, alo = (uint32_t)(M * a.F * 2);
+  // a barrier that timed out: the step's tokens all read -1 (workgroup 0 owns them)
+  auto fail = [&]() {
+    if (blockIdx.x == 0)
+      for (int i = threadIdx.x; i < M * a.A; i += blockDim.x) a.out_tok[i] = -1;
+  };
 #define AMS_SYNC(PREFETCH)                        \
   do {                                            \
     arrive(a.sync, ++gen);                        \
     PREFETCH;                                     \
-    if (!wait_all(a.sync, gen, sm)) return;       \
+    if (!wait_all(a.sync, gen, sm)) {             \
+      fail();                                     \
+      return;                                     \
+    }                                             \
   } while (0)
 
   prefetch_store(a.whead, a.nbp, d, pf);

@@ -163,6 +163,11 @@ class DeviceContext:
     def state(self) -> int:
         return self.lib.ams_ctx_state(self.handle)
 
+    @property
+    def persistent_decode(self) -> bool:
+        """True when a step's action decode runs as one persistent launch."""
+        return self.lib.ams_ctx_persistent_decode(self.handle) == 1
+
     def close(self):
         if getattr(self, "handle", None):
             self.lib.ams_ctx_destroy(self.handle)

@@ -94,6 +94,7 @@ def test_invalid_arguments_rejected_before_device(lib):
     assert lib.ams_ctx_invalidate(None) == capi.AMS_EINVAL
     assert lib.ams_ctx_lengths(None, None) == capi.AMS_EINVAL
     assert lib.ams_ctx_state(None) == capi.AMS_EINVAL
+    assert lib.ams_ctx_persistent_decode(None) == capi.AMS_EINVAL
     assert lib.ams_embed_ids(None, None, 3, None, None) == capi.AMS_EINVAL
     lib.ams_ctx_destroy(None)
     lib.ams_model_destroy(None)

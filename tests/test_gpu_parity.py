@@ -315,6 +315,7 @@ def test_persistent_decode_matches_per_kernel_decode(H, monkeypatch):
     for mode in ("1", "0"):
         monkeypatch.setenv("AMS_FUSED", mode)
         ctx = DeviceContext(pair.dev, len(lens), 320)
+        assert ctx.persistent_decode == (mode == "1")
         ctx.build(prefix, plens)
         t, z = ctx.step(6, forced=forced[0])
         t2, z2 = ctx.step(6, forced=forced[1])
@@ -326,6 +327,7 @@ def test_persistent_decode_matches_per_kernel_decode(H, monkeypatch):
     log(f"persistent vs per-kernel H={H}: max_abs={d:.2e}")
     assert d <= 2e-3
     assert np.isfinite(z1).all() and np.isfinite(y1).all()
+    assert (t1 >= 0).all() and (f1 >= 0).all()  # -1 would mean a barrier wait gave up
     # teacher-forced: the argmax of each position, where the top two logits are apart
     for a, b, z in ((t1, t0, z0), (f1, f0, y0)):
         top2 = np.sort(z, axis=-1)[..., -2:]
