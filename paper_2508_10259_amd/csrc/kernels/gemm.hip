@@ -675,9 +675,12 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
                   wf, *(const half8*)(bp + (size_t)MB * 16 * WIDE_LDK), acc[mb], 0, 0, 0);
           }
         }
-        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, s0 + t + WIDE_WP);
+        // the activation loads go out before the weight loads of this round:
+        // vmcnt retires in issue order, so staging chunk t+2 next round then
+        // waits only for loads older than the newest weight chunk
         if (t + 1 < n) AMS_WIDE_XSTORE((t + 1) & 1);
         if (t + 2 < n) AMS_WIDE_XLOAD(s0 + t + 2);
+        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, s0 + t + WIDE_WP);
         __syncthreads();
       }
     }
