@@ -90,8 +90,11 @@ def time_gate_up_kernel(model, B, iters=240):
     ulo = (u - uhi.float()).half()
     a = torch.empty((B, F), device="cuda", dtype=torch.float16)
     alo = torch.empty((B, F), device="cuda", dtype=torch.float16)
-    # split count of the wide kernel: about two workgroups per CU over 128-row tiles, >= 4 chunks of 128 each
-    wsplit = max(1, min(2 * -(-256 // max(2 * F // 128, 1)), d // 128 // 4))
+    # split count of the wide kernel over its 128-row tiles (the library's rule: the smallest
+    # S <= min(16, chunks / 4) within 5% of the minimum of ceil(tiles * S / 256) / S)
+    tiles, smax = max(2 * F // 128, 1), max(1, min(16, d // 128 // 4))
+    model = {s_: -(-tiles * s_ // 256) / s_ for s_ in range(1, smax + 1)}
+    wsplit = min(s_ for s_, t_ in model.items() if t_ <= 1.05 * min(model.values()))
     part = torch.empty((wsplit, B, 2 * F) if 8 < B <= 64 else (1,), device="cuda", dtype=torch.float32)
     s = torch.cuda.Stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

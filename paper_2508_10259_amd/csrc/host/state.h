@@ -105,14 +105,21 @@ inline int decode_ksplit(int N, int K) {
 }
 
 // K splits of a wide decode GEMM (more than 8 rows; 128 weight rows per
-// workgroup): about two workgroups per CU (two fit at its LDS size), at least
-// 4 chunks of 128 per split.  Against one per CU this measured 2-4% faster
-// decode steps at 16 and 64 rows of the 7B model; three or four per CU were
-// slower again.
+// workgroup, at least 4 chunks of 128 per split, at most 16 splits).  The time
+// model is the rounds of workgroups per CU over the work per workgroup,
+// ceil(tiles * S / 256) / S on the 256 CUs; every further split also adds
+// partial sums and staging, so the smallest S within 5% of the model's minimum
+// is taken.  On the 7B shapes at 16 and 64 rows this is the measured best of
+// S = 1..8 (QKV 8, gate|up 4, O and down 8); counts that leave the last round
+// of workgroups mostly empty lose to both neighbours.
 inline int decode_wsplit(int N, int K) {
-  const int tiles = std::max(N / 128, 1);
-  const int s = std::min(2 * ((256 + tiles - 1) / tiles), (K / 128) / 4);
-  return std::max(1, s);
+  const int tiles = std::max(N / 128, 1), smax = std::max(1, std::min(16, (K / 128) / 4));
+  auto t = [&](int s) { return (double)((tiles * s + 255) / 256) / s; };
+  double best = t(1);
+  for (int s = 2; s <= smax; ++s) best = std::min(best, t(s));
+  int s = 1;
+  while (t(s) > 1.05 * best) ++s;
+  return s;
 }
 
 // Persistent decode (one launch per step) applies up to this many rows.
