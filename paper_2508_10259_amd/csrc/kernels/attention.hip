@@ -9,7 +9,8 @@
 //                     a pass's tokens (a row's new segment at positions
 //                     pos..pos+n-1) over keys 0..pos+n-1 of that row, K/V
 //                     tiles staged in LDS, online softmax; the fp16 kernel
-//                     runs both products on MFMA.
+//                     runs both products on MFMA.  k_attn_extend (fp16) takes
+//                     passes whose segments are at most 16 tokens long.
 //  * k_attn_decode:   one query per row at position p = lens[b] + jpos (a
 //                     fed-back action token).  Appends its own K/V, then
 //                     each workgroup covers one split of the row's keys 0..p
@@ -346,6 +347,204 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   }
 }
 
+
+// Short segments (at most 16 new tokens per row, e.g. a step's observation
+// tokens): one workgroup of 4 waves per (segment, head).  The up to 16
+// queries are the MFMA M side; the waves split the keys in blocks of 32 (wave
+// w takes blocks w, w + 4, ...), each with its own online softmax, and merge
+// in LDS at the end.  K fragments come straight from global memory in the B
+// layout (one key row per lane group); V goes through a per-wave transposed
+// LDS tile as in the long-prefill kernel.
+constexpr int EXT_WAVES = 4, EXT_KB = 32;
+
+template <int DH> struct ExtGeo {
+  static constexpr int NQI = DH / 32;       // MFMA k-steps of S
+  static constexpr int NDJ = DH / 16;       // 16-wide dim blocks of O
+  static constexpr int VPAD = EXT_KB + 2;   // V^T tile row (keys): an odd dword stride
+  static constexpr int PPAD = EXT_KB + 8;
+  static constexpr int VCH = DH / 8;        // 16-byte chunks of a key row
+  static constexpr int VLD = EXT_KB * VCH / 64;  // 16-byte V loads per lane per block
+  static constexpr size_t WAVE_LDS = (size_t)(DH * VPAD + 16 * PPAD) * 2;
+};
+
+template <int DH>
+__global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __restrict__ qkv,
+                                                                const int32_t* __restrict__ row,
+                                                                const int32_t* __restrict__ pos,
+                                                                const int32_t* __restrict__ off, int H, int cap,
+                                                                const float2* __restrict__ rope,
+                                                                const f16* __restrict__ kslab,
+                                                                const f16* __restrict__ vslab, f16* __restrict__ o,
+                                                                float scale) {
+  using G = ExtGeo<DH>;
+  constexpr int NQI = G::NQI, NDJ = G::NDJ, VPAD = G::VPAD, PPAD = G::PPAD, VCH = G::VCH, VLD = G::VLD;
+  constexpr int HALF = DH / 2;
+  extern __shared__ __attribute__((aligned(16))) unsigned char ext_sm[];
+  const int sg = blockIdx.z, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, g = lane >> 4;
+  const int b = row[sg], p0 = pos[sg], t0 = off[sg], n = off[sg + 1] - off[sg];  // n <= 16
+  const int d = H * DH;
+  const int kv_end = p0 + n;  // keys 0 .. p0+n-1
+  f16* VT = (f16*)(ext_sm + wave * G::WAVE_LDS);  // [DH][VPAD]: V^T of this wave's block
+  f16* Pw = VT + DH * VPAD;                        // [16][PPAD]: P of this wave's block
+
+  // Q fragments (A layout): query r, dims 32i + 8g + e, rotated and scaled
+  half8 qf[NQI];
+  {
+    const bool ok = r < n;
+    const float* q = qkv + (size_t)(t0 + (ok ? r : 0)) * 3 * d + h * DH;
+    const float2* rp = rope + (size_t)(p0 + (ok ? r : 0)) * HALF;
+#pragma unroll
+    for (int i = 0; i < NQI / 2; ++i) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int dd = 32 * i + 8 * g + e;  // < HALF; its partner is dd + HALF
+        const float a = ok ? q[dd] : 0.f, c = ok ? q[dd + HALF] : 0.f;
+        const float2 cs = rp[dd];
+        qf[i][e] = (f16)((a * cs.x - c * cs.y) * scale);
+        qf[i + NQI / 2][e] = (f16)((a * cs.y + c * cs.x) * scale);
+      }
+    }
+  }
+  int qp[4];  // positions of this lane's C rows (queries 4g + e); -1 past the segment
+#pragma unroll
+  for (int e = 0; e < 4; ++e) qp[e] = 4 * g + e < n ? p0 + 4 * g + e : -1;
+
+  const f16* Kb = kslab + ((size_t)b * H + h) * cap * DH;
+  const f16* Vb = vslab + ((size_t)b * H + h) * cap * DH;
+  // this lane's V chunks of a block: key (lane / VCH) + (64 / VCH) * v, 16-byte chunk lane % VCH
+  const int vkey = lane / VCH, vch = lane % VCH;
+
+  uint4 kc[2][NQI], vc[VLD];
+  auto load = [&](int kb, uint4 (&kx)[2][NQI], uint4 (&vx)[VLD]) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int key = kb + 16 * c + r;
+      const bool ok = key < kv_end;
+#pragma unroll
+      for (int i = 0; i < NQI; ++i)
+        kx[c][i] = ok ? *(const uint4*)(Kb + (size_t)key * DH + 32 * i + 8 * g) : uint4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int v = 0; v < VLD; ++v) {
+      const int key = kb + vkey + (64 / VCH) * v;
+      vx[v] = key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + vch * 8) : uint4{0u, 0u, 0u, 0u};
+    }
+  };
+
+  float m[4], l[4];
+  f32x4 acc[NDJ];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) { m[e] = -INFINITY; l[e] = 0.f; }
+#pragma unroll
+  for (int j = 0; j < NDJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int kstep = EXT_WAVES * EXT_KB;
+  for (int kb = wave * EXT_KB; kb < kv_end; kb += kstep) {
+    load(kb, kc, vc);
+    // V^T tile of this block (this wave's LDS only)
+#pragma unroll
+    for (int v = 0; v < VLD; ++v) {
+      const half8 vh = __builtin_bit_cast(half8, vc[v]);
+      const int key = vkey + (64 / VCH) * v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) VT[(vch * 8 + e) * VPAD + key] = vh[e];
+    }
+    // S for the two halves of 16 keys
+    f32x4 sc[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      sc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < NQI; ++i)
+        sc[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qf[i], __builtin_bit_cast(half8, kc[c][i]), sc[c], 0, 0, 0);
+    }
+    // causal mask and online softmax per query row 4g+e (its keys sit in the 16 lanes sharing g)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int key = kb + 16 * c + r;
+        if (key > qp[e] || key >= kv_end) sc[c][e] = -INFINITY;
+        mx = fmaxf(mx, sc[c][e]);
+      }
+#pragma unroll
+      for (int o_ = 1; o_ < 16; o_ <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o_, 64));
+      const float m_new = fmaxf(m[e], mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : __expf(m[e] - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float pv = (sc[c][e] == -INFINITY) ? 0.f : __expf(sc[c][e] - m_new);
+        sc[c][e] = pv;
+        rs += pv;
+      }
+#pragma unroll
+      for (int o_ = 1; o_ < 16; o_ <<= 1) rs += __shfl_xor(rs, o_, 64);
+      l[e] = l[e] * alpha + rs;
+      m[e] = m_new;
+#pragma unroll
+      for (int j = 0; j < NDJ; ++j) acc[j][e] *= alpha;
+    }
+    // P (C layout) -> LDS [query][key] -> A layout
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Pw[(4 * g + e) * PPAD + 16 * c + r] = (f16)sc[c][e];
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    const half8 pf = *(const half8*)(Pw + r * PPAD + 8 * g);
+#pragma unroll
+    for (int j = 0; j < NDJ; ++j) {
+      const half8 vf = *(const half8*)(VT + (16 * j + r) * VPAD + 8 * g);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf, vf, acc[j], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // the tile reads are done before the next block overwrites it
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // merge the waves: per-wave (m, l) per query and O rows through LDS (the V^T tiles are free now)
+  __syncthreads();
+  float* wm = (float*)ext_sm;                 // [wave][16]
+  float* wl = wm + EXT_WAVES * 16;            // [wave][16]
+  float* wo = wl + EXT_WAVES * 16;            // [wave][16][DH]
+  if (r == 0)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      wm[wave * 16 + 4 * g + e] = m[e];
+      wl[wave * 16 + 4 * g + e] = l[e];
+    }
+#pragma unroll
+  for (int j = 0; j < NDJ; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) wo[(wave * 16 + 4 * g + e) * DH + 16 * j + r] = acc[j][e];
+  __syncthreads();
+  for (int idx = tid; idx < n * DH; idx += 64 * EXT_WAVES) {
+    const int q = idx / DH, dd = idx % DH;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < EXT_WAVES; ++w) M = fmaxf(M, wm[w * 16 + q]);
+    float L = 0.f, A = 0.f;
+#pragma unroll
+    for (int w = 0; w < EXT_WAVES; ++w) {
+      const float mw = wm[w * 16 + q];
+      if (mw == -INFINITY) continue;  // a wave without keys for this query
+      const float f = __expf(mw - M);
+      L += wl[w * 16 + q] * f;
+      A += wo[(w * 16 + q) * DH + dd] * f;
+    }
+    st<f16>(o + (size_t)(t0 + q) * d + h * DH, dd, A / L);
+  }
+}
+
+template <int DH> constexpr size_t ext_lds() {
+  const size_t tiles = EXT_WAVES * ExtGeo<DH>::WAVE_LDS;
+  const size_t merge = (size_t)(2 * EXT_WAVES * 16 + EXT_WAVES * 16 * DH) * 4;
+  return tiles > merge ? tiles : merge;
+}
+
 template <typename T>
 static hipError_t prefill_t(const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope, const void* k,
                             const void* v, void* o, hipStream_t s) {
@@ -364,8 +563,18 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int ca
                         const void* kslab, const void* vslab, void* o, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;
   if (ct == DT_F32) return prefill_t<float>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
-  const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
   const float scale = 1.0f / sqrtf((float)dh);
+  if (sg.max_len <= 16) {  // short segments: keys split over the waves
+    const dim3 grid(1, H, sg.n_seg);
+    if (dh == 64)
+      hipLaunchKernelGGL((k_attn_extend<64>), grid, dim3(64 * EXT_WAVES), ext_lds<64>(), s, qkv, sg.row, sg.pos,
+                         sg.off, H, cap, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+    else
+      hipLaunchKernelGGL((k_attn_extend<128>), grid, dim3(64 * EXT_WAVES), ext_lds<128>(), s, qkv, sg.row, sg.pos,
+                         sg.off, H, cap, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+    return hipGetLastError();
+  }
+  const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
   if (dh == 64)
     hipLaunchKernelGGL((k_attn_prefill_mfma<64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
                        (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);

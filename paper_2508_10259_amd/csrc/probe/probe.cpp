@@ -66,4 +66,12 @@ int ams_probe_attn_decode(int ct, const float* qkv, const int32_t* lens, int jpo
   return (int)e;
 }
 
+// Causal attention of packed segments (row[s], pos[s], off[s..s+1]) over their rows' slabs.
+int ams_probe_attn_prefill(int ct, const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off,
+                           int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const void* rope,
+                           const void* kslab, const void* vslab, void* o, void* stream) {
+  ams::Segs sg{row, pos, off, n_seg, n_tok, max_len, max_end};
+  return (int)ams::attn_prefill(ct, qkv, sg, H, dh, cap, (const float2*)rope, kslab, vslab, o, (hipStream_t)stream);
+}
+
 }  // extern "C"

@@ -355,6 +355,57 @@ def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     assert np.array_equal(K_after[mask], K[mask]) and np.array_equal(V_after[mask], V[mask])
 
 
+@pytest.mark.parametrize("dh,segs", [
+    (128, [(0, 300, 16), (1, 0, 5), (2, 470, 1), (3, 37, 16)]),   # extension-sized: keys split over waves
+    (64, [(0, 280, 16), (1, 0, 16), (2, 129, 3)]),
+    (128, [(0, 60, 17), (1, 0, 40), (2, 200, 70)]),               # longer segments: 64-query tiles
+    (64, [(1, 33, 100), (0, 0, 1)]),
+])
+def test_attn_prefill(probe, dh, segs):
+    """Causal attention of packed segments (row b, first position p0, n tokens) over keys
+    0..p0+n-1 of each row's slab, fp16: q rotated (rotate-half RoPE) and scaled, against
+    softmax(K q) V in float64 on the same fp16 slab values."""
+    import torch
+    B, H, cap = 4, 2, 512
+    d, half = H * dh, dh // 2
+    log(f"attn_prefill dh={dh} segs={segs}")
+    n_tok = sum(n for _, _, n in segs)
+    qkv = W.random_gaussian((n_tok, 3 * d), 71, dh, n_tok, dtype="f32")
+    K = W.random_gaussian((B, H, cap, dh), 72, dh, dtype="f32").astype(np.float16)
+    V = W.random_gaussian((B, H, cap, dh), 73, dh, dtype="f32").astype(np.float16)
+    tab = _rope_tab(cap, dh)
+    off = np.cumsum([0] + [n for _, _, n in segs]).astype(np.int32)
+    rows = torch.tensor([b for b, _, _ in segs], dtype=torch.int32, device="cuda")
+    pos = torch.tensor([p for _, p, _ in segs], dtype=torch.int32, device="cuda")
+    offd = torch.from_numpy(off).cuda()
+    qkv_d, K_d, V_d, tab_d = _dev(qkv, "f32"), _dev(K, "f16"), _dev(V, "f16"), _dev(tab, "f32")
+    o = torch.full((n_tok, d), float("nan"), dtype=torch.float16, device="cuda")
+    max_len = max(n for _, _, n in segs)
+    max_end = max(p + n for _, p, n in segs)
+    rc = probe.ams_probe_attn_prefill(CT["f16"], _ptr(qkv_d), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok,
+                                      max_len, max_end, H, dh, cap, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(o),
+                                      _stream())
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy().astype(np.float64)
+    for si, (b, p0, n) in enumerate(segs):
+        for i in range(n):
+            t, p = off[si] + i, p0 + i
+            cs = tab[p].astype(np.float64)
+            for h in range(H):
+                q = qkv[t, h * dh:(h + 1) * dh].astype(np.float64)
+                qr = np.concatenate([q[:half] * cs[:, 0] - q[half:] * cs[:, 1],
+                                     q[:half] * cs[:, 1] + q[half:] * cs[:, 0]]) / np.sqrt(dh)
+                qr = qr.astype(np.float16).astype(np.float64)  # the MFMA input is fp16
+                s_ = K[b, h, :p + 1].astype(np.float64) @ qr
+                w = np.exp(s_ - s_.max())
+                ref = (w / w.sum()) @ V[b, h, :p + 1].astype(np.float64)
+                # P enters P.V in fp16 (relative 2^-11), the output is fp16
+                tol = 2e-3 * np.max(np.abs(V[b, h, :p + 1])) + 1e-3 * np.max(np.abs(ref))
+                err = float(np.max(np.abs(got[t, h * dh:(h + 1) * dh] - ref)))
+                assert err <= tol, (si, i, h, err, tol)
+
+
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (100, 256, 384), (256, 512, 1024), (300, 256, 384),
                                    (513, 768, 1024)])
