@@ -103,6 +103,21 @@ void ctx_release(Ctx& c) {
   c.capture_stream = nullptr;
 }
 
+// h += x W^T over the M tokens of a token pass (K inputs per token).  At
+// medium token counts in fp16 the 256 x 256-tile GEMM splits K and a reduction
+// adds the partial sums in split order.
+static hipError_t tokens_resid(Ctx& c, const void* x, const void* W, int M, int K, hipStream_t s) {
+  const Model& md = *c.model;
+  const int d = md.cfg.d_model;
+  const int splits = md.ct == DT_F16 ? prefill_ksplit(M, d, K) : 1;
+  if (splits > 1) {
+    hipError_t e = gemm_big_part(x, W, M, d, K, splits, c.kpart(), s);
+    if (e == hipSuccess) e = part_resid(c.kpart(), splits, M, d, c.h(), nullptr, nullptr, s);
+    return e;
+  }
+  return gemm(md.ct, EPI_RESID, x, W, M, d, K, c.h(), d, s);
+}
+
 // One decoder layer over the M tokens of a token pass.
 static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t s, std::string& err) {
   const Model& md = *c.model;
@@ -113,10 +128,10 @@ static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t
   TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), s));
   TRY(attn_prefill(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), c.o(),
                    s));
-  TRY(gemm(dt, EPI_RESID, c.o(), md.wo(l), M, d, d, c.h(), d, s));
+  TRY(tokens_resid(c, c.o(), md.wo(l), M, d, s));
   TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
   TRY(gemm(dt, EPI_SWIGLU, c.u(), md.wgu(l), M, 2 * F, d, c.a(), F, s));
-  TRY(gemm(dt, EPI_RESID, c.a(), md.wd(l), M, d, F, c.h(), d, s));
+  TRY(tokens_resid(c, c.a(), md.wd(l), M, F, s));
   return hipSuccess;
 }
 

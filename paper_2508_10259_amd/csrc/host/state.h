@@ -155,6 +155,33 @@ inline int fused_split_attn(const Cfg& c, int rows, int capacity, int grid) {
   return s;
 }
 
+// K splits of a residual projection of a token pass (fp16; N = d_model output
+// rows, K inputs): the 256 x 256-tile GEMM takes token counts whose tiles number
+// 160 or more unsplit; below that, when N is a multiple of 256 and the pass has
+// more than 64 tokens, its K steps (of 64) are cut so that tiles x splits
+// reaches about 256 workgroups, each keeping at least 8 K steps.
+inline int prefill_ksplit(int M, int N, int K) {
+  if (M <= 64 || N % 256 != 0 || K % 64 != 0) return 1;
+  const int tiles = (N / 256) * ((M + 255) / 256);
+  if (tiles >= 160) return 1;
+  return std::max(1, std::min((256 + tiles - 1) / tiles, (K / 64) / 8));
+}
+
+// Floats of split-K partial sums the token passes of a context need (at most
+// pass_tokens tokens per pass; the O projection has K = d, the down projection
+// K = F).
+inline size_t prefill_part_floats(const Cfg& c, int pass_tokens) {
+  size_t best = 0;
+  const int d = c.d_model, F = c.d_ffn;
+  for (int M = 65; M <= pass_tokens; M = M < 256 ? 256 : M + 256) {
+    const int m = std::min(M, pass_tokens);
+    const int s = std::max(prefill_ksplit(m, d, d), prefill_ksplit(m, d, F));
+    if (s > 1) best = std::max(best, (size_t)s * m * d);
+    if ((d / 256) * ((m + 255) / 256) >= 160) break;
+  }
+  return best;
+}
+
 inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens, std::string& err) {
   if (batch < 1 || batch > 1024) { err = "batch must be in [1, 1024]"; return S_EINVAL; }
   if (capacity < 64 || capacity % 64 != 0 || capacity > (1 << 20)) {
@@ -193,8 +220,9 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.hlo = o; o = align256(o + B * d * 2);
   x.olo = o; o = align256(o + B * d * 2);
   x.alo = o; o = align256(o + B * F * 2);
-  // split-K partial sums of the decode GEMVs (fp16 compute): the narrow
-  // residual projections at up to 8 rows, every projection above 8 rows
+  // split-K partial sums (fp16 compute): the decode GEMVs' (the narrow residual
+  // projections at up to 8 rows, every projection above 8 rows) and the token
+  // passes' residual projections at medium token counts
   size_t kp = 0;
   const size_t ks = std::max(decode_ksplit((int)d, (int)d), decode_ksplit((int)d, (int)F));
   if (ks > 1) kp = ks * B * d;
@@ -204,6 +232,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
                    decode_wsplit(2 * (int)F, (int)d) * B * 2 * F, decode_wsplit((int)d, (int)F) * B * d,
                    decode_wsplit((int)NB, (int)d) * B * NB});
   }
+  if (es == 2) kp = std::max(kp, prefill_part_floats(c, (int)x.pass_tokens));
   x.kpart = o; o = align256(o + kp * 4);
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);

@@ -419,7 +419,9 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const f16* __restrict__ u, c
 // distinct bank groups.  A wave reuses each A fragment for 8 B fragments and
 // each B fragment for 4 A fragments.  The epilogue runs from registers: a lane
 // holds 4 consecutive tokens of one weight row per 16 x 16 block, and the gate
-// and up blocks of a SwiGLU pair sit side by side in the same lane.
+// and up blocks of a SwiGLU pair sit side by side in the same lane.  With
+// EPI_PART the K steps are cut into gridDim.y splits, each writing its partial
+// sums (for medium token counts, where the tiles alone leave CUs idle).
 
 constexpr int GBM = 256, GBN = 256, GBK = 64;
 constexpr int G_TILE = 256 * 128;         // bytes of one A or B tile (256 rows of 64 fp16)
@@ -466,8 +468,11 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
   const int in_grp = Lx - grp * 8 * tn_n;
   const int m0 = (first_m + in_grp % gm) * GBM, n0 = (in_grp / gm) * GBN;
   const int alast = M - 1 - m0;  // last valid A row of this tile (>= 0)
-  const f16* A = u + (size_t)m0 * K;
-  const f16* B = W + (size_t)n0 * K;
+  // K steps of this workgroup: split blockIdx.y of gridDim.y (EPI_PART; one split otherwise)
+  const int KT_all = K / GBK, sp = blockIdx.y, S = gridDim.y;
+  const int kt0 = sp * KT_all / S, kt1 = (sp + 1) * KT_all / S;
+  const f16* A = u + (size_t)m0 * K + (size_t)kt0 * GBK;
+  const f16* B = W + (size_t)n0 * K + (size_t)kt0 * GBK;
 
   f32x4 acc[4][8];
 #pragma unroll
@@ -477,7 +482,7 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
 
   // fragment rows of this lane: A rows wm*64 + 16 i + r, B rows wn*128 + 16 j + r (all = r mod 8)
   const int sw = r & 7;
-  const int KT = K / GBK;
+  const int KT = kt1 - kt0;
   big_dma(gsm, A, B, K, 0, alast, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -519,11 +524,13 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
           st<f16>((f16*)out, (size_t)tok * ldo + col, silu(acc[i][2 * pr][e]) * acc[i][2 * pr + 1][e]);
         }
       } else {
+        // EPI_PART: this split's partial sums at out[sp][tok][n] (ldo = N)
+        const size_t rowo = ((size_t)(EPI == EPI_PART ? sp * M : 0) + tok) * ldo;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          float* p = (float*)out + (size_t)tok * ldo + n0 + wn * 128 + j * 16 + r;
-          if constexpr (EPI == EPI_STORE) *p = acc[i][j][e];
-          else *p += acc[i][j][e];
+          float* p = (float*)out + rowo + n0 + wn * 128 + j * 16 + r;
+          if constexpr (EPI == EPI_RESID) *p += acc[i][j][e];
+          else *p = acc[i][j][e];
         }
       }
     }
@@ -531,9 +538,10 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
 }
 
 template <int EPI>
-static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm_big<EPI>), dim3((N / GBN) * ((M + GBM - 1) / GBM)), dim3(512), G_LDS, s, u, W, M, N,
-                     K, out, ldo);
+static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
+                             int splits = 1) {
+  hipLaunchKernelGGL((k_gemm_big<EPI>), dim3((N / GBN) * ((M + GBM - 1) / GBM), splits), dim3(512), G_LDS, s, u, W,
+                     M, N, K, out, ldo);
   return hipGetLastError();
 }
 
@@ -833,12 +841,20 @@ static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, i
     const SkinnyArgs a{(const f16*)u, (const f16*)ulo, 0.f, (const f16*)W, M, K, out, ldo, (f16*)o16, (f16*)olo};
     return skinny_dispatch<EPI, false>(a, N, s);
   }
-  // 256 x 256 tiles when they alone fill the chip (one workgroup per CU), 128 x 128 otherwise
-  if (N % GBN == 0 && (size_t)(N / GBN) * ((M + GBM - 1) / GBM) >= 256)
+  // 256 x 256 tiles from 160 of them on (five in eight CUs busy), 128 x 128 below: on the 7B
+  // shapes the big tiles won at 172 (gate|up, 288 tokens) and 192 (QKV, 1024 tokens) tiles and
+  // lost at 96 and 64
+  if (N % GBN == 0 && (size_t)(N / GBN) * ((M + GBM - 1) / GBM) >= 160)
     return launch_big<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
+}
+
+hipError_t gemm_big_part(const void* u, const void* W, int M, int N, int K, int splits, float* part, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (N % GBN != 0 || K % GBK != 0 || splits < 1 || splits > K / GBK) return hipErrorInvalidValue;
+  return launch_big<EPI_PART>((const f16*)u, (const f16*)W, M, N, K, part, N, s, splits);
 }
 
 hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {

@@ -67,6 +67,10 @@ hipError_t part_resid(const float* part, int splits, int M, int N, float* h, voi
 // The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
 // callable for any M (N a multiple of 256, K of 64); same epilogues.
 hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s);
+// Split-K form of it (1 <= splits <= K/64): part[s][m][n] = the s-th of `splits`
+// equal ranges of K steps of sum_k u[m][k] W[n][k]; part holds splits * M * N
+// floats.  part_resid adds them to the residual.
+hipError_t gemm_big_part(const void* u, const void* W, int M, int N, int K, int splits, float* part, hipStream_t s);
 
 // Decode GEMV with the preceding RMSNorm fused (fp16, M <= 16), on the fp16
 // copy x = hhi (+ hlo, its rounding error, when non-NULL) of the residual rows:

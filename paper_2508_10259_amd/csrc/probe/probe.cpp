@@ -17,6 +17,11 @@ int ams_probe_gemm_big(int epi, const void* u, const void* W, int M, int N, int 
   return (int)ams::gemm_big(epi, u, W, M, N, K, out, ldo, (hipStream_t)stream);
 }
 
+int ams_probe_gemm_big_part(const void* u, const void* W, int M, int N, int K, int splits, float* part,
+                            void* stream) {
+  return (int)ams::gemm_big_part(u, W, M, N, K, splits, part, (hipStream_t)stream);
+}
+
 int ams_probe_gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                         void* stream) {
   return (int)ams::gemm_part(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);

@@ -406,6 +406,27 @@ def test_attn_prefill(probe, dh, segs):
                 assert err <= tol, (si, i, h, err, tol)
 
 
+@pytest.mark.parametrize("M,N,K,splits", [(1024, 512, 1024, 4), (300, 256, 704, 3), (65, 768, 384, 6)])
+def test_gemm_big_part(probe, M, N, K, splits):
+    """Split-K form of the 256 x 256-tile GEMM: split s holds the product over its own range
+    of 64-wide K steps (s*KT/S .. (s+1)*KT/S), against the exact fp16 products."""
+    import torch
+    log(f"gemm_big_part M={M} N={N} K={K} splits={splits}")
+    u = _rand((M, K), 44, M, K)
+    Wt = _rand((N, K), 45, N, K, std=0.05)
+    part = torch.full((splits * M * N,), float("nan"), dtype=torch.float32, device="cuda")
+    ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
+    assert probe.ams_probe_gemm_big_part(_ptr(ud), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
+    torch.cuda.synchronize()
+    got = part.view(splits, M, N).cpu().numpy().astype(np.float64)
+    KT = K // 64
+    for sp in range(splits):
+        k0, k1 = sp * KT // splits * 64, (sp + 1) * KT // splits * 64
+        ref = _f(u[:, k0:k1], "f16") @ _f(Wt[:, k0:k1], "f16").T
+        tol = 2e-5 * max(1.0, float(np.max(np.abs(ref)))) * np.sqrt(max(k1 - k0, 64) / 64)
+        assert float(np.max(np.abs(got[sp] - ref))) <= tol, sp
+
+
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (100, 256, 384), (256, 512, 1024), (300, 256, 384),
                                    (513, 768, 1024)])
