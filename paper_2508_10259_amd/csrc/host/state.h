@@ -127,9 +127,11 @@ constexpr int FUSED_MAX_ROWS = 8;
 // Split-K units of its O and down projections: at most this many.
 inline size_t fused_part_units(const Cfg& c) { return std::max<size_t>(c.d_model / 16, 1024); }
 // K splits of a residual projection (d/16 strips over K/128 chunks) in the
-// persistent decode on `grid` workgroups: a unit's weights should fit the 64 KB
-// a workgroup loads while it waits at the barrier before the phase, as long as
-// there are workgroups to spare.
+// persistent decode on `grid` workgroups: a unit's weights should stay within
+// 64 KB (half of what a workgroup loads while it waits at the barrier before
+// the phase: at 128 KB per workgroup the 12-layer d=1024 down projection
+// measured no faster than split in two), as long as there are workgroups to
+// spare.
 inline int fused_split(const Cfg& c, int K, int grid) {
   const int strips = c.d_model / 16, nch = K / 128;
   if (strips >= grid) return 1;
@@ -141,12 +143,12 @@ inline int fused_split(const Cfg& c, int K, int grid) {
 }
 
 // Key splits of its attention.  A split's keys take one round of its 8 waves
-// when they number at most 8 x 5 x (64 / (head_dim / 8)) (320 at head_dim 64,
-// 160 at 128).  Merging splits costs a memory round trip, so more splits than
+// when they number at most 8 waves x (5 or 8 iterations) x (64 / (head_dim / 8))
+// keys per iteration (320 at head_dim 64, 256 at 128).  Merging splits costs a memory round trip, so more splits than
 // that are taken only when (row, head) items would leave at least 3 in 4
 // workgroups idle (then up to 8).  Partials stay within the split-K buffer.
 inline int fused_split_attn(const Cfg& c, int rows, int capacity, int grid) {
-  const int items = rows * c.n_heads, round = 8 * 5 * (64 / (c.head_dim / 8));
+  const int items = rows * c.n_heads, round = 8 * (c.head_dim == 64 ? 5 : 8) * (64 / (c.head_dim / 8));
   const int need = (capacity + round - 1) / round;  // splits for one round each
   const int spare = grid / std::max(items, 1);      // splits the idle workgroups allow
   int s = std::max(need, spare >= 4 ? std::min(spare, 8) : 1);

@@ -96,10 +96,11 @@ struct FusedSmem {
 };
 
 // Registers a wave fills for the next phase while it waits at the barrier:
-// the weights of its first batch of GEMV chunks (a[0..7]), or the first block
-// of keys (a[0..4]) and values (a[5..9]) of its attention unit.
+// the weights of its first two batches of GEMV chunks (a[0..7], a[8..15]), or
+// the first block of keys (a[0..IT-1]) and values (a[IT..2IT-1]) of its
+// attention unit.
 struct Prefetch {
-  uint4 a[10];
+  uint4 a[16];
 };
 
 // Grid barrier number `gen` (1, 2, ... within a launch), in two halves so
@@ -199,19 +200,20 @@ __device__ __forceinline__ void mma_batch(const uint4 (&w)[8], const uint4 (&x)[
   }
 }
 
-// Weights of this wave's first batch of a unit (the part a GEMV unit takes from
-// a Prefetch).
+// Weights of this wave's first two batches of a unit (the part a GEMV unit
+// takes from a Prefetch).
 template <int RB>
 __device__ __forceinline__ void prefetch_gemv(const f16* W, int K, int n0, int c0, int c1, Prefetch& pf) {
   int w0, w1;
   wave_chunks(c0, c1, w0, w1);
   load_w<RB>(W, K, n0, w0, w1, *(uint4(*)[8])pf.a);
+  load_w<RB>(W, K, n0, w0 + GB<RB>::CB, w1, *(uint4(*)[8])(pf.a + 8));
 }
 
 // GEMV of one unit: rows n0 .. n0 + 16*RB - 1 of W [N][K] (fp16) over K chunks
 // [c0, c1) of 128 for up to 8 tokens, input the fp16 pair x = hi + lo read
-// through xr (hi at byte 0, lo at lo_off, each [M][K]); the first batch's
-// weights come from pf when use_pf.  The sums over the waves are left in
+// through xr (hi at byte 0, lo at lo_off, each [M][K]); the first two
+// batches' weights come from pf when use_pf.  The sums over the waves are left in
 // sm.red; NRM also leaves 1/rms of each token (statistic of hi over all of K,
 // which the unit must then cover) in sm.rstd.
 template <int RB, bool NRM>
@@ -231,24 +233,28 @@ __device__ __forceinline__ void gemv_unit(const f16* __restrict__ W, int K, int 
   const int tk = r & 7;
   const uint32_t xo = (r >= 8 ? lo_off : 0u) + (uint32_t)(((tk < M ? tk : 0) * K + g * 8) * 2);
   float ss0 = 0.f, ss1 = 0.f;
-  uint4(&wa)[8] = *(uint4(*)[8])pf.a;  // the prefetched batch is the first of the two stream buffers
-  uint4 xa[8], wb[8], xb[8];
-  if (!use_pf) load_w<RB>(W, K, n0, w0, w1, wa);
+  // the two stream buffers are the prefetch registers: batches alternate between them
+  uint4(&wa)[8] = *(uint4(*)[8])pf.a;
+  uint4(&wb)[8] = *(uint4(*)[8])(pf.a + 8);
+  uint4 xa[8], xb[8];
+  if (!use_pf) {
+    load_w<RB>(W, K, n0, w0, w1, wa);
+    load_w<RB>(W, K, n0, w0 + CB, w1, wb);
+  }
   load_x<RB>(xr, xo, w0, w1, xa);
+  load_x<RB>(xr, xo, w0 + CB, w1, xb);
   for (int cb = w0; cb < w1; cb += 2 * CB) {
-    const int cn = cb + CB;
-    if (cn < w1) {
-      load_w<RB>(W, K, n0, cn, w1, wb);
-      load_x<RB>(xr, xo, cn, w1, xb);
-    }
     mma_batch<RB, NRM>(wa, xa, cb, w1, acc, ss0, ss1);
-    if (cn < w1) {
-      const int cn2 = cn + CB;
-      if (cn2 < w1) {
-        load_w<RB>(W, K, n0, cn2, w1, wa);
-        load_x<RB>(xr, xo, cn2, w1, xa);
+    if (cb + 2 * CB < w1) {
+      load_w<RB>(W, K, n0, cb + 2 * CB, w1, wa);
+      load_x<RB>(xr, xo, cb + 2 * CB, w1, xa);
+    }
+    if (cb + CB < w1) {
+      mma_batch<RB, NRM>(wb, xb, cb + CB, w1, acc, ss0, ss1);
+      if (cb + 3 * CB < w1) {
+        load_w<RB>(W, K, n0, cb + 3 * CB, w1, wb);
+        load_x<RB>(xr, xo, cb + 3 * CB, w1, xb);
       }
-      mma_batch<RB, NRM>(wb, xb, cn, w1, acc, ss0, ss1);
     }
   }
 #pragma unroll
@@ -436,7 +442,7 @@ template <int DH> struct FGeo {
   static constexpr int CH = 8;           // fp16 elements per 16-byte chunk
   static constexpr int NC = DH / CH;     // lanes per key
   static constexpr int KS = 64 / NC;     // keys per wave per iteration
-  static constexpr int IT = 5;           // iterations per block
+  static constexpr int IT = DH == 64 ? 5 : 8;  // iterations per block: all 8 waves busy on ~300 keys at 64
   static constexpr int BK = KS * IT;     // keys per wave per block
 };
 
@@ -473,7 +479,7 @@ __device__ __forceinline__ void key_range(int p, int sp, int S, int& k0, int& k1
 // V into kv[IT..2IT); keys >= k1 and the pass's own position p (its K/V come
 // from registers) read zeros.
 template <int DH>
-__device__ __forceinline__ void attn_block(Rsrc kr, Rsrc vr, uint32_t bh, int kb, int k1, int p, uint4 (&kv)[10]) {
+__device__ __forceinline__ void attn_block(Rsrc kr, Rsrc vr, uint32_t bh, int kb, int k1, int p, uint4 (&kv)[16]) {
   using G = FGeo<DH>;
   const int lane = threadIdx.x & 63, ks = lane / G::NC, i0 = (lane % G::NC) * G::CH;
 #pragma unroll
@@ -528,7 +534,7 @@ __device__ void phase_attn(const FusedArgs& a, int l, int jpos, FusedSmem& sm, P
     key_range(p, sp, S, k0, k1);
     const uint32_t bh = (uint32_t)((b * H + h) * a.cap);
     const int kb0 = k0 + wave * BK;
-    uint4(&kv)[10] = pf.a;  // the first unit's first block was prefetched into these
+    uint4(&kv)[16] = pf.a;  // the first unit's first block was prefetched into these
     if (u != (int)blockIdx.x && kb0 < k1) attn_block<DH>(kr_, vr_, bh, kb0, k1, p, kv);
 
     // this lane's CH dimensions of the rotated, scaled query and of the new key
