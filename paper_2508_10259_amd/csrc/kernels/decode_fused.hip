@@ -16,10 +16,13 @@
 // packed weights, the RoPE table, the row lengths and the bin embeddings
 // (never written during a launch) use plain loads.
 //
-// Barrier: a hierarchical counter (8 groups of workgroups, then one global
-// counter; the last arrival sets one release flag per group) with bounded
-// spinning: a wait that exceeds its bound sets the error word, which makes
-// every other workgroup stop at its next barrier, so the grid always drains.
+// Barrier: eight group counters (workgroup i arrives at counter i mod 8); the
+// last arrival of a group writes the barrier number into its slot of eight
+// replicated flag lines, one line per group, and each workgroup polls its
+// group's line until all eight slots have reached it (so no line is both
+// polled by every workgroup and hit by atomics).  Spinning is bounded: a wait
+// that exceeds its bound sets the error word, which makes every other
+// workgroup stop at its next barrier, so the grid always drains.
 //
 // GEMV phases reuse the decode GEMV's MFMA scheme (weight rows on the M side,
 // the up-to-8 tokens' fp16 pairs hi | lo as the 16 B columns, waves splitting
@@ -77,9 +80,8 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 }  // namespace
 
 // Words of the synchronisation area (256-byte lines).
-constexpr int SYNC_LINE = 64;
-constexpr int SYNC_GLOBAL = 8 * SYNC_LINE;
-constexpr int SYNC_FLAG = 9 * SYNC_LINE;    // + group * SYNC_LINE
+constexpr int SYNC_LINE = 64;              // group counter g at g * SYNC_LINE
+constexpr int SYNC_FLAG = 9 * SYNC_LINE;   // + r * SYNC_LINE + g: group g's flag, replica r
 constexpr int SYNC_ERROR = 17 * SYNC_LINE;
 constexpr int SYNC_STRIP = 32 * SYNC_LINE;  // + strip: split-K arrival counters
 constexpr unsigned SPIN_LIMIT = 1u << 22;   // polls (about a second or more) before a wait gives up
@@ -114,19 +116,23 @@ __device__ void arrive(unsigned* sync, unsigned gen) {
     const unsigned ngrp = G < 8u ? G : 8u;
     const unsigned ng = (G - grp + 7u) / 8u;  // workgroups in this group
     if (add_agent(sync + grp * SYNC_LINE, 1u) == gen * ng - 1u)
-      if (add_agent(sync + SYNC_GLOBAL, 1u) == gen * ngrp - 1u)
-        for (unsigned x = 0; x < ngrp; ++x) st_agent(sync + SYNC_FLAG + x * SYNC_LINE, gen);
+      for (unsigned r = 0; r < ngrp; ++r) st_agent(sync + SYNC_FLAG + r * SYNC_LINE + grp, gen);
   }
 }
+// Wave 0 polls its group's flag line (lane x reads group x mod 8's slot).
 // Returns false once any wait of the launch has timed out.
 __device__ bool wait_all(unsigned* sync, unsigned gen, FusedSmem& sm) {
-  if (threadIdx.x == 0) {
-    const unsigned grp = blockIdx.x & 7u;
+  if (threadIdx.x < 64) {
+    const unsigned G = gridDim.x, x = threadIdx.x & 7u;
+    const unsigned want = x < G ? gen : 0u;
+    const unsigned* flag = sync + SYNC_FLAG + (blockIdx.x & 7u) * SYNC_LINE + x;
     unsigned spins = 0;
-    while (ld_agent(sync + SYNC_FLAG + grp * SYNC_LINE) < gen) {
+    while (!__all(ld_agent(flag) >= want)) {
       if ((++spins & 1023u) == 0 && (spins >= SPIN_LIMIT || ld_agent(sync + SYNC_ERROR) != 0u)) {
-        st_agent(sync + SYNC_ERROR, 1u);
-        sm.stop = 1;
+        if (threadIdx.x == 0) {
+          st_agent(sync + SYNC_ERROR, 1u);
+          sm.stop = 1;
+        }
         break;
       }
     }
