@@ -7,7 +7,9 @@ exposes build / step / invalidate.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes as C
+import weakref
 from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -15,6 +17,23 @@ import torch
 
 from . import capi
 from .workload import MATRICES, ModelSpec, Prefix, Weights
+
+
+# Handles still open when the interpreter exits are released by an exit hook
+# (contexts first, then models) while the HIP runtime that owns their streams
+# and graphs is certainly up, not left to object finalisation at shutdown.
+_live_contexts: "weakref.WeakSet" = weakref.WeakSet()
+_live_models: "weakref.WeakSet" = weakref.WeakSet()
+
+
+@atexit.register
+def _release_live_handles() -> None:
+    for group in (_live_contexts, _live_models):
+        for obj in list(group):
+            try:
+                obj.close()
+            except Exception:
+                pass
 
 
 def torch_dtype(dtype: str) -> torch.dtype:
@@ -76,6 +95,7 @@ class DeviceModel:
                                              _stream(), C.byref(h)), "ams_model_create")
         torch.cuda.current_stream().synchronize()
         self.handle = h
+        _live_models.add(self)
         # the packed copy is all the library reads afterwards, except `embed`
         self.source = src if keep_source else {"embed": self.embed}
 
@@ -128,6 +148,7 @@ class DeviceContext:
                                            nbytes, C.byref(h)), "ams_ctx_create")
         self.handle = h
         self._keep = []
+        _live_contexts.add(self)
 
     def build(self, prefix: torch.Tensor, lens: Sequence[int]) -> None:
         assert prefix.is_contiguous()
