@@ -128,15 +128,16 @@ constexpr int FUSED_MAX_ROWS = 8;
 inline size_t fused_part_units(const Cfg& c) { return std::max<size_t>(c.d_model / 16, 1024); }
 // K splits of a residual projection (d/16 strips over K/128 chunks) in the
 // persistent decode on `grid` workgroups: a unit's weights should stay within
-// 64 KB (half of what a workgroup loads while it waits at the barrier before
-// the phase: at 128 KB per workgroup the 12-layer d=1024 down projection
-// measured no faster than split in two), as long as there are workgroups to
-// spare.
+// 32 KB (the two weight batches a workgroup loads while it waits at the
+// barrier before the phase), as long as there are workgroups to spare.  On the
+// 12-layer d=1024 decoder at 8 rows the down projection (128 KB per strip)
+// measured 8.2 / 6.1 / 5.0 us per phase split 1 / 2 / 4 ways, while splitting
+// the O projection (32 KB per strip) in two cost 1.1 us more.
 inline int fused_split(const Cfg& c, int K, int grid) {
   const int strips = c.d_model / 16, nch = K / 128;
   if (strips >= grid) return 1;
   const size_t unit_bytes = (size_t)16 * K * 2;
-  int s = (int)std::min<size_t>((unit_bytes + 65535) / 65536, (size_t)(grid / std::max(strips, 1)));
+  int s = (int)std::min<size_t>((unit_bytes + 32767) / 32768, (size_t)(grid / std::max(strips, 1)));
   s = std::max(1, std::min({s, nch, FUSED_MAX_SPLIT}));
   while (s > 1 && (size_t)strips * s > fused_part_units(c)) --s;
   return s;
