@@ -394,10 +394,13 @@ __device__ void phase_resid(const FusedArgs& a, const f16* W, int K, int S, Rsrc
   const uint32_t hlo = (uint32_t)(a.M * d * 2);
   for (int u = blockIdx.x; u < units; u += gridDim.x) {
     const int strip = u / S, sp = u % S;
-    gemv_unit<1, false>(W, K, strip * 16, sp * nch / S, (sp + 1) * nch / S, xr, lo_off, a.M, 0.f, sm, pf,
-                        u == (int)blockIdx.x);
     const int ln = threadIdx.x >> 2, i = threadIdx.x & 3, tok = ln & 15, row = 4 * (ln >> 4) + i;
     const bool ok = threadIdx.x < 256 && tok < 8 && tok < a.M;
+    // this thread's residual value, written two phases ago: its load overlaps the GEMV
+    const uint32_t e = (uint32_t)(tok * d + strip * 16 + row);
+    const float h_old = ok ? ldcf(hr, e * 4u) : 0.f;
+    gemv_unit<1, false>(W, K, strip * 16, sp * nch / S, (sp + 1) * nch / S, xr, lo_off, a.M, 0.f, sm, pf,
+                        u == (int)blockIdx.x);
     float y = ok ? gemv_value<1>(sm, 0, ln, i) : 0.f;
     bool fin = true;
     if (S > 1) {
@@ -424,8 +427,7 @@ __device__ void phase_resid(const FusedArgs& a, const f16* W, int K, int S, Rsrc
       }
     }
     if (fin && ok) {
-      const uint32_t e = (uint32_t)(tok * d + strip * 16 + row);
-      const float hn = ldcf(hr, e * 4u) + y;
+      const float hn = h_old + y;
       stcf(hr, e * 4u, hn);
       const f16 hi = sat16(hn);
       stch(hpr, e * 2u, hi);
