@@ -32,6 +32,15 @@ static bool wide_decode(const Ctx& c, int rows, int N) {
   return c.model->ct == DT_F16 && rows > 8 && rows <= 64 && N % 128 == 0;
 }
 
+// On the wide path the RMSNorm of a projection input needs no kernel of its
+// own once a residual reduction has run: part_resid leaves the unnormalised
+// fp16 pair of h in (u, hlo) and its sums of squares per 256 columns, and the
+// projection's reduction (part_store / part_swiglu) divides its rows by rms.
+static bool merge_norm(const Ctx& c, int rows) {
+  const Cfg& m = c.model->cfg;
+  return wide_decode(c, rows, m.d_model) && m.d_model % 256 == 0 && m.d_ffn % 256 == 0 && bins_padded(m) % 256 == 0;
+}
+
 // The persistent decode (decode_fused) serves fp16 compute up to 8 rows when
 // the shapes fit its tiling and its 32-bit buffer offsets; AMS_FUSED=0 turns it
 // off (the per-kernel decode then runs).
@@ -188,6 +197,7 @@ struct Rows {
   void* olo() const { return at(c->lay.olo, c->model->cfg.d_model * 2); }
   void* alo() const { return at(c->lay.alo, c->model->cfg.d_ffn * 2); }
   float* logits() const { return (float*)at(c->lay.logits, bins_padded(c->model->cfg) * 4); }
+  float* ss() const { return (float*)at(c->lay.ss, (size_t)(c->model->cfg.d_model / 256) * 4); }
   int32_t* lens() const { return (int32_t*)at(c->lay.lens, 4); }
   float* part() const {
     const Cfg& m = c->model->cfg;
@@ -207,21 +217,28 @@ struct Rows {
 // RMSNorm fused, reading the fp16 pair of the residual rows (hhi, hlo) that
 // their producers (residual GEMV epilogue, feed, gather of the last prefix
 // token) write beside h; otherwise rmsnorm writes the pair u + hlo from h
-// first (the fused copies are unused then, so hlo serves as u's lo part).
+// first (the fused copies are unused then, so hlo serves as u's lo part) --
+// except on the wide path with ss, where (u, hlo) already hold the
+// unnormalised pair and the reduction divides by rms (merge_norm).
 static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* hhi, const void* hlo, const void* W,
-                            int N, int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err) {
+                            int N, int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err,
+                            const float* ss = nullptr) {
   const Model& md = *g.c->model;
   const float eps = md.cfg.rms_eps;
   if (fused_norm(*g.c, g.n)) {
     TRY(gemv_rmsnorm(md.ct, epi, hhi, eps, W, g.n, N, K, out, ldo, s, hlo, nullptr, olo));
   } else {
     void* ulo = md.ct == DT_F16 ? g.hlo() : nullptr;
-    TRY(rmsnorm(md.ct, h, g.n, K, eps, g.u(), s, ulo));
-    if (wide_decode(*g.c, g.n, N)) {  // partial sums of 128-row tiles, then the epilogue
+    const bool wide = wide_decode(*g.c, g.n, N);
+    if (!(wide && ss)) {
+      ss = nullptr;
+      TRY(rmsnorm(md.ct, h, g.n, K, eps, g.u(), s, ulo));
+    }
+    if (wide) {  // partial sums of 128-row tiles, then the epilogue
       const int splits = decode_wsplit(N, K);
       TRY(gemm_wide(g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), s));
-      if (epi == EPI_SWIGLU) TRY(part_swiglu(g.c->kpart(), splits, g.n, N, out, olo, s));
-      else TRY(part_store(g.c->kpart(), splits, g.n, N, (float*)out, s));
+      if (epi == EPI_SWIGLU) TRY(part_swiglu(g.c->kpart(), splits, g.n, N, out, olo, s, ss, K, eps));
+      else TRY(part_store(g.c->kpart(), splits, g.n, N, (float*)out, s, ss, K, eps));
     } else {
       TRY(gemm(md.ct, epi, g.u(), W, g.n, N, K, out, ldo, s, ulo, nullptr, olo));
     }
@@ -231,16 +248,20 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
 
 // h += W x for the decode rows (x = the pair x + xlo in fp16 compute), writing
 // the fp16 pair of the new rows to (hhi, hlo) when given.  Narrow projections
-// split K over more workgroups and add the partial sums in a reduction kernel.
+// split K over more workgroups and add the partial sums in a reduction kernel;
+// on the wide path with ss that reduction also leaves the unnormalised pair in
+// (u, hlo) and the sums of squares in ss for the next projection.
 static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, const void* W, int K, void* hhi, void* hlo,
-                             hipStream_t s) {
+                             hipStream_t s, float* ss = nullptr) {
   const Ctx& c = *g.c;
   const Model& md = *c.model;
   const int d = md.cfg.d_model;
   if (wide_decode(c, g.n, d)) {
     const int splits = decode_wsplit(d, K);
     hipError_t e = gemm_wide(x, xlo, W, g.n, d, K, splits, c.kpart(), s);
-    if (e == hipSuccess) e = part_resid(c.kpart(), splits, g.n, d, g.h(), hhi, hlo, s);
+    if (e == hipSuccess)
+      e = ss ? part_resid(c.kpart(), splits, g.n, d, g.h(), g.u(), g.hlo(), s, ss)
+             : part_resid(c.kpart(), splits, g.n, d, g.h(), hhi, hlo, s);
     return e;
   }
   const int splits = md.ct == DT_F16 ? decode_ksplit(d, K) : 1;
@@ -263,15 +284,18 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
   void* hlo = fused ? g.hlo() : nullptr;
   void* olo = f16 ? g.olo() : nullptr;   // lo parts of the attention and SwiGLU outputs
   void* alo = f16 ? g.alo() : nullptr;
-  if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err) != hipSuccess)
+  // sums of squares of h from the previous residual reduction (from layer 1 on)
+  float* ss = merge_norm(c, B) ? g.ss() : nullptr;
+  if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err,
+                l > 0 ? ss : nullptr) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
                   g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
-  TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s));
-  if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err) != hipSuccess)
+  TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s, ss));
+  if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err, ss) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(resid_proj(g, g.a(), alo, md.wd(l), F, hhi, hlo, s));
+  TRY(resid_proj(g, g.a(), alo, md.wd(l), F, hhi, hlo, s, ss));
   return hipSuccess;
 }
 
@@ -279,12 +303,14 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
 // projection GEMV over the padded head rows), then argmax/outputs/feed.
 // tok / logits / forced point at the group's first row.
 static hipError_t head(const Rows& g, const float* hin, const void* hhi, const void* hlo, int A, int j, int32_t* tok,
-                       float* logits, const int32_t* forced, hipStream_t s, std::string& err) {
+                       float* logits, const int32_t* forced, hipStream_t s, std::string& err,
+                       const float* ss = nullptr) {
   const Model& md = *g.c->model;
   const Cfg& m = md.cfg;
   const int d = m.d_model, nbp = bins_padded(m);
   const bool fused = fused_norm(*g.c, g.n);
-  if (norm_proj(g, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, g.logits(), nbp, nullptr, s, err) != hipSuccess)
+  if (norm_proj(g, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, g.logits(), nbp, nullptr, s, err, ss) !=
+      hipSuccess)
     return hipErrorLaunchFailure;
   TRY(argmax_feed(md.ct, g.logits(), nbp, md.bin_embed(), g.n, d, m.n_bins, A, j, tok, logits, forced, g.h(),
                   j + 1 < A, s, fused ? g.u() : nullptr, fused ? g.hlo() : nullptr));
@@ -304,7 +330,10 @@ static hipError_t decode_rows(const Rows& g, int A, int32_t* tok, float* logits,
   for (int j = 1; j < A; ++j) {
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_decode(g, l, j - 1, s, err) != hipSuccess) return hipErrorLaunchFailure;
-    if (head(g, g.h(), fused ? g.u() : nullptr, fused ? g.hlo() : nullptr, A, j, gt, gl, gf, s, err) != hipSuccess)
+    // after the last layer's residual reduction: its sums of squares, when kept
+    const float* ss = merge_norm(*g.c, g.n) && m.n_layers > 0 ? g.ss() : nullptr;
+    if (head(g, g.h(), fused ? g.u() : nullptr, fused ? g.hlo() : nullptr, A, j, gt, gl, gf, s, err, ss) !=
+        hipSuccess)
       return hipErrorLaunchFailure;
   }
   return hipSuccess;

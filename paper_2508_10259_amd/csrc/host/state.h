@@ -80,6 +80,7 @@ struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
   size_t slab_layer;  // bytes of K (or V) for one layer
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
+  size_t ss;  // decode rows' sums of squares per 256 residual columns [B][d/256]
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
   // attention output and the SwiGLU output, split-K partials, sync words
   size_t fx_hp, fx_op, fx_ap, fx_part, fx_sync;
@@ -239,6 +240,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.kpart = o; o = align256(o + kp * 4);
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
+  x.ss = o; o = align256(o + B * (size_t)(d / 256 + 1) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
   x.lens = o; o = align256(o + B * 4);
   // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B]

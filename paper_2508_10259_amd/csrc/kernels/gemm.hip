@@ -734,22 +734,45 @@ hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N
   return launch_wide<4, 2>(x, xl, w, M, N, K, splits, part, s);
 }
 
-// out[m][n] = sum_s part[s][m][n] (splits added in order)
-__global__ __launch_bounds__(256) void k_part_store(const float* __restrict__ part, int splits, size_t MN,
+// 1/rms of row m from the partial sums of squares k_part_resid left for it
+// (ss[m][0..nss), added in a fixed order), shared with the whole block;
+// 1 when ss is NULL.  Every thread of the block calls it.
+__device__ float row_rstd(const float* __restrict__ ss, int nss, int m, float inv_n, float eps) {
+  __shared__ float r;
+  if (!ss) return 1.f;
+  if (threadIdx.x < 64) {
+    float t = 0.f;
+    for (int k = threadIdx.x; k < nss; k += 64) t += ss[(size_t)m * nss + k];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+    if (threadIdx.x == 0) r = 1.0f / sqrtf(t * inv_n + eps);
+  }
+  __syncthreads();
+  return r;
+}
+
+// out[m][n] = sum_s part[s][m][n] (splits added in order), times the row's
+// 1/rms when ss is given (N a multiple of 256: a block lies in one row)
+__global__ __launch_bounds__(256) void k_part_store(const float* __restrict__ part, int splits, size_t MN, int N,
+                                                    const float* __restrict__ ss, int nss, float inv_n, float eps,
                                                     float* __restrict__ out) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / N), inv_n, eps);
   if (i >= MN) return;
   float v = 0.f;
   for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
-  out[i] = v;
+  out[i] = v * sc;
 }
 
 // a[m][c] = silu(gate) * up for the packed gate/up rows of output column c
-// (16-row interleave), as an fp16 pair (out, olo)
+// (16-row interleave), as an fp16 pair (out, olo); gate and up times the row's
+// 1/rms when ss is given (N/2 a multiple of 256)
 __global__ __launch_bounds__(256) void k_part_swiglu(const float* __restrict__ part, int splits, int M, int N,
+                                                     const float* __restrict__ ss, int nss, float inv_n, float eps,
                                                      f16* __restrict__ out, f16* __restrict__ olo) {
   const int F = N / 2;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / F), inv_n, eps);
   if (i >= (size_t)M * F) return;
   const int m = (int)(i / F), c = (int)(i % F);
   const size_t gi = (size_t)m * N + (size_t)(c / GU_BLOCK) * 2 * GU_BLOCK + c % GU_BLOCK, MN = (size_t)M * N;
@@ -758,22 +781,27 @@ __global__ __launch_bounds__(256) void k_part_swiglu(const float* __restrict__ p
     gt += part[sp * MN + gi];
     up += part[sp * MN + gi + GU_BLOCK];
   }
-  split16(silu(gt) * up, out, olo, i);
+  split16(silu(gt * sc) * (up * sc), out, olo, i);
 }
 
-hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s) {
+hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s, const float* ss,
+                      int d, float eps) {
   if (M <= 0) return hipSuccess;
+  if (ss && (N % 256 != 0 || d <= 0 || d % 256 != 0)) return hipErrorInvalidValue;
   const size_t MN = (size_t)M * N;
-  hipLaunchKernelGGL(k_part_store, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, MN, out);
+  hipLaunchKernelGGL(k_part_store, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, MN, N, ss,
+                     d / 256, ss ? 1.0f / (float)d : 0.f, eps, out);
   return hipGetLastError();
 }
 
-hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s) {
+hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s,
+                       const float* ss, int d, float eps) {
   if (M <= 0) return hipSuccess;
   if (N % (2 * GU_BLOCK) != 0) return hipErrorInvalidValue;
+  if (ss && ((N / 2) % 256 != 0 || d <= 0 || d % 256 != 0)) return hipErrorInvalidValue;
   const size_t MF = (size_t)M * (N / 2);
-  hipLaunchKernelGGL(k_part_swiglu, dim3((unsigned)((MF + 255) / 256)), dim3(256), 0, s, part, splits, M, N,
-                     (f16*)out, (f16*)olo);
+  hipLaunchKernelGGL(k_part_swiglu, dim3((unsigned)((MF + 255) / 256)), dim3(256), 0, s, part, splits, M, N, ss,
+                     d / 256, ss ? 1.0f / (float)d : 0.f, eps, (f16*)out, (f16*)olo);
   return hipGetLastError();
 }
 
@@ -799,26 +827,39 @@ hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N
 }
 
 // h[m][n] += sum_s part[s][m][n] (splits in order), and the fp16 pair of the
-// updated row when o16 is non-NULL
+// updated row when o16 is non-NULL; with ss, each block (256 columns of one
+// row: N a multiple of 256) also leaves the sum of squares of its new values
+// at ss[blockIdx], i.e. ss[m][n / 256], for the next projection's RMSNorm
 __global__ __launch_bounds__(256) void k_part_resid(const float* __restrict__ part, int splits, int M, int N,
                                                     float* __restrict__ h, f16* __restrict__ o16,
-                                                    f16* __restrict__ olo) {
+                                                    f16* __restrict__ olo, float* __restrict__ ss) {
+  __shared__ float wsq[4];
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t MN = (size_t)M * N;
-  if (i >= MN) return;
-  float v = 0.f;
-  for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
-  const float hn = h[i] + v;
-  h[i] = hn;
-  if (o16) split16(hn, o16, olo, i);
+  float hn = 0.f;
+  if (i < MN) {
+    float v = 0.f;
+    for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
+    hn = h[i] + v;
+    h[i] = hn;
+    if (o16) split16(hn, o16, olo, i);
+  }
+  if (!ss) return;
+  float q = hn * hn;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  if ((threadIdx.x & 63) == 0) wsq[threadIdx.x >> 6] = q;
+  __syncthreads();
+  if (threadIdx.x == 0) ss[blockIdx.x] = (wsq[0] + wsq[1]) + (wsq[2] + wsq[3]);
 }
 
-hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s) {
+hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s,
+                      float* ss) {
   if (M <= 0) return hipSuccess;
-  if (olo && !o16) return hipErrorInvalidValue;
+  if ((olo && !o16) || (ss && N % 256 != 0)) return hipErrorInvalidValue;
   const size_t MN = (size_t)M * N;
   hipLaunchKernelGGL(k_part_resid, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, M, N, h,
-                     (f16*)o16, (f16*)olo);
+                     (f16*)o16, (f16*)olo, ss);
   return hipGetLastError();
 }
 

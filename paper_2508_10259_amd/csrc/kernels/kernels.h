@@ -55,14 +55,24 @@ hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N
 // LDS-staged activations.  The epilogue is one of the part_* reductions.
 hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
-// out[m][n] = sum_s part[s][m][n] (fp32 out).
-hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s);
+// out[m][n] = sum_s part[s][m][n] (fp32 out).  With ss (the sums of squares
+// part_resid left for a residual of width d, both N and d multiples of 256)
+// the GEMM read that residual unnormalised and row m is scaled by its
+// 1/sqrt(sum/d + eps): RMSNorm(h) W^T = (h W^T) / rms(h), the gains being
+// folded into W.
+hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s,
+                      const float* ss = nullptr, int d = 0, float eps = 0.f);
 // out[m][c] = silu(gate) * up of the summed packed gate/up rows of column c
-// (N = 2F packed rows), fp16 with its rounding error in olo (or NULL).
-hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s);
+// (N = 2F packed rows), fp16 with its rounding error in olo (or NULL); ss,
+// d, eps as for part_store (N / 2 a multiple of 256).
+hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, hipStream_t s,
+                       const float* ss = nullptr, int d = 0, float eps = 0.f);
 // h[m][n] += sum_s part[s][m][n], the splits added in order; with o16 (and
-// olo) also the fp16 pair of the updated rows, as gemm()'s EPI_RESID.
-hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s);
+// olo) also the fp16 pair of the updated rows, as gemm()'s EPI_RESID; with ss
+// (N a multiple of 256) the sums of squares of the new rows per 256 columns,
+// ss[m][n / 256], for the next RMSNorm.
+hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s,
+                      float* ss = nullptr);
 
 // The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
 // callable for any M (N a multiple of 256, K of 64); same epilogues.

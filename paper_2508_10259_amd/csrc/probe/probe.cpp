@@ -39,6 +39,18 @@ int ams_probe_gemm_wide(const void* u, const void* ulo, const void* W, int M, in
 int ams_probe_part_store(const float* part, int splits, int M, int N, float* out, void* stream) {
   return (int)ams::part_store(part, splits, M, N, out, (hipStream_t)stream);
 }
+int ams_probe_part_resid_ss(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, float* ss,
+                            void* stream) {
+  return (int)ams::part_resid(part, splits, M, N, h, o16, olo, (hipStream_t)stream, ss);
+}
+int ams_probe_part_store_norm(const float* part, int splits, int M, int N, float* out, const float* ss, int d,
+                              float eps, void* stream) {
+  return (int)ams::part_store(part, splits, M, N, out, (hipStream_t)stream, ss, d, eps);
+}
+int ams_probe_part_swiglu_norm(const float* part, int splits, int M, int N, void* out, void* olo, const float* ss,
+                               int d, float eps, void* stream) {
+  return (int)ams::part_swiglu(part, splits, M, N, out, olo, (hipStream_t)stream, ss, d, eps);
+}
 
 int ams_probe_part_swiglu(const float* part, int splits, int M, int N, void* out, void* olo, void* stream) {
   return (int)ams::part_swiglu(part, splits, M, N, out, olo, (hipStream_t)stream);

@@ -500,6 +500,58 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
         assert torch.equal(olo, (h - h.half().float()).half())
 
 
+@pytest.mark.parametrize("M", [12, 33, 64])
+@pytest.mark.parametrize("splits", [1, 3])
+def test_merge_norm(probe, M, splits):
+    """Wide-path reductions that carry the RMSNorm: the residual reduction leaves the
+    unnormalised fp16 pair and the sums of squares per 256 columns; the projection
+    reductions (store, SwiGLU) divide each row by its rms, RMSNorm(h) W^T = (h W^T) / rms(h)."""
+    import torch
+    d, F, eps = 512, 512, 1e-5
+    Nq = 3 * d
+    log(f"merge_norm M={M} splits={splits}")
+    pr = W.random_gaussian((splits, M, d), 71, M, splits, dtype="f32")
+    h0 = W.random_gaussian((M, d), 72, M, dtype="f32")
+    part = torch.from_numpy(pr.reshape(-1).copy()).cuda()
+    h = torch.from_numpy(h0.copy()).cuda()
+    o16 = torch.zeros((M, d), dtype=torch.float16, device="cuda")
+    olo = torch.zeros((M, d), dtype=torch.float16, device="cuda")
+    ss = torch.full((M, d // 256), float("nan"), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_part_resid_ss(_ptr(part), splits, M, d, _ptr(h), _ptr(o16), _ptr(olo), _ptr(ss),
+                                         _stream()) == 0
+    torch.cuda.synchronize()
+    hn = h.cpu().numpy().astype(np.float64)
+    assert float(np.max(np.abs(hn - (h0 + pr.astype(np.float64).sum(0))))) <= 1e-5
+    assert torch.equal(o16, h.half()) and torch.equal(olo, (h - h.half().float()).half())
+    sq = (hn ** 2).reshape(M, d // 256, 256).sum(-1)
+    assert np.allclose(ss.cpu().numpy(), sq, rtol=1e-5, atol=1e-5)
+    rstd = 1.0 / np.sqrt((hn ** 2).mean(1, keepdims=True) + eps)
+    # store: the summed partials of a projection of the unnormalised rows, scaled by 1/rms
+    pq = W.random_gaussian((splits, M, Nq), 73, M, splits, dtype="f32")
+    out = torch.zeros((M, Nq), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_part_store_norm(_ptr(torch.from_numpy(pq.reshape(-1).copy()).cuda()), splits, M, Nq,
+                                           _ptr(out), _ptr(ss), d, C.c_float(eps), _stream()) == 0
+    torch.cuda.synchronize()
+    ref = pq.astype(np.float64).sum(0) * rstd
+    assert float(np.max(np.abs(out.cpu().numpy() - ref))) <= 2e-5 * max(1.0, float(np.max(np.abs(ref))))
+    # SwiGLU: gate and up both scaled by 1/rms before the product
+    pg = W.random_gaussian((splits, M, 2 * F), 74, M, splits, dtype="f32")
+    a = torch.zeros((M, F), dtype=torch.float16, device="cuda")
+    alo = torch.zeros((M, F), dtype=torch.float16, device="cuda")
+    pgd = torch.from_numpy(pg.reshape(-1).copy()).cuda()
+    assert probe.ams_probe_part_swiglu_norm(_ptr(pgd), splits, M, 2 * F, _ptr(a), _ptr(alo), _ptr(ss), d,
+                                            C.c_float(eps), _stream()) == 0
+    torch.cuda.synchronize()
+    y = pg.astype(np.float64).sum(0) * rstd
+    gg, up = _unpack_gu(y.T, F)
+    ref = (_silu(gg) * up).T
+    got = a.float().cpu().numpy().astype(np.float64) + alo.float().cpu().numpy()
+    assert float(np.max(np.abs(got - ref))) <= 2e-5 * max(1.0, float(np.max(np.abs(ref))))
+    # shapes the scaled reductions do not take are refused
+    assert probe.ams_probe_part_store_norm(_ptr(pgd), splits, M, 384, _ptr(out), _ptr(ss), d, C.c_float(eps),
+                                           _stream()) != 0
+
+
 @pytest.mark.parametrize("M", [5, 17, 33, 64])
 @pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (384, 4096, 8), (256, 1152, 3)])
 @pytest.mark.parametrize("pair", [False, True])
