@@ -85,6 +85,28 @@ def test_small_bf16_ragged(n_layers, d, H, F):
         assert c.band == 1.0
 
 
+@pytest.mark.parametrize("d,H,F", [(512, 8, 1536), (384, 6, 1024)])
+def test_small_bf16_wide_rows(d, H, F):
+    """12 ragged rows decode on the wide path (9-64 rows: LDS-staged GEMM + split-K
+    reductions); d = 512 carries each layer's RMSNorm in the reductions (sums of squares
+    per 256 columns), d = 384 (not a multiple of 256) takes the RMSNorm kernel instead.
+    Gains drawn around 1 so that the folded gains matter."""
+    spec = small_spec("bf16", 2, d, H, F)
+    pair = Pair(spec, seed=11, gains=True)
+    B = 12
+    lens = [1, 5, 17, 33, 40, 64, 65, 90, 100, 128, 129, 150]
+    pre = [W.Prefix(W.make_observation(spec, 12, 100, b, lens[b] - min(6, lens[b] - 1)),
+                    np.arange(min(6, lens[b] - 1), dtype=np.int32) * 5 % 44) for b in range(B)]
+    news = [None,
+            [W.make_observation(spec, 12, 1, b, n) if n else None for b, n in enumerate([2, 0, 1, 3] * 3)]]
+    res = _run(pair, pre, news, 5, 192, forced_from_ref=True, seed_tag=f"wide d={d}")
+    for z_ref, z_gpu, t_gpu, _ in res:
+        c = compare(z_ref, z_gpu, t_gpu, TOL_BF16)
+        log(f"wide rows d={d} max_abs={c.max_abs:.2e} strict={c.strict:.3f} band={c.band:.3f}")
+        assert c.max_abs <= TOL_BF16
+        assert c.band == 1.0
+
+
 def test_small_bf16_nonunit_gains():
     """RMSNorm gains drawn around 1 (folded into the packed weights by the library)."""
     spec = small_spec("bf16", 2, 256, 4, 512)
