@@ -673,24 +673,18 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES) void k_attn_decode(
   const T* Kb = kslab + bh * DH + i0;
   const T* Vb = vslab + bh * DH + i0;
   uint4 kr[IT], vr[IT];
-  // half hf (0 or 1) of a block: key kb + it*KS + ks for iterations it of that
-  // half, into kr/vr[it]; slot p is not read (its K/V come from registers).
-  // While one half is processed the other half's next block is in flight.
-  constexpr int IH = IT / 2;
-  auto load_half = [&](int kb, int hf) {
+  // one block: key kb + it*KS + ks of each iteration; slot p is not read (its K/V come from registers)
+  auto load_block = [&](int kb) {
 #pragma unroll
-    for (int j = 0; j < IH; ++j) {
-      const int it = hf * IH + j, key = kb + it * KS + ks;
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
       const bool ok = key < k1 && key != p;
       kr[it] = ok ? *(const uint4*)(Kb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
       vr[it] = ok ? *(const uint4*)(Vb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
     }
   };
   const int kb0 = k0 + wave * BK;
-  if (kb0 < k1) {  // in flight during the prologue
-    load_half(kb0, 0);
-    load_half(kb0, 1);
-  }
+  if (kb0 < k1) load_block(kb0);  // in flight during the prologue
 
   // this lane's CH dimensions of the rotated, scaled query and of the new
   // token's key and value, rounded to the slab type as every later step reads them
@@ -726,32 +720,31 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES) void k_attn_decode(
 #pragma unroll
   for (int e = 0; e < CH; ++e) acc[e] = 0.f;
 
-  // online softmax over half a block (iterations hf*IH .. hf*IH + IH - 1)
-  auto process_half = [&](int kb, int hf) {
-    float sc[IH];
+  for (int kb = kb0; kb < k1; kb += nw * BK) {
+    if (kb != kb0) load_block(kb);
+    float sc[IT];
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < IH; ++j) {
-      const int it = hf * IH + j, key = kb + it * KS + ks;
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
       float kv[CH];
       Raw<T>::cvt(kr[it], kv);
       float s = 0.f;
 #pragma unroll
       for (int e = 0; e < CH; ++e) s = fmaf(q[e], key == p ? kn[e] : kv[e], s);
       s = group_sum<NC>(s);
-      sc[j] = key < k1 ? s : -INFINITY;
-      mx = fmaxf(mx, sc[j]);
+      sc[it] = key < k1 ? s : -INFINITY;
+      mx = fmaxf(mx, sc[it]);
     }
-    const float m_new = fmaxf(m, cross_max<NC>(mx));
-    // a half with no valid key (only possible for the second half) leaves the state as it is
-    const float alpha = m_new == -INFINITY ? 1.f : __expf(m - m_new);
+    const float m_new = fmaxf(m, cross_max<NC>(mx));  // finite: key kb is valid
+    const float alpha = __expf(m - m_new);           // m = -inf on the first block gives 0
     float ps = 0.f;
 #pragma unroll
     for (int e = 0; e < CH; ++e) acc[e] *= alpha;
 #pragma unroll
-    for (int j = 0; j < IH; ++j) {
-      const int it = hf * IH + j, key = kb + it * KS + ks;
-      const float pe = m_new == -INFINITY ? 0.f : __expf(sc[j] - m_new);  // 0 for masked keys
+    for (int it = 0; it < IT; ++it) {
+      const int key = kb + it * KS + ks;
+      const float pe = __expf(sc[it] - m_new);  // 0 for masked keys
       ps += pe;
       float vv[CH];
       Raw<T>::cvt(vr[it], vv);
@@ -760,13 +753,6 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES) void k_attn_decode(
     }
     l = l * alpha + cross_sum<NC>(ps);
     m = m_new;
-  };
-  for (int kb = kb0; kb < k1; kb += nw * BK) {
-    const int kn_ = kb + nw * BK;  // this wave's next block
-    process_half(kb, 0);
-    if (kn_ < k1) load_half(kn_, 0);
-    process_half(kb, 1);
-    if (kn_ < k1) load_half(kn_, 1);
   }
   // sum the key subgroups; lanes of subgroup 0 then hold the wave's partial output
 #pragma unroll

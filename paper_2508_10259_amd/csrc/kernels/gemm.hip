@@ -757,11 +757,12 @@ __global__ __launch_bounds__(256) void k_part_store(const float* __restrict__ pa
                                                     const float* __restrict__ ss, int nss, float inv_n, float eps,
                                                     float* __restrict__ out) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / N), inv_n, eps);
-  if (i >= MN) return;
   float v = 0.f;
-  for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
-  out[i] = v * sc;
+  if (i < MN)
+    for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + i];
+  // the row's scale after the partial loads are issued: both arrive in one round trip
+  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / N), inv_n, eps);
+  if (i < MN) out[i] = v * sc;
 }
 
 // a[m][c] = silu(gate) * up for the packed gate/up rows of output column c
@@ -772,16 +773,19 @@ __global__ __launch_bounds__(256) void k_part_swiglu(const float* __restrict__ p
                                                      f16* __restrict__ out, f16* __restrict__ olo) {
   const int F = N / 2;
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / F), inv_n, eps);
-  if (i >= (size_t)M * F) return;
-  const int m = (int)(i / F), c = (int)(i % F);
-  const size_t gi = (size_t)m * N + (size_t)(c / GU_BLOCK) * 2 * GU_BLOCK + c % GU_BLOCK, MN = (size_t)M * N;
+  const bool in = i < (size_t)M * F;
   float gt = 0.f, up = 0.f;
-  for (int sp = 0; sp < splits; ++sp) {
-    gt += part[sp * MN + gi];
-    up += part[sp * MN + gi + GU_BLOCK];
+  if (in) {
+    const int m = (int)(i / F), c = (int)(i % F);
+    const size_t gi = (size_t)m * N + (size_t)(c / GU_BLOCK) * 2 * GU_BLOCK + c % GU_BLOCK, MN = (size_t)M * N;
+    for (int sp = 0; sp < splits; ++sp) {
+      gt += part[sp * MN + gi];
+      up += part[sp * MN + gi + GU_BLOCK];
+    }
   }
-  split16(silu(gt * sc) * (up * sc), out, olo, i);
+  // the row's scale after the partial loads are issued: both arrive in one round trip
+  const float sc = row_rstd(ss, nss, (int)((size_t)blockIdx.x * blockDim.x / F), inv_n, eps);
+  if (in) split16(silu(gt * sc) * (up * sc), out, olo, i);
 }
 
 hipError_t part_store(const float* part, int splits, int M, int N, float* out, hipStream_t s, const float* ss,
