@@ -602,7 +602,10 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 // at the end: each writes its partial sums, and a reduction kernel applies
 // the epilogue (part_store / part_resid / part_swiglu).
 
-constexpr int WIDE_ROWS = 128, WIDE_WP = 4, WIDE_LDK = 128 + 8;
+// LDS rows of 128 + 16 halves (288 bytes): the MFMA B-fragment reads (lane r
+// reads row r, lanes 16 apart the next 16 bytes) are free of bank conflicts at
+// that pitch; at 272 bytes every ds_read_b128 took 8 LDS cycles instead of 4.
+constexpr int WIDE_ROWS = 128, WIDE_WP = 4, WIDE_LDK = 128 + 16;
 
 // weight fragments of one chunk of a wave's 16 rows
 __device__ __forceinline__ void wide_wload(uint4 (&w)[4], const f16* wrow, int c) {
