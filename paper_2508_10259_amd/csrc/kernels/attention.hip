@@ -208,7 +208,10 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
                                                            const f16* __restrict__ kslab,
                                                            const f16* __restrict__ vslab, f16* __restrict__ o,
                                                            float scale) {
-  constexpr int QT = 64, KT = 64, HALF = DH / 2, KPAD = DH + 8, VPAD = KT + 8, PPAD = KT + 8;
+  // LDS row pitches: K rows of DH + 16 halves and V^T rows of KT + 16 (288 / 160
+  // bytes) keep the 16-byte fragment reads (lane r reads row r) free of bank
+  // conflicts on gfx950, as every pitch of 32 mod 64 bytes does.
+  constexpr int QT = 64, KT = 64, HALF = DH / 2, KPAD = DH + 16, VPAD = KT + 16, PPAD = KT + 8;
   constexpr int NQI = DH / 32;  // 32-wide dim blocks of a head (MFMA k-steps of S)
   constexpr int NDJ = DH / 16;  // 16-wide dim blocks of O
   __shared__ __attribute__((aligned(16))) f16 Ks[KT * KPAD];
@@ -266,12 +269,27 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
     for (int c = tid; c < KT * CH; c += 256) {
       const int kk = c / CH, ch = c % CH;
       const bool ok = kt + kk < kv_end;
-      uint4 kv = ok ? *(const uint4*)(Kb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
-      uint4 vv = ok ? *(const uint4*)(Vb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
-      *(uint4*)(Ks + kk * KPAD + ch * 8) = kv;
-      const half8 vh = __builtin_bit_cast(half8, vv);
+      *(uint4*)(Ks + kk * KPAD + ch * 8) =
+          ok ? *(const uint4*)(Kb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+    }
+    // V^T: item c takes keys 4(c & 15) .. +3 of the 16-byte dim chunk c >> 4 and
+    // writes, per dim, those 4 keys as one 8-byte word; the 16 lanes of a group
+    // fill one V^T row (64 keys), which keeps the writes free of bank conflicts
+    for (int c = tid; c < (KT / 4) * CH; c += 256) {
+      const int kq = c & 15, ch = c >> 4;
+      half8 vq[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) VT[(ch * 8 + e) * VPAD + kk] = vh[e];
+      for (int i = 0; i < 4; ++i) {
+        const int key = kt + 4 * kq + i;
+        vq[i] = __builtin_bit_cast(half8, key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + ch * 8)
+                                                       : uint4{0u, 0u, 0u, 0u});
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        typedef _Float16 half4v __attribute__((ext_vector_type(4)));
+        const half4v w = {vq[0][e], vq[1][e], vq[2][e], vq[3][e]};
+        *(half4v*)(VT + (ch * 8 + e) * VPAD + 4 * kq) = w;
+      }
     }
     __syncthreads();
 
@@ -354,16 +372,20 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
 // w takes blocks w, w + 4, ...), each with its own online softmax, and merge
 // in LDS at the end.  K fragments come straight from global memory in the B
 // layout (one key row per lane group); V goes through a per-wave transposed
-// LDS tile as in the long-prefill kernel.
+// LDS tile: rows of 32 keys (64 bytes, unpadded) whose four 16-byte key chunks
+// are swizzled by row (chunk ^ ((row >> 1) & 3)), written as 8-byte words of 4
+// keys by lane groups of 8 that fill one row.  On gfx950 that keeps the
+// fragment reads free of bank conflicts and the writes near it.
 constexpr int EXT_WAVES = 4, EXT_KB = 32;
 
 template <int DH> struct ExtGeo {
   static constexpr int NQI = DH / 32;       // MFMA k-steps of S
   static constexpr int NDJ = DH / 16;       // 16-wide dim blocks of O
-  static constexpr int VPAD = EXT_KB + 2;   // V^T tile row (keys): an odd dword stride
+  static constexpr int VPAD = EXT_KB;       // V^T tile row (keys), chunks swizzled
   static constexpr int PPAD = EXT_KB + 8;
   static constexpr int VCH = DH / 8;        // 16-byte chunks of a key row
   static constexpr int VLD = EXT_KB * VCH / 64;  // 16-byte V loads per lane per block
+  static constexpr int VPASS = VCH / 8;          // passes of 8 dim chunks (4 key rows each)
   static constexpr size_t WAVE_LDS = (size_t)(DH * VPAD + 16 * PPAD) * 2;
 };
 
@@ -377,7 +399,7 @@ __global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __r
                                                                 const f16* __restrict__ vslab, f16* __restrict__ o,
                                                                 float scale) {
   using G = ExtGeo<DH>;
-  constexpr int NQI = G::NQI, NDJ = G::NDJ, VPAD = G::VPAD, PPAD = G::PPAD, VCH = G::VCH, VLD = G::VLD;
+  constexpr int NQI = G::NQI, NDJ = G::NDJ, VPAD = G::VPAD, PPAD = G::PPAD, VLD = G::VLD, VPASS = G::VPASS;
   constexpr int HALF = DH / 2;
   extern __shared__ __attribute__((aligned(16))) unsigned char ext_sm[];
   const int sg = blockIdx.z, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
@@ -413,8 +435,10 @@ __global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __r
 
   const f16* Kb = kslab + ((size_t)b * H + h) * cap * DH;
   const f16* Vb = vslab + ((size_t)b * H + h) * cap * DH;
-  // this lane's V chunks of a block: key (lane / VCH) + (64 / VCH) * v, 16-byte chunk lane % VCH
-  const int vkey = lane / VCH, vch = lane % VCH;
+  // this lane's V chunks of a block: keys 4 * vkq .. +3 of the 16-byte dim
+  // chunks vq + 8p (p < VPASS)
+  const int vkq = lane & 7, vq = lane >> 3;
+  static_assert(4 * VPASS == VLD, "V loads per lane");
 
   uint4 kc[2][NQI], vc[VLD];
   auto load = [&](int kb, uint4 (&kx)[2][NQI], uint4 (&vx)[VLD]) {
@@ -427,10 +451,13 @@ __global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __r
         kx[c][i] = ok ? *(const uint4*)(Kb + (size_t)key * DH + 32 * i + 8 * g) : uint4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
-    for (int v = 0; v < VLD; ++v) {
-      const int key = kb + vkey + (64 / VCH) * v;
-      vx[v] = key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + vch * 8) : uint4{0u, 0u, 0u, 0u};
-    }
+    for (int p = 0; p < VPASS; ++p)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kb + 4 * vkq + i;
+        vx[4 * p + i] = key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + (vq + 8 * p) * 8)
+                                     : uint4{0u, 0u, 0u, 0u};
+      }
   };
 
   float m[4], l[4];
@@ -443,13 +470,17 @@ __global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __r
   const int kstep = EXT_WAVES * EXT_KB;
   for (int kb = wave * EXT_KB; kb < kv_end; kb += kstep) {
     load(kb, kc, vc);
-    // V^T tile of this block (this wave's LDS only)
+    // V^T tile of this block (this wave's LDS only): row = dim, 4 keys per write
 #pragma unroll
-    for (int v = 0; v < VLD; ++v) {
-      const half8 vh = __builtin_bit_cast(half8, vc[v]);
-      const int key = vkey + (64 / VCH) * v;
+    for (int p = 0; p < VPASS; ++p) {
+      typedef _Float16 half4v __attribute__((ext_vector_type(4)));
 #pragma unroll
-      for (int e = 0; e < 8; ++e) VT[(vch * 8 + e) * VPAD + key] = vh[e];
+      for (int e = 0; e < 8; ++e) {
+        const int R = (vq + 8 * p) * 8 + e;
+        const half4v w = {__builtin_bit_cast(half8, vc[4 * p + 0])[e], __builtin_bit_cast(half8, vc[4 * p + 1])[e],
+                          __builtin_bit_cast(half8, vc[4 * p + 2])[e], __builtin_bit_cast(half8, vc[4 * p + 3])[e]};
+        *(half4v*)(VT + R * VPAD + (((vkq >> 1) ^ ((R >> 1) & 3)) * 8) + (vkq & 1) * 4) = w;
+      }
     }
     // S for the two halves of 16 keys
     f32x4 sc[2];
@@ -498,7 +529,8 @@ __global__ __launch_bounds__(64 * EXT_WAVES) void k_attn_extend(const float* __r
     const half8 pf = *(const half8*)(Pw + r * PPAD + 8 * g);
 #pragma unroll
     for (int j = 0; j < NDJ; ++j) {
-      const half8 vf = *(const half8*)(VT + (16 * j + r) * VPAD + 8 * g);
+      const int R = 16 * j + r;
+      const half8 vf = *(const half8*)(VT + R * VPAD + ((g ^ ((R >> 1) & 3)) * 8));
       acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf, vf, acc[j], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // the tile reads are done before the next block overwrites it
