@@ -315,7 +315,9 @@ __device__ __forceinline__ void tile_epilogue(const float* Cs, int m0, int n0, i
 // ----------------------------------------------------------------------------
 // tiled f16 MFMA: M > 64
 
-constexpr int TBM = 128, TBN = 128, TBK = 64, TLDK = TBK + 8;
+// Tile rows of TBK + 16 halves (160 bytes): the fragment reads and the staging
+// writes (8 lanes fill one row) are free of LDS bank conflicts on gfx950.
+constexpr int TBM = 128, TBN = 128, TBK = 64, TLDK = TBK + 16;
 constexpr int T_AB_BYTES = 2 * 2 * TBM * TLDK * 2;  // double-buffered A and B tiles (fp16)
 constexpr int T_C_BYTES = TBM * (TBN + 4) * 4;      // fp32 staging for the epilogue
 constexpr int T_LDS = T_AB_BYTES > T_C_BYTES ? T_AB_BYTES : T_C_BYTES;
@@ -331,31 +333,39 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const f16* __restrict__ u, c
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * TBM, n0 = blockIdx.x * TBN;
 
-  // global -> register mapping: thread loads 32 consecutive k of one row of A and of B
-  const int lrow = tid >> 1, lk = (tid & 1) * 32;
-  const bool arow_ok = m0 + lrow < M;
-  const f16* ag = u + (size_t)(arow_ok ? m0 + lrow : 0) * K + lk;
+  // global -> register mapping: thread loads the 16-byte k chunk tid & 7 of rows
+  // tid / 8 + 32 q (q < 4) of A and of B
+  const int lrow = tid >> 3, lk = (tid & 7) * 8;
+  bool aok[4];
+  const f16* ag[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    aok[q] = m0 + lrow + 32 * q < M;
+    ag[q] = u + (size_t)(aok[q] ? m0 + lrow + 32 * q : 0) * K + lk;
+  }
   const f16* bg = W + (size_t)(n0 + lrow) * K + lk;
 
   uint4 ra0, ra1, ra2, ra3, rb0, rb1, rb2, rb3;
 #define AMS_GLOAD(k0)                                                                  \
   do {                                                                                 \
     const uint4 z = {0u, 0u, 0u, 0u};                                                  \
-    ra0 = arow_ok ? *(const uint4*)(ag + (k0)) : z;                                    \
-    ra1 = arow_ok ? *(const uint4*)(ag + (k0) + 8) : z;                                \
-    ra2 = arow_ok ? *(const uint4*)(ag + (k0) + 16) : z;                               \
-    ra3 = arow_ok ? *(const uint4*)(ag + (k0) + 24) : z;                               \
+    ra0 = aok[0] ? *(const uint4*)(ag[0] + (k0)) : z;                                  \
+    ra1 = aok[1] ? *(const uint4*)(ag[1] + (k0)) : z;                                  \
+    ra2 = aok[2] ? *(const uint4*)(ag[2] + (k0)) : z;                                  \
+    ra3 = aok[3] ? *(const uint4*)(ag[3] + (k0)) : z;                                  \
     rb0 = *(const uint4*)(bg + (k0));                                                  \
-    rb1 = *(const uint4*)(bg + (k0) + 8);                                              \
-    rb2 = *(const uint4*)(bg + (k0) + 16);                                             \
-    rb3 = *(const uint4*)(bg + (k0) + 24);                                             \
+    rb1 = *(const uint4*)(bg + (size_t)32 * K + (k0));                                 \
+    rb2 = *(const uint4*)(bg + (size_t)64 * K + (k0));                                 \
+    rb3 = *(const uint4*)(bg + (size_t)96 * K + (k0));                                 \
   } while (0)
 #define AMS_LSTORE(buf)                                                                \
   do {                                                                                 \
-    uint4* a_ = (uint4*)(As + ((buf) * TBM + lrow) * TLDK + lk);                       \
-    uint4* b_ = (uint4*)(Bs + ((buf) * TBN + lrow) * TLDK + lk);                       \
-    a_[0] = ra0; a_[1] = ra1; a_[2] = ra2; a_[3] = ra3;                                \
-    b_[0] = rb0; b_[1] = rb1; b_[2] = rb2; b_[3] = rb3;                                \
+    f16* a_ = As + ((buf) * TBM + lrow) * TLDK + lk;                                   \
+    f16* b_ = Bs + ((buf) * TBN + lrow) * TLDK + lk;                                   \
+    *(uint4*)a_ = ra0; *(uint4*)(a_ + 32 * TLDK) = ra1;                                \
+    *(uint4*)(a_ + 64 * TLDK) = ra2; *(uint4*)(a_ + 96 * TLDK) = ra3;                  \
+    *(uint4*)b_ = rb0; *(uint4*)(b_ + 32 * TLDK) = rb1;                                \
+    *(uint4*)(b_ + 64 * TLDK) = rb2; *(uint4*)(b_ + 96 * TLDK) = rb3;                  \
   } while (0)
 
   f32x4 acc[4][4];
