@@ -231,6 +231,15 @@ def make_inputs(model, wl, seed, steps, device_draws):
     return epochs, pool
 
 
+def roofline_kernel_name(spec, A, B, persistent):
+    """The dominant decode kernel of a workload, as its roofline entry and profiles name it."""
+    if persistent:
+        return f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer)"
+    return ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 8
+            else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
+            if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +251,9 @@ def main():
     ap.add_argument("--cpu-sample-steps", type=int, default=6)
     ap.add_argument("--recompute", action="store_true",
                     help="invalidate + rebuild the prefix before every step (the no-reuse comparison)")
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="time only the roofline kernel (and the calibration copy), print one JSON line and exit: "
+                         "the command the profiles' counter runs use")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decoder shards by episode, "
@@ -266,6 +278,18 @@ def main():
     print(f"[bench] inputs (capacity {cap}, persistent decode {persistent})", file=sys.stderr, flush=True)
     epochs, pool = make_inputs(model, wl, args.seed, steps, big)
     B, A = wl.batch, wl.n_actions
+    if args.roofline_only:
+        if persistent:
+            ctx.build(*epochs[0])
+            t_k = time_persistent_step(ctx, A)
+        else:
+            t_k = time_gate_up_kernel(model, B)
+        copy_calibration()
+        print(json.dumps({"workload": wl.name, "kernel": roofline_kernel_name(spec, A, B, persistent),
+                          "avg_launch_us": round(t_k * 1e6, 3)}), flush=True)
+        ctx.close()
+        model.close()
+        return
     tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
     logits = torch.empty((B, A, spec.n_bins), dtype=torch.float32, device="cuda")
     new_lens = [wl.new_per_step] * B if wl.new_per_step else None
@@ -300,16 +324,13 @@ def main():
     print(f"[bench] build {t_build * 1e3:.3f} ms, {steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
           flush=True)
 
+    kname = roofline_kernel_name(spec, A, B, persistent)
     if persistent:
         # the step's whole decode is one launch: its algorithmic bytes are the step's
         t_k = time_persistent_step(ctx, A)
-        kname = f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer)"
         kb = sb
     else:
         t_k = time_gate_up_kernel(model, B)
-        kname = ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 8
-                 else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
-                 if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)")
         kb = gu_launch_bytes(spec, B)
     achieved = kb / t_k / 1e9
     copy_calibration()
