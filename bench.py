@@ -165,6 +165,49 @@ def time_persistent_step(ctx, n_actions, iters=40):
     return ev0.elapsed_time(ev1) / iters * 1e-3
 
 
+def measured_peaks(nbytes=1 << 30, iters=10):
+    """The two roofs measured on this GPU (the library's peak kernels): HBM stream copy and
+    read of 1 GiB buffers (four times the 256 MB memory-side cache; best of three grid sizes,
+    copy counted as read + write bytes) and the dense fp16 MFMA rate of register-only MFMA
+    chains on every SIMD."""
+    import torch
+    from paper_2508_10259_amd.build import PROBE_LIB
+    lib = C.CDLL(PROBE_LIB)
+    lib.ams_probe_mfma_loop_flops.restype = C.c_double
+    s = torch.cuda.current_stream()
+    sp = C.c_void_p(s.cuda_stream)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    red = torch.empty(8192 * 256, dtype=torch.float32, device="cuda")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def rate(launch, nbytes_moved):
+        for _ in range(2):
+            assert launch() == 0
+        ev0.record(s)
+        for _ in range(iters):
+            launch()
+        ev1.record(s)
+        torch.cuda.synchronize()
+        return nbytes_moved / (ev0.elapsed_time(ev1) / iters * 1e-3) / 1e9
+
+    copy = max(rate(lambda g=g: lib.ams_probe_stream_copy(C.c_void_p(src.data_ptr()), C.c_void_p(dst.data_ptr()),
+                                                          C.c_size_t(nbytes), g, sp), 2 * nbytes)
+               for g in (2048, 4096, 8192))
+    read = max(rate(lambda g=g: lib.ams_probe_stream_read(C.c_void_p(src.data_ptr()), C.c_size_t(nbytes),
+                                                          C.c_void_p(red.data_ptr()), g, sp), nbytes)
+               for g in (2048, 4096, 8192))
+    grid, mi = 2048, 4000
+    fl = lib.ams_probe_mfma_loop_flops(mi, grid)
+    by_shape = [rate(lambda sh=sh: lib.ams_probe_mfma_loop(sh, C.c_float(1.0), mi, C.c_void_p(red.data_ptr()), grid,
+                                                         sp), fl) / 1e3 for sh in (0, 1)]
+    tflops = max(by_shape)
+    del src, dst, red
+    return {"hbm_copy_GBps": round(copy, 1), "hbm_read_GBps": round(read, 1), "mfma_f16_TFLOPs": round(tflops, 1),
+            "mfma_f16_TFLOPs_16x16x32": round(by_shape[0], 1), "mfma_f16_TFLOPs_32x32x16": round(by_shape[1], 1),
+            "how": "stream copy (read + write bytes) and read of 1 GiB; fp16 MFMA 16x16x32 / 32x32x16 register chains, best"}
+
+
 def copy_calibration(nbytes=256 << 20):
     """A device-to-device copy of known size, for scaling the FETCH_SIZE/WRITE_SIZE counters."""
     import torch
@@ -334,9 +377,12 @@ def main():
         kb = gu_launch_bytes(spec, B)
     achieved = kb / t_k / 1e9
     copy_calibration()
+    peaks = measured_peaks()
+    hbm_meas = max(peaks["hbm_copy_GBps"], peaks["hbm_read_GBps"])
     roof = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name, kname.split(" ")[0]),
-            "bytes_per_launch": kb, "avg_launch_us": round(t_k * 1e6, 3)}
+            "bytes_per_launch": kb, "avg_launch_us": round(t_k * 1e6, 3),
+            "frac_vs_measured": round(achieved / hbm_meas, 4)}
 
     out = {
         "metric": "action steps/s per GPU (cached-context decode)",
@@ -353,9 +399,13 @@ def main():
                             + (" (rebuild before every step)" if args.recompute else "")},
         "roofline": roof,
         "step": {"ms": round(t_steps / steps * 1e3, 4), "algorithmic_bytes_no_new_tokens": sb,
-                 "hbm_frac": round(sb / (t_steps / steps) / (HBM_PEAK_GBS * 1e9), 4)},
+                 "hbm_frac": round(sb / (t_steps / steps) / (HBM_PEAK_GBS * 1e9), 4),
+                 "hbm_frac_vs_measured": round(sb / (t_steps / steps) / (hbm_meas * 1e9), 4)},
         "build": {"ms": round(t_build * 1e3, 4), "flops": build_flops(spec, lens),
-                  "mfma_frac": round(build_flops(spec, lens) / t_build / (MFMA_F16_PEAK_TFLOPS * 1e12), 4)},
+                  "mfma_frac": round(build_flops(spec, lens) / t_build / (MFMA_F16_PEAK_TFLOPS * 1e12), 4),
+                  "mfma_frac_vs_measured": round(build_flops(spec, lens) / t_build / (peaks["mfma_f16_TFLOPs"] * 1e12),
+                                                 4)},
+        "measured_peaks": peaks,
     }
     ctx.close()
     model.close()

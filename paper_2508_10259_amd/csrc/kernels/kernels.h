@@ -191,4 +191,16 @@ int fused_sync_words(int d, int H);
 // lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
 
+// Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned
+// pointers and size) from src to dst; a grid-stride read of src whose per-thread
+// sums land in out[grid * 256]; `iters` rounds of fp16 MFMA chains per wave on
+// register operands (all x; shape 0: 8 chains of 16x16x32, 1: 4 of 32x32x16,
+// the same work), each thread's sum of its accumulators in out[grid * 256]
+// (= 1024 x^2 iters while exact in fp32); mfma_loop_flops is the work of one
+// such launch.  Not used by the decoder.
+hipError_t stream_copy(const void* src, void* dst, size_t bytes, int grid, hipStream_t s);
+hipError_t stream_read(const void* src, size_t bytes, float* out, int grid, hipStream_t s);
+hipError_t mfma_loop(int shape, float x, int iters, float* out, int grid, hipStream_t s);
+double mfma_loop_flops(int iters, int grid);
+
 }  // namespace ams

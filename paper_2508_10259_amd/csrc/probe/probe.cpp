@@ -91,4 +91,18 @@ int ams_probe_attn_prefill(int ct, const float* qkv, const int32_t* row, const i
   return (int)ams::attn_prefill(ct, qkv, sg, H, dh, cap, (const float2*)rope, kslab, vslab, o, (hipStream_t)stream);
 }
 
+int ams_probe_stream_copy(const void* src, void* dst, size_t bytes, int grid, void* stream) {
+  return (int)ams::stream_copy(src, dst, bytes, grid, (hipStream_t)stream);
+}
+
+int ams_probe_stream_read(const void* src, size_t bytes, float* out, int grid, void* stream) {
+  return (int)ams::stream_read(src, bytes, out, grid, (hipStream_t)stream);
+}
+
+int ams_probe_mfma_loop(int shape, float x, int iters, float* out, int grid, void* stream) {
+  return (int)ams::mfma_loop(shape, x, iters, out, grid, (hipStream_t)stream);
+}
+
+double ams_probe_mfma_loop_flops(int iters, int grid) { return ams::mfma_loop_flops(iters, grid); }
+
 }  // extern "C"

@@ -598,3 +598,33 @@ def test_gemm_wide(probe, M, N, K, splits, pair):
     ref = (_silu(gg) * up).T
     got = a.float().cpu().numpy().astype(np.float64) + alo.float().cpu().numpy()
     assert float(np.max(np.abs(got - ref))) <= max(tol, 4e-6 * float(np.max(np.abs(ref))))
+
+
+def test_peak_kernels(probe):
+    """The measured-peak kernels compute what they claim: the stream copy reproduces its
+    source, the stream read's per-thread sums add up to the source's sum, and each lane of the
+    MFMA loop ends with 1024 x^2 iters (8 chains x 4 elements x 32 products of x * x per MFMA);
+    sizes that are not whole 16-byte vectors are refused."""
+    import torch
+    log("peak kernels")
+    n = (64 << 20) // 4
+    src = torch.from_numpy(W.random_gaussian((n,), 95, dtype="f32")).cuda()
+    dst = torch.zeros_like(src)
+    assert probe.ams_probe_stream_copy(_ptr(src), _ptr(dst), C.c_size_t(4 * n), 1024, _stream()) == 0
+    ones = torch.ones(n, dtype=torch.float32, device="cuda")
+    out = torch.full((1024 * 256,), float("nan"), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_stream_read(_ptr(ones), C.c_size_t(4 * n), _ptr(out), 1024, _stream()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    assert float(out.double().sum()) == float(n)
+    for shape in (0, 1):
+        for x, iters in ((1.0, 1000), (0.5, 333)):
+            m = torch.full((16 * 256,), float("nan"), dtype=torch.float32, device="cuda")
+            assert probe.ams_probe_mfma_loop(shape, C.c_float(x), iters, _ptr(m), 16, _stream()) == 0
+            torch.cuda.synchronize()
+            assert bool((m == 1024.0 * x * x * iters).all()), (shape, x, iters)
+    assert probe.ams_probe_mfma_loop(2, C.c_float(1.0), 10, _ptr(m), 16, _stream()) != 0
+    probe.ams_probe_mfma_loop_flops.restype = C.c_double
+    assert probe.ams_probe_mfma_loop_flops(1000, 16) == 16 * 4 * 1000 * 8 * 16 * 16 * 32 * 2
+    assert probe.ams_probe_stream_copy(_ptr(src), _ptr(dst), C.c_size_t(4 * n - 4), 1024, _stream()) != 0
+    assert probe.ams_probe_stream_read(_ptr(ones), C.c_size_t(12), _ptr(out), 1024, _stream()) != 0
