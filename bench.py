@@ -291,7 +291,7 @@ def main():
     ap.add_argument("--workload", default="mid-b8")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=6)
+    ap.add_argument("--cpu-sample-steps", type=int, default=100)
     ap.add_argument("--recompute", action="store_true",
                     help="invalidate + rebuild the prefix before every step (the no-reuse comparison)")
     ap.add_argument("--roofline-only", action="store_true",
