@@ -636,6 +636,12 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   const int n0 = blockIdx.x * WIDE_ROWS + wave * 16;
   const int nch = K >> 7, S = gridDim.y, sp = blockIdx.y;
   const int s0 = sp * nch / S, s1 = (sp + 1) * nch / S, n = s1 - s0;
+  // the split's chunks in rotated order, by tile index / 8: the workgroups an XCD
+  // runs at once (ids equal mod 8) start at different columns of their rows.
+  // Measured on the 7B shapes: 1-5% faster at 16 rows (down 20.7 -> 19.6 us),
+  // 0-1.5% at 64; rotating by the tile index itself was slower for gate|up.
+  const int rot = n > 0 ? (int)((blockIdx.x >> 3) % (unsigned)n) : 0;
+  auto chunk = [&](int t) { const int u = t + rot; return s0 + (u >= n ? u - n : u); };
 
   const f16* wrow = W + (size_t)(n0 + r) * K + g * 8;
   uint4 wr[WIDE_WP][4];
@@ -672,10 +678,10 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
 
 #pragma unroll
   for (int p = 0; p < WIDE_WP; ++p)
-    if (p < n) wide_wload(wr[p], wrow, s0 + p);
-  AMS_WIDE_XLOAD(s0);
+    if (p < n) wide_wload(wr[p], wrow, chunk(p));
+  AMS_WIDE_XLOAD(chunk(0));
   AMS_WIDE_XSTORE(0);
-  if (n > 1) AMS_WIDE_XLOAD(s0 + 1);
+  if (n > 1) AMS_WIDE_XLOAD(chunk(1));
   __syncthreads();
 
   for (int tb = 0; tb < n; tb += WIDE_WP) {
@@ -700,8 +706,8 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
         // vmcnt retires in issue order, so staging chunk t+2 next round then
         // waits only for loads older than the newest weight chunk
         if (t + 1 < n) AMS_WIDE_XSTORE((t + 1) & 1);
-        if (t + 2 < n) AMS_WIDE_XLOAD(s0 + t + 2);
-        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, s0 + t + WIDE_WP);
+        if (t + 2 < n) AMS_WIDE_XLOAD(chunk(t + 2));
+        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, chunk(t + WIDE_WP));
         __syncthreads();
       }
     }
