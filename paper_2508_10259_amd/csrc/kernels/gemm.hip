@@ -615,7 +615,11 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 // LDS rows of 128 + 16 halves (288 bytes): the MFMA B-fragment reads (lane r
 // reads row r, lanes 16 apart the next 16 bytes) are free of bank conflicts at
 // that pitch; at 272 bytes every ds_read_b128 took 8 LDS cycles instead of 4.
-constexpr int WIDE_ROWS = 128, WIDE_WP = 4, WIDE_LDK = 128 + 16;
+// Three weight chunks in flight per wave: at 16 rows that fits 80 VGPRs, three
+// workgroups per CU, and on the 7B shapes it beat four chunks by 1-5% (QKV at
+// 16 rows 23.4 -> 22.1 us, O at 64 rows 15.1 -> 14.4 us; only O at 16 rows lost,
+// 9.6 -> 9.9 us); six or eight chunks cost occupancy and were slower.
+constexpr int WIDE_ROWS = 128, WIDE_WP = 3, WIDE_LDK = 128 + 16;
 
 // weight fragments of one chunk of a wave's 16 rows
 __device__ __forceinline__ void wide_wload(uint4 (&w)[4], const f16* wrow, int c) {
