@@ -184,6 +184,19 @@ def pin_bin_embedding_row(D):
         _close(D.bin_embedding(p, b), p.get("embed")[14 + b], 0.0, f"bin {b}")
 
 
+def pin_embed_ids_rows(D):
+    """Instruction ids look up rows of the embedding table directly: id i gives row i,
+    including the first id, the last non-bin id and the last id; no ids give [0, d]."""
+    p = tiny_params(D, key=1, V=20, n_bins=6)
+    table = p.get("embed")
+    ids = [0, 13, 7, 0, 19, 1]  # 13 = V - n_bins - 1, 19 = V - 1
+    out = D.embed_ids(p, ids)
+    assert out.shape == (len(ids), 8)
+    for r, i in enumerate(ids):
+        _close(out[r], table[i], 0.0, f"embed id {i}")
+    assert D.embed_ids(p, []).shape == (0, 8)
+
+
 # ----------------------------------------------------------------------------
 # whole-decoder special cases
 
@@ -356,6 +369,34 @@ def pin_cached_equals_full(D):
             _close(ctx.kv[b][l][1], kv_full[l][1], 1e-12, f"V row {b} layer {l}")
     forced = [np.array([[1, 2, 3], [0, 0, 0], [5, 4, 3]])]
     _ctx_vs_full(D, p, prefixes, [None], n_actions=4, forced=forced)
+
+
+def pin_forced_decoding(D):
+    """Teacher forcing: the logits of action j are those of a plain forward pass over the
+    committed sequence followed by the embeddings (table rows V - n_bins + f) of the forced
+    bins f_0..f_{j-1}, in both the full-recomputation and the cached path; the reported
+    tokens stay the argmax of those logits."""
+    p = tiny_params(D, key=10, V=20, n_bins=6)
+    table = p.get("embed")
+    seq = _rand((5, 8), 70)
+    forced = [4, 1, 5]
+    direct = []
+    for j in range(4):
+        x = np.concatenate([seq] + [table[14 + f][None] for f in forced[:j]], axis=0)
+        h, _ = D.forward(p, x)
+        direct.append(D.bin_logits(p, h[-1]))
+    direct = np.stack(direct)
+    t_full, z_full = D.full_decode(p, seq, 4, forced)
+    _close(z_full, direct, 1e-12, "forced full_decode")
+    assert list(t_full) == [int(np.argmax(z)) for z in direct]
+    ctx = D.ActionContext(p, 1)
+    ctx.build([seq])
+    t_c, z_c = ctx.step(None, 4, np.array([forced]))
+    _close(z_c[0], direct, 1e-12, "forced cached step")
+    assert list(t_c[0]) == list(t_full)
+    # the forced bins differ from the free-running choices, so forcing is observable
+    t_free, _ = D.full_decode(p, seq, 4)
+    assert list(t_free[:3]) != forced
 
 
 def pin_rows_independent(D):

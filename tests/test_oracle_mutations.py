@@ -144,6 +144,22 @@ def _keep_actions(m):
     m.ActionContext.step = step
 
 
+def _text_id_offset(m):
+    m.embed_ids = lambda p, ids: np.stack([p.layer("embed", (int(i) + p.cfg.n_bins) % p.cfg.vocab) for i in ids]) \
+        if len(ids) else np.zeros((0, p.cfg.d_model))
+
+
+def _text_id_off_by_one(m):
+    m.embed_ids = lambda p, ids: np.stack([p.layer("embed", (int(i) + 1) % p.cfg.vocab) for i in ids]) \
+        if len(ids) else np.zeros((0, p.cfg.d_model))
+
+
+def _forced_ignored(m):
+    full, step = m.full_decode, m.ActionContext.step
+    m.full_decode = lambda p, seq, n_actions, forced=None: full(p, seq, n_actions, None)
+    m.ActionContext.step = lambda self, new, n_actions, forced=None: step(self, new, n_actions, None)
+
+
 MUTATIONS = {
     "rope_sign": _rope_sign, "rope_interleaved": _rope_interleaved, "rope_freq": _rope_freq,
     "rms_no_eps": _rms_no_eps, "rms_eps_outside": _rms_eps_outside, "rms_no_gain": _rms_no_gain,
@@ -158,6 +174,8 @@ MUTATIONS = {
     "gate_up_swap": lambda m: _layer_variant(m, "gate_up_swap"),
     "positions_restart": _positions_restart, "bin_id": _bin_id, "argmax_last": _argmax_last,
     "no_commit": _no_commit, "keep_actions": _keep_actions,
+    "text_id_offset": _text_id_offset, "text_id_off_by_one": _text_id_off_by_one,
+    "forced_ignored": _forced_ignored,
 }
 
 

@@ -34,3 +34,20 @@ def test_cached_equals_full_tiny_workload():
     pre = [W.to_f32(W.make_prefix(wl, 0, 0, 0).patches, "f32")]
     obs = [[W.to_f32(W.make_observation(wl.spec, 0, s, 0, 1), "f32")] for s in range(2)]
     _ctx_vs_full(D, p, pre, [None] + obs, n_actions=7)
+
+
+def test_prefix_bridge_text_rows():
+    """The tests' prefix conversion feeds the reference the decoded patch rows followed by
+    exactly the table rows of the instruction ids (the rows the GPU gathers on the device)."""
+    from paper_2508_10259_amd import workload as W
+    from ref_bridge import oracle_params, prefix_f64
+    spec = W.ModelSpec("pin", 1, 128, 2, 64, 128, 300, 256, "bf16")
+    w = W.make_weights(spec, seed=2)
+    p = oracle_params(w)
+    patches = W.random_gaussian((3, 128), 2, 5, dtype="bf16")
+    ids = np.array([0, 43, 1, 17], np.int32)  # 43 = vocab - n_bins - 1
+    x = prefix_f64(p, spec, W.Prefix(patches, ids))
+    table = W.bf16_bits_to_f32(w.embed).astype(np.float64)
+    assert x.shape == (7, 128)
+    assert np.array_equal(x[:3], W.bf16_bits_to_f32(patches).astype(np.float64))
+    assert np.array_equal(x[3:], table[ids])
