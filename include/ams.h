@@ -21,8 +21,9 @@
  *     `stream` is a hipStream_t (NULL = the legacy default stream).
  *   - The caller owns every device buffer: weights, workspaces, inputs and
  *     outputs.  They must outlive the handles that use them.  The library
- *     allocates no device memory; it owns host-side handles, metadata and
- *     captured HIP graphs only.
+ *     allocates no device memory; it owns host-side handles, metadata,
+ *     captured HIP graphs and one pinned host word per context through which
+ *     a kernel reports a failure to the next call.
  *   - Calls are asynchronous: they return after enqueueing on `stream`;
  *     outputs are valid once the caller synchronises that stream.
  *   - Every argument, state and capacity check happens before anything is
@@ -149,7 +150,11 @@ ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t
                           void* ws, size_t ws_bytes, ams_ctx** out);
 void ams_ctx_destroy(ams_ctx* c); /* NULL is a no-op */
 
-/* Builds the context from each row's prefix: `prefix` is a device array
+/* Paper section 3.2.1 (Constructing the Action Context): the intermediate
+ * state of an inference -- here every layer's K/V of the step-invariant prefix
+ * -- is computed once and kept in the context pool for later inferences.
+ *
+ * Builds the context from each row's prefix: `prefix` is a device array
  * [sum_b lens[b]][d] in the model dtype, rows packed one after another
  * (row b's tokens at positions 0..lens[b]-1); `lens` is a host array [batch]
  * with 1 <= lens[b] <= capacity.  Computes and keeps every layer's K/V
@@ -158,7 +163,11 @@ void ams_ctx_destroy(ams_ctx* c); /* NULL is a no-op */
  * Errors: AMS_EINVAL, AMS_ECAPACITY, AMS_EHIP. */
 ams_status ams_ctx_build(ams_ctx* c, const void* prefix, const int32_t* lens, void* stream);
 
-/* One action step.
+/* Paper section 3.2.1: a later inference reuses the cached state instead of
+ * recomputing it, and after the inference the unseen K/V (here the new
+ * observation tokens') is added to the context.
+ *
+ * One action step.
  *   new_tokens: device [sum_b new_lens[b]][d] (model dtype) or NULL;
  *   new_lens:   host [batch] (0 allowed per row) or NULL for no new tokens.
  * The new tokens are appended to the rows' contexts first (their K/V kept:
@@ -181,7 +190,11 @@ ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_l
                         int32_t n_actions, int32_t* out_tokens, float* out_logits,
                         const int32_t* forced, void* stream);
 
-/* Discards the context (host-side only; enqueues nothing).  State -> INVALID;
+/* Paper section 3.3 (Handler, common part): on an exception the current
+ * slice is discarded and the next inference starts from freshly collected
+ * environment data -- the caller then rebuilds from the new prefix.
+ *
+ * Discards the context (host-side only; enqueues nothing).  State -> INVALID;
  * lengths read 0 until the next build. */
 ams_status ams_ctx_invalidate(ams_ctx* c);
 
@@ -196,9 +209,12 @@ int32_t ams_ctx_state(const ams_ctx* c);
  * sequence of per-layer kernels; negative status on error.  The persistent
  * launch serves bf16 models with up to 8 rows (environment AMS_FUSED=0 at
  * context creation turns it off); it keeps one workgroup per compute unit
- * resident and synchronises them between the layers' phases.  Should the
- * device not keep them all resident, its bounded waits give up and every
- * out_tokens entry of that step reads -1 (never a valid bin). */
+ * resident and synchronises them between the layers' phases, so it assumes
+ * no other work holds the compute units meanwhile.  Should the device not keep
+ * them all resident, its bounded waits give up, every out_tokens entry of that
+ * step reads -1 (never a valid bin), and the next ams_ctx_step on the context
+ * returns AMS_EHIP with the context INVALID (ams_ctx_state reads INVALID as
+ * soon as the failed launch has ended; ams_ctx_build recovers). */
 int32_t ams_ctx_persistent_decode(const ams_ctx* c);
 
 #ifdef __cplusplus

@@ -237,6 +237,9 @@ ams_status ams_ctx_build(ams_ctx* c, const void* prefix, const int32_t* lens, vo
   if (!c) return fail(AMS_EINVAL, "context is NULL");
   ams::Ctx& x = c->c;
   std::string e;
+  // a rebuild replaces whatever an earlier failed decode left behind
+  (void)ams::ctx_absorb_status(x, e);
+  e.clear();
   if (int s = x.book.check_build(lens, e)) return fail(s, e);
   size_t tot = 0;
   for (int b = 0; b < x.lay.batch; ++b) tot += (size_t)lens[b];
@@ -258,6 +261,7 @@ ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_l
   if (!c) return fail(AMS_EINVAL, "context is NULL");
   ams::Ctx& x = c->c;
   std::string e;
+  if (int s = ams::ctx_absorb_status(x, e)) return fail(s, e);
   if (int s = x.book.check_step(new_lens, n_actions, e)) return fail(s, e);
   const ams::Cfg& m = x.model->cfg;
   const int B = x.lay.batch, dev = x.model->device;
@@ -302,6 +306,8 @@ ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens) {
 
 int32_t ams_ctx_state(const ams_ctx* c) {
   if (!c) return AMS_EINVAL;
+  // an asynchronously reported decode failure makes the context INVALID
+  if (c->c.status_host && *c->c.status_host) return ams::INVALID;
   return c->c.book.state;
 }
 

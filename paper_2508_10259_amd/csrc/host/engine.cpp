@@ -87,6 +87,11 @@ hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::s
 hipError_t ctx_init(Ctx& c, std::string& err) {
   const Cfg& m = c.model->cfg;
   TRY(hipStreamCreateWithFlags(&c.capture_stream, hipStreamNonBlocking));
+  void* st = nullptr;
+  TRY(hipHostMalloc(&st, 256, hipHostMallocMapped));
+  c.status_host = (volatile unsigned*)st;
+  *c.status_host = 0u;
+  TRY(hipHostGetDevicePointer((void**)&c.status_dev, st, 0));
   hipStream_t s = c.capture_stream;
   TRY(rope_table(c.rope(), c.lay.capacity, m.head_dim, m.rope_theta, s));
   TRY(hipMemsetAsync(c.ws + c.lay.h_last, 0, c.lay.part - c.lay.h_last, s));
@@ -110,6 +115,16 @@ void ctx_release(Ctx& c) {
   c.graph_lru.clear();
   if (c.capture_stream) hipStreamDestroy(c.capture_stream);
   c.capture_stream = nullptr;
+  if (c.status_host) hipHostFree((void*)c.status_host);
+  c.status_host = nullptr;
+  c.status_dev = nullptr;
+}
+
+int ctx_absorb_status(Ctx& c, std::string& err) {
+  if (!c.status_host) return S_OK;
+  const unsigned w = *c.status_host;
+  if (w) *c.status_host = 0u;
+  return c.book.absorb_async_error(w, err);
 }
 
 // h += x W^T over the M tokens of a token pass (K inputs per token).  At
@@ -361,6 +376,7 @@ static hipError_t enqueue_fused(Ctx& c, int A, int32_t* tok, float* logits, cons
   f.hl = c.h_last16(); f.hl_lo = c.h_last16lo();
   f.qkv = c.qkv(); f.op = c.ws + c.lay.fx_op; f.ap = c.ws + c.lay.fx_ap;
   f.logits = c.logits(); f.part = (float*)(c.ws + c.lay.fx_part); f.sync = (unsigned*)(c.ws + c.lay.fx_sync);
+  f.status = c.status_dev;
   f.out_tok = tok; f.out_logits = logits; f.forced = forced;
   TRY(decode_fused(f, c.fused_grid, s));
   return hipSuccess;

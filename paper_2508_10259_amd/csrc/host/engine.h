@@ -56,6 +56,10 @@ struct Ctx {
   int fused_grid = 0;  // workgroups of the persistent decode, 0 when it does not apply
   int split_o = 1, split_d = 1, split_a = 1;
   hipStream_t capture_stream = nullptr;
+  // pinned host word the persistent decode sets when a barrier wait gives up
+  // (host view, device view); read by the next call on the context
+  volatile unsigned* status_host = nullptr;
+  unsigned* status_dev = nullptr;
   std::map<GraphKey, hipGraphExec_t> graphs;
   std::vector<GraphKey> graph_lru;
   std::vector<int32_t> meta_host;  // staging of one call's pass metadata (kept until the next call)
@@ -90,5 +94,8 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
 hipError_t ctx_decode(Ctx& c, int n_actions, int32_t* out_tokens, float* out_logits, const int32_t* forced,
                       hipStream_t s, std::string& err);
 void ctx_release(Ctx& c);
+// Takes in an error a kernel of an earlier call reported asynchronously (see
+// RowBook::absorb_async_error) and clears the word.
+int ctx_absorb_status(Ctx& c, std::string& err);
 
 }  // namespace ams

@@ -308,6 +308,18 @@ struct RowBook {
     std::fill(len.begin(), len.end(), 0);
     state = INVALID;
   }
+
+  // An error that a kernel reported asynchronously (the persistent decode's
+  // status word: nonzero once a barrier wait gave up) is taken in by the next
+  // call on the context: the context becomes INVALID and the call fails with
+  // S_EHIP.  A zero word changes nothing.
+  int absorb_async_error(unsigned word, std::string& err) {
+    if (word == 0) return S_OK;
+    invalidate();
+    err = "an earlier action decode gave up waiting for its workgroups (not all resident at once); "
+          "its tokens read -1 and the context was invalidated";
+    return S_EHIP;
+  }
 };
 
 // ---------------------------------------------------------------------------

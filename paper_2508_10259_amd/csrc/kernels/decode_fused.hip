@@ -321,6 +321,7 @@ struct FusedArgs {
   float* logits;         // [M][nbp]
   float* part;           // split-K partial sums [unit][8][16]
   unsigned* sync;
+  unsigned* status;      // host-visible word: set to 1 when a barrier wait gives up (or NULL)
   int32_t* out_tok;      // [M][A]
   float* out_logits;     // [M][A][n_bins] or NULL
   const int32_t* forced; // [M][A] or NULL
@@ -753,19 +754,11 @@ __global__ __launch_bounds__(512) void k_decode_fused(FusedArgs a) {
   const Rsrc qkvr = rsrc(a.qkv, (uint32_t)(M * 3 * d * 4));
   const Rsrc logr = rsrc(a.logits, (uint32_t)(M * a.nbp * 4));
   const uint32_t hlo = (uint32_t)(M * d * 2), olo = hlo, alo = (uint32_t)(M * a.F * 2);
-  // a barrier that timed out: the step's tokens all read -1 (workgroup 0 owns them)
-  auto fail = [&]() {
-    if (blockIdx.x == 0)
-      for (int i = threadIdx.x; i < M * a.A; i += blockDim.x) a.out_tok[i] = -1;
-  };
 #define AMS_SYNC(PREFETCH)                        \
   do {                                            \
     arrive(a.sync, ++gen);                        \
     PREFETCH;                                     \
-    if (!wait_all(a.sync, gen, sm)) {             \
-      fail();                                     \
-      return;                                     \
-    }                                             \
+    if (!wait_all(a.sync, gen, sm)) goto failed;  \
   } while (0)
 
   prefetch_store(a.whead, a.nbp, d, pf);
@@ -796,6 +789,13 @@ __global__ __launch_bounds__(512) void k_decode_fused(FusedArgs a) {
   AMS_SYNC((void)0);
 #undef AMS_SYNC
   if (blockIdx.x == 0) phase_feed(a, a.A - 1, false, sm);
+  return;
+failed:
+  // a barrier that timed out: the step's tokens all read -1 (workgroup 0 owns them)
+  // and the host-visible status word reports it to the next call on the context
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < M * a.A; i += blockDim.x) a.out_tok[i] = -1;
+  if (threadIdx.x == 0 && a.status) __hip_atomic_store(a.status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 __global__ void k_fused_reset(unsigned* sync, int words) {
@@ -834,7 +834,7 @@ hipError_t decode_fused(const FusedDecode& f, int grid, hipStream_t s) {
   a.h = f.h; a.hp = (f16*)f.hp;
   a.hl = (const f16*)f.hl; a.hl_lo = (uint32_t)((const char*)f.hl_lo - (const char*)f.hl);
   a.qkv = f.qkv; a.op = (f16*)f.op; a.ap = (f16*)f.ap;
-  a.logits = f.logits; a.part = f.part; a.sync = f.sync;
+  a.logits = f.logits; a.part = f.part; a.sync = f.sync; a.status = f.status;
   a.out_tok = f.out_tok; a.out_logits = f.out_logits; a.forced = f.forced;
   const int words = fused_sync_words(f.d, f.H);
   hipLaunchKernelGGL(k_fused_reset, dim3((words + 255) / 256), dim3(256), 0, s, f.sync, words);

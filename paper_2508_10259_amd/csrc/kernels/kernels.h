@@ -178,6 +178,7 @@ struct FusedDecode {
   void *op, *ap;
   float *logits, *part;
   unsigned* sync;
+  unsigned* status;  // device view of a host-visible word, set to 1 when a barrier wait gives up (or NULL)
   int32_t* out_tok;
   float* out_logits;
   const int32_t* forced;

@@ -49,6 +49,24 @@ static void test_book() {
   EXPECT(b.state == READY && b.len[2] == 100);
 }
 
+// The persistent decode reports a barrier wait that gave up through a status
+// word; the next call on the context maps it to S_EHIP and an INVALID context.
+static void test_async_error() {
+  RowBook b;
+  b.init(2, 64);
+  std::string e;
+  int32_t lens[2] = {10, 20};
+  b.commit_build(lens);
+  EXPECT(b.absorb_async_error(0u, e) == S_OK);  // clean word: nothing changes
+  EXPECT(b.state == READY && b.len[1] == 20);
+  EXPECT(b.absorb_async_error(1u, e) == S_EHIP);
+  EXPECT(b.state == INVALID && b.len[0] == 0 && b.len[1] == 0);
+  EXPECT(!e.empty());
+  EXPECT(b.check_step(nullptr, 1, e) == S_ESTATE);  // stepping now needs a rebuild
+  b.commit_build(lens);
+  EXPECT(b.state == READY && b.check_step(nullptr, 1, e) == S_OK);
+}
+
 static void test_plan() {
   // rows 0..5 with ragged counts, one empty; pass budget 100
   int32_t counts[6] = {40, 0, 70, 30, 100, 1};
@@ -122,6 +140,7 @@ static void test_layout() {
 
 int main() {
   test_book();
+  test_async_error();
   test_plan();
   test_layout();
   if (failures) {
