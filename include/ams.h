@@ -44,10 +44,12 @@
  *     stream, norm statistics, softmax and logits are fp32.
  *   A weight matrix maps an input vector x to W x and is stored [out][in].
  *
- * Context state machine
+ * Context state machine (each row has its own state; the context is READY
+ * when every row is, EMPTY while no row has been built, INVALID otherwise)
  *   create -> EMPTY;  build: EMPTY|READY|INVALID -> READY;
- *   step: READY -> READY (EMPTY or INVALID: AMS_ESTATE);
- *   invalidate: any -> INVALID.
+ *   step, append: READY -> READY (EMPTY or INVALID: AMS_ESTATE);
+ *   invalidate: any -> INVALID;  invalidate_rows: the listed rows -> INVALID;
+ *   build_rows: the listed rows -> READY.
  */
 #ifndef AMS_H
 #define AMS_H
@@ -197,6 +199,38 @@ ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_l
  * Discards the context (host-side only; enqueues nothing).  State -> INVALID;
  * lengths read 0 until the next build. */
 ams_status ams_ctx_invalidate(ams_ctx* c);
+
+/* Paper section 3.3 (Handler, common part) applied to one robot of a batch:
+ * the exception handler discards that episode's slice and re-infers from
+ * freshly collected environment data while the other episodes' contexts stay
+ * as they are (section 4 keeps this control on the CPU).
+ *
+ * Rebuilds only the listed rows: `rows` is a host array of n_rows strictly
+ * increasing row indices, `prefix` a device array [sum_i lens[i]][d] of their
+ * new prefixes packed in that order, `lens` a host array [n_rows] with
+ * 1 <= lens[i] <= capacity.  The listed rows' K/V, last hidden state and
+ * length are replaced; every other row is untouched.  Rows may be READY,
+ * INVALID or EMPTY; the context is READY once every row is.
+ * Errors: AMS_EINVAL, AMS_ECAPACITY, AMS_EHIP. */
+ams_status ams_ctx_build_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, const void* prefix,
+                              const int32_t* lens, void* stream);
+
+/* Paper section 3.3 (Handler, common part), one robot of a batch: discards
+ * the listed rows' contexts (host-side only; enqueues nothing).  `rows` as for
+ * ams_ctx_build_rows.  Those rows read length 0 and the context is INVALID
+ * (no ams_ctx_step) until each of them is rebuilt with ams_ctx_build_rows;
+ * the other rows keep their contexts.  Errors: AMS_EINVAL. */
+ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows);
+
+/* Paper section 3.2.1 (the post-inference insert on its own): appends new
+ * observation tokens to the rows' contexts (their K/V kept, lengths grow by
+ * new_lens) without decoding actions -- the first half of ams_ctx_step.
+ *   new_tokens: device [sum_b new_lens[b]][d] (model dtype);
+ *   new_lens:   host [batch], 0 allowed per row.
+ * Requires READY (else AMS_ESTATE) and len[b] + new_lens[b] <= capacity for
+ * every row (else AMS_ECAPACITY).  Errors: AMS_EINVAL, AMS_ESTATE,
+ * AMS_ECAPACITY, AMS_EHIP. */
+ams_status ams_ctx_append(ams_ctx* c, const void* new_tokens, const int32_t* new_lens, void* stream);
 
 /* Committed length of every row into host array lens[batch]. */
 ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens);

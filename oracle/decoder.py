@@ -287,6 +287,13 @@ class ActionContext:
     from the kept last hidden state; each later bin costs one forward pass of
     a single fed-back token against the cache.  Fed-back tokens are not kept.
     ``invalidate`` discards everything; stepping an invalid context is an error.
+
+    The exception handler's common part (paper section 3.3, "Handler")
+    discards a slice and re-infers from fresh environment data; for one robot
+    of a batch that is ``invalidate_rows`` followed by ``build_rows``, which
+    leave the other rows' contexts as they are.  Every row must hold a context
+    before the batch steps.  ``append`` is the post-inference insert of new
+    observation tokens alone (section 3.2.1), without decoding.
     """
 
     def __init__(self, p: Params, batch: int):
@@ -295,22 +302,44 @@ class ActionContext:
         self.kv: List[Optional[list]] = [None] * batch
         self.h_last: List[Optional[np.ndarray]] = [None] * batch
         self.lens = np.zeros(batch, dtype=np.int64)
-        self.valid = False
+        self.row_valid = np.zeros(batch, dtype=bool)
+
+    @property
+    def valid(self) -> bool:
+        return bool(np.all(self.row_valid))
+
+    def _build_row(self, b: int, x: np.ndarray) -> None:
+        x = np.asarray(x, dtype=F64)
+        assert x.shape[0] > 0
+        h, kv = forward(self.p, x)
+        self.kv[b], self.h_last[b], self.lens[b] = kv, h[-1].copy(), x.shape[0]
+        self.row_valid[b] = True
 
     def build(self, prefixes: Sequence[np.ndarray]) -> None:
         assert len(prefixes) == self.batch
         for b, x in enumerate(prefixes):
-            x = np.asarray(x, dtype=F64)
-            assert x.shape[0] > 0
-            h, kv = forward(self.p, x)
-            self.kv[b], self.h_last[b], self.lens[b] = kv, h[-1].copy(), x.shape[0]
-        self.valid = True
+            self._build_row(b, x)
+
+    def build_rows(self, rows: Sequence[int], prefixes: Sequence[np.ndarray]) -> None:
+        assert len(rows) == len(prefixes)
+        for b, x in zip(rows, prefixes):
+            self._build_row(int(b), x)
 
     def invalidate(self) -> None:
-        self.kv = [None] * self.batch
-        self.h_last = [None] * self.batch
-        self.lens[:] = 0
-        self.valid = False
+        self.invalidate_rows(range(self.batch))
+
+    def invalidate_rows(self, rows: Sequence[int]) -> None:
+        for b in rows:
+            b = int(b)
+            self.kv[b], self.h_last[b], self.lens[b] = None, None, 0
+            self.row_valid[b] = False
+
+    def append(self, new: Sequence[Optional[np.ndarray]]) -> None:
+        if not self.valid:
+            raise RuntimeError("append on an invalid action context")
+        for b in range(self.batch):
+            if new[b] is not None and len(new[b]):
+                self._extend(b, np.asarray(new[b], dtype=F64))
 
     def _extend(self, b: int, x: np.ndarray) -> None:
         h, kv = forward(self.p, x, start=int(self.lens[b]), past=self.kv[b])

@@ -45,6 +45,10 @@ SIGNATURES = {
     "ams_ctx_step": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p]),
     "ams_ctx_invalidate": (C.c_int32, [C.c_void_p]),
+    "ams_ctx_build_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
+                                       C.POINTER(C.c_int32), C.c_void_p]),
+    "ams_ctx_invalidate_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32]),
+    "ams_ctx_append": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_void_p]),
     "ams_ctx_lengths": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32)]),
     "ams_ctx_state": (C.c_int32, [C.c_void_p]),
     "ams_ctx_persistent_decode": (C.c_int32, [C.c_void_p]),

@@ -290,6 +290,60 @@ ams_status ams_ctx_step(ams_ctx* c, const void* new_tokens, const int32_t* new_l
   return AMS_OK;
 }
 
+ams_status ams_ctx_build_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, const void* prefix,
+                              const int32_t* lens, void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = ams::ctx_absorb_status(x, e)) return fail(s, e);
+  if (int s = x.book.check_build_rows(rows, n_rows, lens, e)) return fail(s, e);
+  size_t tot = 0;
+  for (int i = 0; i < n_rows; ++i) tot += (size_t)lens[i];
+  const ams::Cfg& m = x.model->cfg;
+  if (!dev_range(prefix, tot * m.d_model * ams::elem_size(m), x.model->device, "prefix", e))
+    return fail(AMS_EINVAL, e);
+  const int B = x.lay.batch;
+  std::vector<int32_t> counts(B, 0), start(B, 0);
+  for (int i = 0; i < n_rows; ++i) counts[rows[i]] = lens[i];
+  if (ams::ctx_forward_tokens(x, prefix, counts.data(), start.data(), 1, (hipStream_t)stream, e) != hipSuccess) {
+    x.book.invalidate();
+    return fail(AMS_EHIP, e);
+  }
+  x.book.commit_build_rows(rows, n_rows, lens);
+  return AMS_OK;
+}
+
+ams_status ams_ctx_append(ams_ctx* c, const void* new_tokens, const int32_t* new_lens, void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = ams::ctx_absorb_status(x, e)) return fail(s, e);
+  if (int s = x.book.check_append(new_lens, e)) return fail(s, e);
+  const ams::Cfg& m = x.model->cfg;
+  size_t n_new = 0;
+  for (int b = 0; b < x.lay.batch; ++b) n_new += (size_t)new_lens[b];
+  if (n_new == 0) return AMS_OK;
+  if (!dev_range(new_tokens, n_new * m.d_model * ams::elem_size(m), x.model->device, "new_tokens", e))
+    return fail(AMS_EINVAL, e);
+  if (ams::ctx_forward_tokens(x, new_tokens, new_lens, x.book.len.data(), 0, (hipStream_t)stream, e) != hipSuccess) {
+    x.book.invalidate();
+    return fail(AMS_EHIP, e);
+  }
+  x.book.commit_new(new_lens);
+  return AMS_OK;
+}
+
+ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  std::string e;
+  if (int s = c->c.book.check_rows(rows, n_rows, e)) return fail(s, e);
+  c->c.book.invalidate_rows(rows, n_rows);
+  return AMS_OK;
+}
+
 ams_status ams_ctx_invalidate(ams_ctx* c) {
   g_err.clear();
   if (!c) return fail(AMS_EINVAL, "context is NULL");

@@ -261,16 +261,32 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
 
 enum CtxState { EMPTY = 0, READY = 1, INVALID = 2 };
 
+// Each row has its own state (EMPTY until first built, READY, INVALID after a
+// row-level or whole-context invalidate); the context is READY when every row
+// is, EMPTY while no row has been built, INVALID otherwise.  Only a READY
+// context steps: a row that an exception handler invalidated must be rebuilt
+// (alone, with the other rows' contexts untouched) before the batch steps on.
 struct RowBook {
   int batch = 0, capacity = 0;
   int state = EMPTY;
   std::vector<int32_t> len;
+  std::vector<int8_t> row_state;
 
   void init(int b, int cap) {
     batch = b;
     capacity = cap;
     state = EMPTY;
     len.assign(b, 0);
+    row_state.assign(b, (int8_t)EMPTY);
+  }
+
+  void refresh_state() {
+    bool all_ready = true, all_empty = true;
+    for (int b = 0; b < batch; ++b) {
+      all_ready = all_ready && row_state[b] == READY;
+      all_empty = all_empty && row_state[b] == EMPTY;
+    }
+    state = all_ready ? READY : all_empty ? EMPTY : INVALID;
   }
 
   int check_build(const int32_t* lens, std::string& err) const {
@@ -282,8 +298,46 @@ struct RowBook {
     return S_OK;
   }
 
+  // rows: n strictly increasing row indices in [0, batch); lens[i]: new prefix
+  // length of rows[i].
+  int check_rows(const int32_t* rows, int n, std::string& err) const {
+    if (!rows || n < 1 || n > batch) { err = "rows must list 1..batch row indices"; return S_EINVAL; }
+    for (int i = 0; i < n; ++i) {
+      if (rows[i] < 0 || rows[i] >= batch) { err = "row index out of range"; return S_EINVAL; }
+      if (i && rows[i] <= rows[i - 1]) { err = "row indices must be strictly increasing"; return S_EINVAL; }
+    }
+    return S_OK;
+  }
+
+  int check_build_rows(const int32_t* rows, int n, const int32_t* lens, std::string& err) const {
+    if (int s = check_rows(rows, n, err)) return s;
+    if (!lens) { err = "lens is NULL"; return S_EINVAL; }
+    for (int i = 0; i < n; ++i) {
+      if (lens[i] < 1) { err = "prefix length must be >= 1 (row " + std::to_string(rows[i]) + ")"; return S_EINVAL; }
+      if (lens[i] > capacity) {
+        err = "prefix longer than capacity (row " + std::to_string(rows[i]) + ")";
+        return S_ECAPACITY;
+      }
+    }
+    return S_OK;
+  }
+
+  // new tokens only (no action decode): every row READY, len + n <= capacity
+  int check_append(const int32_t* new_lens, std::string& err) const {
+    if (state != READY) { err = state == EMPTY ? "context was never built" : "context (or a row of it) is invalidated"; return S_ESTATE; }
+    if (!new_lens) { err = "new_lens is NULL"; return S_EINVAL; }
+    for (int b = 0; b < batch; ++b) {
+      if (new_lens[b] < 0) { err = "negative new length (row " + std::to_string(b) + ")"; return S_EINVAL; }
+      if ((int64_t)len[b] + new_lens[b] > capacity) {
+        err = "row " + std::to_string(b) + " would exceed capacity";
+        return S_ECAPACITY;
+      }
+    }
+    return S_OK;
+  }
+
   int check_step(const int32_t* new_lens, int n_actions, std::string& err) const {
-    if (state != READY) { err = state == EMPTY ? "context was never built" : "context is invalidated"; return S_ESTATE; }
+    if (state != READY) { err = state == EMPTY ? "context was never built" : "context (or a row of it) is invalidated"; return S_ESTATE; }
     if (n_actions < 1 || n_actions > capacity) { err = "n_actions must be in [1, capacity]"; return S_EINVAL; }
     for (int b = 0; b < batch; ++b) {
       const int64_t n = new_lens ? new_lens[b] : 0;
@@ -297,8 +351,18 @@ struct RowBook {
   }
 
   void commit_build(const int32_t* lens) {
-    for (int b = 0; b < batch; ++b) len[b] = lens[b];
+    for (int b = 0; b < batch; ++b) {
+      len[b] = lens[b];
+      row_state[b] = READY;
+    }
     state = READY;
+  }
+  void commit_build_rows(const int32_t* rows, int n, const int32_t* lens) {
+    for (int i = 0; i < n; ++i) {
+      len[rows[i]] = lens[i];
+      row_state[rows[i]] = READY;
+    }
+    refresh_state();
   }
   void commit_new(const int32_t* new_lens) {
     if (!new_lens) return;
@@ -306,7 +370,15 @@ struct RowBook {
   }
   void invalidate() {
     std::fill(len.begin(), len.end(), 0);
+    std::fill(row_state.begin(), row_state.end(), (int8_t)INVALID);
     state = INVALID;
+  }
+  void invalidate_rows(const int32_t* rows, int n) {
+    for (int i = 0; i < n; ++i) {
+      len[rows[i]] = 0;
+      row_state[rows[i]] = INVALID;
+    }
+    refresh_state();
   }
 
   // An error that a kernel reported asynchronously (the persistent decode's

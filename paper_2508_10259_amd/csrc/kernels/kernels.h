@@ -189,7 +189,8 @@ hipError_t decode_fused(const FusedDecode& f, int grid, hipStream_t s);
 int decode_fused_grid(int device, int dh);
 int fused_sync_words(int d, int H);
 
-// lens[b] += add[b] (device arrays), or lens[b] = add[b] when `set`.
+// lens[b] += add[b] (device arrays), or, when `set`, lens[b] = add[b] for the
+// rows with add[b] > 0 (a row-level rebuild leaves the other rows' lengths).
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
 
 // Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned

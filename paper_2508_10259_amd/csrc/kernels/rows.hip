@@ -187,7 +187,10 @@ hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_
 
 __global__ void k_update_lens(int32_t* lens, const int32_t* add, int B, int set) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < B) lens[b] = set ? add[b] : lens[b] + add[b];
+  if (b < B) {
+    const int32_t a = add[b];
+    lens[b] = set ? (a > 0 ? a : lens[b]) : lens[b] + a;  // set: rows with no tokens keep their length
+  }
 }
 
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s) {

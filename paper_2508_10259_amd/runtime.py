@@ -172,6 +172,21 @@ class DeviceContext:
                    "ams_ctx_step")
         return tokens, logits
 
+    def build_rows(self, rows: Sequence[int], prefix: torch.Tensor, lens: Sequence[int]) -> None:
+        """Rebuild only `rows` (strictly increasing) from their new prefixes, packed in that order."""
+        assert prefix.is_contiguous()
+        capi.check(self.lib.ams_ctx_build_rows(self.handle, capi.int_array(rows), len(rows), prefix.data_ptr(),
+                                               capi.int_array(lens), _stream()), "ams_ctx_build_rows")
+
+    def invalidate_rows(self, rows: Sequence[int]) -> None:
+        capi.check(self.lib.ams_ctx_invalidate_rows(self.handle, capi.int_array(rows), len(rows)),
+                   "ams_ctx_invalidate_rows")
+
+    def append(self, new: torch.Tensor, new_lens: Sequence[int]) -> None:
+        """Commit new observation tokens without decoding actions."""
+        capi.check(self.lib.ams_ctx_append(self.handle, new.data_ptr() if new is not None else None,
+                                           capi.int_array(new_lens), _stream()), "ams_ctx_append")
+
     def invalidate(self) -> None:
         capi.check(self.lib.ams_ctx_invalidate(self.handle), "ams_ctx_invalidate")
 

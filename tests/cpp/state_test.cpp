@@ -67,6 +67,55 @@ static void test_async_error() {
   EXPECT(b.state == READY && b.check_step(nullptr, 1, e) == S_OK);
 }
 
+// Row-level invalidate / rebuild inside a live batch, and append-only commits.
+static void test_rows() {
+  RowBook b;
+  b.init(4, 128);
+  std::string e;
+  int32_t r1[1] = {2}, l1[1] = {50};
+  EXPECT(b.check_build_rows(r1, 1, l1, e) == S_OK);
+  b.commit_build_rows(r1, 1, l1);
+  EXPECT(b.state == INVALID);  // rows 0, 1, 3 never built: not steppable
+  EXPECT(b.check_step(nullptr, 1, e) == S_ESTATE);
+  int32_t r3[3] = {0, 1, 3}, l3[3] = {10, 20, 30};
+  b.commit_build_rows(r3, 3, l3);
+  EXPECT(b.state == READY && b.len[2] == 50 && b.len[3] == 30);
+  int32_t unsorted[2] = {3, 1}, dup[2] = {1, 1}, oob[1] = {4};
+  EXPECT(b.check_rows(unsorted, 2, e) == S_EINVAL);
+  EXPECT(b.check_rows(dup, 2, e) == S_EINVAL);
+  EXPECT(b.check_rows(oob, 1, e) == S_EINVAL);
+  EXPECT(b.check_rows(r1, 0, e) == S_EINVAL);
+  int32_t toolong[1] = {129}, zero[1] = {0};
+  EXPECT(b.check_build_rows(r1, 1, toolong, e) == S_ECAPACITY);
+  EXPECT(b.check_build_rows(r1, 1, zero, e) == S_EINVAL);
+  // one robot's exception: row 1 discarded, the others keep their lengths
+  int32_t one[1] = {1};
+  b.invalidate_rows(one, 1);
+  EXPECT(b.state == INVALID && b.len[1] == 0 && b.len[0] == 10 && b.len[3] == 30);
+  int32_t nl[4] = {1, 1, 1, 1};
+  EXPECT(b.check_append(nl, e) == S_ESTATE);
+  EXPECT(b.check_step(nullptr, 1, e) == S_ESTATE);
+  int32_t l9[1] = {9};
+  b.commit_build_rows(one, 1, l9);
+  EXPECT(b.state == READY && b.len[1] == 9 && b.len[2] == 50);
+  // append: len + n <= capacity exactly (no scratch positions needed)
+  int32_t fit[4] = {118, 0, 78, 98};
+  EXPECT(b.check_append(fit, e) == S_OK);
+  int32_t over[4] = {119, 0, 0, 0};
+  EXPECT(b.check_append(over, e) == S_ECAPACITY);
+  int32_t neg[4] = {0, -1, 0, 0};
+  EXPECT(b.check_append(neg, e) == S_EINVAL);
+  EXPECT(b.check_append(nullptr, e) == S_EINVAL);
+  b.commit_new(fit);
+  EXPECT(b.len[0] == 128 && b.len[1] == 9 && b.len[2] == 128 && b.len[3] == 128);
+  // a whole-context invalidate marks every row; a full build restores all
+  b.invalidate();
+  EXPECT(b.state == INVALID && b.row_state[1] == INVALID);
+  int32_t all[4] = {5, 6, 7, 8};
+  b.commit_build(all);
+  EXPECT(b.state == READY && b.row_state[3] == READY && b.len[3] == 8);
+}
+
 static void test_plan() {
   // rows 0..5 with ragged counts, one empty; pass budget 100
   int32_t counts[6] = {40, 0, 70, 30, 100, 1};
@@ -141,6 +190,7 @@ static void test_layout() {
 int main() {
   test_book();
   test_async_error();
+  test_rows();
   test_plan();
   test_layout();
   if (failures) {

@@ -434,4 +434,41 @@ def pin_lifecycle(D):
     _close(a.step(None, 3)[1], c.step(None, 3)[1], 0.0, "rebuild == fresh")
 
 
+def pin_row_lifecycle(D):
+    """One row of a batch invalidated and rebuilt from a new prefix: that row then equals a fresh
+    context built from the new prefix, the other rows equal a batch that never saw the row
+    operations (bit for bit: rows are independent); while the row is invalid the batch cannot
+    step.  append(N) then step() equals step(N)."""
+    p = tiny_params(D, key=12)
+    P = [_rand((4 + 2 * b, 8), 80, b) for b in range(3)]
+    P1 = _rand((7, 8), 81)
+    N = [_rand((2, 8), 82, b) for b in range(3)]
+    a = D.ActionContext(p, 3); a.build(P)
+    ref = D.ActionContext(p, 3); ref.build(P)
+    a.step(N, 3); ref.step(N, 3)
+    a.invalidate_rows([1])
+    assert list(a.lengths()) == [len(P[0]) + 2, 0, len(P[2]) + 2]
+    try:
+        a.step(None, 3)
+        raise AssertionError("step with an invalidated row must fail")
+    except RuntimeError:
+        pass
+    a.build_rows([1], [P1])
+    ta, za = a.step(None, 3)
+    tr, zr = ref.step(None, 3)
+    for b in (0, 2):
+        assert np.array_equal(ta[b], tr[b]) and np.array_equal(za[b], zr[b]), f"row {b} disturbed"
+    fresh = D.ActionContext(p, 1); fresh.build([P1])
+    tf, zf = fresh.step(None, 3)
+    assert np.array_equal(ta[1], tf[0]) and np.array_equal(za[1], zf[0]), "rebuilt row != fresh build"
+    # append-only commit
+    c = D.ActionContext(p, 3); c.build(P)
+    d_ = D.ActionContext(p, 3); d_.build(P)
+    c.append(N)
+    tc, zc = c.step(None, 3)
+    td, zd = d_.step(N, 3)
+    assert np.array_equal(tc, td) and np.array_equal(zc, zd), "append + step != step with new tokens"
+    assert list(c.lengths()) == list(d_.lengths())
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

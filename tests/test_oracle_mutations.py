@@ -160,6 +160,26 @@ def _forced_ignored(m):
     m.ActionContext.step = lambda self, new, n_actions, forced=None: step(self, new, n_actions, None)
 
 
+def _build_rows_all(m):
+    orig = m.ActionContext.build_rows
+
+    def build_rows(self, rows, prefixes):  # also re-runs every other row on the first new prefix
+        orig(self, range(self.batch), [prefixes[0]] * self.batch)
+        orig(self, rows, prefixes)
+    m.ActionContext.build_rows = build_rows
+
+
+def _invalidate_rows_keeps_length(m):
+    def invalidate_rows(self, rows):
+        for b in rows:
+            self.row_valid[int(b)] = False
+    m.ActionContext.invalidate_rows = invalidate_rows
+
+
+def _append_no_commit(m):
+    m.ActionContext.append = lambda self, new: None
+
+
 MUTATIONS = {
     "rope_sign": _rope_sign, "rope_interleaved": _rope_interleaved, "rope_freq": _rope_freq,
     "rms_no_eps": _rms_no_eps, "rms_eps_outside": _rms_eps_outside, "rms_no_gain": _rms_no_gain,
@@ -175,7 +195,8 @@ MUTATIONS = {
     "positions_restart": _positions_restart, "bin_id": _bin_id, "argmax_last": _argmax_last,
     "no_commit": _no_commit, "keep_actions": _keep_actions,
     "text_id_offset": _text_id_offset, "text_id_off_by_one": _text_id_off_by_one,
-    "forced_ignored": _forced_ignored,
+    "forced_ignored": _forced_ignored, "build_rows_all": _build_rows_all,
+    "invalidate_rows_keeps_length": _invalidate_rows_keeps_length, "append_no_commit": _append_no_commit,
 }
 
 
