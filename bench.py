@@ -1,15 +1,22 @@
 """Cached-context action decoding throughput on one MI355X.
 
-Workload (default): the 12-layer d=1024 decoder (16 heads of 64, FFN 4096,
-256 action bins), 8 episodes, each with a cached prefix of 256 patch
-embeddings + 24 instruction tokens, 7 greedy action tokens per step.  The
-timed region is one episode window: ctx_build of the 8 prefixes followed by
-K ctx_steps (K = 500 by default), inputs resident in HBM beforehand.
-Each step = 7 bin-logit evaluations and 6 decode passes over all layers.
+Workload (default): the 7B Llama-style decoder (32 layers, d=4096, 32 heads of
+128, FFN 11008, vocab 32000 with the last 256 ids as action bins), 64 parallel
+episodes with ragged cached prefixes U{200..400} (patches + 32 instruction
+tokens); per step every row commits 16 fresh observation tokens and decodes 7
+greedy action tokens; every row is invalidated and rebuilt every 20 steps.  The
+timed region is K steps (K = 20 by default) of that window -- one build of the
+64 prefixes, then per step the 1,024-token extension (ams_ctx_append) and the
+action decode (ams_ctx_step) -- with every input resident in HBM beforehand.
 
-Prints one JSON line: action steps/s (rows x steps / s), the roofline of the
-dominant kernel (timed live with HIP events on its own stream), and the fp64
-CPU reference timed on a bounded sample on this host.
+Each phase is timed live with HIP events on the stream the library enqueues on:
+the decode against the HBM roofline (its algorithmic bytes: weights once per
+pass, each row's K/V, the bin head), the extension and the rebuild against the
+fp16 MFMA roofline; the whole step against the sum of the three rooflines.
+Extra keys time the other workloads (7B one row, 7B 56-token action chunks with
+and without reuse, the 12-layer model, and the batch-64 workload with row-level
+rebuilds staggered over the steps), and the fp64 CPU reference is timed on a
+bounded sample on this host.  One JSON line.
 """
 from __future__ import annotations
 
@@ -17,6 +24,7 @@ import argparse
 import ctypes as C
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -53,83 +61,19 @@ def build_flops(spec, lens):
     return 2 * spec.matmul_params * m + 4 * d * L * pairs
 
 
-def gu_launch_bytes(spec, B, es=2):
-    """Decode gate|up projection: weights [2F, d] once, the input rows and the [B, F] gated
-    out, both as fp16 pairs (hi + lo, 4 bytes a value); from 9 to 64 rows the wide kernel
-    leaves the out to its split-K reduction."""
-    w = 2 * spec.d_ffn * spec.d_model * es + B * spec.d_model * 4
-    return w + (B * spec.d_ffn * 4 if B <= 8 or B > 64 else 0)
-
-
-def time_gate_up_kernel(model, B, iters=240):
-    """Average duration of the decode gate|up kernel (RMSNorm + gate|up GEMV + SiLU gate,
-    the largest weight stream of a decode pass) in the decode step's launch shape, timed with
-    HIP events on its own stream.  Each launch reads a different copy of a layer's packed
-    weights out of a buffer of at least 1 GiB, four times the 256 MB memory-side cache, so
-    that every launch streams its weights from HBM as it does inside a decode pass."""
-    import torch
-    from paper_2508_10259_amd.build import PROBE_LIB
-    lib = C.CDLL(PROBE_LIB)
-    spec = model.spec
-    d, F, es = spec.d_model, spec.d_ffn, 2
-    # packed layout of the model workspace: [wqkv | wo | wgu | ...], each region 256-byte aligned
-    align = lambda x: (x + 255) // 256 * 256
-    off_gu = align(3 * d * d * es * spec.n_layers) + align(d * d * es * spec.n_layers)
-    slice_b = 2 * F * d * es
-    n_copy = max(4, -(-(1 << 30) // slice_b))
-    wbuf = torch.empty((n_copy, slice_b), dtype=torch.uint8, device="cuda")
-    for i in range(n_copy):
-        l = i % spec.n_layers
-        wbuf[i].copy_(model.ws[off_gu + l * slice_b: off_gu + (l + 1) * slice_b])
-    # the decode pass's form: inputs and SwiGLU output as fp16 pairs (hi + rounding error)
-    h = torch.randn((B, d), device="cuda") * 30.0
-    hhi = h.half()
-    hlo = (h - hhi.float()).half()
-    u = torch.randn((B, d), device="cuda")
-    uhi = u.half()
-    ulo = (u - uhi.float()).half()
-    a = torch.empty((B, F), device="cuda", dtype=torch.float16)
-    alo = torch.empty((B, F), device="cuda", dtype=torch.float16)
-    # split count of the wide kernel over its 128-row tiles (the library's rule: the smallest
-    # S <= min(16, chunks / 4) within 5% of the minimum of ceil(tiles * S / 256) / S)
-    tiles, smax = max(2 * F // 128, 1), max(1, min(16, d // 128 // 4))
-    model = {s_: -(-tiles * s_ // 256) / s_ for s_ in range(1, smax + 1)}
-    wsplit = min(s_ for s_, t_ in model.items() if t_ <= 1.05 * min(model.values()))
-    part = torch.empty((wsplit, B, 2 * F) if 8 < B <= 64 else (1,), device="cuda", dtype=torch.float32)
-    s = torch.cuda.Stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    def launch(l):
-        w = C.c_void_p(wbuf[l % n_copy].data_ptr())
-        if B <= 8:  # the decode pass fuses the RMSNorm up to 8 rows
-            lib.ams_probe_gemv_rmsnorm(2, 2, C.c_void_p(hhi.data_ptr()), C.c_void_p(hlo.data_ptr()),
-                                       C.c_float(spec.rms_eps), w, B, 2 * F, d, C.c_void_p(a.data_ptr()), F,
-                                       C.c_void_p(None), C.c_void_p(alo.data_ptr()), C.c_void_p(s.cuda_stream))
-        elif B <= 64:  # the wide kernel writes split-K partial sums; the reduction is timed apart
-            lib.ams_probe_gemm_wide(C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
-                                    wsplit, C.c_void_p(part.data_ptr()), C.c_void_p(s.cuda_stream))
-        else:
-            lib.ams_probe_gemm(2, 2, C.c_void_p(uhi.data_ptr()), C.c_void_p(ulo.data_ptr()), w, B, 2 * F, d,
-                               C.c_void_p(a.data_ptr()), F, C.c_void_p(None), C.c_void_p(alo.data_ptr()),
-                               C.c_void_p(s.cuda_stream))
-    torch.cuda.synchronize()
-    iters = max(iters, 2 * n_copy)
-    with torch.cuda.stream(s):
-        for l in range(n_copy):
-            launch(l)
-        ev0.record(s)
-        for l in range(iters):
-            launch(l)
-        ev1.record(s)
-    s.synchronize()
-    del wbuf
-    return ev0.elapsed_time(ev1) / iters * 1e-3  # seconds per launch
+def extension_flops(spec, lens_before, n_new):
+    """Matmul + attention FLOPs of appending n_new[b] tokens to rows of committed lengths
+    lens_before[b]: new token i of row b attends to lens_before[b] + i + 1 keys."""
+    d, L = spec.d_model, spec.n_layers
+    m = sum(int(n) for n in n_new)
+    pairs = sum(int(n) * int(l) + int(n) * (int(n) + 1) // 2 for l, n in zip(lens_before, n_new))
+    return 2 * spec.matmul_params * m + 4 * d * L * pairs
 
 
 def profiled_traffic(workload, kernel):
-    """HBM bytes per launch of the roofline kernel from a committed PMC summary
-    (profiles/*_pmc.txt) of this workload and kernel, or None when there is none or
-    the kernel's source has changed since the counters were taken."""
+    """HBM bytes per launch (per step, for a whole phase) from a committed PMC summary
+    (profiles/*_pmc.txt) of this workload and kernel, or None when there is none or a kernel
+    source it covers has changed since the counters were taken."""
     import glob
     import hashlib
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_pmc.txt"))):
@@ -137,32 +81,15 @@ def profiled_traffic(workload, kernel):
             kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
             if kv.get("workload") != workload or kv.get("kernel") != kernel:
                 continue
-            src = open(os.path.join(ROOT, kv["kernel_source"]), "rb").read()
-            if hashlib.sha256(src).hexdigest() != kv["kernel_source_sha256"]:
-                return None
+            srcs = kv.get("kernel_sources", kv.get("kernel_source", "")).split(",")
+            shas = kv.get("kernel_sources_sha256", kv.get("kernel_source_sha256", "")).split(",")
+            for src, sha in zip(srcs, shas):
+                if hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest() != sha:
+                    return None
             return int(kv["traffic_bytes"])
         except (OSError, KeyError, ValueError):
             continue
     return None
-
-
-def time_persistent_step(ctx, n_actions, iters=40):
-    """Average duration of a decode-only ctx_step when the decode is one persistent
-    launch (that launch plus the small kernel that clears its barrier words), timed
-    with HIP events on torch's current stream, where the step's graph runs."""
-    import torch
-    B, nb = ctx.batch, ctx.model.spec.n_bins
-    tokens = torch.empty((B, n_actions), dtype=torch.int32, device="cuda")
-    logits = torch.empty((B, n_actions, nb), dtype=torch.float32, device="cuda")
-    for _ in range(3):
-        ctx.step(n_actions, tokens=tokens, logits=logits)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    for _ in range(iters):
-        ctx.step(n_actions, tokens=tokens, logits=logits)
-    ev1.record()
-    torch.cuda.synchronize()
-    return ev0.elapsed_time(ev1) / iters * 1e-3
 
 
 def measured_peaks(nbytes=1 << 30, iters=10):
@@ -218,85 +145,253 @@ def copy_calibration(nbytes=256 << 20):
     return nbytes
 
 
-def cpu_baseline(wl, w, seed, sample_steps, window_steps):
-    """fp64 reference on row 0 (same weights `w` as the GPU run): build its prefix, then
-    `sample_steps` steps; row-steps/s with the build amortised over the workload's window."""
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    import oracle.decoder as D
-    from ref_bridge import oracle_params, prefix_f64
-    from paper_2508_10259_amd import workload as W
+def lscpu_model():
+    try:
+        out = subprocess.run(["lscpu"], stdout=subprocess.PIPE, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return "unknown"
+
+
+def blas_info():
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                return {"vendor": i.get("internal_api"), "version": i.get("version"),
+                        "threads": int(i.get("num_threads", 1))}
     except Exception:
-        cores = len(os.sched_getaffinity(0))
-    p = oracle_params(w)
-    x = prefix_f64(p, wl.spec, W.make_prefix(wl, seed, 0, 0))
-    new = [W.to_f32(W.make_observation(wl.spec, seed, 0, 0, wl.new_per_step), wl.spec.dtype).astype(np.float64)] \
-        if wl.new_per_step else None
-    for l in range(wl.spec.n_layers):  # decode every weight once before timing
+        pass
+    return {"vendor": "unknown", "version": None, "threads": len(os.sched_getaffinity(0))}
+
+
+def _oracle_sample(wl, p, seed, n_steps, window_steps, n_layers=None):
+    """fp64 reference on row 0 of `wl` (epoch 0): build of its prefix, then `n_steps` steps with
+    the workload's per-step observation tokens.  With `n_layers` the reference runs the first
+    n_layers layers of the model only and both times are scaled to all layers (the head's and
+    the embedding gather's share is below 0.1%).  Returns (row-steps/s, build s, step s, text)."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import oracle.decoder as D
+    from ref_bridge import prefix_f64
+    from paper_2508_10259_amd import workload as W
+    spec = wl.spec
+    if n_layers is not None:
+        c = p.cfg
+        p = D.Params(D.Config(n_layers, c.d_model, c.n_heads, c.head_dim, c.d_ffn, c.vocab, c.n_bins, c.rms_eps,
+                              c.rope_theta), **p.arrays)
+    L = p.cfg.n_layers
+    for l in range(L):  # decode the sampled layers' weights before timing
         for n in W.MATRICES:
             p.layer(n, l)
+    x = prefix_f64(p, spec, W.make_prefix(wl, seed, 0, 0))
     ctx = D.ActionContext(p, 1)
     t0 = time.perf_counter()
     ctx.build([x])
     t1 = time.perf_counter()
-    for _ in range(sample_steps):
+    for s_ in range(n_steps):
+        new = [W.to_f32(W.make_observation(spec, seed, s_, 0, wl.new_per_step), spec.dtype).astype(np.float64)] \
+            if wl.new_per_step else None
         ctx.step(new, wl.n_actions)
     t2 = time.perf_counter()
-    per_step = (t2 - t1) / sample_steps + (t1 - t0) / window_steps
-    return {"value": 1.0 / per_step, "unit": "action-steps/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"row 0 of {wl.name}: build of its {x.shape[0]}-token prefix ({t1 - t0:.2f} s) + "
-                      f"{sample_steps} steps ({t2 - t1:.2f} s), fp64 NumPy; build amortised over "
-                      f"{window_steps} steps as in the timed GPU window"}
+    scale = spec.n_layers / L
+    t_build, t_step = (t1 - t0) * scale, (t2 - t1) / n_steps * scale
+    per_step = t_step + t_build / window_steps
+    what = (f"row 0 of {wl.name}: build of its {x.shape[0]}-token prefix ({t1 - t0:.2f} s) + {n_steps} step(s) "
+            f"({t2 - t1:.2f} s)" + (f" through the first {L} of {spec.n_layers} layers, both scaled x{scale:g} "
+                                    "to all layers" if n_layers is not None else "") +
+            f"; fp64 NumPy; build amortised over {window_steps} steps as in the timed GPU window")
+    return 1.0 / per_step, t_build, t_step, what
 
 
-def make_inputs(model, wl, seed, steps, device_draws):
+def cpu_baseline(wl, weights, seed, window_steps, others=True):
+    """The fp64 reference as it stands, timed on this host's cores on a bounded sample of the
+    timed workload (row 0; for the 7B model 4 of its 32 layers, scaled), plus the 2-layer and
+    12-layer workloads with all BLAS threads and with one."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from ref_bridge import oracle_params
+    from paper_2508_10259_amd import workload as W
+    blas = blas_info()
+    big = wl.spec.matmul_params > 1e9
+    p = oracle_params(weights)
+    v, tb, ts, what = _oracle_sample(wl, p, seed, 1 if big else 20, window_steps, n_layers=4 if big else None)
+    del p
+    out = {"value": v, "unit": "action-steps/s", "cores": blas["threads"], "kind": "oracle", "sample": what,
+           "host_cpu": lscpu_model(), "blas": blas}
+    if not others:
+        return out
+    from threadpoolctl import threadpool_limits
+    extra, one = {}, {}
+    for name, n in (("tiny-b1", 100), ("mid-b8", 10)):
+        ow = W.WORKLOADS[name]
+        if ow.name == wl.name:
+            continue
+        po = oracle_params(W.make_weights(ow.spec, seed))
+        vo, _, _, wo = _oracle_sample(ow, po, seed, n, ow.invalidate_every or 20)
+        extra[name] = {"value": vo, "cores": blas["threads"], "sample": wo}
+        with threadpool_limits(limits=1, user_api="blas"):
+            v1, _, _, w1 = _oracle_sample(ow, po, seed, max(2, n // 5), ow.invalidate_every or 20)
+        one[name] = {"value": v1, "cores": 1, "sample": w1}
+    out["other_workloads"] = extra
+    out["one_thread"] = one
+    return out
+
+
+def make_inputs(model, wl, seed, steps, device_draws, stagger=False):
     """Every input of the timed window, resident in HBM: one packed prefix set per build
-    epoch and a pool of per-step observation tokens (one invalidation window's worth)."""
+    epoch, a pool of per-step observation tokens (one invalidation window's worth) and, for
+    staggered row rebuilds, the fresh prefixes of the rows rebuilt before each step."""
     import torch
     from paper_2508_10259_amd import workload as W
     inv = wl.invalidate_every
-    n_epochs = 1 + (steps - 1) // inv if inv else 1
+    n_epochs = 1 if stagger else (1 + (steps - 1) // inv if inv else 1)
+    draw = W.make_prefix_device if device_draws else W.make_prefix
     epochs = []
     for e in range(n_epochs):
         lens = W.prefix_lengths(wl, seed, e)
-        if device_draws:
-            pre = [W.make_prefix_device(wl, seed, e, b, int(lens[b])) for b in range(wl.batch)]
-        else:
-            pre = [W.make_prefix(wl, seed, e, b, int(lens[b])) for b in range(wl.batch)]
-        epochs.append(model.pack_prefixes(pre))
+        epochs.append(model.pack_prefixes([draw(wl, seed, e, b, int(lens[b])) for b in range(wl.batch)]))
     pool = []
     if wl.new_per_step:
-        for s in range(min(steps, inv or steps)):
-            pool.append(W.make_observation_device(wl.spec, seed, s, wl.batch, wl.new_per_step))
+        for s_ in range(min(steps, inv or steps)):
+            pool.append(W.make_observation_device(wl.spec, seed, s_, wl.batch, wl.new_per_step))
+    rebuild = {}
+    if stagger:  # before step s the rows b with (s + b) % inv == 0: one residue class of s per entry
+        for r in range(inv):
+            rows = [b for b in range(wl.batch) if (r + b) % inv == 0]
+            lens = W.prefix_lengths(wl, seed, 100 + r)
+            packed, plens = model.pack_prefixes([draw(wl, seed, 100 + r, b, int(lens[b])) for b in rows])
+            rebuild[r] = (rows, packed, plens)
     torch.cuda.synchronize()
-    return epochs, pool
+    return epochs, pool, rebuild
 
 
-def roofline_kernel_name(spec, A, B, persistent):
-    """The dominant decode kernel of a workload, as its roofline entry and profiles name it."""
+def run_window(ctx, wl, epochs, pool, rebuild, steps, A, tokens, logits, mode):
+    """One build then `steps` steps with the workload's rebuilds (mode "cached"), a rebuild
+    before every step ("recompute"), or row-level rebuilds of the rows b with
+    (step + b) % invalidate_every == 0 before each step ("staggered").  New observation
+    tokens go in through ams_ctx_append, the action decode through ams_ctx_step (no new
+    tokens), so each phase is bracketed by its own HIP events on the library's stream.
+    Returns the window's duration and per-phase (seconds, algorithmic work) lists."""
+    import torch
+    spec = wl.spec
+    inv = wl.invalidate_every
+    new_lens = [wl.new_per_step] * wl.batch if wl.new_per_step else None
+    marks = []  # (phase, ev0, ev1, work)
+
+    def timed(phase, work, fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        marks.append((phase, e0, e1, work))
+
+    w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0.record()
+    timed("build", build_flops(spec, epochs[0][1]), lambda: ctx.build(*epochs[0]))
+    for s_ in range(steps):
+        if mode == "cached" and inv and s_ and s_ % inv == 0:
+            ctx.invalidate()
+            e = epochs[(s_ // inv) % len(epochs)]
+            timed("build", build_flops(spec, e[1]), lambda e=e: ctx.build(*e))
+        elif mode == "recompute" and s_:
+            ctx.invalidate()
+            timed("build", build_flops(spec, epochs[0][1]), lambda: ctx.build(*epochs[0]))
+        elif mode == "staggered" and s_:
+            rows, packed, plens = rebuild[s_ % inv]
+            ctx.invalidate_rows(rows)
+            timed("build", build_flops(spec, plens), lambda: ctx.build_rows(rows, packed, plens))
+        if new_lens:
+            before = ctx.lengths()
+            new = pool[s_ % len(pool)]
+            timed("extension", extension_flops(spec, before, new_lens), lambda: ctx.append(new, new_lens))
+        lens = ctx.lengths()
+        timed("decode", step_bytes(spec, lens, A), lambda: ctx.step(A, tokens=tokens, logits=logits))
+    w1.record()
+    torch.cuda.synchronize()
+    ph = {"build": [], "extension": [], "decode": []}
+    for phase, e0, e1, work in marks:
+        ph[phase].append((e0.elapsed_time(e1) * 1e-3, work))
+    return w0.elapsed_time(w1) * 1e-3, ph
+
+
+def phase_summary(entries, bound, peak):
+    """Achieved rate of a phase over the window: its algorithmic work / its measured time."""
+    if not entries:
+        return None
+    t = sum(e[0] for e in entries)
+    w = sum(e[1] for e in entries)
+    if bound == "hbm":
+        return {"bound": "hbm", "achieved": round(w / t / 1e9, 1), "peak": peak, "unit": "GB/s",
+                "frac": round(w / t / 1e9 / peak, 4), "bytes_per_launch": int(w / len(entries)),
+                "avg_launch_us": round(t / len(entries) * 1e6, 1), "launches": len(entries)}
+    return {"bound": "mfma", "achieved": round(w / t / 1e12, 1), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(w / t / 1e12 / peak, 4), "flops_per_launch": int(w / len(entries)),
+            "avg_launch_us": round(t / len(entries) * 1e6, 1), "launches": len(entries)}
+
+
+def measure(model, wl, seed, steps, warmup, mode, device_draws):
+    """Warm-up window, then the timed window; returns the workload's figures."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext
+    spec = wl.spec
+    cap = wl.derived_capacity()
+    ctx = DeviceContext(model, wl.batch, cap)
+    epochs, pool, rebuild = make_inputs(model, wl, seed, max(steps, warmup), device_draws,
+                                        stagger=(mode == "staggered"))
+    B, A = wl.batch, wl.n_actions
+    tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
+    logits = torch.empty((B, A, spec.n_bins), dtype=torch.float32, device="cuda")
+    run_window(ctx, wl, epochs, pool, rebuild, warmup, A, tokens, logits, mode)
+    t_win, ph = run_window(ctx, wl, epochs, pool, rebuild, steps, A, tokens, logits, mode)
+    persistent = ctx.persistent_decode
+    ctx.close()
+    del epochs, pool, rebuild
+    dec = phase_summary(ph["decode"], "hbm", HBM_PEAK_GBS)
+    ext = phase_summary(ph["extension"], "mfma", MFMA_F16_PEAK_TFLOPS)
+    bld = phase_summary(ph["build"], "mfma", MFMA_F16_PEAK_TFLOPS)
+    roof_s = (sum(w for _, w in ph["decode"]) / (HBM_PEAK_GBS * 1e9) +
+              sum(w for _, w in ph["extension"] + ph["build"]) / (MFMA_F16_PEAK_TFLOPS * 1e12))
+    return {"workload": wl.name, "mode": mode, "batch": B, "steps": steps, "capacity": cap,
+            "persistent_decode": bool(persistent), "window_s": t_win, "value": B * steps / t_win,
+            "ms_per_step": t_win / steps * 1e3, "decode": dec, "extension": ext, "build": bld,
+            "step": {"ms": round(t_win / steps * 1e3, 4), "roofline_ms": round(roof_s / steps * 1e3, 4),
+                     "frac": round(roof_s / t_win, 4),
+                     "phases_ms": {k: round(sum(e[0] for e in v) / steps * 1e3, 4) for k, v in ph.items()}}}
+
+
+def decode_kernel_name(spec, B, A, persistent):
     if persistent:
-        return f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer)"
-    return ("k_gemm_skinny<2,1,SWIGLU,NRM> (decode RMSNorm + gate|up projection + SiLU gate)" if B <= 8
-            else f"k_gemm_wide<{(B + 15) // 16},2> (decode gate|up projection, split-K partial sums)"
-            if B <= 64 else "k_gemm_tiled or k_gemm_big (decode gate|up projection + SiLU gate)")
+        return (f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer, "
+                "+ the barrier-clearing kernel)")
+    return (f"decode phase of a step: {A - 1} passes x {spec.n_layers} layers of k_gemm_wide<{(B + 15) // 16},2> "
+            "(QKV, O, gate|up, down) + split-K reductions + k_attn_decode, and " f"{A} bin heads")
+
+
+def compact(r):
+    """The figures of an extra workload."""
+    out = {"value": round(r["value"], 2), "unit": "action-steps/s", "ms_per_step": round(r["ms_per_step"], 4),
+           "batch": r["batch"], "steps": r["steps"], "mode": r["mode"], "step": r["step"]}
+    for k in ("decode", "extension", "build"):
+        if r[k]:
+            out[k] = {kk: r[k][kk] for kk in ("frac", "achieved", "unit", "avg_launch_us")}
+    return out
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="default: the workload's step count")
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mid-b8")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="7b-b64-ragged")
+    ap.add_argument("--mode", default="cached", choices=("cached", "recompute", "staggered"))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=100)
-    ap.add_argument("--recompute", action="store_true",
-                    help="invalidate + rebuild the prefix before every step (the no-reuse comparison)")
-    ap.add_argument("--roofline-only", action="store_true",
-                    help="time only the roofline kernel (and the calibration copy), print one JSON line and exit: "
-                         "the command the profiles' counter runs use")
+    ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--counters", action="store_true",
+                    help="for counter runs: build, one append, the calibration copy, then --steps decode-only "
+                         "steps; prints the per-step decode time")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decoder shards by episode, "
@@ -309,110 +404,102 @@ def main():
 
     wl = W.WORKLOADS[args.workload]
     spec = wl.spec
-    steps = args.steps if args.steps is not None else wl.steps
     big = spec.matmul_params > 1e9
     torch.cuda.set_device(0)
     print(f"[bench] {wl.name}: weights", file=sys.stderr, flush=True)
     weights = W.make_device_weights(spec, args.seed) if big else W.make_weights(spec, args.seed)
     model = DeviceModel(weights, "cuda:0")
-    cap = wl.derived_capacity()
-    ctx = DeviceContext(model, wl.batch, cap)
-    persistent = ctx.persistent_decode
-    print(f"[bench] inputs (capacity {cap}, persistent decode {persistent})", file=sys.stderr, flush=True)
-    epochs, pool = make_inputs(model, wl, args.seed, steps, big)
     B, A = wl.batch, wl.n_actions
-    if args.roofline_only:
-        if persistent:
-            ctx.build(*epochs[0])
-            t_k = time_persistent_step(ctx, A)
-        else:
-            t_k = time_gate_up_kernel(model, B)
+
+    if args.counters:
+        ctx = DeviceContext(model, B, wl.derived_capacity())
+        epochs, pool, _ = make_inputs(model, wl, args.seed, 1, big)
+        ctx.build(*epochs[0])
+        if pool:
+            ctx.append(pool[0], [wl.new_per_step] * B)
+        tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
         copy_calibration()
-        print(json.dumps({"workload": wl.name, "kernel": roofline_kernel_name(spec, A, B, persistent),
-                          "avg_launch_us": round(t_k * 1e6, 3)}), flush=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            ctx.step(A, tokens=tokens, want_logits=False)
+        e1.record()
+        torch.cuda.synchronize()
+        print(json.dumps({"workload": wl.name, "decode_steps": args.steps,
+                          "avg_decode_us": round(e0.elapsed_time(e1) / args.steps * 1e3, 1),
+                          "bytes_per_step": step_bytes(spec, ctx.lengths(), A)}), flush=True)
         ctx.close()
         model.close()
         return
-    tokens = torch.empty((B, A), dtype=torch.int32, device="cuda")
-    logits = torch.empty((B, A, spec.n_bins), dtype=torch.float32, device="cuda")
-    new_lens = [wl.new_per_step] * B if wl.new_per_step else None
-    inv = wl.invalidate_every
 
-    def window(n_steps):
-        """One build then n_steps steps, with the workload's rebuilds; returns (t_build, t_steps)."""
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        ev[0].record()
-        ctx.build(*epochs[0])
-        ev[1].record()
-        for s_ in range(n_steps):
-            if inv and s_ and s_ % inv == 0:
-                ctx.invalidate()
-                ctx.build(*epochs[(s_ // inv) % len(epochs)])
-            if args.recompute and s_:
-                ctx.invalidate()
-                ctx.build(*epochs[0])
-            new = pool[s_ % len(pool)] if pool else None
-            ctx.step(A, new, new_lens, tokens=tokens, logits=logits)
-        ev[2].record()
-        torch.cuda.synchronize()
-        return ev[0].elapsed_time(ev[1]) * 1e-3, ev[1].elapsed_time(ev[2]) * 1e-3
-
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    window(min(args.warmup, inv or args.warmup))
-    t_build, t_steps = window(steps)
-    total = t_build + t_steps
-    value = B * steps / total
-    lens = epochs[0][1]
-    sb = step_bytes(spec, lens, A)
-    print(f"[bench] build {t_build * 1e3:.3f} ms, {steps} steps {t_steps * 1e3:.1f} ms", file=sys.stderr,
+    print(f"[bench] {wl.name}: warmup {args.warmup}, timed {args.steps} steps ({args.mode})", file=sys.stderr,
           flush=True)
-
-    kname = roofline_kernel_name(spec, A, B, persistent)
-    if persistent:
-        # the step's whole decode is one launch: its algorithmic bytes are the step's
-        t_k = time_persistent_step(ctx, A)
-        kb = sb
-    else:
-        t_k = time_gate_up_kernel(model, B)
-        kb = gu_launch_bytes(spec, B)
-    achieved = kb / t_k / 1e9
+    r = measure(model, wl, args.seed, args.steps, args.warmup, args.mode, big)
+    print(f"[bench] {wl.name}: {r['value']:.1f} row-steps/s, {r['ms_per_step']:.3f} ms/step", file=sys.stderr,
+          flush=True)
+    extras = {}
+    if not args.no_extras:
+        plan = []
+        if spec.name == "7b":
+            plan = [("7b-b1", "cached", 20), ("7b-chunk56-b16", "cached", 8), ("7b-chunk56-b16", "recompute", 8),
+                    ("7b-b64-ragged", "staggered", 20)]
+        for name, mode, n in plan:
+            if name == wl.name and mode == args.mode:
+                continue
+            print(f"[bench] extra {name} ({mode}, {n} steps)", file=sys.stderr, flush=True)
+            x = measure(model, W.WORKLOADS[name], args.seed, n, 2, mode, big)
+            extras[f"{name}/{mode}" if mode != "cached" else name] = compact(x)
+        if spec.name != "mid":
+            model.close()
+            print("[bench] extra mid-b8 (cached, 100 steps)", file=sys.stderr, flush=True)
+            mw = DeviceModel(W.make_weights(W.MODELS["mid"], args.seed), "cuda:0")
+            extras["mid-b8"] = compact(measure(mw, W.WORKLOADS["mid-b8"], args.seed, 100, 10, "cached", False))
+            mw.close()
+        c5, c5r = extras.get("7b-chunk56-b16"), extras.get("7b-chunk56-b16/recompute")
+        if c5 and c5r:
+            c5["speedup_vs_recompute"] = round(c5["value"] / c5r["value"], 3)
+            c5["actions_per_s"] = round(c5["value"] * 8, 2)  # 56 tokens = 8 actions of 7 tokens
     copy_calibration()
     peaks = measured_peaks()
     hbm_meas = max(peaks["hbm_copy_GBps"], peaks["hbm_read_GBps"])
-    roof = {"kernel": kname, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name, kname.split(" ")[0]),
-            "bytes_per_launch": kb, "avg_launch_us": round(t_k * 1e6, 3),
-            "frac_vs_measured": round(achieved / hbm_meas, 4)}
 
+    dec = dict(r["decode"])
+    kname = decode_kernel_name(spec, B, A, r["persistent_decode"])
+    roof = {"kernel": kname, **dec, "traffic": profiled_traffic(wl.name, "decode-phase"),
+            "frac_vs_measured": round(dec["achieved"] / hbm_meas, 4)}
+    if r["build"]:
+        roof["rebuild"] = {"kernel": "ams_ctx_build: k_gemm_big GEMMs + k_attn_prefill_mfma + row kernels",
+                           **r["build"], "frac_vs_measured": round(r["build"]["achieved"] / peaks["mfma_f16_TFLOPs"], 4)}
+    if r["extension"]:
+        roof["extension"] = {"kernel": "ams_ctx_append: k_gemm_big GEMMs (split-K O/down) + k_attn_extend + row kernels",
+                             **r["extension"],
+                             "frac_vs_measured": round(r["extension"]["achieved"] / peaks["mfma_f16_TFLOPs"], 4)}
     out = {
         "metric": "action steps/s per GPU (cached-context decode)",
-        "value": round(value, 2), "unit": "action-steps/s", "n_gpus": 1, "steps": steps,
-        "warmup": args.warmup, "ms_per_step": round(total / steps * 1e3, 4), "higher_is_better": True,
+        "value": round(r["value"], 2), "unit": "action-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(r["ms_per_step"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "fp16",
-        "data": "synthetic (seeded N(0,0.02) weights stored bf16, N(0,1) patch embeddings, uniform ids)",
+        "data": "synthetic (seeded N(0,0.02) weights stored bf16, N(0,1) patch/observation embeddings, uniform ids)",
         "config": {"workload": wl.name, "n_layers": spec.n_layers, "d_model": spec.d_model,
                    "n_heads": spec.n_heads, "head_dim": spec.head_dim, "d_ffn": spec.d_ffn,
-                   "vocab": spec.vocab, "n_bins": spec.n_bins, "batch": B, "prefix_tokens": int(lens[0]),
-                   "n_actions": A, "capacity": cap, "new_tokens_per_step": wl.new_per_step,
-                   "invalidate_every": inv, "recompute_each_step": bool(args.recompute),
-                   "timed": f"1 build + {steps} steps" + (f" (rebuild every {inv})" if inv else "")
-                            + (" (rebuild before every step)" if args.recompute else "")},
+                   "vocab": spec.vocab, "n_bins": spec.n_bins, "batch": B,
+                   "prefix_tokens": (f"U{{{wl.ragged[0]}..{wl.ragged[1]}}}" if wl.ragged else sum(wl.prefix)),
+                   "n_actions": A, "capacity": r["capacity"], "new_tokens_per_step": wl.new_per_step,
+                   "invalidate_every": wl.invalidate_every, "mode": args.mode,
+                   "timed": f"1 build + {args.steps} steps" + (f" (rebuild every {wl.invalidate_every})"
+                                                                if wl.invalidate_every else "")},
         "roofline": roof,
-        "step": {"ms": round(t_steps / steps * 1e3, 4), "algorithmic_bytes_no_new_tokens": sb,
-                 "hbm_frac": round(sb / (t_steps / steps) / (HBM_PEAK_GBS * 1e9), 4),
-                 "hbm_frac_vs_measured": round(sb / (t_steps / steps) / (hbm_meas * 1e9), 4)},
-        "build": {"ms": round(t_build * 1e3, 4), "flops": build_flops(spec, lens),
-                  "mfma_frac": round(build_flops(spec, lens) / t_build / (MFMA_F16_PEAK_TFLOPS * 1e12), 4),
-                  "mfma_frac_vs_measured": round(build_flops(spec, lens) / t_build / (peaks["mfma_f16_TFLOPs"] * 1e12),
-                                                 4)},
+        "step": {**r["step"], "what": "whole timed window per step against the sum of the decode (HBM), extension "
+                                      "and rebuild (MFMA) rooflines"},
         "measured_peaks": peaks,
     }
-    ctx.close()
-    model.close()
-    del epochs, pool
+    if extras:
+        out["extra_workloads"] = extras
+    del model
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, weights, args.seed, args.cpu_sample_steps if not big else 1, steps)
+        out["cpu_baseline"] = cpu_baseline(wl, weights, args.seed, wl.invalidate_every or args.steps)
     print(json.dumps(out), flush=True)
 
 

@@ -71,3 +71,46 @@ def gpu_new_tokens(spec: W.ModelSpec, news: List[Optional[np.ndarray]], device="
         return None, lens
     packed = np.concatenate([x for x in news if x is not None and x.shape[0] > 0], axis=0)
     return to_device(packed, spec.dtype, device), lens
+
+
+class ForcedRef:
+    """One row of the fp64 reference stepped with given fed-back bins.
+
+    A step's logits come from one forward pass over the step's new tokens followed by the
+    embedding-table rows (vocab - n_bins + bin) of the bins fed back after actions 0..A-2:
+    the logits of action j are those of the sequence's last committed token (j = 0) or of
+    the j-th fed-back token -- the teacher-forced decoding that ``pin_forced_decoding``
+    pins to the reference's own step.  New tokens are committed, fed-back ones dropped
+    (``pin_lifecycle``).  Feeding the GPU's own choices back makes both sides follow one
+    trajectory, so a near-tie flip cannot cascade while every position is still compared.
+    """
+
+    def __init__(self, p, prefix: np.ndarray):
+        self.p = p
+        h, self.kv = D.forward(p, np.asarray(prefix, dtype=np.float64))
+        self.h_last = h[-1].copy()
+        self.len = prefix.shape[0]
+
+    def step(self, new: Optional[np.ndarray], fed) -> np.ndarray:
+        """Logits [A, n_bins]; fed = the A bins chosen (the last one is not fed back)."""
+        p = self.p
+        A = len(fed)
+        n_new = 0 if new is None else int(new.shape[0])
+        parts = ([] if n_new == 0 else [np.asarray(new, dtype=np.float64)]) + \
+            [D.bin_embedding(p, int(f))[None] for f in fed[:A - 1]]
+        if not parts:
+            return D.bin_logits(p, self.h_last[None])
+        h, kv = D.forward(p, np.concatenate(parts, axis=0), start=self.len, past=self.kv)
+        hs = [self.h_last] + list(h[:A - 1]) if n_new == 0 else list(h[n_new - 1:n_new - 1 + A])
+        z = D.bin_logits(p, np.stack(hs))
+        if n_new:
+            self.len += n_new
+            self.kv = [(k[:self.len], v[:self.len]) for k, v in kv]
+            self.h_last = h[n_new - 1].copy()
+        return z
+
+
+def percentiles(errs) -> str:
+    e = np.abs(np.concatenate([np.ravel(x) for x in errs]))
+    q = np.percentile(e, [50, 90, 99, 99.9, 100])
+    return "p50 {:.2e} p90 {:.2e} p99 {:.2e} p99.9 {:.2e} max {:.2e}".format(*q)

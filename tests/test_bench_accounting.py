@@ -1,5 +1,5 @@
 """The work bench.py divides its times by -- the algorithmic bytes of a step, the FLOPs of
-a build, the bytes of the gate|up launch -- against closed forms written here from the model
+a build, the FLOPs of an extension -- against closed forms written here from the model
 shapes alone: matmul parameters n_layers (4 d^2 + 3 d F), K/V bytes per token n_layers * 2 d
 * 2 bytes, causal query-key pairs L (L + 1) / 2, and the per-unit figures they give for the
 12-layer and 7B workloads (3.09 GB and 78.6 GB per step, 0.917 and 3.75 TFLOP per build)."""
@@ -55,18 +55,34 @@ def test_build_flops():
     assert bench.build_flops(s, lens) == sum(bench.build_flops(s, np.array([x])) for x in lens)
 
 
-def test_gate_up_launch_bytes():
-    """Weights [2F, d] in fp16 once, the input rows as fp16 pairs, and the gated output as fp16
-    pairs where the kernel writes it (up to 8 rows; the wide kernel leaves it to its reduction)."""
-    wl, s, L, d, F = _shape("7b-b1")
-    for B, out in ((1, True), (8, True), (16, False), (64, False)):
-        want = 2 * F * d * 2 + B * d * 4 + (B * F * 4 if out else 0)
-        assert bench.gu_launch_bytes(s, B) == want, B
+def test_extension_flops():
+    """Appending n tokens to a row of L committed tokens: 2 P_mm FLOPs per new token, and new token
+    i attends to L + i + 1 keys (4 d n_layers FLOPs per query-key pair).  The 7B batch-64 step
+    (16 tokens per row on rows of about 468) is 13.5 TFLOP."""
+    wl, s, L, d, F = _shape("7b-b64-ragged")
+    P = L * (4 * d * d + 3 * d * F)
+    for Lb, n in ((0, 5), (300, 16), (17, 1)):
+        pairs = sum(Lb + i + 1 for i in range(n))
+        assert bench.extension_flops(s, [Lb], [n]) == 2 * P * n + 4 * d * L * pairs
+    assert bench.extension_flops(s, [300, 10], [0, 0]) == 0
+    got = bench.extension_flops(s, [460] * 64, [16] * 64)
+    assert abs(got / 1e12 - 13.5) < 0.1, got
+    # prefix + extension pairs = the pairs of building the longer prefix
+    assert bench.extension_flops(s, [40], [9]) + bench.build_flops(s, [40]) == bench.build_flops(s, [49])
 
 
-def test_roofline_kernel_names():
+def test_phase_summary():
+    hbm = bench.phase_summary([(0.5, 2e12), (0.5, 2e12)], "hbm", 8000.0)
+    assert hbm["achieved"] == 4000.0 and hbm["frac"] == 0.5 and hbm["bytes_per_launch"] == 2e12
+    assert hbm["avg_launch_us"] == 5e5 and hbm["launches"] == 2
+    mf = bench.phase_summary([(2.0, 2.5e15)], "mfma", 2500.0)
+    assert mf["achieved"] == 1250.0 and mf["frac"] == 0.5
+    assert bench.phase_summary([], "hbm", 8000.0) is None
+
+
+def test_decode_kernel_names():
     mid, s7 = W.MODELS["mid"], W.MODELS["7b"]
-    assert bench.roofline_kernel_name(mid, 7, 8, True).startswith("k_decode_fused<64>")
-    assert bench.roofline_kernel_name(s7, 7, 1, True).startswith("k_decode_fused<128>")
-    assert bench.roofline_kernel_name(s7, 56, 16, False).startswith("k_gemm_wide<1,2>")
-    assert bench.roofline_kernel_name(s7, 7, 64, False).startswith("k_gemm_wide<4,2>")
+    assert bench.decode_kernel_name(mid, 8, 7, True).startswith("k_decode_fused<64>")
+    assert bench.decode_kernel_name(s7, 1, 7, True).startswith("k_decode_fused<128>")
+    assert "k_gemm_wide<1,2>" in bench.decode_kernel_name(s7, 16, 56, False)
+    assert "k_gemm_wide<4,2>" in bench.decode_kernel_name(s7, 64, 7, False)

@@ -229,15 +229,6 @@ def test_7b_single_row_full_size():
     ctx.close()
 
 
-@pytest.fixture(scope="module")
-def model_7b():
-    from paper_2508_10259_amd.runtime import DeviceModel
-    from ref_bridge import oracle_params
-    spec = W.MODELS["7b"]
-    w = W.make_device_weights(spec, seed=0)
-    return spec, DeviceModel(w), oracle_params(w)
-
-
 def _rows_ref(p, spec, prefixes, rows):
     ref = D.ActionContext(p, len(rows))
     ref.build([prefix_f64_of(p, spec, prefixes[b]) for b in rows])

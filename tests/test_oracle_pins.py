@@ -51,3 +51,24 @@ def test_prefix_bridge_text_rows():
     assert x.shape == (7, 128)
     assert np.array_equal(x[:3], W.bf16_bits_to_f32(patches).astype(np.float64))
     assert np.array_equal(x[3:], table[ids])
+
+
+def test_forced_ref_helper_matches_reference_step():
+    """The GPU tests' batched teacher-forced helper equals the reference's own step with the
+    same forced bins (to 1e-12), with and without new tokens, over several steps."""
+    from gpu_util import ForcedRef
+    p = tiny_params(D, key=13, V=20, n_bins=6)
+    pre = _rand((5, 8), 90)
+    ctx = D.ActionContext(p, 1)
+    ctx.build([pre])
+    fr = ForcedRef(p, pre)
+    rng = np.random.default_rng(1)
+    for s, n in enumerate([2, 0, 1, 0, 3]):
+        new = _rand((n, 8), 91, s) if n else None
+        fed = rng.integers(0, 6, size=4)
+        t, z = ctx.step([new], 4, forced=fed[None])
+        zf = fr.step(new, fed)
+        err = float(np.max(np.abs(z[0] - zf)))
+        assert err <= 1e-12, (s, err)
+        assert fr.len == ctx.lengths()[0]
+    assert ForcedRef(p, pre).step(None, [3]).shape == (1, 6)
