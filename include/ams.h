@@ -134,6 +134,35 @@ void ams_model_destroy(ams_model* m); /* NULL is a no-op; destroy contexts first
 ams_status ams_embed_ids(const ams_model* m, const int32_t* ids, int32_t n, void* out,
                          void* stream);
 
+/* ---- action index ----------------------------------------------------- */
+
+/* Paper section 3.2.3 (Action Compression, Virtual Action; Algorithm 1,
+ * Two-Phase Hashing for Action Index): an input serialised to bytes is cut
+ * into ceil(n_bytes / seg_bytes) segments of seg_bytes bytes (the last may be
+ * shorter); phase 1 hashes every segment independently, phase 2 merges the
+ * segment hashes in order into the index value.  The paper says only that
+ * both hash functions are modular; here they are polynomial hashes modulo
+ * p = 2^31 - 1 evaluated with two fixed bases each, the two 31-bit results
+ * packed into one uint64 (first base in the low 32 bits):
+ *   HashFunc1(B_i) = (sum_j u_j r^(seg_bytes/2 - 1 - j)) r + |B_i| mod p,
+ *     u_j the 16-bit little-endian units of B_i zero-padded to seg_bytes,
+ *     |B_i| its unpadded length; r = 0x2545F491, then 0x1B873593;
+ *   H = HashFunc2(h_1..h_k) = (sum_i h_i q^(k - i)) q + n_bytes mod p,
+ *     q = 0x3C6EF372, then 0x0A54FF53.
+ * Bytes of workspace ams_index_hash needs: 8 per segment (0 if the sizes are
+ * invalid). */
+size_t ams_index_hash_workspace_bytes(size_t n_bytes, int32_t seg_bytes);
+
+/* Two-phase hash of n_bytes >= 1 bytes of device memory `data` (16-byte
+ * aligned); seg_bytes a multiple of 16 in [16, 65536].  `ws` (device, 8-byte
+ * aligned, at least ams_index_hash_workspace_bytes bytes, caller-owned) holds
+ * the phase-1 segment hashes h_1..h_k (uint64 each) when the call completes;
+ * *out_hash (device uint64) receives H.  Asynchronous on `stream`.
+ * Errors: AMS_EINVAL (sizes, alignment, pointers not on the current device),
+ * AMS_ENOMEM (ws too small), AMS_ENODEV, AMS_EHIP. */
+ams_status ams_index_hash(const void* data, size_t n_bytes, int32_t seg_bytes, void* ws, size_t ws_bytes,
+                          uint64_t* out_hash, void* stream);
+
 /* ---- context ---------------------------------------------------------- */
 
 /* Bytes of device workspace a context needs: the K/V slab for `batch` rows of

@@ -344,6 +344,36 @@ ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_ro
   return AMS_OK;
 }
 
+size_t ams_index_hash_workspace_bytes(size_t n_bytes, int32_t seg_bytes) {
+  if (n_bytes == 0 || seg_bytes < 16 || seg_bytes > 65536 || seg_bytes % 16) return 0;
+  return ((n_bytes + seg_bytes - 1) / seg_bytes) * 8;
+}
+
+ams_status ams_index_hash(const void* data, size_t n_bytes, int32_t seg_bytes, void* ws, size_t ws_bytes,
+                          uint64_t* out_hash, void* stream) {
+  g_err.clear();
+  std::string e;
+  if (n_bytes == 0) return fail(AMS_EINVAL, "n_bytes must be >= 1");
+  if (seg_bytes < 16 || seg_bytes > 65536 || seg_bytes % 16)
+    return fail(AMS_EINVAL, "seg_bytes must be a multiple of 16 in [16, 65536]");
+  const uint64_t k = (n_bytes + seg_bytes - 1) / seg_bytes;
+  if (k > 0x7FFFFFFFull) return fail(AMS_EINVAL, "too many segments (more than 2^31 - 1)");
+  if (((uintptr_t)data & 15) != 0) return fail(AMS_EINVAL, "data must be 16-byte aligned");
+  if (((uintptr_t)ws & 7) != 0 || ((uintptr_t)out_hash & 7) != 0)
+    return fail(AMS_EINVAL, "ws and out_hash must be 8-byte aligned");
+  if (ws_bytes < k * 8) return fail(AMS_ENOMEM, "index workspace too small: need " + std::to_string(k * 8));
+  int dev = 0;
+  if (int s = current_device(&dev, e)) return fail(s, e);
+  if (!dev_range(data, n_bytes, dev, "data", e) || !dev_range(ws, k * 8, dev, "ws", e) ||
+      !dev_range(out_hash, 8, dev, "out_hash", e))
+    return fail(AMS_EINVAL, e);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t r = ams::hash_segments(data, n_bytes, seg_bytes, (uint64_t*)ws, st);
+  if (r == hipSuccess) r = ams::hash_merge((const uint64_t*)ws, k, n_bytes, out_hash, st);
+  if (r != hipSuccess) return fail(AMS_EHIP, std::string("index hash: ") + hipGetErrorString(r));
+  return AMS_OK;
+}
+
 ams_status ams_ctx_invalidate(ams_ctx* c) {
   g_err.clear();
   if (!c) return fail(AMS_EINVAL, "context is NULL");

@@ -193,6 +193,20 @@ int fused_sync_words(int d, int H);
 // rows with add[b] > 0 (a row-level rebuild leaves the other rows' lengths).
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
 
+// Two-phase hashing for the action index (index.hip).  hash_segments: phase 1,
+// seg_out[g] = HashFunc1 of bytes [g s, g s + s) of data (zero-padded past
+// n_bytes), for g < ceil(n_bytes / s); s a multiple of 16 in [16, 65536], data
+// 16-byte aligned.  hash_merge: phase 2, out[0] = HashFunc2 of seg[0..k) and
+// n_bytes.  hash_page_keys: for each of B rows, keys[b][m] = HashFunc2 of the
+// row's segments (starting at seg + seg_first[b]) covering its first
+// (m + 1) page_bytes bytes, m < min(row_bytes[b] / page_bytes, max_pages)
+// (device arrays; page_bytes a multiple of s).  Values pack the two 31-bit
+// components (first base low).
+hipError_t hash_segments(const void* data, uint64_t n_bytes, int s, uint64_t* seg_out, hipStream_t st);
+hipError_t hash_merge(const uint64_t* seg, uint64_t k, uint64_t n_bytes, uint64_t* out, hipStream_t st);
+hipError_t hash_page_keys(const uint64_t* seg, const int64_t* seg_first, const int64_t* row_bytes, int B,
+                          int64_t page_bytes, int s, int max_pages, uint64_t* keys, hipStream_t st);
+
 // Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned
 // pointers and size) from src to dst; a grid-stride read of src whose per-thread
 // sums land in out[grid * 256]; `iters` rounds of fp16 MFMA chains per wave on

@@ -214,3 +214,22 @@ class DeviceContext:
             self.close()
         except Exception:
             pass
+
+
+def index_hash(data: torch.Tensor, seg_bytes: int, ws: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None):
+    """Two-phase hash (ams_index_hash) of a contiguous device tensor's bytes.  Returns
+    (out [1] int64 tensor holding the uint64 index value, ws: the phase-1 segment hashes)."""
+    lib = capi.load()
+    assert data.is_cuda and data.is_contiguous()
+    n = data.numel() * data.element_size()
+    need = lib.ams_index_hash_workspace_bytes(n, seg_bytes)
+    if need == 0:
+        raise ValueError("invalid index hash sizes")
+    if ws is None:
+        ws = torch.empty(need // 8, dtype=torch.int64, device=data.device)
+    if out is None:
+        out = torch.empty(1, dtype=torch.int64, device=data.device)
+    capi.check(lib.ams_index_hash(data.data_ptr(), n, seg_bytes, ws.data_ptr(), ws.numel() * 8, out.data_ptr(),
+                                  _stream()), "ams_index_hash")
+    return out, ws

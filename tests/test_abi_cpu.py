@@ -122,3 +122,18 @@ def test_host_state_under_sanitizers(tmp_path):
     r = subprocess.run([exe], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert r.returncode == 0, r.stdout
     assert "state_test: ok" in r.stdout
+
+
+def test_index_hash_rejects_before_device(lib):
+    from paper_2508_10259_amd import capi
+    assert lib.ams_index_hash_workspace_bytes(100, 16) == 7 * 8
+    assert lib.ams_index_hash_workspace_bytes(4096, 4096) == 8
+    assert lib.ams_index_hash_workspace_bytes(4097, 4096) == 16
+    for n, s in ((0, 16), (10, 8), (10, 24), (10, 65552)):
+        assert lib.ams_index_hash_workspace_bytes(n, s) == 0
+    out = C.c_void_p(256)
+    assert lib.ams_index_hash(C.c_void_p(256), 0, 16, C.c_void_p(256), 8, out, None) == capi.AMS_EINVAL
+    assert lib.ams_index_hash(C.c_void_p(256), 100, 20, C.c_void_p(256), 64, out, None) == capi.AMS_EINVAL
+    assert lib.ams_index_hash(C.c_void_p(257), 100, 16, C.c_void_p(256), 64, out, None) == capi.AMS_EINVAL
+    assert lib.ams_index_hash(C.c_void_p(256), 100, 16, C.c_void_p(256), 48, out, None) == capi.AMS_ENOMEM
+    assert b"workspace" in lib.ams_last_error()
