@@ -163,6 +163,18 @@ size_t ams_index_hash_workspace_bytes(size_t n_bytes, int32_t seg_bytes);
 ams_status ams_index_hash(const void* data, size_t n_bytes, int32_t seg_bytes, void* ws, size_t ws_bytes,
                           uint64_t* out_hash, void* stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: the same
+ * two-phase hash as ams_index_hash with no workspace argument.  The phase-1
+ * segment hashes go to a static scratch array of the library (1 MiB, one copy
+ * per device, held until the process ends), so at most 131072 segments
+ * (n_bytes <= 131072 * seg_bytes) are accepted, else AMS_EINVAL.  The call
+ * allocates nothing.  Calls on one device share the scratch: calls that
+ * overlap (other streams, other host threads) race; calls on one stream are
+ * ordered.  Other arguments and errors as ams_index_hash. */
+ams_status ams_index_hash_noalloc(const void* data, size_t n_bytes, int32_t seg_bytes, uint64_t* out_hash,
+                                  void* stream);
+
 /* ---- context ---------------------------------------------------------- */
 
 /* Bytes of device workspace a context needs: the K/V slab for `batch` rows of

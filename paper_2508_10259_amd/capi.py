@@ -40,6 +40,7 @@ SIGNATURES = {
     "ams_index_hash_workspace_bytes": (C.c_size_t, [C.c_size_t, C.c_int32]),
     "ams_index_hash": (C.c_int32, [C.c_void_p, C.c_size_t, C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p,
                                    C.c_void_p]),
+    "ams_index_hash_noalloc": (C.c_int32, [C.c_void_p, C.c_size_t, C.c_int32, C.c_void_p, C.c_void_p]),
     "ams_ctx_workspace_bytes": (C.c_size_t, [C.POINTER(ModelCfg), C.c_int32, C.c_int32, C.c_int32]),
     "ams_ctx_create": (C.c_int32, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_size_t,
                                    C.POINTER(C.c_void_p)]),

@@ -374,6 +374,33 @@ ams_status ams_index_hash(const void* data, size_t n_bytes, int32_t seg_bytes, v
   return AMS_OK;
 }
 
+ams_status ams_index_hash_noalloc(const void* data, size_t n_bytes, int32_t seg_bytes, uint64_t* out_hash,
+                                  void* stream) {
+  g_err.clear();
+  std::string e;
+  if (n_bytes == 0) return fail(AMS_EINVAL, "n_bytes must be >= 1");
+  if (seg_bytes < 16 || seg_bytes > 65536 || seg_bytes % 16)
+    return fail(AMS_EINVAL, "seg_bytes must be a multiple of 16 in [16, 65536]");
+  const uint64_t k = (n_bytes + seg_bytes - 1) / seg_bytes;
+  if (k > ams::INDEX_NOALLOC_MAX_SEGMENTS)
+    return fail(AMS_EINVAL, "ams_index_hash_noalloc: " + std::to_string(k) + " segments exceed its scratch of " +
+                                std::to_string(ams::INDEX_NOALLOC_MAX_SEGMENTS) + " (use ams_index_hash)");
+  if (((uintptr_t)data & 15) != 0) return fail(AMS_EINVAL, "data must be 16-byte aligned");
+  if (((uintptr_t)out_hash & 7) != 0) return fail(AMS_EINVAL, "out_hash must be 8-byte aligned");
+  int dev = 0;
+  if (int s = current_device(&dev, e)) return fail(s, e);
+  if (!dev_range(data, n_bytes, dev, "data", e) || !dev_range(out_hash, 8, dev, "out_hash", e))
+    return fail(AMS_EINVAL, e);
+  uint64_t* scratch = nullptr;
+  hipError_t r = ams::index_noalloc_scratch(dev, &scratch);
+  if (r != hipSuccess) return fail(AMS_EHIP, std::string("index scratch: ") + hipGetErrorString(r));
+  hipStream_t st = (hipStream_t)stream;
+  r = ams::hash_segments(data, n_bytes, seg_bytes, scratch, st);
+  if (r == hipSuccess) r = ams::hash_merge(scratch, k, n_bytes, out_hash, st);
+  if (r != hipSuccess) return fail(AMS_EHIP, std::string("index hash: ") + hipGetErrorString(r));
+  return AMS_OK;
+}
+
 ams_status ams_ctx_invalidate(ams_ctx* c) {
   g_err.clear();
   if (!c) return fail(AMS_EINVAL, "context is NULL");

@@ -17,6 +17,8 @@
 // that the idle leading threads contribute the polynomial's leading zeros, and
 // longer segments go block by block.  The work is integer ALU on data read once
 // from HBM.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -186,6 +188,32 @@ __global__ void k_hash_page_keys(const uint64_t* __restrict__ seg, const int64_t
 }
 
 }  // namespace
+
+// Scratch of the allocation-free index hash (ams_index_hash_noalloc): the
+// phase-1 segment hashes of one call, at most INDEX_NOALLOC_MAX_SEGMENTS of
+// them (1 MiB).  Every device the library runs on holds its own copy until the
+// process ends, and every call on that device shares it.  Host code never
+// passes the array's name to a kernel: it takes the device address that
+// hipGetSymbolAddress returned for the current device (index_noalloc_scratch).
+static __device__ __align__(256) uint64_t scratch[INDEX_NOALLOC_MAX_SEGMENTS];
+
+namespace {
+std::mutex g_scratch_mu;
+uint64_t* g_scratch_ptr[64] = {};  // per device id
+}  // namespace
+
+hipError_t index_noalloc_scratch(int device, uint64_t** ptr) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (device < 0 || device >= 64) return hipErrorInvalidDevice;
+  if (!g_scratch_ptr[device]) {  // once per device, with that device current
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = (uint64_t*)p;
+  }
+  *ptr = g_scratch_ptr[device];
+  return hipSuccess;
+}
 
 hipError_t hash_segments(const void* data, uint64_t n_bytes, int s, uint64_t* seg_out, hipStream_t st) {
   const uint64_t k = (n_bytes + s - 1) / s;

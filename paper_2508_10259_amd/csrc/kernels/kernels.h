@@ -207,6 +207,11 @@ hipError_t hash_merge(const uint64_t* seg, uint64_t k, uint64_t n_bytes, uint64_
 hipError_t hash_page_keys(const uint64_t* seg, const int64_t* seg_first, const int64_t* row_bytes, int B,
                           int64_t page_bytes, int s, int max_pages, uint64_t* keys, hipStream_t st);
 
+// The allocation-free variant's scratch: the device address, for `device`
+// (which must be current), of the static array holding its segment hashes.
+constexpr uint64_t INDEX_NOALLOC_MAX_SEGMENTS = 131072;
+hipError_t index_noalloc_scratch(int device, uint64_t** ptr);
+
 // Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned
 // pointers and size) from src to dst; a grid-stride read of src whose per-thread
 // sums land in out[grid * 256]; `iters` rounds of fp16 MFMA chains per wave on
