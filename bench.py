@@ -86,7 +86,7 @@ def profiled_traffic(workload, kernel):
             for src, sha in zip(srcs, shas):
                 if hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest() != sha:
                     return None
-            return int(kv["traffic_bytes"])
+            return int(kv["traffic_bytes"]), int(kv.get("algorithmic_bytes", 0)) or None
         except (OSError, KeyError, ValueError):
             continue
     return None
@@ -466,8 +466,11 @@ def main():
 
     dec = dict(r["decode"])
     kname = decode_kernel_name(spec, B, A, r["persistent_decode"])
-    roof = {"kernel": kname, **dec, "traffic": profiled_traffic(wl.name, "decode-phase"),
+    tr = profiled_traffic(wl.name, "decode-phase")
+    roof = {"kernel": kname, **dec, "traffic": tr[0] if tr else None,
             "frac_vs_measured": round(dec["achieved"] / hbm_meas, 4)}
+    if tr and tr[1]:  # HBM bytes over algorithmic bytes of the counted step (profiles/*_pmc.txt)
+        roof["traffic_vs_algorithmic"] = round(tr[0] / tr[1], 3)
     if r["build"]:
         roof["rebuild"] = {"kernel": "ams_ctx_build: k_gemm_big GEMMs + k_attn_prefill_mfma + row kernels",
                            **r["build"], "frac_vs_measured": round(r["build"]["achieved"] / peaks["mfma_f16_TFLOPs"], 4)}
