@@ -96,6 +96,10 @@ hipError_t ctx_init(Ctx& c, std::string& err) {
   TRY(rope_table(c.rope(), c.lay.capacity, m.head_dim, m.rope_theta, s));
   TRY(hipMemsetAsync(c.ws + c.lay.h_last, 0, c.lay.part - c.lay.h_last, s));
   TRY(hipMemsetAsync(c.ws + c.lay.lens, 0, c.lay.total - c.lay.lens, s));
+  // every row owns the pages of all its positions: row b's page i is b * ppr + i
+  c.pt_host.resize((size_t)c.lay.batch * c.lay.ppr);
+  for (size_t i = 0; i < c.pt_host.size(); ++i) c.pt_host[i] = (int32_t)i;
+  TRY(hipMemcpyAsync(c.pt(), c.pt_host.data(), c.pt_host.size() * 4, hipMemcpyHostToDevice, s));
   TRY(hipStreamSynchronize(s));
   c.splits = decode_splits(c.lay.batch, m.n_heads, c.lay.capacity);
   c.meta_host.assign(c.lay.meta_ints, 0);
@@ -149,8 +153,8 @@ static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t
   const int d = m.d_model, F = m.d_ffn, dt = md.ct;
   TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
   TRY(gemm(dt, EPI_STORE, c.u(), md.wqkv(l), M, 3 * d, d, c.qkv(), 3 * d, s));
-  TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), s));
-  TRY(attn_prefill(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.lay.capacity, c.rope(), c.kslab(l), c.vslab(l), c.o(),
+  TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.pages(), c.rope(), c.kslab(l), c.vslab(l), s));
+  TRY(attn_prefill(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.pages(), c.rope(), c.kslab(l), c.vslab(l), c.o(),
                    s));
   TRY(tokens_resid(c, c.o(), md.wo(l), M, d, s));
   TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
@@ -218,14 +222,10 @@ struct Rows {
     const Cfg& m = c->model->cfg;
     return (float*)at(c->lay.part, (size_t)m.n_heads * c->splits * (m.head_dim + 2) * 4);
   }
-  void* kslab(int l) const {
-    const Cfg& m = c->model->cfg;
-    return (char*)c->kslab(l) + (size_t)r0 * m.n_heads * c->lay.capacity * m.head_dim * ces;
-  }
-  void* vslab(int l) const {
-    const Cfg& m = c->model->cfg;
-    return (char*)c->vslab(l) + (size_t)r0 * m.n_heads * c->lay.capacity * m.head_dim * ces;
-  }
+  // the layer's page pools; the rows' page tables start at row r0
+  void* kslab(int l) const { return c->kslab(l); }
+  void* vslab(int l) const { return c->vslab(l); }
+  KvPages pages() const { return KvPages{c->pt() + (size_t)r0 * c->lay.ppr, c->lay.ppr}; }
 };
 
 // Projection of a normalised input.  Up to 8 fp16 rows run the GEMV with the
@@ -304,7 +304,7 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
   if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err,
                 l > 0 ? ss : nullptr) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, c.splits, c.rope(),
+  TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, g.pages(), c.splits, c.rope(),
                   g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
   TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s, ss));
@@ -372,6 +372,7 @@ static hipError_t enqueue_fused(Ctx& c, int A, int32_t* tok, float* logits, cons
   f.split_o = c.split_o; f.split_d = c.split_d; f.split_a = c.split_a;
   f.lens = c.lens(); f.rope = c.rope();
   f.kv = c.ws + c.lay.kv; f.slab_elems = c.lay.slab_layer / 2;
+  f.pt = c.pt(); f.ppr = c.lay.ppr;
   f.h = c.h(); f.hp = c.ws + c.lay.fx_hp;
   f.hl = c.h_last16(); f.hl_lo = c.h_last16lo();
   f.qkv = c.qkv(); f.op = c.ws + c.lay.fx_op; f.ap = c.ws + c.lay.fx_ap;

@@ -9,6 +9,7 @@
 #include <tuple>
 #include <vector>
 
+#include "kernels.h"
 #include "state.h"
 
 namespace ams {
@@ -63,7 +64,9 @@ struct Ctx {
   std::map<GraphKey, hipGraphExec_t> graphs;
   std::vector<GraphKey> graph_lru;
   std::vector<int32_t> meta_host;  // staging of one call's pass metadata (kept until the next call)
+  std::vector<int32_t> pt_host;    // the page table as last uploaded
 
+  // K/V page pools of layer l; row b's position t sits in page pt()[b * ppr + t / 64]
   void* kslab(int l) const { return ws + lay.kv + (size_t)(2 * l) * lay.slab_layer; }
   void* vslab(int l) const { return ws + lay.kv + (size_t)(2 * l + 1) * lay.slab_layer; }
   float* h() const { return (float*)(ws + lay.h); }
@@ -83,6 +86,8 @@ struct Ctx {
   float2* rope() const { return (float2*)(ws + lay.rope); }
   int32_t* lens() const { return (int32_t*)(ws + lay.lens); }
   int32_t* meta() const { return (int32_t*)(ws + lay.meta); }
+  int32_t* pt() const { return (int32_t*)(ws + lay.pt); }
+  KvPages pages() const { return KvPages{pt(), lay.ppr}; }
 };
 
 // Enqueue-level operations; each returns hipSuccess or the first failure and

@@ -78,13 +78,16 @@ inline ModelLayout model_layout(const Cfg& c) {
 // small device-side tables.
 struct CtxLayout {
   int batch, capacity, pass_tokens, max_splits;
-  size_t slab_layer;  // bytes of K (or V) for one layer
+  int ppr;            // K/V pages per row (capacity / 64)
+  int n_pages;        // pages in each layer's K (and V) pool
+  size_t slab_layer;  // bytes of K (or V) for one layer: n_pages pages of 64 positions
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
   size_t ss;  // decode rows' sums of squares per 256 residual columns [B][d/256]
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
   // attention output and the SwiGLU output, split-K partials, sync words
   size_t fx_hp, fx_op, fx_ap, fx_part, fx_sync;
   size_t meta_ints;
+  size_t pt;  // page table [batch][ppr] int32
 };
 
 inline int default_pass_tokens(int batch, int capacity) {
@@ -200,15 +203,19 @@ inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens
   return S_OK;
 }
 
-inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_tokens) {
+// n_pages: K/V pages per layer pool (0: batch * capacity / 64, a page for every
+// position of every row).
+inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_tokens, int n_pages = 0) {
   CtxLayout x{};
   const size_t es = elem_size(c), d = c.d_model, F = c.d_ffn, L = c.n_layers, B = batch;
   x.batch = batch;
   x.capacity = capacity;
   x.pass_tokens = pass_tokens ? pass_tokens : default_pass_tokens(batch, capacity);
   x.max_splits = capacity / 64;
+  x.ppr = capacity / 64;
+  x.n_pages = n_pages > 0 ? n_pages : batch * x.ppr;
   const size_t T = std::max<size_t>(x.pass_tokens, B);
-  x.slab_layer = B * (size_t)capacity * d * es;
+  x.slab_layer = (size_t)x.n_pages * 64 * d * es;
   size_t o = 0;
   x.kv = o; o = align256(o + 2 * L * x.slab_layer);
   x.h = o; o = align256(o + T * d * 4);
@@ -252,6 +259,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.fx_ap = o; o = align256(o + (fx ? 2 * B * F * 2 : 0));
   x.fx_part = o; o = align256(o + (fx ? fused_part_units(c) * 8 * 16 * 4 : 0));
   x.fx_sync = o; o = align256(o + (fx ? (size_t)(32 * 64 + std::max<size_t>(d / 16, 8 * c.n_heads)) * 4 : 0));
+  x.pt = o; o = align256(o + B * (size_t)x.ppr * 4);
   x.total = o;
   return x;
 }

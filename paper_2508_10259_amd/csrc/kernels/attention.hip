@@ -1,7 +1,10 @@
 // Attention over the cached context.
 //
-// K/V slab of one layer: K and V each [row][head][capacity][head_dim] in the
-// model dtype, so the keys of one (row, head) are one contiguous stream.
+// K/V of one layer: K and V each a pool of pages [page][head][64][head_dim] in
+// the model compute type; row b's position t sits in page pt[b * ppr + t / 64],
+// slot t % 64, so the keys of one (row, head) come in contiguous runs of 64.
+// Every kernel reads or writes keys in blocks that lie within one or two pages
+// and looks their pages up once per block.
 //
 //  * k_kv_append:     new tokens of a pass -> rotate k (RoPE), write k and v
 //                     at their absolute positions.
@@ -29,6 +32,17 @@
 
 namespace ams {
 
+// Element offset of (page, head h, slot) in one layer's K or V pool.
+__device__ __forceinline__ size_t kv_slot(int page, int H, int h, int slot, int dh) {
+  return (((size_t)page * H + h) * KV_PAGE + slot) * dh;
+}
+// Page of row b's position t (t < capacity).
+__device__ __forceinline__ int kv_page(const KvPages& kp, int b, int t) { return kp.pt[(size_t)b * kp.ppr + (t >> 6)]; }
+// The same at a position that is uniform across the wave (a scalar load).
+__device__ __forceinline__ int kv_page_u(const KvPages& kp, int b, int t) {
+  return ld_const_uniform(kp.pt, (size_t)__builtin_amdgcn_readfirstlane(b) * kp.ppr + __builtin_amdgcn_readfirstlane(t >> 6));
+}
+
 __device__ __forceinline__ int find_seg(const int32_t* off, int n_seg, int i) {
   int lo = 0, hi = n_seg - 1;
   while (lo < hi) {
@@ -54,11 +68,12 @@ __device__ __forceinline__ void load8(const f16* p, float* v) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_kv_append(const float* __restrict__ qkv, const int32_t* __restrict__ row,
                                                    const int32_t* __restrict__ pos, const int32_t* __restrict__ off,
-                                                   int n_seg, int H, int dh, int cap, const float2* __restrict__ rope,
+                                                   int n_seg, int H, int dh, KvPages kp, const float2* __restrict__ rope,
                                                    T* __restrict__ kslab, T* __restrict__ vslab) {
   const int i = blockIdx.x;
   const int s = find_seg(off, n_seg, i);
   const int b = row[s], p = pos[s] + (i - off[s]);
+  const int pg = kv_page(kp, b, p);
   const int d = H * dh, half = dh / 2;
   const float* k = qkv + (size_t)i * 3 * d + d;
   const float* v = k + d;
@@ -66,25 +81,25 @@ __global__ __launch_bounds__(256) void k_kv_append(const float* __restrict__ qkv
     const int h = e / half, ii = e % half;
     const float2 cs = rope[(size_t)p * half + ii];
     const float a = k[h * dh + ii], c = k[h * dh + ii + half];
-    T* dst = kslab + (((size_t)b * H + h) * cap + p) * dh;
+    T* dst = kslab + kv_slot(pg, H, h, p & (KV_PAGE - 1), dh);
     st<T>(dst, ii, a * cs.x - c * cs.y);
     st<T>(dst, ii + half, a * cs.y + c * cs.x);
   }
   for (int e = threadIdx.x; e < d; e += blockDim.x) {
     const int h = e / dh, dd = e % dh;
-    st<T>(vslab + (((size_t)b * H + h) * cap + p) * dh, dd, v[e]);
+    st<T>(vslab + kv_slot(pg, H, h, p & (KV_PAGE - 1), dh), dd, v[e]);
   }
 }
 
-hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;
   if (ct == DT_F32)
     hipLaunchKernelGGL(k_kv_append<float>, dim3(sg.n_tok), dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off,
-                       sg.n_seg, H, dh, cap, rope, (float*)kslab, (float*)vslab);
+                       sg.n_seg, H, dh, kp, rope, (float*)kslab, (float*)vslab);
   else
     hipLaunchKernelGGL(k_kv_append<f16>, dim3(sg.n_tok), dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off,
-                       sg.n_seg, H, dh, cap, rope, (f16*)kslab, (f16*)vslab);
+                       sg.n_seg, H, dh, kp, rope, (f16*)kslab, (f16*)vslab);
   return hipGetLastError();
 }
 
@@ -93,7 +108,7 @@ hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, int cap, 
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ qkv, const int32_t* __restrict__ row,
                                                       const int32_t* __restrict__ pos,
-                                                      const int32_t* __restrict__ off, int H, int cap,
+                                                      const int32_t* __restrict__ off, int H, KvPages kp,
                                                       const float2* __restrict__ rope, const T* __restrict__ kslab,
                                                       const T* __restrict__ vslab, T* __restrict__ o, float scale) {
   constexpr int QT = 64, KT = 32, HALF = DH / 2, DPT = DH / 4;
@@ -126,19 +141,18 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   const bool valid = q_lo + qi < n;
   const int qpos = valid ? p0 + q_lo + qi : -1;
   const int kv_end = p0 + (n < q_lo + QT ? n : q_lo + QT);  // exclusive
-  const T* Kb = kslab + ((size_t)b * H + h) * cap * DH;
-  const T* Vb = vslab + ((size_t)b * H + h) * cap * DH;
   float m = -INFINITY, l = 0.f, acc[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) acc[i] = 0.f;
 
   for (int k0 = 0; k0 < kv_end; k0 += KT) {
     __syncthreads();  // Qs ready on the first pass; Ks/Vs/Ps free on later ones
+    const size_t tb = kv_slot(kv_page(kp, b, k0), H, h, k0 & (KV_PAGE - 1), DH);  // the tile lies in one page
     for (int e = tid; e < KT * DH; e += blockDim.x) {
       const int kk = e / DH, dd = e % DH;
       const bool ok = k0 + kk < kv_end;
-      Ks[kk][dd] = ok ? ld<T>(Kb, (size_t)(k0 + kk) * DH + dd) : 0.f;
-      Vs[kk][dd] = ok ? ld<T>(Vb, (size_t)(k0 + kk) * DH + dd) : 0.f;
+      Ks[kk][dd] = ok ? ld<T>(kslab, tb + (size_t)kk * DH + dd) : 0.f;
+      Vs[kk][dd] = ok ? ld<T>(vslab, tb + (size_t)kk * DH + dd) : 0.f;
     }
     __syncthreads();
     float sc[KT / 4];
@@ -203,7 +217,7 @@ template <int DH>
 __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv,
                                                            const int32_t* __restrict__ row,
                                                            const int32_t* __restrict__ pos,
-                                                           const int32_t* __restrict__ off, int H, int cap,
+                                                           const int32_t* __restrict__ off, int H, KvPages kp,
                                                            const float2* __restrict__ rope,
                                                            const f16* __restrict__ kslab,
                                                            const f16* __restrict__ vslab, f16* __restrict__ o,
@@ -259,18 +273,19 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
 #pragma unroll
   for (int j = 0; j < NDJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const f16* Kb = kslab + ((size_t)b * H + h) * cap * DH;
-  const f16* Vb = vslab + ((size_t)b * H + h) * cap * DH;
   f16* Pw = Ps + wave * 16 * PPAD;
   constexpr int CH = DH / 8;  // 16-byte chunks per key row
 
   for (int kt = 0; kt < kv_end; kt += KT) {
     __syncthreads();  // previous tile's Ks / VT / Ps reads are done
+    const size_t tb = kv_slot(kv_page_u(kp, b, kt), H, h, 0, DH);  // a 64-key tile is one page
+    const f16* Kb = kslab + tb;
+    const f16* Vb = vslab + tb;
     for (int c = tid; c < KT * CH; c += 256) {
       const int kk = c / CH, ch = c % CH;
       const bool ok = kt + kk < kv_end;
       *(uint4*)(Ks + kk * KPAD + ch * 8) =
-          ok ? *(const uint4*)(Kb + (size_t)(kt + kk) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+          ok ? *(const uint4*)(Kb + (size_t)kk * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
     }
     // V^T: item c takes keys 4(c & 15) .. +3 of the 16-byte dim chunk c >> 4 and
     // writes, per dim, those 4 keys as one 8-byte word; the 16 lanes of a group
@@ -281,7 +296,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kt + 4 * kq + i;
-        vq[i] = __builtin_bit_cast(half8, key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + ch * 8)
+        vq[i] = __builtin_bit_cast(half8, key < kv_end ? *(const uint4*)(Vb + (size_t)(key - kt) * DH + ch * 8)
                                                        : uint4{0u, 0u, 0u, 0u});
       }
 #pragma unroll
@@ -393,7 +408,7 @@ template <int DH>
 __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* __restrict__ qkv,
                                                                 const int32_t* __restrict__ row,
                                                                 const int32_t* __restrict__ pos,
-                                                                const int32_t* __restrict__ off, int H, int cap,
+                                                                const int32_t* __restrict__ off, int H, KvPages kp,
                                                                 const float2* __restrict__ rope,
                                                                 const f16* __restrict__ kslab,
                                                                 const f16* __restrict__ vslab, f16* __restrict__ o,
@@ -433,8 +448,6 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
 #pragma unroll
   for (int e = 0; e < 4; ++e) qp[e] = 4 * g + e < n ? p0 + 4 * g + e : -1;
 
-  const f16* Kb = kslab + ((size_t)b * H + h) * cap * DH;
-  const f16* Vb = vslab + ((size_t)b * H + h) * cap * DH;
   // this lane's V chunks of a block: keys 4 * vkq .. +3 of the 16-byte dim
   // chunks vq + 8p (p < VPASS)
   const int vkq = lane & 7, vq = lane >> 3;
@@ -442,20 +455,25 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
 
   uint4 kc[2][NQI], vc[VLD];
   auto load = [&](int kb, uint4 (&kx)[2][NQI], uint4 (&vx)[VLD]) __attribute__((always_inline)) {
+    // a block of EXT_KB = 32 keys starts at a multiple of 32 and lies in one page
+    const size_t pb = kv_slot(kv_page_u(kp, b, kb), H, h, 0, DH);
+    const f16* Kb = kslab + pb;
+    const f16* Vb = vslab + pb;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       const int key = kb + 16 * c + r;
       const bool ok = key < kv_end;
 #pragma unroll
       for (int i = 0; i < NQI; ++i)
-        kx[c][i] = ok ? *(const uint4*)(Kb + (size_t)key * DH + 32 * i + 8 * g) : uint4{0u, 0u, 0u, 0u};
+        kx[c][i] = ok ? *(const uint4*)(Kb + (size_t)(key & (KV_PAGE - 1)) * DH + 32 * i + 8 * g)
+                      : uint4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int p = 0; p < VPASS; ++p)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kb + 4 * vkq + i;
-        vx[4 * p + i] = key < kv_end ? *(const uint4*)(Vb + (size_t)key * DH + (vq + 8 * p) * 8)
+        vx[4 * p + i] = key < kv_end ? *(const uint4*)(Vb + (size_t)(key & (KV_PAGE - 1)) * DH + (vq + 8 * p) * 8)
                                      : uint4{0u, 0u, 0u, 0u};
       }
   };
@@ -601,40 +619,40 @@ template <int DH> constexpr size_t ext_lds() {
 }
 
 template <typename T>
-static hipError_t prefill_t(const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope, const void* k,
+static hipError_t prefill_t(const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope, const void* k,
                             const void* v, void* o, hipStream_t s) {
   const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
   const float scale = 1.0f / sqrtf((float)dh);
   if (dh == 64)
-    hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+    hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, kp, rope,
                        (const T*)k, (const T*)v, (T*)o, scale);
   else
-    hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+    hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, kp, rope,
                        (const T*)k, (const T*)v, (T*)o, scale);
   return hipGetLastError();
 }
 
-hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                         const void* kslab, const void* vslab, void* o, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;
-  if (ct == DT_F32) return prefill_t<float>(qkv, sg, H, dh, cap, rope, kslab, vslab, o, s);
+  if (ct == DT_F32) return prefill_t<float>(qkv, sg, H, dh, kp, rope, kslab, vslab, o, s);
   const float scale = 1.0f / sqrtf((float)dh);
   if (sg.max_len <= 16) {  // short segments: keys split over the waves
     const dim3 grid(1, H, sg.n_seg);
     if (dh == 64)
       hipLaunchKernelGGL((k_attn_extend<64>), grid, dim3(64 * EXT_WAVES), ext_lds<64>(), s, qkv, sg.row, sg.pos,
-                         sg.off, H, cap, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
     else
       hipLaunchKernelGGL((k_attn_extend<128>), grid, dim3(64 * EXT_WAVES), ext_lds<128>(), s, qkv, sg.row, sg.pos,
-                         sg.off, H, cap, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
     return hipGetLastError();
   }
   const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
   if (dh == 64)
-    hipLaunchKernelGGL((k_attn_prefill_mfma<64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+    hipLaunchKernelGGL((k_attn_prefill_mfma<64>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, kp, rope,
                        (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
   else
-    hipLaunchKernelGGL((k_attn_prefill_mfma<128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, cap, rope,
+    hipLaunchKernelGGL((k_attn_prefill_mfma<128>), grid, dim3(256), 0, s, qkv, sg.row, sg.pos, sg.off, H, kp, rope,
                        (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
   return hipGetLastError();
 }
@@ -712,7 +730,7 @@ template <int N> __device__ __forceinline__ float cross_sum(float v) {
 
 template <typename T, int DH>
 __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
-    const float* __restrict__ qkv, const int32_t* __restrict__ lens, int jpos, int H, int cap, int splits,
+    const float* __restrict__ qkv, const int32_t* __restrict__ lens, int jpos, int H, KvPages kp, int splits,
     const float2* __restrict__ rope, T* __restrict__ kslab, T* __restrict__ vslab, float* __restrict__ part,
     T* __restrict__ o, T* __restrict__ olo, float scale) {
   using G = DecGeo<T, DH>;
@@ -728,18 +746,21 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
   const int k0 = sp * chunk < T_ ? sp * chunk : T_;
   const int k1 = (k0 + chunk < T_) ? k0 + chunk : T_;
 
-  const size_t bh = ((size_t)b * H + h) * cap;
-  const T* Kb = kslab + bh * DH + i0;
-  const T* Vb = vslab + bh * DH + i0;
   uint4 kr[IT], vr[IT];
-  // one block: key kb + it*KS + ks of each iteration; slot p is not read (its K/V come from registers)
+  // one block: key kb + it*KS + ks of each iteration; slot p is not read (its K/V come from registers).
+  // The block's BK <= 64 keys (kb < k1) lie in at most two pages, looked up once.
   auto load_block = [&](int kb) {
+    // kb is uniform across the wave: the page indices are scalar loads (scalar cache)
+    const int ka = __builtin_amdgcn_readfirstlane(kb >> 6);
+    const int kz = __builtin_amdgcn_readfirstlane(min(kb + BK - 1, k1 - 1) >> 6);
+    const int pa = ld_const_uniform(kp.pt, (size_t)b * kp.ppr + ka), pz = ld_const_uniform(kp.pt, (size_t)b * kp.ppr + kz);
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int key = kb + it * KS + ks;
       const bool ok = key < k1 && key != p;
-      kr[it] = ok ? *(const uint4*)(Kb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
-      vr[it] = ok ? *(const uint4*)(Vb + (size_t)key * DH) : uint4{0u, 0u, 0u, 0u};
+      const size_t e = kv_slot((key >> 6) == ka ? pa : pz, H, h, key & (KV_PAGE - 1), DH) + i0;
+      kr[it] = ok ? *(const uint4*)(kslab + e) : uint4{0u, 0u, 0u, 0u};
+      vr[it] = ok ? *(const uint4*)(vslab + e) : uint4{0u, 0u, 0u, 0u};
     }
   };
   const int kb0 = k0 + wave * BK;
@@ -768,10 +789,12 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
     }
   }
   if (k0 <= p && p < k1 && wave == 0 && ks == 0) {  // the split holding p appends the token
+    const int pg = ld_const_uniform(kp.pt, (size_t)b * kp.ppr + __builtin_amdgcn_readfirstlane(p >> 6));
+    const size_t ep = kv_slot(pg, H, h, p & (KV_PAGE - 1), DH) + i0;
 #pragma unroll
     for (int e = 0; e < CH; ++e) {
-      st<T>(kslab + (bh + p) * DH + i0, e, kn[e]);
-      st<T>(vslab + (bh + p) * DH + i0, e, vn[e]);
+      st<T>(kslab + ep, e, kn[e]);
+      st<T>(vslab + ep, e, vn[e]);
     }
   }
 
@@ -867,7 +890,8 @@ __global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, 
 }
 
 template <typename T>
-static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, int splits,
+static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
+                           int splits,
                            const float2* rope, void* k, void* v, float* part, void* o, void* olo, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)dh);
   const dim3 grid(splits, H, B);
@@ -878,22 +902,22 @@ static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int 
   int nw = (keys + bk - 1) / bk;
   nw = nw < dh / 64 ? dh / 64 : (nw > DECODE_MAX_WAVES ? DECODE_MAX_WAVES : nw);
   if (dh == 64)
-    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, cap, splits, rope,
+    hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
                        (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
   else
-    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, cap, splits, rope,
+    hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
                        (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
   return hipGetLastError();
 }
 
-hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
+hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
                        int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s,
                        void* olo) {
   if (ct == DT_F32) {
     if (olo) return hipErrorInvalidValue;
-    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, nullptr, s);
+    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, nullptr, s);
   }
-  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, splits, rope, kslab, vslab, part, o, olo, s);
+  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, olo, s);
 }
 
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s,

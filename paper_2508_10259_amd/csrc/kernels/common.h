@@ -79,6 +79,14 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// Load of an int that stays constant while the kernel runs (a page-table
+// entry), at a wave-uniform address: read through the constant address space
+// so that it becomes a scalar load served by the scalar cache.
+__device__ __forceinline__ int ld_const_uniform(const int32_t* p, size_t i) {
+  typedef const int32_t __attribute__((address_space(4))) cint;
+  return ((cint*)p)[i];
+}
+
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
 }  // namespace ams

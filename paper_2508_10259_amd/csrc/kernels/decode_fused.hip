@@ -311,7 +311,8 @@ struct FusedArgs {
   int split_a;           // key splits of the attention
   const int32_t* lens;
   const float2* rope;
-  f16* kv; size_t slab;  // K slab of layer l at kv + 2l*slab elements, V at (2l+1)*slab
+  f16* kv; size_t slab;  // K page pool of layer l at kv + 2l*slab elements, V at (2l+1)*slab
+  const int32_t* pt; int ppr;  // row b's position t: page pt[b * ppr + t / 64], slot t % 64
   float* h;              // [M][d] residual stream
   f16* hp;               // [2][M][d] its fp16 pair
   const f16* hl; uint32_t hl_lo;  // pair of the last committed position (hi, lo at +hl_lo bytes)
@@ -484,18 +485,32 @@ __device__ __forceinline__ void key_range(int p, int sp, int S, int& k0, int& k1
   k1 = k0 + ch < T_ ? k0 + ch : T_;
 }
 
-// One block of keys kb + it*KS + ks (it < IT) of a (row, head): K into kv[0..IT),
-// V into kv[IT..2IT); keys >= k1 and the pass's own position p (its K/V come
-// from registers) read zeros.
+// Byte offset of (row b's position t, head h, dimension i0) in a layer's K or V
+// page pool, given t's page.
 template <int DH>
-__device__ __forceinline__ void attn_block(Rsrc kr, Rsrc vr, uint32_t bh, int kb, int k1, int p, uint4 (&kv)[16]) {
+__device__ __forceinline__ uint32_t kv_off(int page, int H, int h, int t, int i0) {
+  return ((((uint32_t)page * H + h) * 64u + (uint32_t)(t & 63)) * DH + i0) * 2u;
+}
+
+// One block of keys kb + it*KS + ks (it < IT) of row b, head h (kb < k1): K into
+// kv[0..IT), V into kv[IT..2IT); keys >= k1 and the pass's own position p (its
+// K/V come from registers) read zeros.  The block's BK <= 64 keys lie in at most
+// two pages, looked up once.
+template <int DH>
+__device__ __forceinline__ void attn_block(const FusedArgs& a, Rsrc kr, Rsrc vr, int b, int h, int kb, int k1, int p,
+                                           uint4 (&kv)[16]) {
   using G = FGeo<DH>;
   const int lane = threadIdx.x & 63, ks = lane / G::NC, i0 = (lane % G::NC) * G::CH;
+  // kb and b are uniform across the wave: the page indices are scalar loads (scalar cache)
+  const size_t r = (size_t)__builtin_amdgcn_readfirstlane(b) * a.ppr;
+  const int ka = __builtin_amdgcn_readfirstlane(kb >> 6);
+  const int kz = __builtin_amdgcn_readfirstlane(min(kb + G::BK - 1, k1 - 1) >> 6);
+  const int pa = ld_const_uniform(a.pt, r + ka), pz = ld_const_uniform(a.pt, r + kz);
 #pragma unroll
   for (int it = 0; it < G::IT; ++it) {
     const int key = kb + it * G::KS + ks;
     const bool ok = key < k1 && key != p;
-    const uint32_t off = ((bh + (uint32_t)key) * DH + i0) * 2u;
+    const uint32_t off = kv_off<DH>((key >> 6) == ka ? pa : pz, a.H, h, key, i0);
     kv[it] = ok ? ldc16(kr, off) : uint4{0u, 0u, 0u, 0u};
     kv[G::IT + it] = ok ? ldc16(vr, off) : uint4{0u, 0u, 0u, 0u};
   }
@@ -513,7 +528,7 @@ __device__ __forceinline__ void prefetch_attn(const FusedArgs& a, int l, int jpo
   if (kb0 >= k1) return;
   const Rsrc kr = rsrc(a.kv + (size_t)(2 * l) * a.slab, (uint32_t)(a.slab * 2));
   const Rsrc vr = rsrc(a.kv + (size_t)(2 * l + 1) * a.slab, (uint32_t)(a.slab * 2));
-  attn_block<DH>(kr, vr, (uint32_t)((b * a.H + h) * a.cap), kb0, k1, p, pf.a);
+  attn_block<DH>(a, kr, vr, b, h, kb0, k1, p, pf.a);
 }
 
 // One query per (row, head) at position p = lens[b] + jpos over keys 0..p, the
@@ -541,10 +556,9 @@ __device__ void phase_attn(const FusedArgs& a, int l, int jpos, FusedSmem& sm, P
     const int p = a.lens[b] + jpos;
     int k0, k1;
     key_range(p, sp, S, k0, k1);
-    const uint32_t bh = (uint32_t)((b * H + h) * a.cap);
     const int kb0 = k0 + wave * BK;
     uint4(&kv)[16] = pf.a;  // the first unit's first block was prefetched into these
-    if (u != (int)blockIdx.x && kb0 < k1) attn_block<DH>(kr_, vr_, bh, kb0, k1, p, kv);
+    if (u != (int)blockIdx.x && kb0 < k1) attn_block<DH>(a, kr_, vr_, b, h, kb0, k1, p, kv);
 
     // this lane's CH dimensions of the rotated, scaled query and of the new key
     // and value, rounded to fp16 as the slab holds them
@@ -581,7 +595,9 @@ __device__ void phase_attn(const FusedArgs& a, int l, int jpos, FusedSmem& sm, P
         kh[e] = (f16)kn[e];
         vh[e] = (f16)vn[e];
       }
-      const uint32_t off = ((bh + (uint32_t)p) * DH + i0) * 2u;
+      const int pg = ld_const_uniform(a.pt, (size_t)__builtin_amdgcn_readfirstlane(b) * a.ppr +
+                                                __builtin_amdgcn_readfirstlane(p >> 6));
+      const uint32_t off = kv_off<DH>(pg, H, h, p, i0);
       stc16(kr_, off, __builtin_bit_cast(uint4, kh));
       stc16(vr_, off, __builtin_bit_cast(uint4, vh));
     }
@@ -590,7 +606,7 @@ __device__ void phase_attn(const FusedArgs& a, int l, int jpos, FusedSmem& sm, P
 #pragma unroll
     for (int e = 0; e < CH; ++e) acc[e] = 0.f;
     for (int kb = kb0; kb < k1; kb += 8 * BK) {
-      if (kb != kb0) attn_block<DH>(kr_, vr_, bh, kb, k1, p, kv);
+      if (kb != kb0) attn_block<DH>(a, kr_, vr_, b, h, kb, k1, p, kv);
       float sc[IT];
       float mx = -INFINITY;
 #pragma unroll
@@ -831,6 +847,7 @@ hipError_t decode_fused(const FusedDecode& f, int grid, hipStream_t s) {
   a.split_o = f.split_o; a.split_d = f.split_d; a.split_a = f.split_a;
   a.lens = f.lens; a.rope = f.rope;
   a.kv = (f16*)f.kv; a.slab = f.slab_elems;
+  a.pt = f.pt; a.ppr = f.ppr;
   a.h = f.h; a.hp = (f16*)f.hp;
   a.hl = (const f16*)f.hl; a.hl_lo = (uint32_t)((const char*)f.hl_lo - (const char*)f.hl);
   a.qkv = f.qkv; a.op = (f16*)f.op; a.ap = (f16*)f.ap;

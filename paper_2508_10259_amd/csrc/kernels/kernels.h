@@ -19,6 +19,16 @@ enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 /* interna
 // Packed-token pass metadata (device arrays).  Segment s covers tokens
 // off[s]..off[s+1]-1 of the pass, which belong to row `row[s]` at positions
 // pos[s], pos[s]+1, ...
+// K/V of a context, per layer: K and V each a pool of pages [page][head][64][head_dim]
+// (model compute type).  Row b's position t sits in page pt[b * ppr + t / 64] at
+// slot t % 64; pt is a device int32 array [rows][ppr].  Rows whose inputs agree
+// up to a page's end may point at the same page.
+constexpr int KV_PAGE = 64;
+struct KvPages {
+  const int32_t* pt;
+  int ppr;  // pages per row (capacity / 64)
+};
+
 struct Segs {
   const int32_t* row;
   const int32_t* pos;
@@ -127,11 +137,11 @@ hipError_t convert(int st, int ct, const void* src, size_t rows, int cols, const
 hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s);
 
 // Rotates the new tokens' keys and writes K/V into the slab of one layer.
-hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, int cap, const float2* rope,
+hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s);
 
 // Causal attention of the pass's tokens over each row's slab (cache + new).
-hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int cap,
+hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp,
                         const float2* rope, const void* kslab, const void* vslab, void* o,
                         hipStream_t s);
 
@@ -141,7 +151,7 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, int ca
 // go to `part` for attn_merge.  olo (fp16 only, or NULL): the rounding error of
 // the fp16 output o, written by whichever of the two kernels writes o.
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh,
-                       int cap, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
+                       int cap, KvPages kp, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
                        hipStream_t s, void* olo = nullptr);
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
                       hipStream_t s, void* olo = nullptr);
@@ -171,6 +181,8 @@ struct FusedDecode {
   const float2* rope;
   void* kv;
   size_t slab_elems;
+  const int32_t* pt;  // page table [M][ppr] of the context's K/V pages
+  int ppr;
   float* h;
   void* hp;
   const void *hl, *hl_lo;

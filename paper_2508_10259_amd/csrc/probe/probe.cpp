@@ -72,23 +72,25 @@ int ams_probe_gemv_rmsnorm(int ct, int epi, const void* hhi, const void* hlo, fl
   return (int)ams::gemv_rmsnorm(ct, epi, hhi, eps, W, M, N, K, out, ldo, (hipStream_t)stream, hlo, o16, olo);
 }
 
-// decode attention of one pass (jpos) for B rows, merged when splits > 1
+// decode attention of one pass (jpos) for B rows, merged when splits > 1; K/V in
+// page pools [page][H][64][dh] with row b's page table at pt + b * (cap / 64)
 int ams_probe_attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
-                          int splits, const void* rope, void* kslab, void* vslab, float* part, void* o, void* olo,
-                          void* stream) {
+                          const int32_t* pt, int splits, const void* rope, void* kslab, void* vslab, float* part,
+                          void* o, void* olo, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = ams::attn_decode(ct, qkv, lens, jpos, B, H, dh, cap, splits, (const float2*)rope, kslab, vslab,
-                                  part, o, s, olo);
+  hipError_t e = ams::attn_decode(ct, qkv, lens, jpos, B, H, dh, cap, ams::KvPages{pt, cap / 64}, splits,
+                                  (const float2*)rope, kslab, vslab, part, o, s, olo);
   if (e == hipSuccess && splits > 1) e = ams::attn_merge(ct, part, B, H, dh, splits, o, s, olo);
   return (int)e;
 }
 
-// Causal attention of packed segments (row[s], pos[s], off[s..s+1]) over their rows' slabs.
+// Causal attention of packed segments (row[s], pos[s], off[s..s+1]) over their rows' K/V pages.
 int ams_probe_attn_prefill(int ct, const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off,
-                           int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const void* rope,
-                           const void* kslab, const void* vslab, void* o, void* stream) {
+                           int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const int32_t* pt,
+                           const void* rope, const void* kslab, const void* vslab, void* o, void* stream) {
   ams::Segs sg{row, pos, off, n_seg, n_tok, max_len, max_end};
-  return (int)ams::attn_prefill(ct, qkv, sg, H, dh, cap, (const float2*)rope, kslab, vslab, o, (hipStream_t)stream);
+  return (int)ams::attn_prefill(ct, qkv, sg, H, dh, ams::KvPages{pt, cap / 64}, (const float2*)rope, kslab, vslab, o,
+                                (hipStream_t)stream);
 }
 
 int ams_probe_stream_copy(const void* src, void* dst, size_t bytes, int grid, void* stream) {

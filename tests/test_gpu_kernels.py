@@ -280,6 +280,27 @@ def _rope_tab(cap, dh, theta=10000.0):
     return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)  # [cap][half][2]
 
 
+def _to_pages(X, perm):
+    """Logical K or V [B][H][cap][dh] -> a page pool [B * cap/64][H][64][dh] in which row b's
+    page i (positions 64i .. 64i+63) sits at pool page perm[b * cap/64 + i]."""
+    B, H, cap, dh = X.shape
+    ppr = cap // 64
+    pool = np.zeros((B * ppr, H, 64, dh), X.dtype)
+    for b in range(B):
+        for i in range(ppr):
+            pool[perm[b * ppr + i]] = X[b, :, 64 * i:64 * (i + 1)]
+    return pool
+
+
+def _from_pages(pool, perm, B, cap):
+    ppr = cap // 64
+    X = np.zeros((B, pool.shape[1], cap, pool.shape[3]), pool.dtype)
+    for b in range(B):
+        for i in range(ppr):
+            X[b, :, 64 * i:64 * (i + 1)] = pool[perm[b * ppr + i]]
+    return X
+
+
 def _round(x, dtype):
     return x.astype(np.float16).astype(np.float64) if dtype == "f16" else x.astype(np.float32).astype(np.float64)
 
@@ -296,7 +317,8 @@ def _round(x, dtype):
 def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     """Decode attention of one fed-back token per row against the plain definition: the
     query and the new key rotated (rotate-half RoPE), the new key and value rounded to the
-    slab type and appended at p = lens[b] + jpos, softmax(K q / sqrt(dh)) V over keys 0..p."""
+    slab type and appended at p = lens[b] + jpos, softmax(K q / sqrt(dh)) V over keys 0..p.
+    The rows' 64-position K/V pages sit in the pool in a random order (page table)."""
     import torch
     B, H = len(lens), 2
     d, half = H * dh, dh // 2
@@ -306,14 +328,18 @@ def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     K = W.random_gaussian((B, H, cap, dh), 32, dh, cap, dtype="f32").astype(np_t)
     V = W.random_gaussian((B, H, cap, dh), 33, dh, cap, dtype="f32").astype(np_t)
     tab = _rope_tab(cap, dh)
-    qkv_d, K_d, V_d = _dev(qkv, dtype), _dev(K, dtype), _dev(V, dtype)
+    # the K/V pages of the rows scattered over the pool in a random order
+    perm = np.random.default_rng(cap + dh).permutation(B * (cap // 64)).astype(np.int32)
+    pt_d = torch.from_numpy(perm).cuda()
+    qkv_d, K_d, V_d = _dev(qkv, dtype), _dev(_to_pages(K, perm), dtype), _dev(_to_pages(V, perm), dtype)
     tab_d = _dev(tab, "f32")
     lens_d = torch.tensor(lens, dtype=torch.int32, device="cuda")
     part = torch.zeros((B * H * (cap // 64) * (dh + 2),), dtype=torch.float32, device="cuda")
     o = torch.zeros((B, d), dtype=torch.float16 if dtype == "f16" else torch.float32, device="cuda")
     olo = torch.zeros((B, d), dtype=torch.float16, device="cuda") if dtype == "f16" else None  # rounding error of o
     rc = probe.ams_probe_attn_decode(CT[dtype], C.c_void_p(qkv_d.data_ptr()), C.c_void_p(lens_d.data_ptr()), jpos,
-                                     B, H, dh, cap, splits, C.c_void_p(tab_d.data_ptr()), C.c_void_p(K_d.data_ptr()),
+                                     B, H, dh, cap, _ptr(pt_d), splits, C.c_void_p(tab_d.data_ptr()),
+                                     C.c_void_p(K_d.data_ptr()),
                                      C.c_void_p(V_d.data_ptr()), C.c_void_p(part.data_ptr()),
                                      C.c_void_p(o.data_ptr()), _ptr(olo), _stream())
     assert rc == 0
@@ -321,7 +347,8 @@ def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     got = o.float().cpu().numpy().astype(np.float64)
     if olo is not None:  # the output as the fp16 pair carries it
         got = got + olo.float().cpu().numpy()
-    K_after, V_after = K_d.cpu().numpy(), V_d.cpu().numpy()
+    K_after = _from_pages(K_d.cpu().numpy(), perm, B, cap)
+    V_after = _from_pages(V_d.cpu().numpy(), perm, B, cap)
     for b in range(B):
         p = lens[b] + jpos
         cs = tab[p].astype(np.float64)  # [half][2]
@@ -375,15 +402,19 @@ def test_attn_prefill(probe, dh, segs):
     V = W.random_gaussian((B, H, cap, dh), 73, dh, dtype="f32").astype(np.float16)
     tab = _rope_tab(cap, dh)
     off = np.cumsum([0] + [n for _, _, n in segs]).astype(np.int32)
+    perm = np.random.default_rng(dh + n_tok).permutation(B * (cap // 64)).astype(np.int32)
+    pt_d = torch.from_numpy(perm).cuda()
     rows = torch.tensor([b for b, _, _ in segs], dtype=torch.int32, device="cuda")
     pos = torch.tensor([p for _, p, _ in segs], dtype=torch.int32, device="cuda")
     offd = torch.from_numpy(off).cuda()
-    qkv_d, K_d, V_d, tab_d = _dev(qkv, "f32"), _dev(K, "f16"), _dev(V, "f16"), _dev(tab, "f32")
+    qkv_d, tab_d = _dev(qkv, "f32"), _dev(tab, "f32")
+    K_d, V_d = _dev(_to_pages(K, perm), "f16"), _dev(_to_pages(V, perm), "f16")
     o = torch.full((n_tok, d), float("nan"), dtype=torch.float16, device="cuda")
     max_len = max(n for _, _, n in segs)
     max_end = max(p + n for _, p, n in segs)
     rc = probe.ams_probe_attn_prefill(CT["f16"], _ptr(qkv_d), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok,
-                                      max_len, max_end, H, dh, cap, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(o),
+                                      max_len, max_end, H, dh, cap, _ptr(pt_d), _ptr(tab_d), _ptr(K_d), _ptr(V_d),
+                                      _ptr(o),
                                       _stream())
     assert rc == 0
     torch.cuda.synchronize()
