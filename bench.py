@@ -331,13 +331,14 @@ def phase_summary(entries, bound, peak):
             "avg_launch_us": round(t / len(entries) * 1e6, 1), "launches": len(entries)}
 
 
-def measure(model, wl, seed, steps, warmup, mode, device_draws):
-    """Warm-up window, then the timed window; returns the workload's figures."""
+def measure(model, wl, seed, steps, warmup, mode, device_draws, share=False):
+    """Warm-up window, then the timed window; returns the workload's figures.  share: a paged
+    context whose rows share prefix pages (the build computes only unshared pages)."""
     import torch
     from paper_2508_10259_amd.runtime import DeviceContext
     spec = wl.spec
     cap = wl.derived_capacity()
-    ctx = DeviceContext(model, wl.batch, cap)
+    ctx = DeviceContext(model, wl.batch, cap, share_prefix=share)
     epochs, pool, rebuild = make_inputs(model, wl, seed, max(steps, warmup), device_draws,
                                         stagger=(mode == "staggered"))
     B, A = wl.batch, wl.n_actions
@@ -346,6 +347,7 @@ def measure(model, wl, seed, steps, warmup, mode, device_draws):
     run_window(ctx, wl, epochs, pool, rebuild, warmup, A, tokens, logits, mode)
     t_win, ph = run_window(ctx, wl, epochs, pool, rebuild, steps, A, tokens, logits, mode)
     persistent = ctx.persistent_decode
+    pages_in_use = ctx.pages()[2] if share else None
     ctx.close()
     del epochs, pool, rebuild
     dec = phase_summary(ph["decode"], "hbm", HBM_PEAK_GBS)
@@ -356,6 +358,7 @@ def measure(model, wl, seed, steps, warmup, mode, device_draws):
     return {"workload": wl.name, "mode": mode, "batch": B, "steps": steps, "capacity": cap,
             "persistent_decode": bool(persistent), "window_s": t_win, "value": B * steps / t_win,
             "ms_per_step": t_win / steps * 1e3, "decode": dec, "extension": ext, "build": bld,
+            "pages_in_use": pages_in_use, "pages_total": wl.batch * (cap // 64),
             "step": {"ms": round(t_win / steps * 1e3, 4), "roofline_ms": round(roof_s / steps * 1e3, 4),
                      "frac": round(roof_s / t_win, 4),
                      "phases_ms": {k: round(sum(e[0] for e in v) / steps * 1e3, 4) for k, v in ph.items()}}}
@@ -373,6 +376,8 @@ def compact(r):
     """The figures of an extra workload."""
     out = {"value": round(r["value"], 2), "unit": "action-steps/s", "ms_per_step": round(r["ms_per_step"], 4),
            "batch": r["batch"], "steps": r["steps"], "mode": r["mode"], "step": r["step"]}
+    if r.get("pages_in_use") is not None:
+        out["pages_in_use"], out["pages_total"] = r["pages_in_use"], r["pages_total"]
     for k in ("decode", "extension", "build"):
         if r[k]:
             out[k] = {kk: r[k][kk] for kk in ("frac", "achieved", "unit", "avg_launch_us")}
@@ -442,14 +447,17 @@ def main():
     if not args.no_extras:
         plan = []
         if spec.name == "7b":
-            plan = [("7b-b1", "cached", 20), ("7b-chunk56-b16", "cached", 8), ("7b-chunk56-b16", "recompute", 8),
-                    ("7b-b64-ragged", "staggered", 20)]
-        for name, mode, n in plan:
+            plan = [("7b-b1", "cached", 20, False), ("7b-chunk56-b16", "cached", 8, False),
+                    ("7b-chunk56-b16", "recompute", 8, False), ("7b-b64-ragged", "staggered", 20, False),
+                    ("7b-b64-shared", "cached", 20, False), ("7b-b64-shared", "cached", 20, True)]
+        for name, mode, n, share in plan:
             if name == wl.name and mode == args.mode:
                 continue
-            print(f"[bench] extra {name} ({mode}, {n} steps)", file=sys.stderr, flush=True)
-            x = measure(model, W.WORKLOADS[name], args.seed, n, 2, mode, big)
-            extras[f"{name}/{mode}" if mode != "cached" else name] = compact(x)
+            print(f"[bench] extra {name} ({mode}, {n} steps{', shared prefix pages' if share else ''})",
+                  file=sys.stderr, flush=True)
+            x = measure(model, W.WORKLOADS[name], args.seed, n, 2, mode, big, share=share)
+            key = (f"{name}/{mode}" if mode != "cached" else name) + ("/shared-pages" if share else "")
+            extras[key] = compact(x)
         if spec.name != "mid":
             model.close()
             print("[bench] extra mid-b8 (cached, 100 steps)", file=sys.stderr, flush=True)

@@ -193,6 +193,46 @@ ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t
                           void* ws, size_t ws_bytes, ams_ctx** out);
 void ams_ctx_destroy(ams_ctx* c); /* NULL is a no-op */
 
+/* Paper section 3.2.3 (Action Compression, Virtual Action): a context whose
+ * K/V live in a pool of pages, each page holding 64 consecutive positions of
+ * one row for every layer and head, with a reference count per page.  With
+ * AMS_CTX_SHARE_PREFIX, building a row computes the page keys of its prefix --
+ * the two-phase hash (ams_index_hash's functions, seg_bytes the largest power of
+ * two <= 4096 dividing d_model * element size) of the row's prefix bytes up to
+ * the end of each full page that does not hold its last token -- and every such
+ * page whose key is already published (by another row, in this call or an
+ * earlier one) is referenced instead of being computed and stored again; the
+ * row computes its K/V from its first unshared page on.  Pages the row computes
+ * are published under their keys.  Invalidating a row drops one reference to
+ * each of its pages; a page whose count reaches zero returns to the pool and
+ * leaves the index.  A build first reads the keys back from the device (it
+ * synchronises `stream`).  Rows hold pages for their whole capacity from the
+ * build on, so a pool smaller than batch * capacity / 64 pages fits the batch
+ * when rows share enough prefix pages; a build that needs more pages than are
+ * free fails with AMS_ECAPACITY and changes nothing.  Results equal an unshared
+ * context's up to rounding (shared pages may come from a pass of other rows). */
+#define AMS_CTX_SHARE_PREFIX 1
+
+/* Bytes of workspace of a paged context: as ams_ctx_workspace_bytes with
+ * n_pages K/V pages per layer pool (0: batch * capacity / 64) and `flags`
+ * (0 or AMS_CTX_SHARE_PREFIX).  0 if an argument is invalid. */
+size_t ams_ctx_workspace_bytes_paged(const ams_model_cfg* cfg, int32_t batch, int32_t capacity,
+                                     int32_t max_pass_tokens, int32_t n_pages, int32_t flags);
+
+/* Creates a paged context (arguments as ams_ctx_create, plus n_pages in
+ * [0, batch * capacity / 64] and flags).  Errors: AMS_EINVAL, AMS_ENOMEM,
+ * AMS_EHIP. */
+ams_status ams_ctx_create_paged(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens,
+                                int32_t n_pages, int32_t flags, void* ws, size_t ws_bytes, ams_ctx** out);
+
+/* The page table (host int32 [batch][capacity / 64]: the pool page of each
+ * row's 64-position block, -1 for a row that holds no pages: never built or
+ * invalidated), the reference count of every pool page (host
+ * int32 [n_pages]) and the number of pages in use; any output may be NULL.
+ * A context created with ams_ctx_create keeps page b * capacity / 64 + i for
+ * row b's block i and reports every page in use. */
+ams_status ams_ctx_pages(const ams_ctx* c, int32_t* page_table, int32_t* refs, int32_t* pages_in_use);
+
 /* Paper section 3.2.1 (Constructing the Action Context): the intermediate
  * state of an inference -- here every layer's K/V of the step-invariant prefix
  * -- is computed once and kept in the context pool for later inferences.

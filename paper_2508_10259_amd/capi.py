@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libams.so")
 
 AMS_OK, AMS_EINVAL, AMS_ESTATE, AMS_ECAPACITY, AMS_ENODEV, AMS_EHIP, AMS_ENOMEM = 0, -1, -2, -3, -4, -5, -6
 AMS_F32, AMS_BF16 = 0, 1
+AMS_CTX_SHARE_PREFIX = 1
 STATE_EMPTY, STATE_READY, STATE_INVALID = 0, 1, 2
 
 
@@ -45,6 +46,11 @@ SIGNATURES = {
     "ams_ctx_create": (C.c_int32, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_size_t,
                                    C.POINTER(C.c_void_p)]),
     "ams_ctx_destroy": (None, [C.c_void_p]),
+    "ams_ctx_workspace_bytes_paged": (C.c_size_t, [C.POINTER(ModelCfg), C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                                   C.c_int32]),
+    "ams_ctx_create_paged": (C.c_int32, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                         C.c_void_p, C.c_size_t, C.POINTER(C.c_void_p)]),
+    "ams_ctx_pages": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(C.c_int32)]),
     "ams_ctx_build": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_void_p]),
     "ams_ctx_step": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p]),

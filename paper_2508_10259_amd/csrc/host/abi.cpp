@@ -5,6 +5,8 @@
 
 #include <string.h>
 
+#include <algorithm>
+
 #include <string>
 #include <vector>
 
@@ -199,13 +201,38 @@ size_t ams_ctx_workspace_bytes(const ams_model_cfg* cfg, int32_t batch, int32_t 
   return ams::ctx_layout(c, batch, capacity, max_pass_tokens).total;
 }
 
-ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens, void* ws,
-                          size_t ws_bytes, ams_ctx** out) {
+static int check_paged(int batch, int capacity, int32_t n_pages, int32_t flags, std::string& e) {
+  if (flags & ~AMS_CTX_SHARE_PREFIX) {
+    e = "unknown context flags";
+    return AMS_EINVAL;
+  }
+  if (n_pages < 0 || (int64_t)n_pages > (int64_t)batch * (capacity / 64)) {
+    e = "n_pages must be in [0, batch * capacity / 64]";
+    return AMS_EINVAL;
+  }
+  return AMS_OK;
+}
+
+size_t ams_ctx_workspace_bytes_paged(const ams_model_cfg* cfg, int32_t batch, int32_t capacity,
+                                     int32_t max_pass_tokens, int32_t n_pages, int32_t flags) {
+  if (!cfg) return 0;
+  std::string e;
+  const ams::Cfg c = to_cfg(*cfg);
+  if (ams::check_cfg(c, e) != ams::S_OK) return 0;
+  if (ams::check_ctx_args(c, batch, capacity, max_pass_tokens, e) != ams::S_OK) return 0;
+  if (check_paged(batch, capacity, n_pages, flags, e) != AMS_OK) return 0;
+  return ams::ctx_layout(c, batch, capacity, max_pass_tokens, n_pages, flags & AMS_CTX_SHARE_PREFIX).total;
+}
+
+static ams_status ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens,
+                             int32_t n_pages, int32_t flags, bool pooled, void* ws, size_t ws_bytes, ams_ctx** out) {
   g_err.clear();
   if (!m || !out) return fail(AMS_EINVAL, "model and out must not be NULL");
   std::string e;
   if (int s = ams::check_ctx_args(m->m.cfg, batch, capacity, max_pass_tokens, e)) return fail(s, e);
-  const ams::CtxLayout lay = ams::ctx_layout(m->m.cfg, batch, capacity, max_pass_tokens);
+  if (int s = check_paged(batch, capacity, n_pages, flags, e)) return fail(s, e);
+  const ams::CtxLayout lay =
+      ams::ctx_layout(m->m.cfg, batch, capacity, max_pass_tokens, n_pages, flags & AMS_CTX_SHARE_PREFIX);
   if (!ws) return fail(AMS_EINVAL, "workspace is NULL");
   if (!aligned256(ws)) return fail(AMS_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < lay.total) return fail(AMS_ENOMEM, "context workspace too small: need " + std::to_string(lay.total));
@@ -214,6 +241,7 @@ ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t
   c->c.model = &m->m;
   c->c.lay = lay;
   c->c.ws = (char*)ws;
+  c->c.pooled = pooled;
   c->c.book.init(batch, capacity);
   if (ams::ctx_init(c->c, e) != hipSuccess) {
     ams::ctx_release(c->c);
@@ -222,6 +250,30 @@ ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t
   }
   m->m.live_ctx++;
   *out = c;
+  return AMS_OK;
+}
+
+ams_status ams_ctx_create(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens, void* ws,
+                          size_t ws_bytes, ams_ctx** out) {
+  return ctx_create(m, batch, capacity, max_pass_tokens, 0, 0, false, ws, ws_bytes, out);
+}
+
+ams_status ams_ctx_create_paged(ams_model* m, int32_t batch, int32_t capacity, int32_t max_pass_tokens,
+                                int32_t n_pages, int32_t flags, void* ws, size_t ws_bytes, ams_ctx** out) {
+  return ctx_create(m, batch, capacity, max_pass_tokens, n_pages, flags, true, ws, ws_bytes, out);
+}
+
+ams_status ams_ctx_pages(const ams_ctx* c, int32_t* page_table, int32_t* refs, int32_t* pages_in_use) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  const ams::Ctx& x = c->c;
+  if (page_table) std::copy(x.pt_host.begin(), x.pt_host.end(), page_table);
+  if (refs) {
+    if (x.pooled) std::copy(x.pool.refs.begin(), x.pool.refs.end(), refs);
+    else
+      for (int p = 0; p < x.lay.n_pages; ++p) refs[p] = 1;
+  }
+  if (pages_in_use) *pages_in_use = x.pooled ? x.pool.in_use() : x.lay.n_pages;
   return AMS_OK;
 }
 
@@ -246,10 +298,15 @@ ams_status ams_ctx_build(ams_ctx* c, const void* prefix, const int32_t* lens, vo
   const ams::Cfg& m = x.model->cfg;
   if (!dev_range(prefix, tot * m.d_model * ams::elem_size(m), x.model->device, "prefix", e))
     return fail(AMS_EINVAL, e);
-  std::vector<int32_t> start(x.lay.batch, 0);
-  if (ams::ctx_forward_tokens(x, prefix, lens, start.data(), 1, (hipStream_t)stream, e) != hipSuccess) {
-    x.book.invalidate();
-    return fail(AMS_EHIP, e);
+  if (x.lay.share && ((uintptr_t)prefix & 15) != 0) return fail(AMS_EINVAL, "prefix must be 16-byte aligned");
+  std::vector<int32_t> rows(x.lay.batch);
+  for (int b = 0; b < x.lay.batch; ++b) rows[b] = b;
+  if (int s = ams::ctx_build_rows(x, prefix, rows.data(), x.lay.batch, lens, (hipStream_t)stream, e)) {
+    if (s == AMS_EHIP) {
+      x.book.invalidate();
+      ams::ctx_release_rows(x, rows.data(), x.lay.batch);
+    }
+    return fail(s, e);
   }
   x.book.commit_build(lens);
   return AMS_OK;
@@ -303,12 +360,15 @@ ams_status ams_ctx_build_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, c
   const ams::Cfg& m = x.model->cfg;
   if (!dev_range(prefix, tot * m.d_model * ams::elem_size(m), x.model->device, "prefix", e))
     return fail(AMS_EINVAL, e);
-  const int B = x.lay.batch;
-  std::vector<int32_t> counts(B, 0), start(B, 0);
-  for (int i = 0; i < n_rows; ++i) counts[rows[i]] = lens[i];
-  if (ams::ctx_forward_tokens(x, prefix, counts.data(), start.data(), 1, (hipStream_t)stream, e) != hipSuccess) {
-    x.book.invalidate();
-    return fail(AMS_EHIP, e);
+  if (x.lay.share && ((uintptr_t)prefix & 15) != 0) return fail(AMS_EINVAL, "prefix must be 16-byte aligned");
+  if (int s = ams::ctx_build_rows(x, prefix, rows, n_rows, lens, (hipStream_t)stream, e)) {
+    if (s == AMS_EHIP) {
+      x.book.invalidate();
+      std::vector<int32_t> all(x.lay.batch);
+      for (int b = 0; b < x.lay.batch; ++b) all[b] = b;
+      ams::ctx_release_rows(x, all.data(), x.lay.batch);
+    }
+    return fail(s, e);
   }
   x.book.commit_build_rows(rows, n_rows, lens);
   return AMS_OK;
@@ -341,6 +401,7 @@ ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_ro
   std::string e;
   if (int s = c->c.book.check_rows(rows, n_rows, e)) return fail(s, e);
   c->c.book.invalidate_rows(rows, n_rows);
+  ams::ctx_release_rows(c->c, rows, n_rows);
   return AMS_OK;
 }
 
@@ -405,6 +466,9 @@ ams_status ams_ctx_invalidate(ams_ctx* c) {
   g_err.clear();
   if (!c) return fail(AMS_EINVAL, "context is NULL");
   c->c.book.invalidate();
+  std::vector<int32_t> all(c->c.lay.batch);
+  for (int b = 0; b < c->c.lay.batch; ++b) all[b] = b;
+  ams::ctx_release_rows(c->c, all.data(), c->c.lay.batch);
   return AMS_OK;
 }
 

@@ -84,6 +84,13 @@ hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::s
   return hipSuccess;
 }
 
+// The page table to the device, rows without pages pointing at page 0.
+static hipError_t upload_pages(Ctx& c, hipStream_t s) {
+  c.pt_dev_host.resize(c.pt_host.size());
+  for (size_t i = 0; i < c.pt_host.size(); ++i) c.pt_dev_host[i] = c.pt_host[i] < 0 ? 0 : c.pt_host[i];
+  return hipMemcpyAsync(c.pt(), c.pt_dev_host.data(), c.pt_dev_host.size() * 4, hipMemcpyHostToDevice, s);
+}
+
 hipError_t ctx_init(Ctx& c, std::string& err) {
   const Cfg& m = c.model->cfg;
   TRY(hipStreamCreateWithFlags(&c.capture_stream, hipStreamNonBlocking));
@@ -96,10 +103,13 @@ hipError_t ctx_init(Ctx& c, std::string& err) {
   TRY(rope_table(c.rope(), c.lay.capacity, m.head_dim, m.rope_theta, s));
   TRY(hipMemsetAsync(c.ws + c.lay.h_last, 0, c.lay.part - c.lay.h_last, s));
   TRY(hipMemsetAsync(c.ws + c.lay.lens, 0, c.lay.total - c.lay.lens, s));
-  // every row owns the pages of all its positions: row b's page i is b * ppr + i
-  c.pt_host.resize((size_t)c.lay.batch * c.lay.ppr);
-  for (size_t i = 0; i < c.pt_host.size(); ++i) c.pt_host[i] = (int32_t)i;
-  TRY(hipMemcpyAsync(c.pt(), c.pt_host.data(), c.pt_host.size() * 4, hipMemcpyHostToDevice, s));
+  // fixed pages: row b's page i is b * ppr + i; pooled: no row holds a page yet
+  // (-1 on the host; the device table holds page 0 there, never read before a build)
+  c.pt_host.assign((size_t)c.lay.batch * c.lay.ppr, -1);
+  if (c.pooled) c.pool.init(c.lay.n_pages);
+  else
+    for (size_t i = 0; i < c.pt_host.size(); ++i) c.pt_host[i] = (int32_t)i;
+  TRY(upload_pages(c, s));
   TRY(hipStreamSynchronize(s));
   c.splits = decode_splits(c.lay.batch, m.n_heads, c.lay.capacity);
   c.meta_host.assign(c.lay.meta_ints, 0);
@@ -122,6 +132,75 @@ void ctx_release(Ctx& c) {
   if (c.status_host) hipHostFree((void*)c.status_host);
   c.status_host = nullptr;
   c.status_dev = nullptr;
+}
+
+void ctx_release_rows(Ctx& c, const int32_t* rows, int n_rows) {
+  if (!c.pooled) return;
+  // the released rows' entries become -1 on the host; the device keeps the stale
+  // ones, which no kernel reads before those rows are rebuilt
+  release_row_pages(c.pool, c.pt_host, c.lay.ppr, rows, n_rows);
+}
+
+int ctx_build_rows(Ctx& c, const void* prefix, const int32_t* rows, int n_rows, const int32_t* lens, hipStream_t s,
+                   std::string& err) {
+  const Cfg& m = c.model->cfg;
+  const int B = c.lay.batch, ppr = c.lay.ppr;
+  const size_t tb = (size_t)m.d_model * elem_size(m);
+  std::vector<int32_t> counts(B, 0), start(B, 0), src(B, 0), lens_set(B, 0);
+  if (!c.pooled) {
+    for (int i = 0; i < n_rows; ++i) counts[rows[i]] = lens_set[rows[i]] = lens[i];
+    return ctx_forward_tokens(c, prefix, counts.data(), start.data(), 1, s, err) == hipSuccess ? (int)S_OK
+                                                                                                : (int)S_EHIP;
+  }
+  std::vector<int32_t> share(n_rows, 0), first(n_rows, 0);
+  size_t tok = 0;
+  for (int i = 0; i < n_rows; ++i) {
+    first[i] = (int32_t)tok;
+    tok += lens[i];
+    share[i] = c.lay.share ? shareable_pages(lens[i]) : 0;
+  }
+  c.keys_host.assign((size_t)n_rows * ppr, 0);
+  if (c.lay.share) {  // page keys: Algorithm 1 over each row's input bytes up to every page end
+    const int sg = c.lay.key_seg;
+    const size_t nseg = tok * tb / sg;
+    uint64_t* seg = (uint64_t*)(c.ws + c.lay.hk_seg);
+    uint64_t* keys = (uint64_t*)(c.ws + c.lay.hk_keys);
+    int64_t* hk = (int64_t*)(c.ws + c.lay.hk_rows);
+    c.hk_rows_host.assign(2 * (size_t)n_rows, 0);
+    for (int i = 0; i < n_rows; ++i) {
+      c.hk_rows_host[i] = (int64_t)first[i] * (int64_t)(tb / sg);
+      c.hk_rows_host[n_rows + i] = (int64_t)lens[i] * (int64_t)tb;
+    }
+    if (hash_segments(prefix, tok * tb, sg, seg, s) != hipSuccess ||
+        hipMemcpyAsync(hk, c.hk_rows_host.data(), c.hk_rows_host.size() * 8, hipMemcpyHostToDevice, s) !=
+            hipSuccess ||
+        hash_page_keys(seg, hk, hk + n_rows, n_rows, (int64_t)64 * tb, sg, ppr, keys, s) != hipSuccess ||
+        hipMemcpyAsync(c.keys_host.data(), keys, c.keys_host.size() * 8, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) {
+      err = "page keys of the prefix failed";
+      return S_EHIP;
+    }
+    (void)nseg;
+  }
+  std::vector<int32_t> st;
+  if (int r = plan_row_pages(c.pool, c.pt_host, ppr, rows, n_rows, share.data(), c.keys_host.data(), ppr,
+                             c.lay.share, st, err))
+    return r;
+  if (upload_pages(c, s) != hipSuccess) {
+    err = "page table upload failed";
+    return S_EHIP;
+  }
+  for (int i = 0; i < n_rows; ++i) {
+    const int b = rows[i];
+    start[b] = st[i];
+    counts[b] = lens[i] - st[i];
+    src[b] = first[i] + st[i];
+    lens_set[b] = lens[i];
+  }
+  return ctx_forward_tokens(c, prefix, counts.data(), start.data(), 1, s, err, src.data(), lens_set.data()) ==
+                 hipSuccess
+             ? (int)S_OK
+             : (int)S_EHIP;
 }
 
 int ctx_absorb_status(Ctx& c, std::string& err) {
@@ -164,25 +243,30 @@ static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t
 }
 
 hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, const int32_t* start, int set_lens,
-                              hipStream_t s, std::string& err) {
+                              hipStream_t s, std::string& err, const int32_t* src, const int32_t* lens_set) {
   const Cfg& m = c.model->cfg;
   const int B = c.lay.batch;
   const size_t es = elem_size(m), d = m.d_model;
   Plan p = plan_passes(B, counts, start, c.lay.pass_tokens);
-  // meta layout: row[B] pos[B] off[2B+1] lensv[B]
+  // meta layout: row[B] pos[B] off[2B+1] lensv[B] src[B] (src per segment: its first input token)
   std::vector<int32_t>& h = c.meta_host;
   std::fill(h.begin(), h.end(), 0);
   std::copy(p.row.begin(), p.row.end(), h.begin());
   std::copy(p.pos.begin(), p.pos.end(), h.begin() + B);
   std::copy(p.off.begin(), p.off.end(), h.begin() + 2 * B);
-  for (int b = 0; b < B; ++b) h[4 * B + 1 + b] = counts[b];
+  for (int b = 0; b < B; ++b) h[4 * B + 1 + b] = lens_set ? lens_set[b] : counts[b];
+  if (src)
+    for (size_t i = 0; i < p.row.size(); ++i) h[5 * B + 1 + i] = src[p.row[i]];
   int32_t* md = c.meta();
   TRY(hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
   for (size_t pi = 0; pi < p.passes.size(); ++pi) {
     const Pass& ps = p.passes[pi];
     Segs sg{md + ps.seg_begin, md + B + ps.seg_begin, md + 2 * B + ps.seg_begin + (int)pi, ps.n_seg, ps.n_tok,
             ps.max_len, ps.max_end};
-    TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
+    if (src)  // the rows' tokens to process start at their own places in x
+      TRY(ingest_segs(c.model->st, x, sg, md + 5 * B + 1 + ps.seg_begin, (int)d, c.h(), s));
+    else
+      TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
     for (int l = 0; l < m.n_layers; ++l)
       if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
     const bool f16 = c.model->ct == DT_F16;  // the fp16 pair of h_last feeds fused-RMSNorm heads

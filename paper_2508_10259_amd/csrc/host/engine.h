@@ -64,7 +64,15 @@ struct Ctx {
   std::map<GraphKey, hipGraphExec_t> graphs;
   std::vector<GraphKey> graph_lru;
   std::vector<int32_t> meta_host;  // staging of one call's pass metadata (kept until the next call)
-  std::vector<int32_t> pt_host;    // the page table as last uploaded
+  std::vector<int32_t> pt_host;      // the page table (-1: no page)
+  std::vector<int32_t> pt_dev_host;  // staging of its last upload
+  // pooled pages (created with a page count or prefix sharing): rows take pages
+  // from `pool` when built and return them when invalidated; otherwise row b
+  // keeps pages b * ppr .. b * ppr + ppr - 1 for the context's life
+  bool pooled = false;
+  PagePool pool;
+  std::vector<uint64_t> keys_host;
+  std::vector<int64_t> hk_rows_host;
 
   // K/V page pools of layer l; row b's position t sits in page pt()[b * ppr + t / 64]
   void* kslab(int l) const { return ws + lay.kv + (size_t)(2 * l) * lay.slab_layer; }
@@ -94,11 +102,28 @@ struct Ctx {
 // fills `err`.
 hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::string& err);
 hipError_t ctx_init(Ctx& c, std::string& err);
+// Runs every layer over counts[b] tokens of each row b at positions start[b]..;
+// the tokens come from x packed row after row in row order, or, with src, from
+// input tokens src[b].. of x.  Lengths afterwards: lens[b] += counts[b], or, with
+// set_lens, lens[b] = lens_set[b] (counts[b] when lens_set is NULL) for the rows
+// with counts[b] > 0.
 hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, const int32_t* start, int set_lens,
-                              hipStream_t s, std::string& err);
+                              hipStream_t s, std::string& err, const int32_t* src = nullptr,
+                              const int32_t* lens_set = nullptr);
 hipError_t ctx_decode(Ctx& c, int n_actions, int32_t* out_tokens, float* out_logits, const int32_t* forced,
                       hipStream_t s, std::string& err);
 void ctx_release(Ctx& c);
+// Builds the listed rows (strictly increasing; lens[i] tokens each, packed in
+// order in `prefix`): pages first (the pool's shared prefix pages when the
+// context shares them -- their keys hashed on the device and read back, the
+// only synchronisation), then the forward passes over each row's tokens from
+// its first unshared page on.  S_OK, S_ECAPACITY (no free page; nothing
+// changed) or S_EHIP.
+int ctx_build_rows(Ctx& c, const void* prefix, const int32_t* rows, int n_rows, const int32_t* lens, hipStream_t s,
+                   std::string& err);
+// Returns the listed rows' pages to the pool (pooled contexts; host only).
+void ctx_release_rows(Ctx& c, const int32_t* rows, int n_rows);
+
 // Takes in an error a kernel of an earlier call reported asynchronously (see
 // RowBook::absorb_async_error) and clears the word.
 int ctx_absorb_status(Ctx& c, std::string& err);

@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <cmath>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "fused_limits.h"
@@ -27,6 +28,15 @@ struct Cfg {
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Segment size of the page keys: the largest power of two <= 4096 dividing the
+// bytes of one token's input, so that rows and pages start on segment bounds.
+inline int page_key_segment(size_t token_bytes) {
+  int s = 4096;
+  while (s > 16 && token_bytes % s) s >>= 1;
+  return s;
+}
+
 
 inline int check_cfg(const Cfg& c, std::string& err) {
   auto bad = [&](const char* m) { err = m; return (int)S_EINVAL; };
@@ -88,6 +98,11 @@ struct CtxLayout {
   size_t fx_hp, fx_op, fx_ap, fx_part, fx_sync;
   size_t meta_ints;
   size_t pt;  // page table [batch][ppr] int32
+  // shared prefix pages: segment hashes of a build's input, page keys [batch][ppr]
+  // and per-row [segment offset, input bytes] (int64) of the hashed rows
+  bool share;
+  int key_seg;  // segment size of the page keys (bytes)
+  size_t hk_seg, hk_keys, hk_rows;
 };
 
 inline int default_pass_tokens(int batch, int capacity) {
@@ -204,8 +219,9 @@ inline int check_ctx_args(const Cfg& c, int batch, int capacity, int pass_tokens
 }
 
 // n_pages: K/V pages per layer pool (0: batch * capacity / 64, a page for every
-// position of every row).
-inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_tokens, int n_pages = 0) {
+// position of every row); share: rows may share prefix pages (hash scratch).
+inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_tokens, int n_pages = 0,
+                            bool share = false) {
   CtxLayout x{};
   const size_t es = elem_size(c), d = c.d_model, F = c.d_ffn, L = c.n_layers, B = batch;
   x.batch = batch;
@@ -250,8 +266,8 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.ss = o; o = align256(o + B * (size_t)(d / 256 + 1) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
   x.lens = o; o = align256(o + B * 4);
-  // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B]
-  x.meta_ints = 5 * B + 1;
+  // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B], src[B]
+  x.meta_ints = 6 * B + 1;
   x.meta = o; o = align256(o + x.meta_ints * 4);
   const bool fx = batch <= FUSED_MAX_ROWS && es == 2;
   x.fx_hp = o; o = align256(o + (fx ? 2 * B * d * 2 : 0));
@@ -260,6 +276,12 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.fx_part = o; o = align256(o + (fx ? fused_part_units(c) * 8 * 16 * 4 : 0));
   x.fx_sync = o; o = align256(o + (fx ? (size_t)(32 * 64 + std::max<size_t>(d / 16, 8 * c.n_heads)) * 4 : 0));
   x.pt = o; o = align256(o + B * (size_t)x.ppr * 4);
+  x.share = share;
+  x.key_seg = page_key_segment(d * es);
+  const size_t max_segs = share ? B * (size_t)capacity * (d * es / x.key_seg) : 0;
+  x.hk_seg = o; o = align256(o + max_segs * 8);
+  x.hk_keys = o; o = align256(o + (share ? B * (size_t)x.ppr * 8 : 0));
+  x.hk_rows = o; o = align256(o + (share ? 2 * B * 8 : 0));
   x.total = o;
   return x;
 }
@@ -401,6 +423,127 @@ struct RowBook {
     return S_EHIP;
   }
 };
+
+// ---------------------------------------------------------------------------
+// K/V page pool with shared prefix pages (paper section 3.2.3, Virtual Action):
+// every page of a context has a reference count; a page holding a row's input
+// up to its end can be published under its key (the two-phase hash of that
+// input prefix, Algorithm 1), and a later row whose input agrees up to the same
+// page end references that page instead of computing and storing its own.
+// Attaching increments the count, invalidating a row decrements the counts of
+// its pages, and a page whose count reaches zero leaves the index and returns
+// to the free list.
+
+struct PagePool {
+  std::vector<int32_t> refs;
+  std::vector<uint64_t> key;        // published key of a page (valid when indexed[p])
+  std::vector<uint8_t> indexed;
+  std::vector<int32_t> free_pages;  // stack; the lowest free page on top
+  std::unordered_map<uint64_t, int32_t> index;
+
+  void init(int n) {
+    refs.assign(n, 0);
+    key.assign(n, 0);
+    indexed.assign(n, 0);
+    free_pages.resize(n);
+    for (int i = 0; i < n; ++i) free_pages[i] = n - 1 - i;
+    index.clear();
+  }
+  int n_pages() const { return (int)refs.size(); }
+  int in_use() const { return n_pages() - (int)free_pages.size(); }
+  int alloc() {  // a fresh page with one reference, -1 when none is free
+    if (free_pages.empty()) return -1;
+    const int p = free_pages.back();
+    free_pages.pop_back();
+    refs[p] = 1;
+    return p;
+  }
+  void retain(int p) { ++refs[p]; }
+  void release(int p) {
+    if (p < 0 || refs[p] <= 0) return;
+    if (--refs[p] == 0) {
+      if (indexed[p]) {
+        auto it = index.find(key[p]);
+        if (it != index.end() && it->second == p) index.erase(it);
+        indexed[p] = 0;
+      }
+      free_pages.push_back(p);
+    }
+  }
+  int lookup(uint64_t k) const {
+    auto it = index.find(k);
+    return it == index.end() ? -1 : it->second;
+  }
+  void publish(int p, uint64_t k) {
+    key[p] = k;
+    indexed[p] = 1;
+    index[k] = p;
+  }
+};
+
+// Pages of rows about to be built.  Each listed row (in order) first releases
+// the pages it held, then takes, for its leading full pages that do not hold its
+// last token (i < share[i_row], keys[i_row][i]), the published page of the same
+// key when there is one (the row starts computing after the run of pages it
+// could attach), else a fresh page that it publishes; its remaining ppr pages
+// are fresh.  Writes the rows' page-table rows into pt ([batch][ppr]) and the
+// first position each row computes into start[i_row].  Fails with S_ECAPACITY,
+// pool and pt unchanged, when the pool runs out of free pages.
+inline int plan_row_pages(PagePool& pool, std::vector<int32_t>& pt, int ppr, const int32_t* rows, int n_rows,
+                          const int32_t* share, const uint64_t* keys, int keys_stride, bool sharing,
+                          std::vector<int32_t>& start, std::string& err) {
+  PagePool saved = pool;
+  std::vector<int32_t> saved_pt = pt;
+  for (int i = 0; i < n_rows; ++i)
+    for (int j = 0; j < ppr; ++j) {
+      int32_t& e = pt[(size_t)rows[i] * ppr + j];
+      if (e >= 0) pool.release(e);
+      e = -1;
+    }
+  start.assign(n_rows, 0);
+  for (int i = 0; i < n_rows; ++i) {
+    int32_t* row = &pt[(size_t)rows[i] * ppr];
+    int attached = 0;
+    for (int j = 0; j < ppr; ++j) {
+      const bool shareable = sharing && j < share[i];
+      if (shareable && j == attached) {
+        const uint64_t k = keys[(size_t)i * keys_stride + j];
+        const int p = pool.lookup(k);
+        if (p >= 0) {
+          pool.retain(p);
+          row[j] = p;
+          ++attached;
+          continue;
+        }
+      }
+      const int p = pool.alloc();
+      if (p < 0) {
+        pool = saved;
+        pt = saved_pt;
+        err = "the context's K/V page pool has no free page left (row " + std::to_string(rows[i]) + ")";
+        return S_ECAPACITY;
+      }
+      row[j] = p;
+      if (shareable) pool.publish(p, keys[(size_t)i * keys_stride + j]);
+    }
+    start[i] = attached * 64;
+  }
+  return S_OK;
+}
+
+// Releases the pages of the listed rows (their page-table entries become -1).
+inline void release_row_pages(PagePool& pool, std::vector<int32_t>& pt, int ppr, const int32_t* rows, int n_rows) {
+  for (int i = 0; i < n_rows; ++i)
+    for (int j = 0; j < ppr; ++j) {
+      int32_t& e = pt[(size_t)rows[i] * ppr + j];
+      if (e >= 0) pool.release(e);
+      e = -1;
+    }
+}
+
+// Pages of a row that may be shared: the full 64-position pages before the one
+// holding its last token (that token's hidden state must be computed).
+inline int shareable_pages(int len) { return (len - 1) / 64; }
 
 // ---------------------------------------------------------------------------
 // pass planner: rows with pending tokens, packed in row order into passes of

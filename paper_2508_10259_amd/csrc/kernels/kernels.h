@@ -121,6 +121,9 @@ hipError_t embed_rows(int st, const void* E, const int32_t* ids, int n, int d, i
 
 // h[i] = float(x[i]) for n rows of d (x in the storage type).
 hipError_t ingest(int st, const void* x, int n, int d, float* h, hipStream_t s);
+// The same per segment of a pass: its tokens come from input tokens src[s] ..
+// (device array, one entry per segment of sg).
+hipError_t ingest_segs(int st, const void* x, Segs sg, const int32_t* src, int d, float* h, hipStream_t s);
 
 // Gate/up interleave of one layer: dst [2F][d] (compute type) from gate [F][d]
 // and up [F][d] (storage type), each column k scaled by gain[k] (the RMSNorm

@@ -85,6 +85,33 @@ __global__ __launch_bounds__(256) void k_ingest(const T* __restrict__ x, size_t 
     h[i] = ld<T>(x, i);
 }
 
+// Token i of a pass belongs to segment s (off[s] <= i < off[s+1]) and comes from
+// input token src[s] + (i - off[s]).
+template <typename T>
+__global__ __launch_bounds__(256) void k_ingest_segs(const T* __restrict__ x, const int32_t* __restrict__ off,
+                                                     const int32_t* __restrict__ src, int n_seg, int d,
+                                                     float* __restrict__ h) {
+  const int i = blockIdx.x;
+  int lo = 0, hi = n_seg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  const size_t from = (size_t)(src[lo] + (i - off[lo])) * d, to = (size_t)i * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) h[to + e] = ld<T>(x, from + e);
+}
+
+hipError_t ingest_segs(int st, const void* x, Segs sg, const int32_t* src, int d, float* h, hipStream_t s) {
+  if (sg.n_tok <= 0) return hipSuccess;
+  if (st == DT_F32)
+    hipLaunchKernelGGL(k_ingest_segs<float>, dim3(sg.n_tok), dim3(256), 0, s, (const float*)x, sg.off, src, sg.n_seg,
+                       d, h);
+  else
+    hipLaunchKernelGGL(k_ingest_segs<bf16>, dim3(sg.n_tok), dim3(256), 0, s, (const bf16*)x, sg.off, src, sg.n_seg,
+                       d, h);
+  return hipGetLastError();
+}
+
 hipError_t ingest(int st, const void* x, int n, int d, float* h, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const size_t tot = (size_t)n * d;

@@ -112,13 +112,14 @@ class DeviceModel:
         out = torch.empty((sum(lens), spec.d_model), dtype=torch_dtype(spec.dtype), device=self.device)
         o = 0
         for p in prefixes:
-            n_p = p.patches.shape[0]
+            n_p, n_t = p.patches.shape[0], len(p.text_ids)
+            po, to = (o + n_t, o) if p.text_first else (o, o + n_p)
             if n_p:
                 src = p.patches if isinstance(p.patches, torch.Tensor) else to_device(p.patches, spec.dtype, self.device)
-                out[o:o + n_p].copy_(src)
-            if len(p.text_ids):
+                out[po:po + n_p].copy_(src)
+            if n_t:
                 ids = torch.from_numpy(p.text_ids.astype(np.int32)).to(self.device)
-                self.embed_ids(ids, out[o + n_p:o + p.length])
+                self.embed_ids(ids, out[to:to + n_t])
             o += p.length
         return out, lens
 
@@ -137,15 +138,30 @@ class DeviceModel:
 class DeviceContext:
     """Per-row cached context: K/V slab + activations in one workspace."""
 
-    def __init__(self, model: DeviceModel, batch: int, capacity: int, max_pass_tokens: int = 0):
+    def __init__(self, model: DeviceModel, batch: int, capacity: int, max_pass_tokens: int = 0,
+                 n_pages: Optional[int] = None, share_prefix: bool = False):
+        """n_pages / share_prefix: a paged context (ams_ctx_create_paged) with that many K/V pages per
+        layer (0: a page for every position) whose rows share prefix pages when share_prefix."""
         self.lib, self.model, self.batch, self.capacity = model.lib, model, batch, capacity
-        nbytes = self.lib.ams_ctx_workspace_bytes(C.byref(model.cfg), batch, capacity, max_pass_tokens)
+        paged = n_pages is not None or share_prefix
+        flags = capi.AMS_CTX_SHARE_PREFIX if share_prefix else 0
+        if paged:
+            nbytes = self.lib.ams_ctx_workspace_bytes_paged(C.byref(model.cfg), batch, capacity, max_pass_tokens,
+                                                            n_pages or 0, flags)
+        else:
+            nbytes = self.lib.ams_ctx_workspace_bytes(C.byref(model.cfg), batch, capacity, max_pass_tokens)
         if nbytes == 0:
             raise ValueError("invalid context arguments")
         self.ws = torch.empty(nbytes, dtype=torch.uint8, device=model.device)
+        self.n_pages = n_pages or batch * (capacity // 64)
         h = C.c_void_p()
-        capi.check(self.lib.ams_ctx_create(model.handle, batch, capacity, max_pass_tokens, self.ws.data_ptr(),
-                                           nbytes, C.byref(h)), "ams_ctx_create")
+        if paged:
+            capi.check(self.lib.ams_ctx_create_paged(model.handle, batch, capacity, max_pass_tokens, n_pages or 0,
+                                                     flags, self.ws.data_ptr(), nbytes, C.byref(h)),
+                       "ams_ctx_create_paged")
+        else:
+            capi.check(self.lib.ams_ctx_create(model.handle, batch, capacity, max_pass_tokens, self.ws.data_ptr(),
+                                               nbytes, C.byref(h)), "ams_ctx_create")
         self.handle = h
         self._keep = []
         _live_contexts.add(self)
@@ -189,6 +205,15 @@ class DeviceContext:
 
     def invalidate(self) -> None:
         capi.check(self.lib.ams_ctx_invalidate(self.handle), "ams_ctx_invalidate")
+
+    def pages(self):
+        """(page table [batch][capacity/64], reference counts [n_pages], pages in use) as numpy / int."""
+        pt = np.zeros((self.batch, self.capacity // 64), dtype=np.int32)
+        refs = np.zeros(self.n_pages, dtype=np.int32)
+        used = C.c_int32()
+        capi.check(self.lib.ams_ctx_pages(self.handle, pt.ctypes.data, refs.ctypes.data, C.byref(used)),
+                   "ams_ctx_pages")
+        return pt, refs, int(used.value)
 
     def lengths(self) -> List[int]:
         arr = (C.c_int32 * self.batch)()

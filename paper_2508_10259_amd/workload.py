@@ -314,6 +314,10 @@ class Workload:
     invalidate_every: int = 0
     recompute_each_step: bool = False
     capacity: int = 0  # 0: derived
+    # rows in `shared[0]` groups (row b in group b % shared[0]): every row of a group starts with
+    # the group's instruction (shared[1] ids) and scene (shared[2] patch embeddings), then its own
+    # patches; ragged lengths count all of it
+    shared: Optional[Tuple[int, int, int]] = None
 
     @property
     def spec(self) -> ModelSpec:
@@ -347,6 +351,10 @@ WORKLOADS: Dict[str, Workload] = {
                               new_per_step=16, invalidate_every=20, capacity=768),
     # 7B, action chunking: 56 tokens per step against a 600-token prefix, batch 16
     "7b-chunk56-b16": Workload("7b-chunk56-b16", "7b", 16, 56, 50, prefix=(568, 32)),
+    # as 7b-b64-ragged, with the 64 rows in 8 tasks: a row's prefix is its task's 32 instruction
+    # ids and 224 scene patches, then U{0..144} patches of its own (lengths U{256..400})
+    "7b-b64-shared": Workload("7b-b64-shared", "7b", 64, 7, 200, ragged=(256, 400, 32), new_per_step=16,
+                              invalidate_every=20, capacity=768, shared=(8, 32, 224)),
 }
 
 
@@ -371,20 +379,41 @@ def text_id_range(spec: ModelSpec) -> Tuple[int, int]:
 
 @dataclass
 class Prefix:
-    """One row's prefix: ``patches`` [n_patch, d] (encoded) then ``text_ids`` [n_text]."""
+    """One row's prefix: ``patches`` [n_patch, d] (encoded) then ``text_ids`` [n_text], or the ids
+    first when ``text_first``."""
 
     patches: np.ndarray
     text_ids: np.ndarray
+    text_first: bool = False
 
     @property
     def length(self) -> int:
         return self.patches.shape[0] + self.text_ids.shape[0]
 
 
+def _shared_prefix(wl: Workload, seed: int, epoch: int, row: int, length: int, device=None) -> Prefix:
+    spec = wl.spec
+    groups, n_text, n_scene = wl.shared
+    g = row % groups
+    lo, hi = text_id_range(spec)
+    ids = _rng(seed, _T_IDS, epoch, 1 << 20, g).integers(lo, hi, size=n_text).astype(np.int32)
+    own = length - n_text - n_scene
+    if device is None:
+        scene = _rng(seed, _T_PATCH, epoch, 1 << 20, g).standard_normal((n_scene, spec.d_model), dtype=np.float32)
+        mine = _rng(seed, _T_PATCH, epoch, row).standard_normal((own, spec.d_model), dtype=np.float32)
+        return Prefix(encode(np.concatenate([scene, mine]), spec.dtype), ids, text_first=True)
+    import torch
+    scene = device_normal((n_scene, spec.d_model), 1.0, spec.dtype, device, seed, _T_PATCH, epoch, 1 << 20, g)
+    mine = device_normal((own, spec.d_model), 1.0, spec.dtype, device, seed, _T_PATCH, epoch, row)
+    return Prefix(torch.cat([scene, mine]), ids, text_first=True)
+
+
 def make_prefix(wl: Workload, seed: int, epoch: int, row: int, length: Optional[int] = None) -> Prefix:
     spec = wl.spec
     if length is None:
         length = int(prefix_lengths(wl, seed, epoch)[row])
+    if wl.shared:
+        return _shared_prefix(wl, seed, epoch, row, length)
     n_text = min(_n_text(wl), length)
     n_patch = length - n_text
     x = _rng(seed, _T_PATCH, epoch, row).standard_normal((n_patch, spec.d_model), dtype=np.float32)
@@ -404,6 +433,8 @@ def make_prefix_device(wl: Workload, seed: int, epoch: int, row: int, length: Op
     spec = wl.spec
     if length is None:
         length = int(prefix_lengths(wl, seed, epoch)[row])
+    if wl.shared:
+        return _shared_prefix(wl, seed, epoch, row, length, device)
     n_text = min(_n_text(wl), length)
     x = device_normal((length - n_text, spec.d_model), 1.0, spec.dtype, device, seed, _T_PATCH, epoch, row)
     lo, hi = text_id_range(spec)

@@ -116,6 +116,64 @@ static void test_rows() {
   EXPECT(b.state == READY && b.row_state[3] == READY && b.len[3] == 8);
 }
 
+// Shared prefix pages: reference counts, the key index, attach / publish / free.
+static void test_pages() {
+  PagePool pool;
+  pool.init(12);
+  EXPECT(pool.in_use() == 0 && pool.alloc() == 0 && pool.alloc() == 1 && pool.in_use() == 2);
+  pool.publish(1, 77);
+  EXPECT(pool.lookup(77) == 1 && pool.lookup(78) == -1);
+  pool.retain(1);
+  pool.release(1);
+  EXPECT(pool.refs[1] == 1 && pool.lookup(77) == 1);  // still referenced: stays indexed
+  pool.release(1);
+  EXPECT(pool.refs[1] == 0 && pool.lookup(77) == -1 && pool.in_use() == 1);  // freed at zero
+  pool.release(0);
+  EXPECT(pool.in_use() == 0);
+
+  // 3 rows of 3 pages; rows 0 and 1 agree on their first two pages, row 2 on the first
+  const int ppr = 3;
+  pool.init(9);
+  std::vector<int32_t> pt(3 * ppr, -1), start;
+  std::string e;
+  int32_t rows[3] = {0, 1, 2}, share[3] = {2, 2, 2};
+  uint64_t keys[9] = {10, 11, 0, 10, 11, 0, 10, 12, 0};
+  EXPECT(plan_row_pages(pool, pt, ppr, rows, 3, share, keys, ppr, true, start, e) == S_OK);
+  EXPECT(pt[0] == pt[3] && pt[1] == pt[4] && pt[2] != pt[5]);  // row 1 attaches row 0's two pages
+  EXPECT(pt[6] == pt[0] && pt[7] != pt[1]);                    // row 2 attaches only the first
+  EXPECT(start[0] == 0 && start[1] == 128 && start[2] == 64);
+  EXPECT(pool.refs[pt[0]] == 3 && pool.refs[pt[1]] == 2 && pool.refs[pt[7]] == 1);
+  EXPECT(pool.in_use() == 3 + 1 + 2);  // row 0: 3 pages; row 1: its last; row 2: its last two
+  EXPECT(pool.lookup(12) == pt[7]);                // row 2 published the page it computed
+  // without sharing every row takes fresh pages: the pool of 9 is then full
+  PagePool p2;
+  p2.init(9);
+  std::vector<int32_t> pt2(3 * ppr, -1);
+  EXPECT(plan_row_pages(p2, pt2, ppr, rows, 3, share, keys, ppr, false, start, e) == S_OK);
+  EXPECT(p2.in_use() == 9 && start[1] == 0 && p2.lookup(10) == -1);
+  // a pool too small: ECAPACITY, nothing changed
+  PagePool p3;
+  p3.init(5);
+  std::vector<int32_t> pt3(3 * ppr, -1);
+  EXPECT(plan_row_pages(p3, pt3, ppr, rows, 3, share, keys, ppr, true, start, e) == S_ECAPACITY);
+  EXPECT(p3.in_use() == 0 && pt3[0] == -1 && !e.empty());
+  // row 0 invalidated: its pages lose a reference; the shared ones stay with rows 1 and 2
+  int32_t r0[1] = {0};
+  const int first = pt[0], own0 = pt[2];
+  release_row_pages(pool, pt, ppr, r0, 1);
+  EXPECT(pool.refs[first] == 2 && pool.refs[own0] == 0 && pt[0] == -1 && pool.lookup(10) == first);
+  // rebuilt with a different first page: nothing to attach, three fresh pages
+  uint64_t k0[3] = {20, 21, 0};
+  int32_t s0[1] = {2};
+  EXPECT(plan_row_pages(pool, pt, ppr, r0, 1, s0, k0, ppr, true, start, e) == S_OK);
+  EXPECT(start[0] == 0 && pt[0] != first && pool.lookup(20) == pt[0]);
+  // every row released: the pool is empty and the index too
+  release_row_pages(pool, pt, ppr, rows, 3);
+  EXPECT(pool.in_use() == 0 && pool.index.empty());
+  EXPECT(shareable_pages(64) == 0 && shareable_pages(65) == 1 && shareable_pages(128) == 1 && shareable_pages(300) == 4);
+  EXPECT(page_key_segment(8192) == 4096 && page_key_segment(768) == 256 && page_key_segment(512) == 512);
+}
+
 static void test_plan() {
   // rows 0..5 with ragged counts, one empty; pass budget 100
   int32_t counts[6] = {40, 0, 70, 30, 100, 1};
@@ -191,6 +249,7 @@ int main() {
   test_book();
   test_async_error();
   test_rows();
+  test_pages();
   test_plan();
   test_layout();
   if (failures) {

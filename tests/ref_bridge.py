@@ -36,7 +36,13 @@ def oracle_params(w):
 
 
 def prefix_f64(p, spec, prefix):
-    """Prefix embeddings: patch rows, then embedding rows of the instruction ids."""
-    x = W.to_f32(prefix.patches, spec.dtype).astype(np.float64)
+    """Prefix embeddings: patch rows, then embedding rows of the instruction ids (ids first when
+    the prefix says so)."""
+    pt = prefix.patches
+    if hasattr(pt, "cpu"):  # drawn on the device
+        pt = pt.float().cpu().numpy()
+        x = pt.astype(np.float64)
+    else:
+        x = W.to_f32(pt, spec.dtype).astype(np.float64)
     t = D.embed_ids(p, prefix.text_ids)
-    return np.concatenate([x, t], axis=0)
+    return np.concatenate([t, x] if getattr(prefix, "text_first", False) else [x, t], axis=0)
