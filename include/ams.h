@@ -313,6 +313,22 @@ ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_ro
  * AMS_ECAPACITY, AMS_EHIP. */
 ams_status ams_ctx_append(ams_ctx* c, const void* new_tokens, const int32_t* new_lens, void* stream);
 
+/* Paper sections 3.2.2 (Layered Storage of Action Context) and 3.2.3 (Auto
+ * Eviction): which rows to evict from the GPU to free pages_needed pages.
+ * Host-only arithmetic over host arrays [n_rows]: priority (lower goes
+ * first), last_use (a tick of the caller's, larger = more recent), pages held,
+ * droppable (nonzero: the caller keeps the row's inputs, so dropping and
+ * recomputing it is allowed), resident (nonzero: on the GPU), pinned (nonzero:
+ * never evicted).  The resident unpinned rows are taken in increasing
+ * (priority, last_use, row) order until the pages taken reach pages_needed;
+ * action[r] = 0 keep, 1 offload to host memory (ams_ctx_offload_rows), 2 drop
+ * (ams_ctx_invalidate_rows, later ams_ctx_build_rows).  *pages_freed (may be
+ * NULL) receives the pages the taken rows hold, less than pages_needed when
+ * the candidates hold fewer.  Errors: AMS_EINVAL. */
+ams_status ams_tier_plan(int32_t n_rows, const int32_t* priority, const int64_t* last_use, const int32_t* pages,
+                         const int32_t* droppable, const int32_t* resident, const int32_t* pinned,
+                         int64_t pages_needed, int32_t* action, int64_t* pages_freed);
+
 /* Committed length of every row into host array lens[batch]. */
 ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens);
 

@@ -55,6 +55,8 @@ SIGNATURES = {
     "ams_ctx_step": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p]),
     "ams_ctx_invalidate": (C.c_int32, [C.c_void_p]),
+    "ams_tier_plan": (C.c_int32, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                  C.c_int64, C.c_void_p, C.POINTER(C.c_int64)]),
     "ams_ctx_build_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
                                        C.POINTER(C.c_int32), C.c_void_p]),
     "ams_ctx_invalidate_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32]),

@@ -462,6 +462,19 @@ ams_status ams_index_hash_noalloc(const void* data, size_t n_bytes, int32_t seg_
   return AMS_OK;
 }
 
+ams_status ams_tier_plan(int32_t n_rows, const int32_t* priority, const int64_t* last_use, const int32_t* pages,
+                         const int32_t* droppable, const int32_t* resident, const int32_t* pinned,
+                         int64_t pages_needed, int32_t* action, int64_t* pages_freed) {
+  g_err.clear();
+  if (n_rows < 0) return fail(AMS_EINVAL, "n_rows must be >= 0");
+  if (n_rows > 0 && (!priority || !last_use || !pages || !droppable || !resident || !pinned || !action))
+    return fail(AMS_EINVAL, "an array is NULL");
+  const int64_t f = ams::tier_plan(n_rows, priority, last_use, pages, droppable, resident, pinned, pages_needed,
+                                   action);
+  if (pages_freed) *pages_freed = f;
+  return AMS_OK;
+}
+
 ams_status ams_ctx_invalidate(ams_ctx* c) {
   g_err.clear();
   if (!c) return fail(AMS_EINVAL, "context is NULL");

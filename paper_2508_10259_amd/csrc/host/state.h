@@ -546,6 +546,39 @@ inline void release_row_pages(PagePool& pool, std::vector<int32_t>& pt, int ppr,
 inline int shareable_pages(int len) { return (len - 1) / 64; }
 
 // ---------------------------------------------------------------------------
+// Eviction plan of the layered store (paper sections 3.2.2 and 3.2.3, Auto
+// Eviction): to free `need` pages, the resident unpinned rows are taken in
+// increasing (priority, last use, row) order -- lowest priority first, least
+// recently used within a priority -- until the pages taken reach `need`; a
+// taken row is dropped (recomputed from its inputs later) when droppable and
+// offloaded to host memory otherwise.  Returns the pages the taken rows hold.
+
+enum TierAction { TIER_KEEP = 0, TIER_OFFLOAD = 1, TIER_DROP = 2 };
+
+inline int64_t tier_plan(int n, const int32_t* priority, const int64_t* last_use, const int32_t* pages,
+                         const int32_t* droppable, const int32_t* resident, const int32_t* pinned, int64_t need,
+                         int32_t* action) {
+  std::vector<int> order;
+  for (int r = 0; r < n; ++r) {
+    action[r] = TIER_KEEP;
+    if (resident[r] && !pinned[r]) order.push_back(r);
+  }
+  if (need <= 0) return 0;
+  std::sort(order.begin(), order.end(), [&](int a, int b) {
+    if (priority[a] != priority[b]) return priority[a] < priority[b];
+    if (last_use[a] != last_use[b]) return last_use[a] < last_use[b];
+    return a < b;
+  });
+  int64_t freed = 0;
+  for (int r : order) {
+    if (freed >= need) break;
+    action[r] = droppable[r] ? TIER_DROP : TIER_OFFLOAD;
+    freed += pages[r];
+  }
+  return freed;
+}
+
+// ---------------------------------------------------------------------------
 // pass planner: rows with pending tokens, packed in row order into passes of
 // at most `pass_tokens` tokens (a row is never split: its count <= capacity
 // <= pass_tokens).
