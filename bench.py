@@ -364,6 +364,45 @@ def measure(model, wl, seed, steps, warmup, mode, device_draws, share=False):
                      "phases_ms": {k: round(sum(e[0] for e in v) / steps * 1e3, 4) for k, v in ph.items()}}}
 
 
+def tier_rates(model, wl, seed, rows=8, device_draws=True):
+    """The host tier on the workload's first build: `rows` rows moved to pinned host memory and
+    back (library kernels writing / reading the host images), timed with HIP events, against
+    dropping the same rows and rebuilding them from their inputs."""
+    import torch
+    from paper_2508_10259_amd.runtime import DeviceContext
+    cap = wl.derived_capacity()
+    ctx = DeviceContext(model, wl.batch, cap, n_pages=0)
+    epochs, _, _ = make_inputs(model, wl, seed, 1, device_draws)
+    ctx.build(*epochs[0])
+    sel = list(range(rows))
+    lens = ctx.lengths()
+    bufs = [torch.empty(ctx.row_host_bytes(lens[r]), dtype=torch.uint8).pin_memory() for r in sel]
+    from paper_2508_10259_amd import workload as W
+    draw = W.make_prefix_device if device_draws else W.make_prefix
+    packed, plens = model.pack_prefixes([draw(wl, seed, 0, b, int(lens[b])) for b in sel])
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for rep in range(2):  # the second round is timed
+        ev[0].record()
+        ctx.offload_rows(sel, bufs)
+        ev[1].record()
+        ctx.reload_rows(sel, bufs)
+        ev[2].record()
+        ctx.invalidate_rows(sel)
+        ev[3].record()
+        ctx.build_rows(sel, packed, plens)
+        ev[4].record()
+        torch.cuda.synchronize()
+    nbytes = sum(b.numel() for b in bufs)
+    t_off, t_re, t_build = (ev[0].elapsed_time(ev[1]) * 1e-3, ev[1].elapsed_time(ev[2]) * 1e-3,
+                            ev[3].elapsed_time(ev[4]) * 1e-3)
+    ctx.close()
+    return {"rows": rows, "tokens": int(sum(lens[r] for r in sel)), "host_bytes": int(nbytes),
+            "offload_ms": round(t_off * 1e3, 3), "offload_GBps": round(nbytes / t_off / 1e9, 2),
+            "reload_ms": round(t_re * 1e3, 3), "reload_GBps": round(nbytes / t_re / 1e9, 2),
+            "rebuild_ms": round(t_build * 1e3, 3),
+            "what": "rows moved to pinned host memory and back by the library's kernels vs dropped and rebuilt"}
+
+
 def decode_kernel_name(spec, B, A, persistent):
     if persistent:
         return (f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer, "
@@ -458,6 +497,9 @@ def main():
             x = measure(model, W.WORKLOADS[name], args.seed, n, 2, mode, big, share=share)
             key = (f"{name}/{mode}" if mode != "cached" else name) + ("/shared-pages" if share else "")
             extras[key] = compact(x)
+        if spec.name == "7b":
+            print("[bench] host tier: 8 rows of 7b-b64-ragged to host memory and back", file=sys.stderr, flush=True)
+            extras["host-tier/7b-b64-ragged"] = tier_rates(model, W.WORKLOADS["7b-b64-ragged"], args.seed)
         if spec.name != "mid":
             model.close()
             print("[bench] extra mid-b8 (cached, 100 steps)", file=sys.stderr, flush=True)

@@ -313,6 +313,41 @@ ams_status ams_ctx_invalidate_rows(ams_ctx* c, const int32_t* rows, int32_t n_ro
  * AMS_ECAPACITY, AMS_EHIP. */
 ams_status ams_ctx_append(ams_ctx* c, const void* new_tokens, const int32_t* new_lens, void* stream);
 
+/* Paper section 3.2.2 (Layered Storage of Action Context): rarely used
+ * context moves from GPU memory to CPU memory and back.
+ *
+ * Bytes of the host image of a row of `len` positions (0 if len is outside
+ * [1, capacity]): a 256-byte header, every layer's K and V of the row's
+ * positions ([layer][K|V][head][len][head_dim] in the compute type: fp16 for
+ * bf16 models, fp32 otherwise), the last position's hidden state (fp32 [d])
+ * and its fp16 pair ([d] + [d]). */
+size_t ams_ctx_row_host_bytes(const ams_ctx* c, int32_t len);
+
+/* Copies each listed row's context (READY rows; strictly increasing indices)
+ * into host[i]: pinned host memory (hipHostMalloc, mapped), 16-byte aligned,
+ * at least ams_ctx_row_host_bytes(c, row length) bytes, caller-owned.  The
+ * library's kernels write the images through the buffers' device addresses
+ * (the header is written by the host at once).  The rows become OFFLOADED
+ * (length 0, not steppable; the context reads INVALID) and, in a paged
+ * context, their pages return to the pool; later work on the same stream
+ * may reuse them.  The images are complete once the stream has passed the
+ * call.  Errors: AMS_EINVAL, AMS_ESTATE, AMS_EHIP. */
+ams_status ams_ctx_offload_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, void* const* host, void* stream);
+
+/* Restores rows from host images written by ams_ctx_offload_rows (of a
+ * context of the same model; host[i] as there): rows[i] gets the image's
+ * context -- every layer's K/V, its length and last hidden state -- on fresh
+ * pages of a paged context, and is READY afterwards.  A listed row must not be
+ * READY.  Errors: AMS_EINVAL (not an image of this model), AMS_ESTATE,
+ * AMS_ECAPACITY (image longer than the capacity, or not enough free pages:
+ * nothing changed), AMS_EHIP. */
+ams_status ams_ctx_reload_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, const void* const* host,
+                               void* stream);
+
+/* Each row's state into host array states[batch]: 0 EMPTY, 1 READY,
+ * 2 INVALID, 3 OFFLOADED. */
+ams_status ams_ctx_row_states(const ams_ctx* c, int32_t* states);
+
 /* Paper sections 3.2.2 (Layered Storage of Action Context) and 3.2.3 (Auto
  * Eviction): which rows to evict from the GPU to free pages_needed pages.
  * Host-only arithmetic over host arrays [n_rows]: priority (lower goes

@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libams.so")
 AMS_OK, AMS_EINVAL, AMS_ESTATE, AMS_ECAPACITY, AMS_ENODEV, AMS_EHIP, AMS_ENOMEM = 0, -1, -2, -3, -4, -5, -6
 AMS_F32, AMS_BF16 = 0, 1
 AMS_CTX_SHARE_PREFIX = 1
-STATE_EMPTY, STATE_READY, STATE_INVALID = 0, 1, 2
+STATE_EMPTY, STATE_READY, STATE_INVALID, STATE_OFFLOADED = 0, 1, 2, 3
 
 
 class ModelCfg(C.Structure):
@@ -55,6 +55,12 @@ SIGNATURES = {
     "ams_ctx_step": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p]),
     "ams_ctx_invalidate": (C.c_int32, [C.c_void_p]),
+    "ams_ctx_row_host_bytes": (C.c_size_t, [C.c_void_p, C.c_int32]),
+    "ams_ctx_offload_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_void_p),
+                                         C.c_void_p]),
+    "ams_ctx_reload_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_void_p),
+                                        C.c_void_p]),
+    "ams_ctx_row_states": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32)]),
     "ams_tier_plan": (C.c_int32, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                   C.c_int64, C.c_void_p, C.POINTER(C.c_int64)]),
     "ams_ctx_build_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,

@@ -462,6 +462,102 @@ ams_status ams_index_hash_noalloc(const void* data, size_t n_bytes, int32_t seg_
   return AMS_OK;
 }
 
+namespace {
+constexpr uint32_t ROW_IMAGE_MAGIC = 0x52534D41u;  // "AMSR"
+struct RowImageHeader {
+  uint32_t magic, version;
+  int32_t len, n_layers, d_model, head_dim, n_heads, dtype;
+};
+
+// Device address of pinned host memory (EINVAL when `p` is not pinned and mapped).
+bool host_device_ptr(const void* p, void** dev, std::string& err) {
+  hipPointerAttribute_t a;
+  if (!p || hipPointerGetAttributes(&a, p) != hipSuccess || a.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    err = "a host buffer is not pinned host memory (hipHostMalloc)";
+    return false;
+  }
+  if (hipHostGetDevicePointer(dev, (void*)p, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    err = "a host buffer is not mapped for the device";
+    return false;
+  }
+  return true;
+}
+}  // namespace
+
+size_t ams_ctx_row_host_bytes(const ams_ctx* c, int32_t len) {
+  if (!c || len < 1 || len > c->c.lay.capacity) return 0;
+  return ams::row_host_bytes(c->c.model->cfg, len);
+}
+
+ams_status ams_ctx_offload_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, void* const* host, void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = ams::ctx_absorb_status(x, e)) return fail(s, e);
+  if (int s = x.book.check_offload(rows, n_rows, e)) return fail(s, e);
+  if (!host) return fail(AMS_EINVAL, "host is NULL");
+  std::vector<void*> dev(n_rows);
+  std::vector<int32_t> lens(n_rows);
+  for (int i = 0; i < n_rows; ++i) {
+    if (!host_device_ptr(host[i], &dev[i], e)) return fail(AMS_EINVAL, e);
+    if (((uintptr_t)host[i] & 15) != 0) return fail(AMS_EINVAL, "host buffers must be 16-byte aligned");
+    lens[i] = x.book.len[rows[i]];
+  }
+  const ams::Cfg& m = x.model->cfg;
+  for (int i = 0; i < n_rows; ++i) {
+    RowImageHeader hd{ROW_IMAGE_MAGIC, 1u, lens[i], m.n_layers, m.d_model, m.head_dim, m.n_heads, m.dtype};
+    memcpy(host[i], &hd, sizeof(hd));
+  }
+  if (int s = ams::ctx_offload_rows(x, rows, n_rows, lens.data(), dev.data(), (hipStream_t)stream, e)) {
+    x.book.invalidate();
+    return fail(s, e);
+  }
+  x.book.offload_rows(rows, n_rows);
+  return AMS_OK;
+}
+
+ams_status ams_ctx_reload_rows(ams_ctx* c, const int32_t* rows, int32_t n_rows, const void* const* host,
+                               void* stream) {
+  g_err.clear();
+  if (!c) return fail(AMS_EINVAL, "context is NULL");
+  ams::Ctx& x = c->c;
+  std::string e;
+  if (int s = ams::ctx_absorb_status(x, e)) return fail(s, e);
+  if (int s = x.book.check_reload(rows, n_rows, e)) return fail(s, e);
+  if (!host) return fail(AMS_EINVAL, "host is NULL");
+  const ams::Cfg& m = x.model->cfg;
+  std::vector<void*> dev(n_rows);
+  std::vector<int32_t> lens(n_rows);
+  for (int i = 0; i < n_rows; ++i) {
+    if (!host_device_ptr(host[i], &dev[i], e)) return fail(AMS_EINVAL, e);
+    if (((uintptr_t)host[i] & 15) != 0) return fail(AMS_EINVAL, "host buffers must be 16-byte aligned");
+    RowImageHeader hd;
+    memcpy(&hd, host[i], sizeof(hd));
+    if (hd.magic != ROW_IMAGE_MAGIC || hd.version != 1u || hd.n_layers != m.n_layers || hd.d_model != m.d_model ||
+        hd.head_dim != m.head_dim || hd.n_heads != m.n_heads || hd.dtype != m.dtype)
+      return fail(AMS_EINVAL, "host buffer " + std::to_string(i) + " holds no row image of this model");
+    if (hd.len < 1 || hd.len > x.lay.capacity)
+      return fail(AMS_ECAPACITY, "host buffer " + std::to_string(i) + ": row longer than the capacity");
+    lens[i] = hd.len;
+  }
+  if (int s = ams::ctx_reload_rows(x, rows, n_rows, lens.data(), dev.data(), (hipStream_t)stream, e)) {
+    if (s == AMS_EHIP) x.book.invalidate();
+    return fail(s, e);
+  }
+  x.book.commit_build_rows(rows, n_rows, lens.data());
+  return AMS_OK;
+}
+
+ams_status ams_ctx_row_states(const ams_ctx* c, int32_t* states) {
+  g_err.clear();
+  if (!c || !states) return fail(AMS_EINVAL, "context and states must not be NULL");
+  for (int b = 0; b < c->c.lay.batch; ++b) states[b] = c->c.book.row_state[b];
+  return AMS_OK;
+}
+
 ams_status ams_tier_plan(int32_t n_rows, const int32_t* priority, const int64_t* last_use, const int32_t* pages,
                          const int32_t* droppable, const int32_t* resident, const int32_t* pinned,
                          int64_t pages_needed, int32_t* action, int64_t* pages_freed) {

@@ -203,6 +203,57 @@ int ctx_build_rows(Ctx& c, const void* prefix, const int32_t* rows, int n_rows, 
              : (int)S_EHIP;
 }
 
+static int rows_xfer_enqueue(Ctx& c, bool to_host, const int32_t* rows, int n_rows, const int32_t* lens,
+                             void* const* host_dev, hipStream_t s, std::string& err) {
+  const Cfg& m = c.model->cfg;
+  c.xfer_host.resize(n_rows);
+  for (int i = 0; i < n_rows; ++i) c.xfer_host[i] = XferRow{rows[i], lens[i], host_dev[i]};
+  XferRow* xd = (XferRow*)(c.ws + c.lay.xfer);
+  if (hipMemcpyAsync(xd, c.xfer_host.data(), n_rows * sizeof(XferRow), hipMemcpyHostToDevice, s) != hipSuccess ||
+      rows_xfer(to_host, xd, n_rows, m.n_layers, m.n_heads, m.head_dim, (int)(c.model->ct == DT_F16 ? 2 : 4),
+                c.ws + c.lay.kv, c.lay.slab_layer, c.pt(), c.lay.ppr, c.h_last(), c.h_last16(), c.h_last16lo(),
+                m.d_model, s) != hipSuccess) {
+    err = to_host ? "offload to host memory failed" : "reload from host memory failed";
+    return S_EHIP;
+  }
+  return S_OK;
+}
+
+int ctx_offload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* lens, void* const* host_dev,
+                     hipStream_t s, std::string& err) {
+  if (int r = rows_xfer_enqueue(c, true, rows, n_rows, lens, host_dev, s, err)) return r;
+  // the pages go back to the pool now; work enqueued later on the same stream,
+  // which may reuse them, runs after the copies
+  ctx_release_rows(c, rows, n_rows);
+  return S_OK;
+}
+
+int ctx_reload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* lens, void* const* host_dev,
+                    hipStream_t s, std::string& err) {
+  const int B = c.lay.batch;
+  if (c.pooled) {
+    std::vector<int32_t> share(n_rows, 0), st;
+    if (int r = plan_row_pages(c.pool, c.pt_host, c.lay.ppr, rows, n_rows, share.data(), nullptr, 0, false, st, err))
+      return r;
+    if (upload_pages(c, s) != hipSuccess) {
+      err = "page table upload failed";
+      return S_EHIP;
+    }
+  }
+  if (int r = rows_xfer_enqueue(c, false, rows, n_rows, lens, host_dev, s, err)) return r;
+  // the rows' device lengths: set mode of the length update over a [B] array
+  std::vector<int32_t>& h = c.meta_host;
+  std::fill(h.begin(), h.end(), 0);
+  for (int i = 0; i < n_rows; ++i) h[4 * B + 1 + rows[i]] = lens[i];
+  int32_t* md = c.meta();
+  if (hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess ||
+      update_lens(c.lens(), md + 4 * B + 1, B, 1, s) != hipSuccess) {
+    err = "length update failed";
+    return S_EHIP;
+  }
+  return S_OK;
+}
+
 int ctx_absorb_status(Ctx& c, std::string& err) {
   if (!c.status_host) return S_OK;
   const unsigned w = *c.status_host;

@@ -73,6 +73,7 @@ struct Ctx {
   PagePool pool;
   std::vector<uint64_t> keys_host;
   std::vector<int64_t> hk_rows_host;
+  std::vector<XferRow> xfer_host;  // staging of the last host-tier call's descriptors
 
   // K/V page pools of layer l; row b's position t sits in page pt()[b * ppr + t / 64]
   void* kslab(int l) const { return ws + lay.kv + (size_t)(2 * l) * lay.slab_layer; }
@@ -123,6 +124,15 @@ int ctx_build_rows(Ctx& c, const void* prefix, const int32_t* rows, int n_rows, 
                    std::string& err);
 // Returns the listed rows' pages to the pool (pooled contexts; host only).
 void ctx_release_rows(Ctx& c, const int32_t* rows, int n_rows);
+
+// Host tier: copies the listed rows (lens[i] positions each) to / from the host
+// images at host_dev[i] (device addresses of pinned host memory).  Reloading
+// into a pooled context first takes fresh pages for the rows (S_ECAPACITY when
+// there are not enough; nothing changed) and sets their device lengths.
+int ctx_offload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* lens, void* const* host_dev,
+                     hipStream_t s, std::string& err);
+int ctx_reload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* lens, void* const* host_dev,
+                    hipStream_t s, std::string& err);
 
 // Takes in an error a kernel of an earlier call reported asynchronously (see
 // RowBook::absorb_async_error) and clears the word.

@@ -103,7 +103,13 @@ struct CtxLayout {
   bool share;
   int key_seg;  // segment size of the page keys (bytes)
   size_t hk_seg, hk_keys, hk_rows;
+  size_t xfer;  // host-tier transfer descriptors [batch] (16 bytes each)
 };
+
+// Bytes of the host image of a row of `len` positions (see the host tier).
+inline size_t row_host_bytes(const Cfg& c, int len) {
+  return 256 + (size_t)2 * c.n_layers * len * c.d_model * elem_size(c) + (size_t)c.d_model * (4 + 2 + 2);
+}
 
 inline int default_pass_tokens(int batch, int capacity) {
   const int64_t bc = (int64_t)batch * capacity;
@@ -282,6 +288,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.hk_seg = o; o = align256(o + max_segs * 8);
   x.hk_keys = o; o = align256(o + (share ? B * (size_t)x.ppr * 8 : 0));
   x.hk_rows = o; o = align256(o + (share ? 2 * B * 8 : 0));
+  x.xfer = o; o = align256(o + B * 16);
   x.total = o;
   return x;
 }
@@ -289,7 +296,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
 // ---------------------------------------------------------------------------
 // length book: the host-side truth of each row's committed length
 
-enum CtxState { EMPTY = 0, READY = 1, INVALID = 2 };
+enum CtxState { EMPTY = 0, READY = 1, INVALID = 2, OFFLOADED = 3 };  // OFFLOADED: rows only
 
 // Each row has its own state (EMPTY until first built, READY, INVALID after a
 // row-level or whole-context invalidate); the context is READY when every row
@@ -310,7 +317,7 @@ struct RowBook {
     row_state.assign(b, (int8_t)EMPTY);
   }
 
-  void refresh_state() {
+  void refresh_state() {  // (an offloaded row makes the context INVALID until reloaded)
     bool all_ready = true, all_empty = true;
     for (int b = 0; b < batch; ++b) {
       all_ready = all_ready && row_state[b] == READY;
@@ -409,6 +416,34 @@ struct RowBook {
       row_state[rows[i]] = INVALID;
     }
     refresh_state();
+  }
+  // rows whose contexts moved to host memory: not steppable until reloaded
+  // (length 0 meanwhile); every listed row must be READY
+  int check_offload(const int32_t* rows, int n, std::string& err) const {
+    if (int s = check_rows(rows, n, err)) return s;
+    for (int i = 0; i < n; ++i)
+      if (row_state[rows[i]] != READY) {
+        err = "row " + std::to_string(rows[i]) + " holds no context to offload";
+        return S_ESTATE;
+      }
+    return S_OK;
+  }
+  void offload_rows(const int32_t* rows, int n) {
+    for (int i = 0; i < n; ++i) {
+      len[rows[i]] = 0;
+      row_state[rows[i]] = OFFLOADED;
+    }
+    refresh_state();
+  }
+  // a row may be reloaded unless it holds a context (READY)
+  int check_reload(const int32_t* rows, int n, std::string& err) const {
+    if (int s = check_rows(rows, n, err)) return s;
+    for (int i = 0; i < n; ++i)
+      if (row_state[rows[i]] == READY) {
+        err = "row " + std::to_string(rows[i]) + " holds a context (invalidate or offload it first)";
+        return S_ESTATE;
+      }
+    return S_OK;
   }
 
   // An error that a kernel reported asynchronously (the persistent decode's

@@ -227,6 +227,21 @@ hipError_t hash_page_keys(const uint64_t* seg, const int64_t* seg_first, const i
 constexpr uint64_t INDEX_NOALLOC_MAX_SEGMENTS = 131072;
 hipError_t index_noalloc_scratch(int device, uint64_t** ptr);
 
+// Host tier (tier.hip): copies whole rows between the K/V page pools (pool =
+// the context's K/V region, layer l's K at 2l * slab_layer bytes, V at
+// (2l + 1) * slab_layer) plus the last hidden state (h_last fp32 [rows][d] and
+// its fp16 pair h16 / h16lo) and host images at rows[i].host (a device-usable
+// address of pinned host memory): after a 256-byte header, K/V
+// [layer][K|V][head][len][dh] in the compute type (es bytes), then h_last [d]
+// fp32 and the pair [d] + [d] fp16.  `rows` is a device array.
+struct XferRow {
+  int32_t row, len;
+  void* host;
+};
+hipError_t rows_xfer(bool to_host, const XferRow* rows, int n_rows, int L, int H, int dh, int es, void* pool,
+                     size_t slab_layer, const int32_t* pt, int ppr, float* h_last, void* h16, void* h16lo, int d,
+                     hipStream_t s);
+
 // Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned
 // pointers and size) from src to dst; a grid-stride read of src whose per-thread
 // sums land in out[grid * 256]; `iters` rounds of fp16 MFMA chains per wave on

@@ -215,6 +215,25 @@ class DeviceContext:
                    "ams_ctx_pages")
         return pt, refs, int(used.value)
 
+    def row_host_bytes(self, length: int) -> int:
+        return int(self.lib.ams_ctx_row_host_bytes(self.handle, length))
+
+    def offload_rows(self, rows: Sequence[int], host: Sequence[torch.Tensor]) -> None:
+        """Move rows' contexts into pinned host tensors (torch pin_memory, >= row_host_bytes)."""
+        ptrs = (C.c_void_p * len(rows))(*[h.data_ptr() for h in host])
+        capi.check(self.lib.ams_ctx_offload_rows(self.handle, capi.int_array(rows), len(rows), ptrs, _stream()),
+                   "ams_ctx_offload_rows")
+
+    def reload_rows(self, rows: Sequence[int], host: Sequence[torch.Tensor]) -> None:
+        ptrs = (C.c_void_p * len(rows))(*[h.data_ptr() for h in host])
+        capi.check(self.lib.ams_ctx_reload_rows(self.handle, capi.int_array(rows), len(rows), ptrs, _stream()),
+                   "ams_ctx_reload_rows")
+
+    def row_states(self) -> List[int]:
+        arr = (C.c_int32 * self.batch)()
+        capi.check(self.lib.ams_ctx_row_states(self.handle, arr), "ams_ctx_row_states")
+        return list(arr)
+
     def lengths(self) -> List[int]:
         arr = (C.c_int32 * self.batch)()
         capi.check(self.lib.ams_ctx_lengths(self.handle, arr), "ams_ctx_lengths")

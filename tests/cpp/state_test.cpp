@@ -174,6 +174,35 @@ static void test_pages() {
   EXPECT(page_key_segment(8192) == 4096 && page_key_segment(768) == 256 && page_key_segment(512) == 512);
 }
 
+// Rows moved to host memory: OFFLOADED until reloaded; only READY rows offload,
+// only rows not READY reload.
+static void test_offload_states() {
+  RowBook b;
+  b.init(3, 128);
+  std::string e;
+  int32_t lens[3] = {10, 20, 30};
+  b.commit_build(lens);
+  int32_t r1[1] = {1};
+  EXPECT(b.check_reload(r1, 1, e) == S_ESTATE);  // READY rows are not reloaded
+  EXPECT(b.check_offload(r1, 1, e) == S_OK);
+  b.offload_rows(r1, 1);
+  EXPECT(b.row_state[1] == OFFLOADED && b.len[1] == 0 && b.state == INVALID);
+  EXPECT(b.check_offload(r1, 1, e) == S_ESTATE);  // nothing left to offload
+  EXPECT(b.check_step(nullptr, 1, e) == S_ESTATE);
+  EXPECT(b.check_reload(r1, 1, e) == S_OK);
+  int32_t l1[1] = {20};
+  b.commit_build_rows(r1, 1, l1);
+  EXPECT(b.state == READY && b.len[1] == 20);
+  // tier plan: priority first, LRU within it, pinned and non-resident rows kept
+  int32_t prio[5] = {1, 0, 0, 2, 0}, pages[5] = {4, 2, 3, 8, 1}, drop[5] = {0, 1, 0, 0, 1};
+  int32_t res[5] = {1, 1, 1, 1, 0}, pin[5] = {0, 0, 0, 0, 0}, act[5];
+  int64_t last[5] = {5, 9, 3, 1, 3};
+  EXPECT(tier_plan(5, prio, last, pages, drop, res, pin, 4, act) == 5);
+  EXPECT(act[0] == TIER_KEEP && act[1] == TIER_DROP && act[2] == TIER_OFFLOAD && act[3] == TIER_KEEP &&
+         act[4] == TIER_KEEP);
+  EXPECT(tier_plan(5, prio, last, pages, drop, res, pin, 0, act) == 0 && act[2] == TIER_KEEP);
+}
+
 static void test_plan() {
   // rows 0..5 with ragged counts, one empty; pass budget 100
   int32_t counts[6] = {40, 0, 70, 30, 100, 1};
@@ -250,6 +279,7 @@ int main() {
   test_async_error();
   test_rows();
   test_pages();
+  test_offload_states();
   test_plan();
   test_layout();
   if (failures) {
