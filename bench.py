@@ -403,6 +403,37 @@ def tier_rates(model, wl, seed, rows=8, device_draws=True):
             "what": "rows moved to pinned host memory and back by the library's kernels vs dropped and rebuilt"}
 
 
+def flow_rates(model, wl, seed, a=7, n_tokens=8, cold_steps=10, warm_steps=4, warm_tau=0.6, device_draws=True):
+    """Flow-matching action head on the workload's rows (an 8 x 7 action chunk per row): a cold
+    start from noise (cold_steps Euler steps from tau 0) against a warm start from a stored latent
+    (warm_steps steps from warm_tau), timed with HIP events."""
+    import torch
+    from paper_2508_10259_amd import workload as W
+    from paper_2508_10259_amd.runtime import DeviceContext, DeviceFlowHead
+    ctx = DeviceContext(model, wl.batch, wl.derived_capacity())
+    epochs, _, _ = make_inputs(model, wl, seed, 1, device_draws)
+    ctx.build(*epochs[0])
+    head = DeviceFlowHead(wl.spec, *W.make_flow_head(wl.spec, a, seed), n_tokens=n_tokens)
+    x = torch.from_numpy(W.make_latent(seed, 0, wl.batch, n_tokens, a)).cuda()
+    out = {}
+    for name, tau0, k in (("cold", 0.0, cold_steps), ("warm", warm_tau, warm_steps)):
+        ctx.flow(head, x, tau0, k)  # warm-up
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            ctx.flow(head, x, tau0, k)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 3
+        out[name] = {"tau0": tau0, "euler_steps": k, "ms_per_chunk": round(ms, 3),
+                     "row_chunks_per_s": round(wl.batch / (ms * 1e-3), 2)}
+    out["warm_speedup"] = round(out["cold"]["ms_per_chunk"] / out["warm"]["ms_per_chunk"], 3)
+    out["what"] = (f"{wl.batch} rows x {sum(wl.prefix) if wl.prefix else wl.ragged[1]} cached tokens, "
+                   f"chunk of {n_tokens} action tokens x {a} values per row")
+    ctx.close()
+    return out
+
+
 def decode_kernel_name(spec, B, A, persistent):
     if persistent:
         return (f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer, "
@@ -500,6 +531,8 @@ def main():
         if spec.name == "7b":
             print("[bench] host tier: 8 rows of 7b-b64-ragged to host memory and back", file=sys.stderr, flush=True)
             extras["host-tier/7b-b64-ragged"] = tier_rates(model, W.WORKLOADS["7b-b64-ragged"], args.seed)
+            print("[bench] flow head: cold vs warm start on 7b-chunk56-b16 rows", file=sys.stderr, flush=True)
+            extras["flow-head/7b-chunk56-b16"] = flow_rates(model, W.WORKLOADS["7b-chunk56-b16"], args.seed)
         if spec.name != "mid":
             model.close()
             print("[bench] extra mid-b8 (cached, 100 steps)", file=sys.stderr, flush=True)

@@ -364,6 +364,32 @@ ams_status ams_tier_plan(int32_t n_rows, const int32_t* priority, const int64_t*
                          const int32_t* droppable, const int32_t* resident, const int32_t* pinned,
                          int64_t pages_needed, int32_t* action, int64_t* pages_freed);
 
+/* Paper section 3.2.1 (the diffusion model's latent vectors are cached action
+ * context) and section 3.4.2 (Action Regeneration: generation starts from a
+ * stored successful latent instead of noise): a flow-matching action head over
+ * the cached context.  Each row's action chunk is a latent of n_tokens tokens
+ * of action_dim values.  The velocity runs every decoder layer over the tokens
+ * W_in x_i + tau w_t at the positions right after the row's committed
+ * sequence (causal attention over the cache and the earlier chunk tokens;
+ * their K/V are scratch, the context is unchanged), then reads out
+ * W_out (h_i / rms(h_i)) (rms with the model's epsilon, no gain).
+ * Weights in the model dtype: w_in [d][action_dim], w_t [d],
+ * w_out [action_dim][d], device, caller-owned. */
+typedef struct {
+  const void *w_in, *w_t, *w_out;
+  int32_t action_dim; /* 1..256 */
+  int32_t n_tokens;   /* >= 1 */
+} ams_flow_head;
+
+/* Euler integration of every row's latent from tau0 (in [0, 1)) to 1 in
+ * n_steps equal steps, in place: x is device fp32 [batch][n_tokens][action_dim]
+ * holding the initial latents (noise for a cold start at tau0 = 0, a stored
+ * latent for a warm start at a later tau0) and receiving the final ones.
+ * Requires READY and len[b] + n_tokens <= capacity for every row.
+ * Errors: AMS_EINVAL, AMS_ESTATE, AMS_ECAPACITY, AMS_EHIP. */
+ams_status ams_ctx_flow(ams_ctx* c, const ams_flow_head* head, float* x, float tau0, int32_t n_steps,
+                        void* stream);
+
 /* Committed length of every row into host array lens[batch]. */
 ams_status ams_ctx_lengths(const ams_ctx* c, int32_t* lens);
 

@@ -28,6 +28,11 @@ class Weights(C.Structure):
                                           "g_attn", "g_ffn", "g_final", "embed", "head_bins")]
 
 
+class FlowHead(C.Structure):
+    _fields_ = [("w_in", C.c_void_p), ("w_t", C.c_void_p), ("w_out", C.c_void_p), ("action_dim", C.c_int32),
+                ("n_tokens", C.c_int32)]
+
+
 # name -> (restype, argtypes)
 SIGNATURES = {
     "ams_status_str": (C.c_char_p, [C.c_int32]),
@@ -61,6 +66,7 @@ SIGNATURES = {
     "ams_ctx_reload_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_void_p),
                                         C.c_void_p]),
     "ams_ctx_row_states": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32)]),
+    "ams_ctx_flow": (C.c_int32, [C.c_void_p, C.POINTER(FlowHead), C.c_void_p, C.c_float, C.c_int32, C.c_void_p]),
     "ams_tier_plan": (C.c_int32, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                   C.c_int64, C.c_void_p, C.POINTER(C.c_int64)]),
     "ams_ctx_build_rows": (C.c_int32, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_void_p,

@@ -558,6 +558,37 @@ ams_status ams_ctx_row_states(const ams_ctx* c, int32_t* states) {
   return AMS_OK;
 }
 
+ams_status ams_ctx_flow(ams_ctx* c, const ams_flow_head* head, float* x, float tau0, int32_t n_steps,
+                        void* stream) {
+  g_err.clear();
+  if (!c || !head) return fail(AMS_EINVAL, "context and head must not be NULL");
+  ams::Ctx& x_ = c->c;
+  std::string e;
+  if (int s = ams::ctx_absorb_status(x_, e)) return fail(s, e);
+  if (x_.book.state != ams::READY) return fail(AMS_ESTATE, "context (or a row of it) is not built");
+  const int a = head->action_dim, T = head->n_tokens;
+  if (a < 1 || a > ams::FLOW_MAX_ACTION_DIM) return fail(AMS_EINVAL, "action_dim must be in [1, 256]");
+  if (T < 1) return fail(AMS_EINVAL, "n_tokens must be >= 1");
+  if (n_steps < 0) return fail(AMS_EINVAL, "n_steps must be >= 0");
+  if (!(tau0 >= 0.f && tau0 < 1.f)) return fail(AMS_EINVAL, "tau0 must be in [0, 1)");
+  for (int b = 0; b < x_.lay.batch; ++b)
+    if (x_.book.len[b] + T > x_.lay.capacity)
+      return fail(AMS_ECAPACITY, "row " + std::to_string(b) + ": context + action tokens exceed the capacity");
+  const ams::Cfg& m = x_.model->cfg;
+  const size_t es = ams::elem_size(m), d = m.d_model, B = x_.lay.batch;
+  const int dev = x_.model->device;
+  if (!dev_range(head->w_in, d * a * es, dev, "w_in", e) || !dev_range(head->w_t, d * es, dev, "w_t", e) ||
+      !dev_range(head->w_out, (size_t)a * d * es, dev, "w_out", e) ||
+      !dev_range(x, B * (size_t)T * a * 4, dev, "x", e))
+    return fail(AMS_EINVAL, e);
+  const ams::FlowHeadView fh{head->w_in, head->w_t, head->w_out, a, T};
+  if (ams::ctx_flow(x_, fh, x, tau0, n_steps, (hipStream_t)stream, e) != hipSuccess) {
+    x_.book.invalidate();
+    return fail(AMS_EHIP, e);
+  }
+  return AMS_OK;
+}
+
 ams_status ams_tier_plan(int32_t n_rows, const int32_t* priority, const int64_t* last_use, const int32_t* pages,
                          const int32_t* droppable, const int32_t* resident, const int32_t* pinned,
                          int64_t pages_needed, int32_t* action, int64_t* pages_freed) {

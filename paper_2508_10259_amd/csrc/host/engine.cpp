@@ -327,6 +327,37 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
   return hipSuccess;
 }
 
+hipError_t ctx_flow(Ctx& c, const FlowHeadView& fh, float* x, float tau0, int n_steps, hipStream_t s,
+                    std::string& err) {
+  const Cfg& m = c.model->cfg;
+  const int B = c.lay.batch, T = fh.n_tokens, a = fh.a, d = m.d_model;
+  if (n_steps <= 0) return hipSuccess;
+  std::vector<int32_t> counts(B, T), start(c.book.len.begin(), c.book.len.end());
+  Plan p = plan_passes(B, counts.data(), start.data(), c.lay.pass_tokens);
+  std::vector<int32_t>& h = c.meta_host;
+  std::fill(h.begin(), h.end(), 0);
+  std::copy(p.row.begin(), p.row.end(), h.begin());
+  std::copy(p.pos.begin(), p.pos.end(), h.begin() + B);
+  std::copy(p.off.begin(), p.off.end(), h.begin() + 2 * B);
+  int32_t* md = c.meta();
+  TRY(hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  const float dt = (1.0f - tau0) / (float)n_steps;
+  for (int k = 0; k < n_steps; ++k) {
+    const float tau = tau0 + (float)k * dt;
+    for (size_t pi = 0; pi < p.passes.size(); ++pi) {
+      const Pass& ps = p.passes[pi];
+      Segs sg{md + ps.seg_begin, md + B + ps.seg_begin, md + 2 * B + ps.seg_begin + (int)pi, ps.n_seg, ps.n_tok,
+              ps.max_len, ps.max_end};
+      float* xp = x + (size_t)ps.tok_src * a;  // every row brings T tokens: the pass's first token
+      TRY(flow_embed(c.model->st, xp, fh.w_in, fh.w_t, tau, ps.n_tok, a, d, c.h(), s));
+      for (int l = 0; l < m.n_layers; ++l)
+        if (layer_tokens(c, l, ps.n_tok, sg, s, err) != hipSuccess) return hipErrorLaunchFailure;
+      TRY(flow_update(c.model->st, c.h(), fh.w_out, m.rms_eps, dt, ps.n_tok, a, d, xp, s));
+    }
+  }
+  return hipSuccess;
+}
+
 // Decode-pass GEMV inputs are fp16 pairs (hi + lo, lo the rounding error of
 // hi) in fp16 compute, so the action tokens' own products see their inputs to
 // about 22 significant bits; the MFMA count doubles at most, the weight stream

@@ -134,6 +134,17 @@ int ctx_offload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* len
 int ctx_reload_rows(Ctx& c, const int32_t* rows, int n_rows, const int32_t* lens, void* const* host_dev,
                     hipStream_t s, std::string& err);
 
+// Flow-matching sampling of every row's action chunk (x: device fp32
+// [batch][n_tokens][a], updated in place): n_steps Euler steps from tau0, each
+// running the chunk's tokens through every layer at positions lens[b].. (their
+// K/V are scratch) between the head's input and output projections.
+struct FlowHeadView {
+  const void *w_in, *w_t, *w_out;
+  int a, n_tokens;
+};
+hipError_t ctx_flow(Ctx& c, const FlowHeadView& fh, float* x, float tau0, int n_steps, hipStream_t s,
+                    std::string& err);
+
 // Takes in an error a kernel of an earlier call reported asynchronously (see
 // RowBook::absorb_async_error) and clears the word.
 int ctx_absorb_status(Ctx& c, std::string& err);

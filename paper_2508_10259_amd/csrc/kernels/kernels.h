@@ -242,6 +242,16 @@ hipError_t rows_xfer(bool to_host, const XferRow* rows, int n_rows, int L, int H
                      size_t slab_layer, const int32_t* pt, int ppr, float* h_last, void* h16, void* h16lo, int d,
                      hipStream_t s);
 
+// Flow-matching action head (flow.hip), over the n_tok tokens of a pass (x and
+// h of the pass's first token): flow_embed h[t] = W_in x[t] + tau w_t (W_in
+// [d][a], w_t [d] in the storage type st); flow_update x[t] += dt W_out
+// (h[t] / sqrt(mean(h[t]^2) + eps)) (W_out [a][d]).  1 <= a <= FLOW_MAX_ACTION_DIM.
+constexpr int FLOW_MAX_ACTION_DIM = 256;
+hipError_t flow_embed(int st, const float* x, const void* w_in, const void* w_t, float tau, int n_tok, int a, int d,
+                      float* h, hipStream_t s);
+hipError_t flow_update(int st, const float* h, const void* w_out, float eps, float dt, int n_tok, int a, int d,
+                       float* x, hipStream_t s);
+
 // Measured peaks (peaks.hip): a grid-stride copy of `bytes` (16-byte aligned
 // pointers and size) from src to dst; a grid-stride read of src whose per-thread
 // sums land in out[grid * 256]; `iters` rounds of fp16 MFMA chains per wave on

@@ -215,6 +215,13 @@ class DeviceContext:
                    "ams_ctx_pages")
         return pt, refs, int(used.value)
 
+    def flow(self, head: "DeviceFlowHead", x: torch.Tensor, tau0: float, n_steps: int) -> torch.Tensor:
+        """Euler-integrate every row's action latent x [batch][n_tokens][action_dim] (fp32, in place)."""
+        assert x.dtype == torch.float32 and x.is_contiguous() and x.shape[0] == self.batch
+        capi.check(self.lib.ams_ctx_flow(self.handle, C.byref(head.c), x.data_ptr(), C.c_float(tau0), n_steps,
+                                         _stream()), "ams_ctx_flow")
+        return x
+
     def row_host_bytes(self, length: int) -> int:
         return int(self.lib.ams_ctx_row_host_bytes(self.handle, length))
 
@@ -277,3 +284,14 @@ def index_hash(data: torch.Tensor, seg_bytes: int, ws: Optional[torch.Tensor] = 
     capi.check(lib.ams_index_hash(data.data_ptr(), n, seg_bytes, ws.data_ptr(), ws.numel() * 8, out.data_ptr(),
                                   _stream()), "ams_index_hash")
     return out, ws
+
+
+class DeviceFlowHead:
+    """A flow-matching action head's weights on the device (model dtype): w_in [d][a], w_t [d],
+    w_out [a][d], from encoded numpy arrays."""
+
+    def __init__(self, spec, w_in: np.ndarray, w_t: np.ndarray, w_out: np.ndarray, n_tokens: int, device="cuda"):
+        self.t = [to_device(w, spec.dtype, device) for w in (w_in, w_t, w_out)]
+        a = w_in.shape[1]
+        self.c = capi.FlowHead(self.t[0].data_ptr(), self.t[1].data_ptr(), self.t[2].data_ptr(), a, n_tokens)
+        self.action_dim, self.n_tokens = a, n_tokens

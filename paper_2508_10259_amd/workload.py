@@ -453,6 +453,25 @@ def make_observation(spec: ModelSpec, seed: int, step: int, row: int, n: int) ->
     return encode(x, spec.dtype)
 
 
+_T_FLOW = 9
+
+
+def make_flow_head(spec: ModelSpec, action_dim: int, seed: int = 0):
+    """Weights of a flow-matching action head (encoded in the model dtype): w_in [d][a] with
+    N(0, 1/a) entries (unit-scale token embeddings from unit-scale latents), w_t [d] N(0, 1),
+    w_out [a][d] N(0, 0.02)."""
+    d = spec.d_model
+    w_in = _rng(seed, _T_FLOW, 1).standard_normal((d, action_dim), dtype=np.float32) / np.float32(np.sqrt(action_dim))
+    w_t = _rng(seed, _T_FLOW, 2).standard_normal((d,), dtype=np.float32)
+    w_out = _rng(seed, _T_FLOW, 3).standard_normal((action_dim, d), dtype=np.float32) * np.float32(0.02)
+    return encode(w_in, spec.dtype), encode(w_t, spec.dtype), encode(w_out, spec.dtype)
+
+
+def make_latent(seed: int, key: int, rows: int, n_tokens: int, action_dim: int) -> np.ndarray:
+    """N(0, 1) action latents [rows][n_tokens][action_dim] (fp32): the noise of a cold start."""
+    return _rng(seed, _T_FLOW, 100, key).standard_normal((rows, n_tokens, action_dim), dtype=np.float32)
+
+
 def random_gaussian(shape: Sequence[int], seed: int, *key: int, dtype: str = "f32",
                     std: float = 1.0) -> np.ndarray:
     """A generic seeded N(0, std) array, encoded in ``dtype`` (for kernel-level tests)."""
