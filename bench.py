@@ -53,12 +53,27 @@ def step_bytes(spec, lens, n_actions, es=2):
     return total
 
 
-def build_flops(spec, lens):
-    """Matmul + attention FLOPs of ctx_build."""
+def build_flops(spec, lens, starts=None):
+    """Matmul + attention FLOPs of ctx_build; starts[b]: the first position row b computes
+    (the positions before it sit in prefix pages it shares with an earlier row)."""
     d, L = spec.d_model, spec.n_layers
-    m = sum(int(l) for l in lens)
-    pairs = sum(int(l) * (int(l) + 1) // 2 for l in lens)
+    starts = starts if starts is not None else [0] * len(lens)
+    m = sum(int(l) - int(s) for l, s in zip(lens, starts))
+    pairs = sum(int(l) * (int(l) + 1) // 2 - int(s) * (int(s) + 1) // 2 for l, s in zip(lens, starts))
     return 2 * spec.matmul_params * m + 4 * d * L * pairs
+
+
+def shared_starts(pt, lens, page=64):
+    """First computed position of every row of a build that shares prefix pages: row b attaches
+    the leading run of its pages that an earlier row of the same build holds."""
+    seen, starts = set(), []
+    for b, l in enumerate(lens):
+        k = 0
+        while k < (int(l) - 1) // page and int(pt[b, k]) in seen:
+            k += 1
+        starts.append(k * page)
+        seen.update(int(x) for x in pt[b, :(int(l) + page - 1) // page])
+    return starts
 
 
 def extension_flops(spec, lens_before, n_new):
@@ -287,17 +302,27 @@ def run_window(ctx, wl, epochs, pool, rebuild, steps, A, tokens, logits, mode):
         e1.record()
         marks.append((phase, e0, e1, work))
 
+    def build_work(lens):
+        # a build that shares prefix pages computes only the pages no earlier row holds (the
+        # page table is the library's host copy: reading it does not wait for the GPU)
+        if not ctx.share_prefix:
+            return build_flops(spec, lens)
+        return build_flops(spec, lens, shared_starts(ctx.pages()[0], lens))
+
     w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     w0.record()
-    timed("build", build_flops(spec, epochs[0][1]), lambda: ctx.build(*epochs[0]))
+    timed("build", 0, lambda: ctx.build(*epochs[0]))
+    marks[-1] = marks[-1][:3] + (build_work(epochs[0][1]),)
     for s_ in range(steps):
         if mode == "cached" and inv and s_ and s_ % inv == 0:
             ctx.invalidate()
             e = epochs[(s_ // inv) % len(epochs)]
-            timed("build", build_flops(spec, e[1]), lambda e=e: ctx.build(*e))
+            timed("build", 0, lambda e=e: ctx.build(*e))
+            marks[-1] = marks[-1][:3] + (build_work(e[1]),)
         elif mode == "recompute" and s_:
             ctx.invalidate()
-            timed("build", build_flops(spec, epochs[0][1]), lambda: ctx.build(*epochs[0]))
+            timed("build", 0, lambda: ctx.build(*epochs[0]))
+            marks[-1] = marks[-1][:3] + (build_work(epochs[0][1]),)
         elif mode == "staggered" and s_:
             rows, packed, plens = rebuild[s_ % inv]
             ctx.invalidate_rows(rows)

@@ -143,6 +143,7 @@ class DeviceContext:
         """n_pages / share_prefix: a paged context (ams_ctx_create_paged) with that many K/V pages per
         layer (0: a page for every position) whose rows share prefix pages when share_prefix."""
         self.lib, self.model, self.batch, self.capacity = model.lib, model, batch, capacity
+        self.share_prefix = bool(share_prefix)
         paged = n_pages is not None or share_prefix
         flags = capi.AMS_CTX_SHARE_PREFIX if share_prefix else 0
         if paged:

@@ -55,6 +55,26 @@ def test_build_flops():
     assert bench.build_flops(s, lens) == sum(bench.build_flops(s, np.array([x])) for x in lens)
 
 
+def test_shared_build_flops():
+    """A row that attaches k shared prefix pages computes positions 64 k .. L - 1 only: the FLOPs of
+    its build are those of the whole row less those of a row of 64 k tokens; the first positions
+    are read from the page table (the leading run of pages an earlier row of the build holds)."""
+    wl, s, L, d, F = _shape("7b-b64-ragged")
+    lens = [300, 250, 130, 200]
+    pt = np.array([[0, 1, 2, 3, 4],
+                   [0, 1, 5, 6, 7],   # attaches pages 0, 1
+                   [0, 8, 9, 10, 11],  # attaches page 0 only (page 8 is its own)
+                   [12, 1, 13, 14, 15]])  # page 0 differs: nothing attached, though page 1 repeats
+    starts = bench.shared_starts(pt, lens)
+    assert starts == [0, 128, 64, 0]
+    # at most floor((L - 1) / 64) pages are attached: the row's last position is always computed
+    assert bench.shared_starts(np.array([[0, 1, 2], [0, 1, 2]]), [192, 128]) == [0, 64]
+    got = bench.build_flops(s, lens, starts)
+    want = sum(bench.build_flops(s, [l]) - bench.build_flops(s, [k]) for l, k in zip(lens, starts))
+    assert got == want
+    assert bench.build_flops(s, lens, [0] * 4) == bench.build_flops(s, lens)
+
+
 def test_extension_flops():
     """Appending n tokens to a row of L committed tokens: 2 P_mm FLOPs per new token, and new token
     i attends to L + i + 1 keys (4 d n_layers FLOPs per query-key pair).  The 7B batch-64 step
