@@ -737,7 +737,8 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
   constexpr int CH = G::CH, NC = G::NC, KS = G::KS, BK = G::BK, IT = G::IT, HALF = DH / 2;
   __shared__ float wm[DECODE_MAX_WAVES], wl[DECODE_MAX_WAVES], wacc[DECODE_MAX_WAVES][DH];
   const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, nw = blockDim.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: block loops branch on scalars
   const int ks = lane / NC, dc = lane % NC, i0 = dc * CH;  // this lane: key subgroup, first dimension
   const int d = H * DH;
   const int p = lens[b] + jpos;  // position of this pass's token
@@ -746,12 +747,16 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
   const int k0 = sp * chunk < T_ ? sp * chunk : T_;
   const int k1 = (k0 + chunk < T_) ? k0 + chunk : T_;
 
-  uint4 kr[IT], vr[IT];
   // one block: key kb + it*KS + ks of each iteration; slot p is not read (its K/V come from registers).
-  // The block's BK <= 64 keys (kb < k1) lie in at most two pages, looked up once.
-  auto load_block = [&](int kb) {
+  // The block's BK <= 64 keys lie in at most two pages, looked up once.  Every lane
+  // loads whether or not its key exists (a key past the split or slot p reads 16
+  // bytes of this row's query instead), so the loads in flight follow one fixed
+  // pattern and the wait before a block covers only its own data; the block
+  // replaces those values where they are used.
+  const uint4* dummy = (const uint4*)(qkv + (size_t)b * 3 * d);
+  auto load_block = [&](int kb, uint4 (&kr)[IT], uint4 (&vr)[IT]) {
     // kb is uniform across the wave: the page indices are scalar loads (scalar cache)
-    const int ka = __builtin_amdgcn_readfirstlane(kb >> 6);
+    const int ka = __builtin_amdgcn_readfirstlane(min(kb, k1 - 1) >> 6);
     const int kz = __builtin_amdgcn_readfirstlane(min(kb + BK - 1, k1 - 1) >> 6);
     const int pa = ld_const_uniform(kp.pt, (size_t)b * kp.ppr + ka), pz = ld_const_uniform(kp.pt, (size_t)b * kp.ppr + kz);
 #pragma unroll
@@ -759,12 +764,21 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
       const int key = kb + it * KS + ks;
       const bool ok = key < k1 && key != p;
       const size_t e = kv_slot((key >> 6) == ka ? pa : pz, H, h, key & (KV_PAGE - 1), DH) + i0;
-      kr[it] = ok ? *(const uint4*)(kslab + e) : uint4{0u, 0u, 0u, 0u};
-      vr[it] = ok ? *(const uint4*)(vslab + e) : uint4{0u, 0u, 0u, 0u};
+      // the address is chosen by a select the compiler cannot see through, so it
+      // stays one unconditional load instead of a branch per source
+      uint64_t ak = ok ? (uint64_t)(kslab + e) : (uint64_t)dummy;
+      uint64_t av = ok ? (uint64_t)(vslab + e) : (uint64_t)dummy;
+      asm("" : "+v"(ak), "+v"(av));
+      typedef unsigned u32x4g __attribute__((ext_vector_type(4)));
+      typedef const u32x4g __attribute__((address_space(1))) gvec;  // global, not flat
+      const u32x4g kx = *(gvec*)ak, vx = *(gvec*)av;
+      kr[it] = uint4{kx[0], kx[1], kx[2], kx[3]};  // what a key that does not exist loaded is never used (see block)
+      vr[it] = uint4{vx[0], vx[1], vx[2], vx[3]};
     }
   };
   const int kb0 = k0 + wave * BK;
-  if (kb0 < k1) load_block(kb0);  // in flight during the prologue
+  uint4 kA[IT], vA[IT], kB[IT], vB[IT];
+  load_block(kb0, kA, vA);  // in flight during the prologue
 
   // this lane's CH dimensions of the rotated, scaled query and of the new
   // token's key and value, rounded to the slab type as every later step reads them
@@ -802,8 +816,8 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
 #pragma unroll
   for (int e = 0; e < CH; ++e) acc[e] = 0.f;
 
-  for (int kb = kb0; kb < k1; kb += nw * BK) {
-    if (kb != kb0) load_block(kb);
+  // one block of keys: scores, online-softmax rescale, P.V
+  auto block = [&](int kb, const uint4 (&kr)[IT], const uint4 (&vr)[IT]) {
     float sc[IT];
     float mx = -INFINITY;
 #pragma unroll
@@ -831,10 +845,23 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
       float vv[CH];
       Raw<T>::cvt(vr[it], vv);
 #pragma unroll
-      for (int e = 0; e < CH; ++e) acc[e] = fmaf(pe, key == p ? vn[e] : vv[e], acc[e]);
+      // keys past the split: weight 0 and value 0 (what they loaded may not be finite)
+      for (int e = 0; e < CH; ++e) acc[e] = fmaf(pe, key == p ? vn[e] : (key < k1 ? vv[e] : 0.f), acc[e]);
     }
     l = l * alpha + cross_sum<NC>(ps);
     m = m_new;
+  };
+  // two register sets: the next block's loads are in flight while this one computes
+  const int stride = nw * BK;
+  // (the scheduling barriers keep each block's arithmetic, and with it the wait
+  // for its data, after the next block's loads are issued)
+  for (int kb = kb0; kb < k1; kb += 2 * stride) {
+    load_block(kb + stride, kB, vB);
+    __builtin_amdgcn_sched_barrier(0);
+    block(kb, kA, vA);
+    load_block(kb + 2 * stride, kA, vA);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kb + stride < k1) block(kb + stride, kB, vB);
   }
   // sum the key subgroups; lanes of subgroup 0 then hold the wave's partial output
 #pragma unroll

@@ -619,6 +619,14 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 // workgroups per CU, and on the 7B shapes it beat four chunks by 1-5% (QKV at
 // 16 rows 23.4 -> 22.1 us, O at 64 rows 15.1 -> 14.4 us; only O at 16 rows lost,
 // 9.6 -> 9.9 us); six or eight chunks cost occupancy and were slower.
+// The activation fragments of a K step are all requested before its first
+// MFMA, so their LDS round trips overlap (one per MFMA otherwise); with 8 or
+// more fragments a wave keeps two weight chunks in flight instead of three,
+// which holds it at 120 VGPRs (four waves per SIMD).  On the 7B shapes at 64
+// rows: gate|up 54.0 -> 50.8 us, QKV 32.7 -> 31.6 us, down 29.3 -> 25.5 us.
+// Reducing the split-K partial sums in each tile's last split to finish
+// (a counter per tile) instead of a separate kernel measured 1-5 us slower
+// per projection: the O and down projections' 32 tiles then reduce on 32 CUs.
 constexpr int WIDE_ROWS = 128, WIDE_WP = 3, WIDE_LDK = 128 + 16;
 
 // weight fragments of one chunk of a wave's 16 rows
@@ -633,6 +641,7 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   constexpr int NX = LO == 2 ? 2 : 1;               // activation arrays (hi, lo)
   constexpr int XCH = NX * MB * 16 * 16;             // 16-byte pieces of one staged chunk
   constexpr int XPT = (XCH + 511) / 512;             // pieces per thread
+  constexpr int WP = MB * NX >= 6 ? 2 : WIDE_WP;     // weight chunks in flight
   extern __shared__ __attribute__((aligned(16))) f16 xs[];  // [2 stages][NX][MB*16][WIDE_LDK]
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -648,7 +657,7 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   auto chunk = [&](int t) { const int u = t + rot; return s0 + (u >= n ? u - n : u); };
 
   const f16* wrow = W + (size_t)(n0 + r) * K + g * 8;
-  uint4 wr[WIDE_WP][4];
+  uint4 wr[WP][4];
   // activation staging, up to 4 pieces of 16 bytes per thread (named registers:
   // an array here ends up on the stack).  Piece e = tid + 512 q: array
   // e / (MB*256), token row (e / 16) % (MB*16) (rows past M read row M-1: they
@@ -681,37 +690,41 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
-  for (int p = 0; p < WIDE_WP; ++p)
+  for (int p = 0; p < WP; ++p)
     if (p < n) wide_wload(wr[p], wrow, chunk(p));
   AMS_WIDE_XLOAD(chunk(0));
   AMS_WIDE_XSTORE(0);
   if (n > 1) AMS_WIDE_XLOAD(chunk(1));
   __syncthreads();
 
-  for (int tb = 0; tb < n; tb += WIDE_WP) {
+  for (int tb = 0; tb < n; tb += WP) {
 #pragma unroll
-    for (int p = 0; p < WIDE_WP; ++p) {
+    for (int p = 0; p < WP; ++p) {
       const int t = tb + p;
       if (t < n) {  // uniform across the workgroup (n is)
         const f16* xb = xs + (size_t)((t & 1) * NX) * MB * 16 * WIDE_LDK;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+          // every activation fragment of this K step requested before its first MFMA
+          half8 bf[NX][MB];
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int a = 0; a < NX; ++a)
+              bf[a][mb] = *(const half8*)(xb + (size_t)(a * MB * 16 + mb * 16 + r) * WIDE_LDK + 32 * i + 8 * g);
           const half8 wf = as_half8(wr[p][i]);
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const f16* bp = xb + (size_t)(mb * 16 + r) * WIDE_LDK + 32 * i + 8 * g;
-            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, *(const half8*)bp, acc[mb], 0, 0, 0);
-            if constexpr (LO == 2)
-              acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                  wf, *(const half8*)(bp + (size_t)MB * 16 * WIDE_LDK), acc[mb], 0, 0, 0);
-          }
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int a = 0; a < NX; ++a)
+              acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, bf[a][mb], acc[mb], 0, 0, 0);
         }
         // the activation loads go out before the weight loads of this round:
         // vmcnt retires in issue order, so staging chunk t+2 next round then
         // waits only for loads older than the newest weight chunk
         if (t + 1 < n) AMS_WIDE_XSTORE((t + 1) & 1);
         if (t + 2 < n) AMS_WIDE_XLOAD(chunk(t + 2));
-        if (t + WIDE_WP < n) wide_wload(wr[p], wrow, chunk(t + WIDE_WP));
+        if (t + WP < n) wide_wload(wr[p], wrow, chunk(t + WP));
         __syncthreads();
       }
     }

@@ -584,12 +584,15 @@ def test_merge_norm(probe, M, splits):
 
 
 @pytest.mark.parametrize("M", [5, 17, 33, 64])
-@pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (384, 4096, 8), (256, 1152, 3)])
+@pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (384, 4096, 8), (256, 1152, 3), (2048, 4096, 8),
+                                        (1024, 5120, 8), (1152, 1408, 4), (512, 512, 4)])
 @pytest.mark.parametrize("pair", [False, True])
 def test_gemm_wide(probe, M, N, K, splits, pair):
     """Wide decode GEMM (128 weight rows per workgroup, LDS-staged activations) and its
     reductions: partial sums per K split, store / residual / SwiGLU epilogues, against the
-    exact products of the fp16 (pair) inputs."""
+    exact products of the fp16 (pair) inputs.  The splits cover 1 to 8 chunks of 128, uneven
+    splits (11 chunks over 4) and chunk counts that are not multiples of the kernel's two or
+    three weight chunks in flight."""
     import torch
     log(f"gemm_wide M={M} N={N} K={K} splits={splits} pair={pair}")
     x = W.random_gaussian((M, K), 61, M, K, dtype="f32")
