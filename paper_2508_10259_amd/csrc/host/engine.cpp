@@ -403,7 +403,7 @@ struct Rows {
 // unnormalised pair and the reduction divides by rms (merge_norm).
 static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* hhi, const void* hlo, const void* W,
                             int N, int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err,
-                            const float* ss = nullptr) {
+                            const float* ss = nullptr, QkvParts* defer = nullptr) {
   const Model& md = *g.c->model;
   const float eps = md.cfg.rms_eps;
   if (fused_norm(*g.c, g.n)) {
@@ -418,8 +418,13 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
     if (wide) {  // partial sums of 128-row tiles, then the epilogue
       const int splits = decode_wsplit(N, K);
       TRY(gemm_wide(g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), s));
-      if (epi == EPI_SWIGLU) TRY(part_swiglu(g.c->kpart(), splits, g.n, N, out, olo, s, ss, K, eps));
-      else TRY(part_store(g.c->kpart(), splits, g.n, N, (float*)out, s, ss, K, eps));
+      if (defer) {  // the consumer adds the partial sums itself
+        *defer = QkvParts{g.c->kpart(), splits, ss, K / 256, eps};
+      } else if (epi == EPI_SWIGLU) {
+        TRY(part_swiglu(g.c->kpart(), splits, g.n, N, out, olo, s, ss, K, eps));
+      } else {
+        TRY(part_store(g.c->kpart(), splits, g.n, N, (float*)out, s, ss, K, eps));
+      }
     } else {
       TRY(gemm(md.ct, epi, g.u(), W, g.n, N, K, out, ldo, s, ulo, nullptr, olo));
     }
@@ -467,11 +472,13 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
   void* alo = f16 ? g.alo() : nullptr;
   // sums of squares of h from the previous residual reduction (from layer 1 on)
   float* ss = merge_norm(c, B) ? g.ss() : nullptr;
+  // on the wide path the attention adds the QKV projection's partial sums itself
+  QkvParts qp{};
   if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err,
-                l > 0 ? ss : nullptr) != hipSuccess)
+                l > 0 ? ss : nullptr, &qp) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, g.pages(), c.splits, c.rope(),
-                  g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo));
+                  g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo, qp));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
   TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s, ss));
   if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err, ss) != hipSuccess)

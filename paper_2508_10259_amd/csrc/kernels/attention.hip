@@ -732,10 +732,11 @@ template <typename T, int DH>
 __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
     const float* __restrict__ qkv, const int32_t* __restrict__ lens, int jpos, int H, KvPages kp, int splits,
     const float2* __restrict__ rope, T* __restrict__ kslab, T* __restrict__ vslab, float* __restrict__ part,
-    T* __restrict__ o, T* __restrict__ olo, float scale) {
+    T* __restrict__ o, T* __restrict__ olo, float scale, QkvParts qp) {
   using G = DecGeo<T, DH>;
   constexpr int CH = G::CH, NC = G::NC, KS = G::KS, BK = G::BK, IT = G::IT, HALF = DH / 2;
   __shared__ float wm[DECODE_MAX_WAVES], wl[DECODE_MAX_WAVES], wacc[DECODE_MAX_WAVES][DH];
+  __shared__ float qs[3 * DH];  // this head's q, k, v of row b when they come as partial sums
   const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, nw = blockDim.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: block loops branch on scalars
@@ -785,20 +786,41 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
   float q[CH], kn[CH], vn[CH];
   {
     const float* qrow = qkv + (size_t)b * 3 * d + h * DH;
+    int kstride = d;  // q, k, v of the head at qrow, qrow + kstride, qrow + 2 kstride
+    if (qp.part) {
+      // the split-K partial sums of the QKV projection, added in split order and
+      // divided by the row's rms as the projection's own reduction would
+      float t = 0.f;
+      if (qp.ss)
+        for (int k = lane; k < qp.nss; k += 64) t += qp.ss[(size_t)b * qp.nss + k];
+#pragma unroll
+      for (int o_ = 32; o_ > 0; o_ >>= 1) t += __shfl_xor(t, o_, 64);
+      const float rr = qp.ss ? 1.0f / sqrtf(t * (1.0f / (float)d) + qp.eps) : 1.f;
+      const size_t MN = (size_t)gridDim.z * 3 * d;
+      for (int x = tid; x < 3 * DH; x += blockDim.x) {
+        const size_t col = (size_t)b * 3 * d + (size_t)(x / DH) * d + h * DH + x % DH;
+        float v = 0.f;
+        for (int sp_ = 0; sp_ < qp.splits; ++sp_) v += qp.part[sp_ * MN + col];
+        qs[x] = v * rr;
+      }
+      __syncthreads();
+      qrow = qs;
+      kstride = DH;
+    }
     const bool lo = i0 < HALF;  // chunks never straddle the rotation halves
     const int j0 = lo ? i0 : i0 - HALF;
 #pragma unroll
     for (int e = 0; e < CH; ++e) {
       const float2 cs = rope[(size_t)p * HALF + j0 + e];
       const float qa = qrow[j0 + e], qc = qrow[j0 + e + HALF];
-      const float ka = qrow[d + j0 + e], kc = qrow[d + j0 + e + HALF];
+      const float ka = qrow[kstride + j0 + e], kc = qrow[kstride + j0 + e + HALF];
       const float qr = lo ? qa * cs.x - qc * cs.y : qa * cs.y + qc * cs.x;
       const float kr_ = lo ? ka * cs.x - kc * cs.y : ka * cs.y + kc * cs.x;
       q[e] = qr * scale;
       T t;
       st<T>(&t, 0, kr_);
       kn[e] = ld<T>(&t, 0);
-      st<T>(&t, 0, qrow[2 * d + i0 + e]);
+      st<T>(&t, 0, qrow[2 * kstride + i0 + e]);
       vn[e] = ld<T>(&t, 0);
     }
   }
@@ -919,7 +941,8 @@ __global__ void k_attn_merge(const float* __restrict__ part, int H, int splits, 
 template <typename T>
 static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
                            int splits,
-                           const float2* rope, void* k, void* v, float* part, void* o, void* olo, hipStream_t s) {
+                           const float2* rope, void* k, void* v, float* part, void* o, void* olo, hipStream_t s,
+                           QkvParts qp) {
   const float scale = 1.0f / sqrtf((float)dh);
   const dim3 grid(splits, H, B);
   // waves: enough for the longest split (ceil(cap / splits) keys) at one block
@@ -930,21 +953,22 @@ static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int 
   nw = nw < dh / 64 ? dh / 64 : (nw > DECODE_MAX_WAVES ? DECODE_MAX_WAVES : nw);
   if (dh == 64)
     hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
-                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp);
   else
     hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
-                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale);
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp);
   return hipGetLastError();
 }
 
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
                        int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s,
-                       void* olo) {
+                       void* olo, QkvParts qp) {
+  if (qp.part && (qp.splits < 1 || (qp.ss && qp.nss < 1))) return hipErrorInvalidValue;
   if (ct == DT_F32) {
     if (olo) return hipErrorInvalidValue;
-    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, nullptr, s);
+    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, nullptr, s, qp);
   }
-  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, olo, s);
+  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, olo, s, qp);
 }
 
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s,

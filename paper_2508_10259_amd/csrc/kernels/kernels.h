@@ -153,9 +153,20 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPage
 // otherwise the keys are cut into `splits` chunks whose partials (m, l, acc)
 // go to `part` for attn_merge.  olo (fp16 only, or NULL): the rounding error of
 // the fp16 output o, written by whichever of the two kernels writes o.
+// The QKV projection's split-K partial sums (splits x [B][3d] floats) in place of
+// qkv: the attention adds them in split order and divides row b by its rms
+// from ss[b][0..nss) (sums of squares of the unnormalised residual, width d;
+// NULL: no scale), as part_store would.
+struct QkvParts {
+  const float* part = nullptr;
+  int splits = 0;
+  const float* ss = nullptr;
+  int nss = 0;
+  float eps = 0.f;
+};
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh,
                        int cap, KvPages kp, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
-                       hipStream_t s, void* olo = nullptr);
+                       hipStream_t s, void* olo = nullptr, QkvParts qp = QkvParts{});
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
                       hipStream_t s, void* olo = nullptr);
 

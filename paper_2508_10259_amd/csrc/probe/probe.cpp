@@ -85,6 +85,23 @@ int ams_probe_attn_decode(int ct, const float* qkv, const int32_t* lens, int jpo
 }
 
 // Causal attention of packed segments (row[s], pos[s], off[s..s+1]) over their rows' K/V pages.
+int ams_probe_attn_decode_parts(int ct, const float* qpart, int qsplits, const float* ss, int nss, float eps,
+                                const int32_t* lens, int jpos, int B, int H, int dh, int cap, const int32_t* pt,
+                                int splits, const void* rope, void* kslab, void* vslab, float* part, void* o, void* olo,
+                                void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  ams::QkvParts qp;
+  qp.part = qpart;
+  qp.splits = qsplits;
+  qp.ss = ss;
+  qp.nss = nss;
+  qp.eps = eps;
+  hipError_t e = ams::attn_decode(ct, qpart, lens, jpos, B, H, dh, cap, ams::KvPages{pt, cap / 64}, splits,
+                                  (const float2*)rope, kslab, vslab, part, o, s, olo, qp);
+  if (e == hipSuccess && splits > 1) e = ams::attn_merge(ct, part, B, H, dh, splits, o, s, olo);
+  return (int)e;
+}
+
 int ams_probe_attn_prefill(int ct, const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off,
                            int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const int32_t* pt,
                            const void* rope, const void* kslab, const void* vslab, void* o, void* stream) {

@@ -531,6 +531,55 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
         assert torch.equal(olo, (h - h.half().float()).half())
 
 
+@pytest.mark.parametrize("qsplits,norm", [(1, True), (4, True), (8, False)])
+@pytest.mark.parametrize("splits", [1, 3])
+def test_attn_decode_parts(probe, qsplits, norm, splits):
+    """Decode attention fed the QKV projection's split-K partial sums (and the row sums of
+    squares for its RMSNorm scale) gives, bit for bit, the output and the appended K/V of the
+    attention fed the reduced projection (part_store with the same scale)."""
+    import torch
+    B, H, dh, cap, jpos, eps = 5, 4, 128, 256, 2, 1e-5
+    d = H * dh
+    lens = [3, 60, 64, 130, 190]
+    log(f"attn_decode_parts qsplits={qsplits} norm={norm} splits={splits}")
+    pq = W.random_gaussian((qsplits, B, 3 * d), 91, qsplits, dtype="f32")
+    ssv = (np.random.default_rng(92).random((B, d // 256)) * 300 + 10).astype(np.float32)
+    K = W.random_gaussian((B, H, cap, dh), 93, cap, dtype="f32").astype(np.float16)
+    V = W.random_gaussian((B, H, cap, dh), 94, cap, dtype="f32").astype(np.float16)
+    perm = np.random.default_rng(95).permutation(B * (cap // 64)).astype(np.int32)
+    pt_d = torch.from_numpy(perm).cuda()
+    tab_d = _dev(_rope_tab(cap, dh), "f32")
+    lens_d = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    pq_d = torch.from_numpy(pq.reshape(-1).copy()).cuda()
+    ss_d = torch.from_numpy(ssv).cuda() if norm else None
+    qkv = torch.zeros((B, 3 * d), dtype=torch.float32, device="cuda")
+    if norm:
+        assert probe.ams_probe_part_store_norm(_ptr(pq_d), qsplits, B, 3 * d, _ptr(qkv), _ptr(ss_d), d,
+                                               C.c_float(eps), _stream()) == 0
+    else:
+        assert probe.ams_probe_part_store(_ptr(pq_d), qsplits, B, 3 * d, _ptr(qkv), _stream()) == 0
+    res = []
+    for fused in (False, True):
+        K_d, V_d = _dev(_to_pages(K, perm), "f16"), _dev(_to_pages(V, perm), "f16")
+        part = torch.zeros((B * H * (cap // 64) * (dh + 2),), dtype=torch.float32, device="cuda")
+        o = torch.zeros((B, d), dtype=torch.float16, device="cuda")
+        olo = torch.zeros_like(o)
+        if fused:
+            rc = probe.ams_probe_attn_decode_parts(CT["f16"], _ptr(pq_d), qsplits, _ptr(ss_d), d // 256,
+                                                   C.c_float(eps), _ptr(lens_d), jpos, B, H, dh, cap, _ptr(pt_d),
+                                                   splits, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(part), _ptr(o),
+                                                   _ptr(olo), _stream())
+        else:
+            rc = probe.ams_probe_attn_decode(CT["f16"], _ptr(qkv), _ptr(lens_d), jpos, B, H, dh, cap, _ptr(pt_d),
+                                             splits, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(part), _ptr(o),
+                                             _ptr(olo), _stream())
+        assert rc == 0
+        torch.cuda.synchronize()
+        res.append((o, olo, K_d, V_d))
+    for x, y in zip(res[0], res[1]):
+        assert torch.equal(x, y)
+
+
 @pytest.mark.parametrize("M", [12, 33, 64])
 @pytest.mark.parametrize("splits", [1, 3])
 def test_merge_norm(probe, M, splits):
