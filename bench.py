@@ -464,7 +464,8 @@ def decode_kernel_name(spec, B, A, persistent):
         return (f"k_decode_fused<{spec.head_dim}> (persistent decode: head, feed and {A - 1} passes of every layer, "
                 "+ the barrier-clearing kernel)")
     return (f"decode phase of a step: {A - 1} passes x {spec.n_layers} layers of k_gemm_wide<{(B + 15) // 16},2> "
-            "(QKV, O, gate|up, down) + split-K reductions + k_attn_decode, and " f"{A} bin heads")
+            "(QKV, O, gate|up, down) + the O, gate|up and down split-K reductions + k_attn_decode (which adds the "
+            f"QKV partial sums), and {A} bin heads")
 
 
 def compact(r):

@@ -416,7 +416,11 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
       TRY(rmsnorm(md.ct, h, g.n, K, eps, g.u(), s, ulo));
     }
     if (wide) {  // partial sums of 128-row tiles, then the epilogue
-      const int splits = decode_wsplit(N, K);
+      // When the attention adds the partial sums, every split costs each of its
+      // workgroups another read of its q, k, v slices: two splits measured
+      // best on the 7B decoder at 64 rows (decode 47.2 / 45.9 / 45.0 / 44.8 ms
+      // per step at 8 / 4 / 5 / 2 splits).
+      const int splits = defer ? std::max(1, std::min(2, K >> 7)) : decode_wsplit(N, K);
       TRY(gemm_wide(g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), s));
       if (defer) {  // the consumer adds the partial sums itself
         *defer = QkvParts{g.c->kpart(), splits, ss, K / 256, eps};
