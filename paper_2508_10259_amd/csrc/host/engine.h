@@ -90,6 +90,7 @@ struct Ctx {
   void* olo() const { return ws + lay.olo; }
   void* alo() const { return ws + lay.alo; }
   float* kpart() const { return (float*)(ws + lay.kpart); }
+  unsigned* wcnt() const { return (unsigned*)(ws + lay.wcnt); }
   float* part() const { return (float*)(ws + lay.part); }
   float* logits() const { return (float*)(ws + lay.logits); }
   float2* rope() const { return (float2*)(ws + lay.rope); }

@@ -92,7 +92,8 @@ struct CtxLayout {
   int n_pages;        // pages in each layer's K (and V) pool
   size_t slab_layer;  // bytes of K (or V) for one layer: n_pages pages of 64 positions
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
-  size_t ss;  // decode rows' sums of squares per 256 residual columns [B][d/256]
+  size_t ss;  // decode rows' sums of squares per 128 residual columns [B][d/128]
+  size_t wcnt;  // arrival counters of the wide decode GEMM's weight tiles (zero between launches)
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
   // attention output and the SwiGLU output, split-K partials, sync words
   size_t fx_hp, fx_op, fx_ap, fx_part, fx_sync;
@@ -269,7 +270,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.kpart = o; o = align256(o + kp * 4);
   x.part = o; o = align256(o + B * (size_t)c.n_heads * x.max_splits * (c.head_dim + 2) * 4);
   x.logits = o; o = align256(o + B * (size_t)bins_padded(c) * 4);
-  x.ss = o; o = align256(o + B * (size_t)(d / 256 + 1) * 4);
+  x.ss = o; o = align256(o + B * (size_t)(d / 128 + 1) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
   x.lens = o; o = align256(o + B * 4);
   // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B], src[B]
@@ -289,6 +290,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.hk_keys = o; o = align256(o + (share ? B * (size_t)x.ppr * 8 : 0));
   x.hk_rows = o; o = align256(o + (share ? 2 * B * 8 : 0));
   x.xfer = o; o = align256(o + B * 16);
+  x.wcnt = o; o = align256(o + std::max({3 * d, 2 * F, (size_t)bins_padded(c), d}) / 128 * 4);
   x.total = o;
   return x;
 }

@@ -619,14 +619,6 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ u, c
 // workgroups per CU, and on the 7B shapes it beat four chunks by 1-5% (QKV at
 // 16 rows 23.4 -> 22.1 us, O at 64 rows 15.1 -> 14.4 us; only O at 16 rows lost,
 // 9.6 -> 9.9 us); six or eight chunks cost occupancy and were slower.
-// The activation fragments of a K step are all requested before its first
-// MFMA, so their LDS round trips overlap (one per MFMA otherwise); with 8 or
-// more fragments a wave keeps two weight chunks in flight instead of three,
-// which holds it at 120 VGPRs (four waves per SIMD).  On the 7B shapes at 64
-// rows: gate|up 54.0 -> 50.8 us, QKV 32.7 -> 31.6 us, down 29.3 -> 25.5 us.
-// Reducing the split-K partial sums in each tile's last split to finish
-// (a counter per tile) instead of a separate kernel measured 1-5 us slower
-// per projection: the O and down projections' 32 tiles then reduce on 32 CUs.
 constexpr int WIDE_ROWS = 128, WIDE_WP = 3, WIDE_LDK = 128 + 16;
 
 // weight fragments of one chunk of a wave's 16 rows
@@ -634,10 +626,129 @@ __device__ __forceinline__ void wide_wload(uint4 (&w)[4], const f16* wrow, int c
 #pragma unroll
   for (int i = 0; i < 4; ++i) w[i] = *(const uint4*)(wrow + (c << 7) + 32 * i);
 }
-template <int MB, int LO>
+
+typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
+constexpr int WIDE_SC1 = 16;  // cache-policy bits of a buffer access: device scope (sc1)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t wide_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// The reduction of one 128-column tile by the last of its splits to finish
+// (EPI_STORE / EPI_SWIGLU / EPI_RESID): every split's partial sums went out
+// with device-scope stores, completed before the split counted itself in, so
+// the last arrival reads them all (device-scope loads: the XCDs' L2s are not
+// coherent with each other) and adds them in split order, the order the
+// part_* reductions use.
+struct WideEpi {
+  unsigned* cnt;        // per-tile arrival counters, zero between launches (the last arrival resets its own)
+  void* out;            // STORE: float [M][ldo]; SWIGLU: fp16 [M][ldo] (ldo = N / 2)
+  void* olo;            // SWIGLU: rounding error of out (fp16) or NULL
+  int ldo;
+  float* h;             // RESID: residual [M][N] (+= the product)
+  void* o16;            // RESID: fp16 pair of the new rows (o16, olo2) or NULL
+  void* olo2;
+  float* ss_out;        // RESID: sums of squares of the new rows per 128 columns, [M][N / 128], or NULL
+  const float* ss_in;   // STORE / SWIGLU: the sums of squares of the unnormalised input rows, [M][K / 128], or NULL
+  float eps;
+};
+
+template <int EPI>
+__device__ void wide_reduce(const WideEpi& e, __amdgpu_buffer_rsrc_t pr, int S, int M, int N, int K, int n0) {
+  __shared__ float rs[64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if constexpr (EPI != EPI_RESID) {  // 1/rms of each input row, as row_rstd computes it
+    const int nss = K / 128;
+    for (int m = wave; m < M; m += 8) {
+      float t = 0.f;
+      if (e.ss_in)
+        for (int k = lane; k < nss; k += 64) t += e.ss_in[(size_t)m * nss + k];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+      if (lane == 0) rs[m] = e.ss_in ? 1.0f / sqrtf(t * (1.0f / (float)K) + e.eps) : 1.f;
+    }
+    __syncthreads();
+  }
+  auto sum4 = [&](int m, int n) {  // the S partials of 4 columns, added in split order
+    float4 v = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < S; s0 += 4) {
+      u32x4v q[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < S)
+          q[j] = __builtin_amdgcn_raw_buffer_load_b128(pr, (uint32_t)((((size_t)(s0 + j) * M + m) * N + n) * 4), 0,
+                                                       WIDE_SC1);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < S) {
+          v.x += __uint_as_float(q[j][0]);
+          v.y += __uint_as_float(q[j][1]);
+          v.z += __uint_as_float(q[j][2]);
+          v.w += __uint_as_float(q[j][3]);
+        }
+    }
+    return v;
+  };
+  if constexpr (EPI == EPI_SWIGLU) {
+    // packed rows 32i + j (gate, j < 16) and 32i + 16 + j (up) give output column n0/2 + 16i + j
+    for (int x = tid; x < M * 16; x += blockDim.x) {
+      const int m = x >> 4, q = x & 15, i = q >> 2, j4 = (q & 3) * 4;
+      const float4 gt = sum4(m, n0 + 32 * i + j4), up = sum4(m, n0 + 32 * i + 16 + j4);
+      const float sc = rs[m];
+      const size_t o = (size_t)m * e.ldo + (n0 >> 1) + 16 * i + j4;
+      split16(silu(gt.x * sc) * (up.x * sc), (f16*)e.out, (f16*)e.olo, o);
+      split16(silu(gt.y * sc) * (up.y * sc), (f16*)e.out, (f16*)e.olo, o + 1);
+      split16(silu(gt.z * sc) * (up.z * sc), (f16*)e.out, (f16*)e.olo, o + 2);
+      split16(silu(gt.w * sc) * (up.w * sc), (f16*)e.out, (f16*)e.olo, o + 3);
+    }
+  } else {
+    // 32 threads (half a wave) per row, 4 columns each
+    for (int x = tid; x < ((M + 15) & ~15) * 32; x += blockDim.x) {
+      const int m = x >> 5, n = n0 + 4 * (x & 31);
+      const bool in = m < M;  // uniform over each half wave
+      float4 v = {0.f, 0.f, 0.f, 0.f};
+      if (in) v = sum4(m, n);
+      if constexpr (EPI == EPI_STORE) {
+        if (in) {
+          const float sc = rs[m];
+          *(float4*)((float*)e.out + (size_t)m * e.ldo + n) = float4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
+        }
+      } else {
+        float q = 0.f;
+        if (in) {
+          float4* hp = (float4*)(e.h + (size_t)m * N + n);
+          float4 hv = *hp;
+          hv.x += v.x; hv.y += v.y; hv.z += v.z; hv.w += v.w;
+          *hp = hv;
+          if (e.o16) {
+            const size_t o = (size_t)m * N + n;
+            split16(hv.x, (f16*)e.o16, (f16*)e.olo2, o);
+            split16(hv.y, (f16*)e.o16, (f16*)e.olo2, o + 1);
+            split16(hv.z, (f16*)e.o16, (f16*)e.olo2, o + 2);
+            split16(hv.w, (f16*)e.o16, (f16*)e.olo2, o + 3);
+          }
+          q = (hv.x * hv.x + hv.y * hv.y) + (hv.z * hv.z + hv.w * hv.w);
+        }
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+        if (in && e.ss_out && (x & 31) == 0) e.ss_out[(size_t)m * (N / 128) + (n0 >> 7)] = q;
+      }
+    }
+  }
+}
+
+// The activation fragments of a K step are all requested before its first
+// MFMA, so their LDS round trips overlap (one per MFMA otherwise); with 8 or
+// more fragments a wave keeps two weight chunks in flight instead of three,
+// which holds it at 120 VGPRs (four waves per SIMD).  On the 7B shapes at 64
+// rows: gate|up 54.0 -> 50.8 us, QKV 32.7 -> 31.6 us, down 29.3 -> 25.5 us.
+// The reduction fused into the last split (EPI_STORE / _SWIGLU / _RESID)
+// measured 1-2 us faster per projection than GEMM + reduction kernel at 16
+// rows and 1-5 us slower at 64, where the O and down projections' 32 tiles
+// then reduce on 32 CUs; the engine uses it up to 16 rows.
+template <int MB, int LO, int EPI>
 __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, const f16* __restrict__ xlo,
                                                    const f16* __restrict__ W, int M, int K,
-                                                   float* __restrict__ part, int N) {
+                                                   float* __restrict__ part, int N, WideEpi ep) {
   constexpr int NX = LO == 2 ? 2 : 1;               // activation arrays (hi, lo)
   constexpr int XCH = NX * MB * 16 * 16;             // 16-byte pieces of one staged chunk
   constexpr int XPT = (XCH + 511) / 512;             // pieces per thread
@@ -705,7 +816,6 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
         const f16* xb = xs + (size_t)((t & 1) * NX) * MB * 16 * WIDE_LDK;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          // every activation fragment of this K step requested before its first MFMA
           half8 bf[NX][MB];
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -736,38 +846,95 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
 #undef AMS_WIDE_XSTORE
 
   // lane (r, g) holds rows n0 + 4g + i for token mb*16 + r
+  if constexpr (EPI == EPI_PART) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int tok = mb * 16 + r;
-    if (tok >= M) continue;
-    float* dst = part + ((size_t)sp * M + tok) * N + n0 + 4 * g;
-    *(float4*)dst = float4{acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]};
+    for (int mb = 0; mb < MB; ++mb) {
+      const int tok = mb * 16 + r;
+      if (tok >= M) continue;
+      float* dst = part + ((size_t)sp * M + tok) * N + n0 + 4 * g;
+      *(float4*)dst = float4{acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]};
+    }
+  } else {
+    __shared__ int last;
+    const __amdgpu_buffer_rsrc_t pr = wide_rsrc(part, (uint32_t)((size_t)S * M * N * 4));
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int tok = mb * 16 + r;
+      if (tok >= M) continue;
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4v{__float_as_uint(acc[mb][0]), __float_as_uint(acc[mb][1]),
+                                                    __float_as_uint(acc[mb][2]), __float_as_uint(acc[mb][3])},
+                                             pr, (uint32_t)((((size_t)sp * M + tok) * N + n0 + 4 * g) * 4), 0,
+                                             WIDE_SC1);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's partial sums are stored
+    __syncthreads();
+    if (tid == 0) {
+      unsigned* c = ep.cnt + blockIdx.x;
+      const bool l = __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(S - 1);
+      if (l) __hip_atomic_store(c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // every split is in
+      last = l;
+    }
+    __syncthreads();
+    if (last) wide_reduce<EPI>(ep, pr, S, M, N, K, blockIdx.x * WIDE_ROWS);
   }
 }
 
-template <int MB, int LO>
+template <int MB, int LO, int EPI>
 static hipError_t launch_wide(const f16* x, const f16* xlo, const f16* W, int M, int N, int K, int splits,
-                              float* part, hipStream_t s) {
+                              float* part, const WideEpi& ep, hipStream_t s) {
   const size_t lds = (size_t)2 * (LO == 2 ? 2 : 1) * MB * 16 * WIDE_LDK * sizeof(f16);
-  hipLaunchKernelGGL((k_gemm_wide<MB, LO>), dim3(N / WIDE_ROWS, splits), dim3(512), lds, s, x, xlo, W, M, K, part, N);
+  hipLaunchKernelGGL((k_gemm_wide<MB, LO, EPI>), dim3(N / WIDE_ROWS, splits), dim3(512), lds, s, x, xlo, W, M, K,
+                     part, N, ep);
   return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t wide_epi(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
+                           const WideEpi& ep, hipStream_t s) {
+  const f16 *x = (const f16*)u, *xl = (const f16*)ulo, *w = (const f16*)W;
+  if (!ulo) {
+    if (M <= 16) return launch_wide<1, 0, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+    if (M <= 32) return launch_wide<2, 0, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+    if (M <= 48) return launch_wide<3, 0, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+    return launch_wide<4, 0, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+  }
+  if (M <= 16) return launch_wide<1, 2, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+  if (M <= 32) return launch_wide<2, 2, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+  if (M <= 48) return launch_wide<3, 2, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+  return launch_wide<4, 2, EPI>(x, xl, w, M, N, K, splits, part, ep, s);
+}
+
+static bool wide_shape_ok(int M, int N, int K, int splits) {
+  return M <= 64 && N % WIDE_ROWS == 0 && K % 128 == 0 && splits >= 1 && (K >> 7) >= splits;
 }
 
 hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (M > 64 || N % WIDE_ROWS != 0 || splits < 1 || (K >> 7) < splits) return hipErrorInvalidValue;
-  const f16 *x = (const f16*)u, *xl = (const f16*)ulo, *w = (const f16*)W;
-  if (!ulo) {
-    if (M <= 16) return launch_wide<1, 0>(x, xl, w, M, N, K, splits, part, s);
-    if (M <= 32) return launch_wide<2, 0>(x, xl, w, M, N, K, splits, part, s);
-    if (M <= 48) return launch_wide<3, 0>(x, xl, w, M, N, K, splits, part, s);
-    return launch_wide<4, 0>(x, xl, w, M, N, K, splits, part, s);
+  if (!wide_shape_ok(M, N, K, splits)) return hipErrorInvalidValue;
+  return wide_epi<EPI_PART>(u, ulo, W, M, N, K, splits, part, WideEpi{}, s);
+}
+
+hipError_t gemm_wide_reduce(int epi, const void* u, const void* ulo, const void* W, int M, int N, int K, int splits,
+                            float* part, unsigned* counters, void* out, void* olo, int ldo, float* h, void* o16,
+                            void* olo2, float* ss_out, const float* ss_in, float eps, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (!wide_shape_ok(M, N, K, splits) || !counters || !part) return hipErrorInvalidValue;
+  if ((size_t)splits * M * N * 4 >= (size_t)1 << 31) return hipErrorInvalidValue;  // 32-bit buffer offsets
+  WideEpi ep{counters, out, olo, ldo, h, o16, olo2, ss_out, ss_in, eps};
+  switch (epi) {
+    case EPI_STORE:
+      if (!out || ldo < N) return hipErrorInvalidValue;
+      return wide_epi<EPI_STORE>(u, ulo, W, M, N, K, splits, part, ep, s);
+    case EPI_SWIGLU:
+      if (!out || N % (2 * GU_BLOCK) != 0 || ldo < N / 2) return hipErrorInvalidValue;
+      return wide_epi<EPI_SWIGLU>(u, ulo, W, M, N, K, splits, part, ep, s);
+    case EPI_RESID:
+      if (!h || (olo2 && !o16)) return hipErrorInvalidValue;
+      return wide_epi<EPI_RESID>(u, ulo, W, M, N, K, splits, part, ep, s);
+    default:
+      return hipErrorInvalidValue;
   }
-  if (M <= 16) return launch_wide<1, 2>(x, xl, w, M, N, K, splits, part, s);
-  if (M <= 32) return launch_wide<2, 2>(x, xl, w, M, N, K, splits, part, s);
-  if (M <= 48) return launch_wide<3, 2>(x, xl, w, M, N, K, splits, part, s);
-  return launch_wide<4, 2>(x, xl, w, M, N, K, splits, part, s);
 }
 
 // 1/rms of row m from the partial sums of squares k_part_resid left for it
@@ -830,7 +997,7 @@ hipError_t part_store(const float* part, int splits, int M, int N, float* out, h
   if (ss && (N % 256 != 0 || d <= 0 || d % 256 != 0)) return hipErrorInvalidValue;
   const size_t MN = (size_t)M * N;
   hipLaunchKernelGGL(k_part_store, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, part, splits, MN, N, ss,
-                     d / 256, ss ? 1.0f / (float)d : 0.f, eps, out);
+                     d / 128, ss ? 1.0f / (float)d : 0.f, eps, out);
   return hipGetLastError();
 }
 
@@ -841,7 +1008,7 @@ hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, v
   if (ss && ((N / 2) % 256 != 0 || d <= 0 || d % 256 != 0)) return hipErrorInvalidValue;
   const size_t MF = (size_t)M * (N / 2);
   hipLaunchKernelGGL(k_part_swiglu, dim3((unsigned)((MF + 255) / 256)), dim3(256), 0, s, part, splits, M, N, ss,
-                     d / 256, ss ? 1.0f / (float)d : 0.f, eps, (f16*)out, (f16*)olo);
+                     d / 128, ss ? 1.0f / (float)d : 0.f, eps, (f16*)out, (f16*)olo);
   return hipGetLastError();
 }
 
@@ -868,8 +1035,9 @@ hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N
 
 // h[m][n] += sum_s part[s][m][n] (splits in order), and the fp16 pair of the
 // updated row when o16 is non-NULL; with ss, each block (256 columns of one
-// row: N a multiple of 256) also leaves the sum of squares of its new values
-// at ss[blockIdx], i.e. ss[m][n / 256], for the next projection's RMSNorm
+// row: N a multiple of 256) also leaves the sums of squares of its new values
+// per 128 columns at ss[2 blockIdx ..], i.e. ss[m][n / 128], for the next
+// projection's RMSNorm
 __global__ __launch_bounds__(256) void k_part_resid(const float* __restrict__ part, int splits, int M, int N,
                                                     float* __restrict__ h, f16* __restrict__ o16,
                                                     f16* __restrict__ olo, float* __restrict__ ss) {
@@ -890,7 +1058,7 @@ __global__ __launch_bounds__(256) void k_part_resid(const float* __restrict__ pa
   for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
   if ((threadIdx.x & 63) == 0) wsq[threadIdx.x >> 6] = q;
   __syncthreads();
-  if (threadIdx.x == 0) ss[blockIdx.x] = (wsq[0] + wsq[1]) + (wsq[2] + wsq[3]);
+  if (threadIdx.x < 2) ss[2 * blockIdx.x + threadIdx.x] = wsq[2 * threadIdx.x] + wsq[2 * threadIdx.x + 1];
 }
 
 hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s,

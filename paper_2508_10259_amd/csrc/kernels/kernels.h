@@ -65,8 +65,24 @@ hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N
 // LDS-staged activations.  The epilogue is one of the part_* reductions.
 hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
+// The wide decode GEMM with its reduction fused: each split stores its partial
+// sums (part, splits * M * N floats) and the last split of every 128-row weight
+// tile to finish (per-tile counters, zero before the first call, left zero)
+// adds them in split order and applies the epilogue, with the results of the
+// part_* reductions:
+//   EPI_STORE : out[m*ldo + n] = y / rms_m        (rms_m from ss_in, or 1 when NULL)
+//   EPI_SWIGLU: out/olo[m*ldo + c] = silu(gate / rms_m) * (up / rms_m), fp16 pair
+//   EPI_RESID : h[m][n] += y, the fp16 pair (o16, olo2) of the new rows when
+//               o16 is non-NULL, and the sums of squares of the new rows per 128
+//               columns in ss_out[m][n / 128] when non-NULL
+// ss_in: sums of squares of the unnormalised input rows per 128 columns
+// ([M][K / 128]), rms_m = sqrt(sum / K + eps).  counters: N / 128 entries.
+hipError_t gemm_wide_reduce(int epi, const void* u, const void* ulo, const void* W, int M, int N, int K, int splits,
+                            float* part, unsigned* counters, void* out, void* olo, int ldo, float* h, void* o16,
+                            void* olo2, float* ss_out, const float* ss_in, float eps, hipStream_t s);
 // out[m][n] = sum_s part[s][m][n] (fp32 out).  With ss (the sums of squares
-// part_resid left for a residual of width d, both N and d multiples of 256)
+// per 128 columns part_resid left for a residual of width d, both N and d
+// multiples of 256)
 // the GEMM read that residual unnormalised and row m is scaled by its
 // 1/sqrt(sum/d + eps): RMSNorm(h) W^T = (h W^T) / rms(h), the gains being
 // folded into W.
@@ -79,8 +95,8 @@ hipError_t part_swiglu(const float* part, int splits, int M, int N, void* out, v
                        const float* ss = nullptr, int d = 0, float eps = 0.f);
 // h[m][n] += sum_s part[s][m][n], the splits added in order; with o16 (and
 // olo) also the fp16 pair of the updated rows, as gemm()'s EPI_RESID; with ss
-// (N a multiple of 256) the sums of squares of the new rows per 256 columns,
-// ss[m][n / 256], for the next RMSNorm.
+// (N a multiple of 256) the sums of squares of the new rows per 128 columns,
+// ss[m][n / 128], for the next RMSNorm.
 hipError_t part_resid(const float* part, int splits, int M, int N, float* h, void* o16, void* olo, hipStream_t s,
                       float* ss = nullptr);
 
@@ -155,8 +171,8 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPage
 // the fp16 output o, written by whichever of the two kernels writes o.
 // The QKV projection's split-K partial sums (splits x [B][3d] floats) in place of
 // qkv: the attention adds them in split order and divides row b by its rms
-// from ss[b][0..nss) (sums of squares of the unnormalised residual, width d;
-// NULL: no scale), as part_store would.
+// from ss[b][0..nss) (sums of squares of the unnormalised residual per 128
+// columns, width d; NULL: no scale), as part_store would.
 struct QkvParts {
   const float* part = nullptr;
   int splits = 0;

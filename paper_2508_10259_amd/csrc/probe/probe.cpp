@@ -36,6 +36,13 @@ int ams_probe_gemm_wide(const void* u, const void* ulo, const void* W, int M, in
   return (int)ams::gemm_wide(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);
 }
 
+int ams_probe_gemm_wide_reduce(int epi, const void* u, const void* ulo, const void* W, int M, int N, int K,
+                               int splits, float* part, unsigned* counters, void* out, void* olo, int ldo, float* h,
+                               void* o16, void* olo2, float* ss_out, const float* ss_in, float eps, void* stream) {
+  return (int)ams::gemm_wide_reduce(epi, u, ulo, W, M, N, K, splits, part, counters, out, olo, ldo, h, o16, olo2,
+                                    ss_out, ss_in, eps, (hipStream_t)stream);
+}
+
 int ams_probe_part_store(const float* part, int splits, int M, int N, float* out, void* stream) {
   return (int)ams::part_store(part, splits, M, N, out, (hipStream_t)stream);
 }

@@ -543,7 +543,7 @@ def test_attn_decode_parts(probe, qsplits, norm, splits):
     lens = [3, 60, 64, 130, 190]
     log(f"attn_decode_parts qsplits={qsplits} norm={norm} splits={splits}")
     pq = W.random_gaussian((qsplits, B, 3 * d), 91, qsplits, dtype="f32")
-    ssv = (np.random.default_rng(92).random((B, d // 256)) * 300 + 10).astype(np.float32)
+    ssv = (np.random.default_rng(92).random((B, d // 128)) * 300 + 10).astype(np.float32)
     K = W.random_gaussian((B, H, cap, dh), 93, cap, dtype="f32").astype(np.float16)
     V = W.random_gaussian((B, H, cap, dh), 94, cap, dtype="f32").astype(np.float16)
     perm = np.random.default_rng(95).permutation(B * (cap // 64)).astype(np.int32)
@@ -565,7 +565,7 @@ def test_attn_decode_parts(probe, qsplits, norm, splits):
         o = torch.zeros((B, d), dtype=torch.float16, device="cuda")
         olo = torch.zeros_like(o)
         if fused:
-            rc = probe.ams_probe_attn_decode_parts(CT["f16"], _ptr(pq_d), qsplits, _ptr(ss_d), d // 256,
+            rc = probe.ams_probe_attn_decode_parts(CT["f16"], _ptr(pq_d), qsplits, _ptr(ss_d), d // 128,
                                                    C.c_float(eps), _ptr(lens_d), jpos, B, H, dh, cap, _ptr(pt_d),
                                                    splits, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(part), _ptr(o),
                                                    _ptr(olo), _stream())
@@ -584,7 +584,7 @@ def test_attn_decode_parts(probe, qsplits, norm, splits):
 @pytest.mark.parametrize("splits", [1, 3])
 def test_merge_norm(probe, M, splits):
     """Wide-path reductions that carry the RMSNorm: the residual reduction leaves the
-    unnormalised fp16 pair and the sums of squares per 256 columns; the projection
+    unnormalised fp16 pair and the sums of squares per 128 columns; the projection
     reductions (store, SwiGLU) divide each row by its rms, RMSNorm(h) W^T = (h W^T) / rms(h)."""
     import torch
     d, F, eps = 512, 512, 1e-5
@@ -596,14 +596,14 @@ def test_merge_norm(probe, M, splits):
     h = torch.from_numpy(h0.copy()).cuda()
     o16 = torch.zeros((M, d), dtype=torch.float16, device="cuda")
     olo = torch.zeros((M, d), dtype=torch.float16, device="cuda")
-    ss = torch.full((M, d // 256), float("nan"), dtype=torch.float32, device="cuda")
+    ss = torch.full((M, d // 128), float("nan"), dtype=torch.float32, device="cuda")
     assert probe.ams_probe_part_resid_ss(_ptr(part), splits, M, d, _ptr(h), _ptr(o16), _ptr(olo), _ptr(ss),
                                          _stream()) == 0
     torch.cuda.synchronize()
     hn = h.cpu().numpy().astype(np.float64)
     assert float(np.max(np.abs(hn - (h0 + pr.astype(np.float64).sum(0))))) <= 1e-5
     assert torch.equal(o16, h.half()) and torch.equal(olo, (h - h.half().float()).half())
-    sq = (hn ** 2).reshape(M, d // 256, 256).sum(-1)
+    sq = (hn ** 2).reshape(M, d // 128, 128).sum(-1)
     assert np.allclose(ss.cpu().numpy(), sq, rtol=1e-5, atol=1e-5)
     rstd = 1.0 / np.sqrt((hn ** 2).mean(1, keepdims=True) + eps)
     # store: the summed partials of a projection of the unnormalised rows, scaled by 1/rms
@@ -681,6 +681,87 @@ def test_gemm_wide(probe, M, N, K, splits, pair):
     ref = (_silu(gg) * up).T
     got = a.float().cpu().numpy().astype(np.float64) + alo.float().cpu().numpy()
     assert float(np.max(np.abs(got - ref))) <= max(tol, 4e-6 * float(np.max(np.abs(ref))))
+
+
+@pytest.mark.parametrize("M", [5, 33, 64])
+@pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (512, 4096, 8), (1152, 1408, 4), (2048, 1024, 3),
+                                        (256, 2048, 16)])
+def test_gemm_wide_reduce(probe, M, N, K, splits):
+    """The wide decode GEMM with its reduction fused (the last split of each 128-row tile adds
+    the partial sums in split order): store, SwiGLU and residual results equal those of the
+    separate reduction kernels bit for bit, the residual's sums of squares per 128 columns
+    match the new rows, the RMSNorm scale from given sums of squares matches the separate
+    scaled reductions (or the closed form where they do not take the shape), and the tile
+    counters are back at zero, so a second call gives the same results."""
+    import torch
+    log(f"gemm_wide_reduce M={M} N={N} K={K} splits={splits}")
+    eps = 1e-5
+    x = W.random_gaussian((M, K), 81, M, K, dtype="f32")
+    u, ulo = _pair(x)
+    Wt = _rand((N, K), 82, N, K, std=0.05)
+    ud, ulod, Wd = _dev(u, "f16"), _dev(ulo, "f16"), _dev(Wt, "f16")
+    part = torch.empty((splits * M * N,), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_gemm_wide(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
+    part2 = torch.empty_like(part)
+    cnt = torch.zeros((N // 128,), dtype=torch.int32, device="cuda")
+    ss_in = torch.from_numpy((np.random.default_rng(M + N).random((M, K // 128)) * 50 + 1).astype(np.float32)).cuda()
+    f = C.c_float(eps)
+
+    def fused(epi, out=None, olo=None, ldo=0, h=None, o16=None, olo2=None, ss_out=None, ss=None):
+        assert probe.ams_probe_gemm_wide_reduce(epi, _ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part2),
+                                                _ptr(cnt), _ptr(out), _ptr(olo), ldo, _ptr(h), _ptr(o16),
+                                                _ptr(olo2), _ptr(ss_out), _ptr(ss), f, _stream()) == 0
+        torch.cuda.synchronize()
+        assert int(cnt.abs().sum()) == 0
+
+    # store, without and with the RMSNorm scale
+    ref = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    assert probe.ams_probe_part_store(_ptr(part), splits, M, N, _ptr(ref), _stream()) == 0
+    for _ in range(2):
+        out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        fused(0, out=out, ldo=N)
+        assert torch.equal(out, ref)
+    out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    fused(0, out=out, ldo=N, ss=ss_in)
+    rstd = 1.0 / np.sqrt(ss_in.cpu().numpy().astype(np.float64).sum(1, keepdims=True) / K + eps)
+    if N % 256 == 0 and K % 256 == 0:
+        ref_n = torch.zeros_like(out)
+        assert probe.ams_probe_part_store_norm(_ptr(part), splits, M, N, _ptr(ref_n), _ptr(ss_in), K, f,
+                                               _stream()) == 0
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_n)
+    want = ref.cpu().numpy().astype(np.float64) * rstd
+    assert float(np.max(np.abs(out.cpu().numpy() - want))) <= 1e-6 * max(1.0, float(np.max(np.abs(want))))
+    # SwiGLU (fp16 pair out)
+    a = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
+    alo = torch.zeros_like(a)
+    assert probe.ams_probe_part_swiglu(_ptr(part), splits, M, N, _ptr(a), _ptr(alo), _stream()) == 0
+    a2, alo2 = torch.full_like(a, float("nan")), torch.full_like(alo, float("nan"))
+    fused(2, out=a2, olo=alo2, ldo=N // 2)
+    assert torch.equal(a, a2) and torch.equal(alo, alo2)
+    if (N // 2) % 256 == 0 and K % 256 == 0:
+        assert probe.ams_probe_part_swiglu_norm(_ptr(part), splits, M, N, _ptr(a), _ptr(alo), _ptr(ss_in), K, f,
+                                                _stream()) == 0
+        fused(2, out=a2, olo=alo2, ldo=N // 2, ss=ss_in)
+        assert torch.equal(a, a2) and torch.equal(alo, alo2)
+    # residual with the fp16 pair and the sums of squares per 128 columns
+    h0 = torch.from_numpy(W.random_gaussian((M, N), 83, M, dtype="f32")).cuda()
+    h, o16, olo = h0.clone(), torch.zeros((M, N), dtype=torch.float16, device="cuda"), None
+    olo = torch.zeros_like(o16)
+    assert probe.ams_probe_part_resid(_ptr(part), splits, M, N, _ptr(h), _ptr(o16), _ptr(olo), _stream()) == 0
+    h2, o16b, olob = h0.clone(), torch.full_like(o16, float("nan")), torch.full_like(olo, float("nan"))
+    ss2 = torch.full((M, N // 128), float("nan"), dtype=torch.float32, device="cuda")
+    fused(1, h=h2, o16=o16b, olo2=olob, ss_out=ss2)
+    assert torch.equal(h, h2) and torch.equal(o16, o16b) and torch.equal(olo, olob)
+    hn = h2.cpu().numpy().astype(np.float64)
+    assert np.allclose(ss2.cpu().numpy(), (hn ** 2).reshape(M, N // 128, 128).sum(-1), rtol=1e-5, atol=1e-5)
+    # shapes and arguments it does not take are refused
+    bad = probe.ams_probe_gemm_wide_reduce(3, _ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part2),
+                                           _ptr(cnt), _ptr(out), None, N, None, None, None, None, None, f, _stream())
+    assert bad != 0
+    bad = probe.ams_probe_gemm_wide_reduce(0, _ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part2),
+                                           None, _ptr(out), None, N, None, None, None, None, None, f, _stream())
+    assert bad != 0
 
 
 def test_peak_kernels(probe):
