@@ -112,7 +112,12 @@ int32_t ams_device_count(void);
 
 /* ---- model ------------------------------------------------------------ */
 
-/* Bytes of device workspace ams_model_create needs for `cfg` (0 if cfg is invalid). */
+/* Bytes of device workspace ams_model_create needs for `cfg` (0 if cfg is invalid).
+ * fp16 compute (bf16 and fp16 models) keeps each layer matrix and the action
+ * head twice: row-major for the prefix passes and the decode of up to 8 rows
+ * outside the persistent kernel, and in MFMA fragment order for the wider
+ * decode passes and the persistent decode, so such a model needs about twice
+ * its weight bytes. */
 size_t ams_model_workspace_bytes(const ams_model_cfg* cfg);
 
 /* Validates cfg and weights, then packs the weights into `ws` (device memory of

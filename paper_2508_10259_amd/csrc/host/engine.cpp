@@ -88,6 +88,15 @@ hipError_t model_pack(Model& m, const ams_weights_view& w, hipStream_t s, std::s
   TRY(convert(st, ct, w.head_bins, c.n_bins, (int)d, w.g_final, m.ws + m.lay.head_bins, s));
   TRY(convert(st, ct, off(w.embed, (size_t)(c.vocab - c.n_bins) * d * es), c.n_bins, (int)d, nullptr,
               m.ws + m.lay.bin_embed, s));
+  if (ct == DT_F16) {  // the decode passes' copies in MFMA fragment order
+    for (int l = 0; l < c.n_layers; ++l) {
+      TRY(frag_pack(m.wqkv(l), 3 * (int)d, (int)d, (void*)m.fqkv(l), s));
+      TRY(frag_pack(m.wo(l), (int)d, (int)d, (void*)m.fo(l), s));
+      TRY(frag_pack(m.wgu(l), 2 * (int)F, (int)d, (void*)m.fgu(l), s));
+      TRY(frag_pack(m.wd(l), (int)d, (int)F, (void*)m.fd(l), s));
+    }
+    TRY(frag_pack(m.head_bins(), bins_padded(c), (int)d, (void*)m.fhead(), s));
+  }
   return hipSuccess;
 }
 
@@ -409,8 +418,8 @@ struct Rows {
 // except on the wide path with ss, where (u, hlo) already hold the
 // unnormalised pair and the reduction divides by rms (merge_norm).
 static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* hhi, const void* hlo, const void* W,
-                            int N, int K, void* out, int ldo, void* olo, hipStream_t s, std::string& err,
-                            const float* ss = nullptr, QkvParts* defer = nullptr) {
+                            const void* Wf, int N, int K, void* out, int ldo, void* olo, hipStream_t s,
+                            std::string& err, const float* ss = nullptr, QkvParts* defer = nullptr) {
   const Model& md = *g.c->model;
   const float eps = md.cfg.rms_eps;
   if (fused_norm(*g.c, g.n)) {
@@ -429,10 +438,10 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
       // per step at 8 / 4 / 5 / 2 splits).
       const int splits = defer ? std::max(1, std::min(2, K >> 7)) : decode_wsplit(N, K);
       if (!defer && wide_fused_reduce(g.n)) {
-        TRY(gemm_wide_reduce(epi, g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), g.c->wcnt(), out, olo, ldo, nullptr,
+        TRY(gemm_wide_reduce(epi, g.u(), ulo, Wf, g.n, N, K, splits, g.c->kpart(), g.c->wcnt(), out, olo, ldo, nullptr,
                              nullptr, nullptr, nullptr, ss, eps, s));
       } else {
-        TRY(gemm_wide(g.u(), ulo, W, g.n, N, K, splits, g.c->kpart(), s));
+        TRY(gemm_wide(g.u(), ulo, Wf, g.n, N, K, splits, g.c->kpart(), s));
         if (defer) {  // the consumer adds the partial sums itself
           *defer = QkvParts{g.c->kpart(), splits, ss, K / 128, eps};
         } else if (epi == EPI_SWIGLU) {
@@ -453,8 +462,8 @@ static hipError_t norm_proj(const Rows& g, int epi, const float* h, const void* 
 // split K over more workgroups and add the partial sums in a reduction kernel;
 // on the wide path with ss that reduction also leaves the unnormalised pair in
 // (u, hlo) and the sums of squares in ss for the next projection.
-static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, const void* W, int K, void* hhi, void* hlo,
-                             hipStream_t s, float* ss = nullptr) {
+static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, const void* W, const void* Wf, int K,
+                             void* hhi, void* hlo, hipStream_t s, float* ss = nullptr) {
   const Ctx& c = *g.c;
   const Model& md = *c.model;
   const int d = md.cfg.d_model;
@@ -463,9 +472,9 @@ static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, cons
     void* o16 = ss ? g.u() : hhi;
     void* olo = ss ? g.hlo() : hlo;
     if (wide_fused_reduce(g.n))
-      return gemm_wide_reduce(EPI_RESID, x, xlo, W, g.n, d, K, splits, c.kpart(), c.wcnt(), nullptr, nullptr, 0, g.h(),
-                              o16, olo, ss, nullptr, 0.f, s);
-    hipError_t e = gemm_wide(x, xlo, W, g.n, d, K, splits, c.kpart(), s);
+      return gemm_wide_reduce(EPI_RESID, x, xlo, Wf, g.n, d, K, splits, c.kpart(), c.wcnt(), nullptr, nullptr, 0,
+                              g.h(), o16, olo, ss, nullptr, 0.f, s);
+    hipError_t e = gemm_wide(x, xlo, Wf, g.n, d, K, splits, c.kpart(), s);
     if (e == hipSuccess) e = part_resid(c.kpart(), splits, g.n, d, g.h(), o16, olo, s, ss);
     return e;
   }
@@ -493,16 +502,16 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
   float* ss = merge_norm(c, B) ? g.ss() : nullptr;
   // on the wide path the attention adds the QKV projection's partial sums itself
   QkvParts qp{};
-  if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err,
+  if (norm_proj(g, EPI_STORE, g.h(), hhi, hlo, md.wqkv(l), md.fqkv(l), 3 * d, d, g.qkv(), 3 * d, nullptr, s, err,
                 l > 0 ? ss : nullptr, &qp) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, g.pages(), c.splits, c.rope(),
                   g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo, qp));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
-  TRY(resid_proj(g, g.o(), olo, md.wo(l), d, hhi, hlo, s, ss));
-  if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), 2 * F, d, g.a(), F, alo, s, err, ss) != hipSuccess)
+  TRY(resid_proj(g, g.o(), olo, md.wo(l), md.fo(l), d, hhi, hlo, s, ss));
+  if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), md.fgu(l), 2 * F, d, g.a(), F, alo, s, err, ss) != hipSuccess)
     return hipErrorLaunchFailure;
-  TRY(resid_proj(g, g.a(), alo, md.wd(l), F, hhi, hlo, s, ss));
+  TRY(resid_proj(g, g.a(), alo, md.wd(l), md.fd(l), F, hhi, hlo, s, ss));
   return hipSuccess;
 }
 
@@ -516,7 +525,7 @@ static hipError_t head(const Rows& g, const float* hin, const void* hhi, const v
   const Cfg& m = md.cfg;
   const int d = m.d_model, nbp = bins_padded(m);
   const bool fused = fused_norm(*g.c, g.n);
-  if (norm_proj(g, EPI_STORE, hin, hhi, hlo, md.head_bins(), nbp, d, g.logits(), nbp, nullptr, s, err, ss) !=
+  if (norm_proj(g, EPI_STORE, hin, hhi, hlo, md.head_bins(), md.fhead(), nbp, d, g.logits(), nbp, nullptr, s, err, ss) !=
       hipSuccess)
     return hipErrorLaunchFailure;
   TRY(argmax_feed(md.ct, g.logits(), nbp, md.bin_embed(), g.n, d, m.n_bins, A, j, tok, logits, forced, g.h(),
@@ -552,11 +561,11 @@ static hipError_t enqueue_fused(Ctx& c, int A, int32_t* tok, float* logits, cons
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   FusedDecode f{};
-  f.wqkv = md.wqkv(0); f.s_qkv = md.lay.per_layer_qkv;
-  f.wo = md.wo(0); f.s_o = md.lay.per_layer_o;
-  f.wgu = md.wgu(0); f.s_gu = md.lay.per_layer_gu;
-  f.wd = md.wd(0); f.s_d = md.lay.per_layer_d;
-  f.whead = md.head_bins();
+  f.wqkv = md.fqkv(0); f.s_qkv = md.lay.per_layer_qkv;  // fragment-ordered copies
+  f.wo = md.fo(0); f.s_o = md.lay.per_layer_o;
+  f.wgu = md.fgu(0); f.s_gu = md.lay.per_layer_gu;
+  f.wd = md.fd(0); f.s_d = md.lay.per_layer_d;
+  f.whead = md.fhead();
   f.bin_embed = md.bin_embed();
   f.L = m.n_layers; f.d = m.d_model; f.H = m.n_heads; f.dh = m.head_dim; f.F = m.d_ffn;
   f.nbp = bins_padded(m); f.n_bins = m.n_bins; f.eps = m.rms_eps;

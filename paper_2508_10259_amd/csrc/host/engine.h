@@ -36,6 +36,12 @@ struct Model {
   const void* wd(int l) const { return ws + lay.wd + l * lay.per_layer_d; }
   const void* head_bins() const { return ws + lay.head_bins; }
   const void* bin_embed() const { return ws + lay.bin_embed; }
+  // the fragment-ordered copies (fp16 compute)
+  const void* fqkv(int l) const { return ws + lay.fqkv + l * lay.per_layer_qkv; }
+  const void* fo(int l) const { return ws + lay.fo + l * lay.per_layer_o; }
+  const void* fgu(int l) const { return ws + lay.fgu + l * lay.per_layer_gu; }
+  const void* fd(int l) const { return ws + lay.fd + l * lay.per_layer_d; }
+  const void* fhead() const { return ws + lay.fhead; }
 };
 
 struct GraphKey {

@@ -64,6 +64,9 @@ inline int bins_padded(const Cfg& c) { return (c.n_bins + 63) / 64 * 64; }
 struct ModelLayout {
   size_t wqkv, wo, wgu, wd, head_bins, bin_embed, total;
   size_t per_layer_qkv, per_layer_o, per_layer_gu, per_layer_d;  // bytes per layer
+  // fp16 compute: a second copy of the decode-pass matrices in MFMA fragment
+  // order (frag_pack), same per-layer strides; 0 / unused for fp32 models
+  size_t fqkv, fo, fgu, fd, fhead;
 };
 
 inline ModelLayout model_layout(const Cfg& c) {
@@ -80,6 +83,13 @@ inline ModelLayout model_layout(const Cfg& c) {
   m.wd = o; o = align256(o + L * m.per_layer_d);
   m.head_bins = o; o = align256(o + (size_t)bins_padded(c) * d * es);
   m.bin_embed = o; o = align256(o + (size_t)c.n_bins * d * es);
+  if (es == 2) {
+    m.fqkv = o; o = align256(o + L * m.per_layer_qkv);
+    m.fo = o; o = align256(o + L * m.per_layer_o);
+    m.fgu = o; o = align256(o + L * m.per_layer_gu);
+    m.fd = o; o = align256(o + L * m.per_layer_d);
+    m.fhead = o; o = align256(o + (size_t)bins_padded(c) * d * es);
+  }
   m.total = o;
   return m;
 }

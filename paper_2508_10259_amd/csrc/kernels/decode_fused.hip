@@ -153,18 +153,20 @@ __device__ __forceinline__ void wave_chunks(int c0, int c1, int& w0, int& w1) {
   w1 = c0 + (wave + 1) * (c1 - c0) / 8;
 }
 
+// W is in MFMA fragment order (frag_pack): the A fragment of rows 16 s .. 16 s + 15
+// and columns 128 c + 32 i .. + 31 is 1 KB of contiguous memory at block
+// (s * K / 128 + c) * 4 + i, lane l's 16 bytes at l * 16.
 template <int RB>
 __device__ __forceinline__ void load_w(const f16* W, int K, int n0, int cb, int w1, uint4 (&w)[8]) {
-  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int lane = threadIdx.x & 63, nch = K >> 7;
 #pragma unroll
   for (int j = 0; j < GB<RB>::CB; ++j) {
     if (cb + j < w1) {
-      const int kb = (cb + j) << 7;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const f16* row = W + (size_t)(n0 + rb * 16 + r) * K + kb + g * 8;
+        const f16* blk = W + (((size_t)((n0 >> 4) + rb) * nch + cb + j) * 4) * 512 + lane * 8;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) w[(j * RB + rb) * 4 + i] = *(const uint4*)(row + 32 * i);
+        for (int i = 0; i < 4; ++i) w[(j * RB + rb) * 4 + i] = *(const uint4*)(blk + i * 512);
       }
     }
   }
@@ -296,12 +298,12 @@ __device__ __forceinline__ float gemv_value(const FusedSmem& sm, int rb, int ln,
 }
 
 struct FusedArgs {
-  // packed model (per-layer byte strides)
+  // packed model in MFMA fragment order (per-layer byte strides)
   const f16* wqkv; size_t s_qkv;
   const f16* wo; size_t s_o;
   const f16* wgu; size_t s_gu;
   const f16* wd; size_t s_d;
-  const f16* whead;      // [nbp][d]
+  const f16* whead;      // [nbp][d], fragment order like the layers' matrices
   const f16* bin_embed;  // [n_bins][d]
   int L, d, H, F, nbp, n_bins;
   float eps, scale;

@@ -60,16 +60,25 @@ hipError_t gemm(int ct, int epi, const void* u, const void* W, int M, int N, int
 // fp16 input or the pair u + ulo as in gemm().  part holds splits * M * N floats.
 hipError_t gemm_part(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
-// Wide decode GEMM (fp16, 16 < M <= 64 typical, N a multiple of 128): the
-// same partial sums as gemm_part, with 128 weight rows per workgroup sharing
-// LDS-staged activations.  The epilogue is one of the part_* reductions.
+// MFMA fragment order of an fp16 matrix W [N][K] (N a multiple of 16, K of
+// 128): 16-row strip s, 128-column chunk c and 32-column step i of it form one
+// 1 KB block, lane l of a wave holding row 16 s + l % 16, columns
+// 128 c + 32 i + 8 (l / 16) .. +8:
+//   Wf[(((s * K/128 + c) * 4 + i) * 64 + l) * 8 + e] = W[16 s + l % 16][128 c + 32 i + 8 (l / 16) + e]
+// so a wave reads the A fragments of one MFMA step as 1 KB of contiguous memory.
+hipError_t frag_pack(const void* W, int N, int K, void* Wf, hipStream_t s);
+
+// Wide decode GEMM (fp16, 16 < M <= 64 typical, N a multiple of 128, W in
+// fragment order): the same partial sums as gemm_part, with 128 weight rows
+// per workgroup sharing LDS-staged activations.  The epilogue is one of the
+// part_* reductions.
 hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
-// The wide decode GEMM with its reduction fused: each split stores its partial
-// sums (part, splits * M * N floats) and the last split of every 128-row weight
-// tile to finish (per-tile counters, zero before the first call, left zero)
-// adds them in split order and applies the epilogue, with the results of the
-// part_* reductions:
+// The wide decode GEMM (W in fragment order) with its reduction fused: each
+// split stores its partial sums (part, splits * M * N floats) and the last
+// split of every 128-row weight tile to finish (per-tile counters, zero before
+// the first call, left zero) adds them in split order and applies the
+// epilogue, with the results of the part_* reductions:
 //   EPI_STORE : out[m*ldo + n] = y / rms_m        (rms_m from ss_in, or 1 when NULL)
 //   EPI_SWIGLU: out/olo[m*ldo + c] = silu(gate / rms_m) * (up / rms_m), fp16 pair
 //   EPI_RESID : h[m][n] += y, the fp16 pair (o16, olo2) of the new rows when
@@ -202,7 +211,7 @@ hipError_t gather_last(const float* h, Segs sg, int d, float* h_last, hipStream_
 // split-K sums and for M*H*split_a attention partials of dh + 2 floats) and
 // sync fused_sync_words(d, H) words.  The launch first clears sync with a kernel.
 struct FusedDecode {
-  const void *wqkv, *wo, *wgu, *wd, *whead, *bin_embed;
+  const void *wqkv, *wo, *wgu, *wd, *whead, *bin_embed;  // matrices in fragment order (frag_pack)
   size_t s_qkv, s_o, s_gu, s_d;
   int L, d, H, dh, F, nbp, n_bins;
   float eps;

@@ -31,6 +31,9 @@ int ams_probe_part_resid(const float* part, int splits, int M, int N, float* h, 
   return (int)ams::part_resid(part, splits, M, N, h, o16, olo, (hipStream_t)stream);
 }
 
+int ams_probe_frag_pack(const void* W, int N, int K, void* Wf, void* stream) {
+  return (int)ams::frag_pack(W, N, K, Wf, (hipStream_t)stream);
+}
 int ams_probe_gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                         void* stream) {
   return (int)ams::gemm_wide(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);

@@ -58,7 +58,10 @@ def test_workspace_sizes(lib):
     c = _cfg()
     mb = lib.ams_model_workspace_bytes(C.byref(c))
     params = 12 * (4 * 1024 ** 2 + 3 * 1024 * 4096)
-    assert params * 2 <= mb <= params * 2 + 64 * 1024 * 1024
+    # fp16 compute: row-major and fragment-ordered copies of every layer matrix
+    assert params * 4 <= mb <= params * 4 + 64 * 1024 * 1024
+    mb32 = lib.ams_model_workspace_bytes(C.byref(_cfg(dtype=0)))
+    assert params * 4 <= mb32 <= params * 4 + 64 * 1024 * 1024
     kb = lib.ams_ctx_workspace_bytes(C.byref(c), 8, 320, 0)
     assert kb >= 12 * 2 * 8 * 320 * 1024 * 2
     assert kb % 256 == 0

@@ -69,6 +69,15 @@ def _unpack_gu(Wp, F):
     return gate, up
 
 
+def _frag(Wt):
+    """MFMA fragment order of W [N][K]: 16-row strip s, 128-column chunk c and 32-column
+    step i form one block of 64 lanes x 8 values, lane l holding row 16 s + l % 16 and
+    columns 128 c + 32 i + 8 (l / 16) .. + 8 (the layout the wide decode GEMM and the
+    persistent decode read)."""
+    N, K = Wt.shape
+    return np.ascontiguousarray(Wt.reshape(N // 16, 16, K // 128, 4, 4, 8).transpose(0, 2, 3, 4, 1, 5)).reshape(N, K)
+
+
 def _pair(x):
     """fp16 pair of x: hi = fp16(x), lo = fp16(x - hi)."""
     hi = x.astype(np.float16)
@@ -632,13 +641,39 @@ def test_merge_norm(probe, M, splits):
                                            _stream()) != 0
 
 
+@pytest.mark.parametrize("N,K", [(16, 128), (48, 384), (1024, 4096), (4096, 11008), (22016, 4096)])
+def test_frag_pack(probe, N, K):
+    """frag_pack moves every 16 bytes of W to the block and lane its fragment-order formula
+    names (bit for bit), checked against the NumPy transposition, which the smallest case also
+    checks against the formula entry by entry; shapes off the 16 x 128 grid are refused."""
+    import torch
+    log(f"frag_pack N={N} K={K}")
+    Wt = _rand((N, K), 91, N, K)
+    ref = _frag(Wt).reshape(-1)
+    if N * K <= 48 * 384:
+        for s in range(N // 16):
+            for c in range(K // 128):
+                for i in range(4):
+                    for ln in range(64):
+                        o = (((s * (K // 128) + c) * 4 + i) * 64 + ln) * 8
+                        col = 128 * c + 32 * i + 8 * (ln // 16)
+                        assert np.array_equal(ref[o:o + 8], Wt[16 * s + ln % 16, col:col + 8])
+    src = _dev(Wt, "f16")
+    dst = torch.full((N * K,), float("nan"), dtype=torch.float16, device="cuda")
+    assert probe.ams_probe_frag_pack(_ptr(src), N, K, _ptr(dst), _stream()) == 0
+    torch.cuda.synchronize()
+    assert np.array_equal(dst.cpu().numpy().view(np.uint16), ref.view(np.uint16))
+    assert probe.ams_probe_frag_pack(_ptr(src), N - 8, K, _ptr(dst), _stream()) != 0
+    assert probe.ams_probe_frag_pack(_ptr(src), N, K - 64, _ptr(dst), _stream()) != 0
+
+
 @pytest.mark.parametrize("M", [5, 17, 33, 64])
 @pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (384, 4096, 8), (256, 1152, 3), (2048, 4096, 8),
                                         (1024, 5120, 8), (1152, 1408, 4), (512, 512, 4)])
 @pytest.mark.parametrize("pair", [False, True])
 def test_gemm_wide(probe, M, N, K, splits, pair):
-    """Wide decode GEMM (128 weight rows per workgroup, LDS-staged activations) and its
-    reductions: partial sums per K split, store / residual / SwiGLU epilogues, against the
+    """Wide decode GEMM (128 weight rows per workgroup, LDS-staged activations, weights in
+    fragment order) and its reductions: partial sums per K split, store / residual / SwiGLU epilogues, against the
     exact products of the fp16 (pair) inputs.  The splits cover 1 to 8 chunks of 128, uneven
     splits (11 chunks over 4) and chunk counts that are not multiples of the kernel's two or
     three weight chunks in flight."""
@@ -653,7 +688,7 @@ def test_gemm_wide(probe, M, N, K, splits, pair):
         xin = u.astype(np.float64)
     Wt = _rand((N, K), 62, N, K, std=0.05)
     y = xin @ _f(Wt, "f16").T
-    ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
+    ud, Wd = _dev(u, "f16"), _dev(_frag(Wt), "f16")
     ulod = _dev(ulo, "f16") if pair else None
     part = torch.full((splits * M * N,), float("nan"), dtype=torch.float32, device="cuda")
     assert probe.ams_probe_gemm_wide(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
@@ -699,7 +734,7 @@ def test_gemm_wide_reduce(probe, M, N, K, splits):
     x = W.random_gaussian((M, K), 81, M, K, dtype="f32")
     u, ulo = _pair(x)
     Wt = _rand((N, K), 82, N, K, std=0.05)
-    ud, ulod, Wd = _dev(u, "f16"), _dev(ulo, "f16"), _dev(Wt, "f16")
+    ud, ulod, Wd = _dev(u, "f16"), _dev(ulo, "f16"), _dev(_frag(Wt), "f16")
     part = torch.empty((splits * M * N,), dtype=torch.float32, device="cuda")
     assert probe.ams_probe_gemm_wide(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, splits, _ptr(part), _stream()) == 0
     part2 = torch.empty_like(part)
