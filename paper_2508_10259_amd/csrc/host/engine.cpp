@@ -324,12 +324,14 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
   for (int b = 0; b < B; ++b) h[4 * B + 1 + b] = lens_set ? lens_set[b] : counts[b];
   if (src)
     for (size_t i = 0; i < p.row.size(); ++i) h[5 * B + 1 + i] = src[p.row[i]];
+  const std::vector<int32_t> ord = pass_orders(p, counts);
+  std::copy(ord.begin(), ord.end(), h.begin() + 6 * B + 1);
   int32_t* md = c.meta();
   TRY(hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
   for (size_t pi = 0; pi < p.passes.size(); ++pi) {
     const Pass& ps = p.passes[pi];
     Segs sg{md + ps.seg_begin, md + B + ps.seg_begin, md + 2 * B + ps.seg_begin + (int)pi, ps.n_seg, ps.n_tok,
-            ps.max_len, ps.max_end};
+            ps.max_len, ps.max_end, md + 6 * B + 1 + ps.seg_begin};
     if (src)  // the rows' tokens to process start at their own places in x
       TRY(ingest_segs(c.model->st, x, sg, md + 5 * B + 1 + ps.seg_begin, (int)d, c.h(), s));
     else
@@ -355,6 +357,8 @@ hipError_t ctx_flow(Ctx& c, const FlowHeadView& fh, float* x, float tau0, int n_
   std::copy(p.row.begin(), p.row.end(), h.begin());
   std::copy(p.pos.begin(), p.pos.end(), h.begin() + B);
   std::copy(p.off.begin(), p.off.end(), h.begin() + 2 * B);
+  const std::vector<int32_t> ord = pass_orders(p, counts.data());
+  std::copy(ord.begin(), ord.end(), h.begin() + 6 * B + 1);
   int32_t* md = c.meta();
   TRY(hipMemcpyAsync(md, h.data(), h.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
   const float dt = (1.0f - tau0) / (float)n_steps;
@@ -363,7 +367,7 @@ hipError_t ctx_flow(Ctx& c, const FlowHeadView& fh, float* x, float tau0, int n_
     for (size_t pi = 0; pi < p.passes.size(); ++pi) {
       const Pass& ps = p.passes[pi];
       Segs sg{md + ps.seg_begin, md + B + ps.seg_begin, md + 2 * B + ps.seg_begin + (int)pi, ps.n_seg, ps.n_tok,
-              ps.max_len, ps.max_end};
+              ps.max_len, ps.max_end, md + 6 * B + 1 + ps.seg_begin};
       float* xp = x + (size_t)ps.tok_src * a;  // every row brings T tokens: the pass's first token
       TRY(flow_embed(c.model->st, xp, fh.w_in, fh.w_t, tau, ps.n_tok, a, d, c.h(), s));
       for (int l = 0; l < m.n_layers; ++l)
@@ -400,6 +404,7 @@ struct Rows {
   float* logits() const { return (float*)at(c->lay.logits, bins_padded(c->model->cfg) * 4); }
   float* ss() const { return (float*)at(c->lay.ss, (size_t)(c->model->cfg.d_model / 128) * 4); }
   int32_t* lens() const { return (int32_t*)at(c->lay.lens, 4); }
+  int32_t* order() const { return (int32_t*)at(c->lay.order, 4); }
   float* part() const {
     const Cfg& m = c->model->cfg;
     return (float*)at(c->lay.part, (size_t)m.n_heads * c->splits * (m.head_dim + 2) * 4);
@@ -506,7 +511,7 @@ static hipError_t layer_decode(const Rows& g, int l, int jpos, hipStream_t s, st
                 l > 0 ? ss : nullptr, &qp) != hipSuccess)
     return hipErrorLaunchFailure;
   TRY(attn_decode(dt, g.qkv(), g.lens(), jpos, B, m.n_heads, m.head_dim, c.lay.capacity, g.pages(), c.splits, c.rope(),
-                  g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo, qp));
+                  g.kslab(l), g.vslab(l), g.part(), g.o(), s, olo, qp, B > 1 ? g.order() : nullptr));
   if (c.splits > 1) TRY(attn_merge(dt, g.part(), B, m.n_heads, m.head_dim, c.splits, g.o(), s, olo));
   TRY(resid_proj(g, g.o(), olo, md.wo(l), md.fo(l), d, hhi, hlo, s, ss));
   if (norm_proj(g, EPI_SWIGLU, g.h(), hhi, hlo, md.wgu(l), md.fgu(l), 2 * F, d, g.a(), F, alo, s, err, ss) != hipSuccess)
@@ -540,6 +545,9 @@ static hipError_t decode_rows(const Rows& g, int A, int32_t* tok, float* logits,
   int32_t* gt = tok + (size_t)g.r0 * A;
   float* gl = logits ? logits + (size_t)g.r0 * A * m.n_bins : nullptr;
   const int32_t* gf = forced ? forced + (size_t)g.r0 * A : nullptr;
+  // the rows longest first for the decode attention's dispatch (one order per
+  // step: every pass adds one position to every row)
+  if (g.n > 1 && A > 1) TRY(len_order(g.lens(), g.n, g.order(), s));
   if (head(g, g.h_last(), fused ? g.h_last16() : nullptr, fused ? g.h_last16lo() : nullptr, A, 0, gt, gl, gf, s,
            err) != hipSuccess)
     return hipErrorLaunchFailure;

@@ -102,6 +102,7 @@ struct CtxLayout {
   int n_pages;        // pages in each layer's K (and V) pool
   size_t slab_layer;  // bytes of K (or V) for one layer: n_pages pages of 64 positions
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
+  size_t order;  // the rows by decreasing length [B] int32 (decode attention dispatch order)
   size_t ss;  // decode rows' sums of squares per 128 residual columns [B][d/128]
   size_t wcnt;  // arrival counters of the wide decode GEMM's weight tiles (zero between launches)
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
@@ -283,8 +284,10 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.ss = o; o = align256(o + B * (size_t)(d / 128 + 1) * 4);
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
   x.lens = o; o = align256(o + B * 4);
-  // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B], src[B]
-  x.meta_ints = 6 * B + 1;
+  x.order = o; o = align256(o + B * 4);
+  // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B], src[B],
+  // order[B] (each pass's segments by decreasing pos + len, indices local to the pass)
+  x.meta_ints = 7 * B + 1;
   x.meta = o; o = align256(o + x.meta_ints * 4);
   const bool fx = batch <= FUSED_MAX_ROWS && es == 2;
   x.fx_hp = o; o = align256(o + (fx ? 2 * B * d * 2 : 0));
@@ -672,6 +675,19 @@ inline Plan plan_passes(int batch, const int32_t* counts, const int32_t* start, 
   }
   flush();
   return p;
+}
+
+// Each pass's segments by decreasing key count (pos + len; ties by index),
+// as indices local to the pass, at the pass's first segment.
+inline std::vector<int32_t> pass_orders(const Plan& p, const int32_t* counts) {
+  std::vector<int32_t> ord(p.row.size());
+  for (const Pass& ps : p.passes) {
+    auto keys = [&](int i) { const int s = ps.seg_begin + i; return p.pos[s] + counts[p.row[s]]; };
+    int32_t* o = ord.data() + ps.seg_begin;
+    for (int i = 0; i < ps.n_seg; ++i) o[i] = i;
+    std::stable_sort(o, o + ps.n_seg, [&](int a, int b) { return keys(a) > keys(b); });
+  }
+  return ord;
 }
 
 // Key splits of the decode attention.  One workgroup per (row, head) covers

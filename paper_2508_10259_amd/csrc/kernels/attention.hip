@@ -412,12 +412,14 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
                                                                 const float2* __restrict__ rope,
                                                                 const f16* __restrict__ kslab,
                                                                 const f16* __restrict__ vslab, f16* __restrict__ o,
-                                                                float scale) {
+                                                                float scale, const int32_t* __restrict__ order) {
   using G = ExtGeo<DH>;
   constexpr int NQI = G::NQI, NDJ = G::NDJ, VPAD = G::VPAD, PPAD = G::PPAD, VLD = G::VLD, VPASS = G::VPASS;
   constexpr int HALF = DH / 2;
   extern __shared__ __attribute__((aligned(16))) unsigned char ext_sm[];
-  const int sg = blockIdx.z, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+  // segments with the most keys first (order), so the launch does not end on them
+  const int sg = order ? __builtin_amdgcn_readfirstlane(order[blockIdx.z]) : (int)blockIdx.z;
+  const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, g = lane >> 4;
   const int b = row[sg], p0 = pos[sg], t0 = off[sg], n = off[sg + 1] - off[sg];  // n <= 16
@@ -641,10 +643,10 @@ hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPage
     const dim3 grid(1, H, sg.n_seg);
     if (dh == 64)
       hipLaunchKernelGGL((k_attn_extend<64>), grid, dim3(64 * EXT_WAVES), ext_lds<64>(), s, qkv, sg.row, sg.pos,
-                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale, sg.order);
     else
       hipLaunchKernelGGL((k_attn_extend<128>), grid, dim3(64 * EXT_WAVES), ext_lds<128>(), s, qkv, sg.row, sg.pos,
-                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale);
+                         sg.off, H, kp, rope, (const f16*)kslab, (const f16*)vslab, (f16*)o, scale, sg.order);
     return hipGetLastError();
   }
   const dim3 grid((sg.max_len + 63) / 64, H, sg.n_seg);
@@ -732,12 +734,16 @@ template <typename T, int DH>
 __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
     const float* __restrict__ qkv, const int32_t* __restrict__ lens, int jpos, int H, KvPages kp, int splits,
     const float2* __restrict__ rope, T* __restrict__ kslab, T* __restrict__ vslab, float* __restrict__ part,
-    T* __restrict__ o, T* __restrict__ olo, float scale, QkvParts qp) {
+    T* __restrict__ o, T* __restrict__ olo, float scale, QkvParts qp, const int32_t* __restrict__ order) {
   using G = DecGeo<T, DH>;
   constexpr int CH = G::CH, NC = G::NC, KS = G::KS, BK = G::BK, IT = G::IT, HALF = DH / 2;
   __shared__ float wm[DECODE_MAX_WAVES], wl[DECODE_MAX_WAVES], wacc[DECODE_MAX_WAVES][DH];
   __shared__ float qs[3 * DH];  // this head's q, k, v of row b when they come as partial sums
-  const int sp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  // order (when given) lists the rows longest first, so the workgroups of long
+  // rows are dispatched before those of short ones and the launch does not end
+  // waiting on a long row's heads
+  const int sp = blockIdx.x, h = blockIdx.y;
+  const int b = order ? __builtin_amdgcn_readfirstlane(order[blockIdx.z]) : (int)blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, nw = blockDim.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: block loops branch on scalars
   const int ks = lane / NC, dc = lane % NC, i0 = dc * CH;  // this lane: key subgroup, first dimension
@@ -942,7 +948,7 @@ template <typename T>
 static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
                            int splits,
                            const float2* rope, void* k, void* v, float* part, void* o, void* olo, hipStream_t s,
-                           QkvParts qp) {
+                           QkvParts qp, const int32_t* order) {
   const float scale = 1.0f / sqrtf((float)dh);
   const dim3 grid(splits, H, B);
   // waves: enough for the longest split (ceil(cap / splits) keys) at one block
@@ -953,22 +959,23 @@ static hipError_t decode_t(const float* qkv, const int32_t* lens, int jpos, int 
   nw = nw < dh / 64 ? dh / 64 : (nw > DECODE_MAX_WAVES ? DECODE_MAX_WAVES : nw);
   if (dh == 64)
     hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
-                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp);
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp, order);
   else
     hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * nw), 0, s, qkv, lens, jpos, H, kp, splits, rope,
-                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp);
+                       (T*)k, (T*)v, part, (T*)o, (T*)olo, scale, qp, order);
   return hipGetLastError();
 }
 
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap, KvPages kp,
                        int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o, hipStream_t s,
-                       void* olo, QkvParts qp) {
+                       void* olo, QkvParts qp, const int32_t* order) {
   if (qp.part && (qp.splits < 1 || (qp.ss && qp.nss < 1))) return hipErrorInvalidValue;
   if (ct == DT_F32) {
     if (olo) return hipErrorInvalidValue;
-    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, nullptr, s, qp);
+    return decode_t<float>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, nullptr, s, qp,
+                           order);
   }
-  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, olo, s, qp);
+  return decode_t<f16>(qkv, lens, jpos, B, H, dh, cap, kp, splits, rope, kslab, vslab, part, o, olo, s, qp, order);
 }
 
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o, hipStream_t s,

@@ -434,17 +434,21 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const f16* __restrict__ u, c
 // sums (for medium token counts, where the tiles alone leave CUs idle).
 
 constexpr int GBM = 256, GBN = 256, GBK = 64;
-constexpr int G_TILE = 256 * 128;         // bytes of one A or B tile (256 rows of 64 fp16)
-constexpr int G_LDS = 2 * 2 * G_TILE;      // double-buffered A and B
+constexpr int G_TILE = 256 * 128;         // bytes of one 256-row A or B tile (rows of 64 fp16)
+
+// LDS of a BN-wide tile pair, double-buffered: [2 stages][A tile | B tile]
+template <int BN> constexpr int g_lds() { return 2 * (G_TILE + BN * 128); }
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
-// DMA of one K step: wave w moves 1 KB blocks 4w..4w+3 of the A tile and of
-// the B tile (8 rows each).  Lane i of a block: row R0 + i/8, slot i%8, source
-// chunk (i%8) ^ (row & 7).  A rows past the last valid one (alast) read it
-// again: they only feed outputs that are never stored.
+// DMA of one K step: wave w moves 1 KB blocks 4w..4w+3 of the A tile and
+// BN/64 blocks of the B tile (8 rows each).  Lane i of a block: row R0 + i/8,
+// slot i%8, source chunk (i%8) ^ (row & 7).  A rows past the last valid one
+// (alast) read it again: they only feed outputs that are never stored.
+template <int BN>
 __device__ __forceinline__ void big_dma(unsigned char* stage, const f16* A, const f16* B, int K, int k0, int alast,
                                         int wave, int lane) {
+  constexpr int BQ = BN / 64;  // B blocks per wave
   const int slot = lane & 7;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -454,29 +458,40 @@ __device__ __forceinline__ void big_dma(unsigned char* stage, const f16* A, cons
     const int ar = row <= alast ? row : alast;
     __builtin_amdgcn_global_load_lds((const void*)(A + (size_t)ar * K + k0 + c * 8), (lds_ptr)(stage + blk * 1024),
                                      16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(B + (size_t)row * K + k0 + c * 8),
-                                     (lds_ptr)(stage + G_TILE + blk * 1024), 16, 0, 0);
+    if (q < BQ) {
+      const int bblk = wave * BQ + q;
+      const int brow = bblk * 8 + (lane >> 3);
+      const int bc = slot ^ (brow & 7);
+      __builtin_amdgcn_global_load_lds((const void*)(B + (size_t)brow * K + k0 + bc * 8),
+                                       (lds_ptr)(stage + G_TILE + bblk * 1024), 16, 0, 0);
+    }
   }
 }
 
-template <int EPI>
+// BN = 256, or 192 for shapes whose 256-wide tiles leave a round of CUs mostly
+// idle (QKV of the 1,024-token extension: 192 tiles of 256 x 256 on 256 CUs,
+// 256 tiles of 256 x 192); each wave then covers 64 x BN/2.
+template <int EPI, int BN = GBN>
 __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, const f16* __restrict__ W, int M,
                                                   int N, int K, void* __restrict__ out, int ldo) {
+  constexpr int WN = BN / 2, NJ = WN / 16;  // weight rows per wave, 16-row blocks per wave
+  constexpr int STAGE = G_TILE + BN * 128;
+  static_assert(EPI != EPI_SWIGLU || NJ % 2 == 0, "gate and up blocks come in pairs");
   extern __shared__ __attribute__((aligned(16))) unsigned char gsm[];  // [2 stages][A tile | B tile]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;  // wave tile: tokens wm*64.., weight rows wn*128..
+  const int wm = wave >> 1, wn = wave & 1;  // wave tile: tokens wm*64.., weight rows wn*WN..
   // tile order: workgroups are dispatched round-robin over the 8 XCDs, so XCD x
   // (ids = x mod 8) takes a contiguous range of the tile sequence, which walks
   // groups of 8 token tiles down each weight tile: tiles that share a weight
   // (or token) tile run close together on one XCD's L2
-  const int tm_n = (M + GBM - 1) / GBM, tn_n = N / GBN, T = tm_n * tn_n;
+  const int tm_n = (M + GBM - 1) / GBM, tn_n = N / BN, T = tm_n * tn_n;
   const int L = blockIdx.x, xcd = L & 7, per = T >> 3, rem = T & 7;
   const int Lx = xcd * per + (xcd < rem ? xcd : rem) + (L >> 3);
   const int grp = Lx / (8 * tn_n), first_m = grp * 8;
   const int gm = tm_n - first_m < 8 ? tm_n - first_m : 8;
   const int in_grp = Lx - grp * 8 * tn_n;
-  const int m0 = (first_m + in_grp % gm) * GBM, n0 = (in_grp / gm) * GBN;
+  const int m0 = (first_m + in_grp % gm) * GBM, n0 = (in_grp / gm) * BN;
   const int alast = M - 1 - m0;  // last valid A row of this tile (>= 0)
   // K steps of this workgroup: split blockIdx.y of gridDim.y (EPI_PART; one split otherwise)
   const int KT_all = K / GBK, sp = blockIdx.y, S = gridDim.y;
@@ -484,23 +499,23 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
   const f16* A = u + (size_t)m0 * K + (size_t)kt0 * GBK;
   const f16* B = W + (size_t)n0 * K + (size_t)kt0 * GBK;
 
-  f32x4 acc[4][8];
+  f32x4 acc[4][NJ];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // fragment rows of this lane: A rows wm*64 + 16 i + r, B rows wn*128 + 16 j + r (all = r mod 8)
+  // fragment rows of this lane: A rows wm*64 + 16 i + r, B rows wn*WN + 16 j + r (all = r mod 8)
   const int sw = r & 7;
   const int KT = kt1 - kt0;
-  big_dma(gsm, A, B, K, 0, alast, wave, lane);
+  big_dma<BN>(gsm, A, B, K, 0, alast, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int kt = 0; kt < KT; ++kt) {
-    unsigned char* cur = gsm + (kt & 1) * 2 * G_TILE;
-    if (kt + 1 < KT) big_dma(gsm + ((kt + 1) & 1) * 2 * G_TILE, A, B, K, (kt + 1) * GBK, alast, wave, lane);
+    unsigned char* cur = gsm + (kt & 1) * STAGE;
+    if (kt + 1 < KT) big_dma<BN>(gsm + ((kt + 1) & 1) * STAGE, A, B, K, (kt + 1) * GBK, alast, wave, lane);
     const unsigned char* Ab = cur + (wm * 64 + r) * 128;
-    const unsigned char* Bb = cur + G_TILE + (wn * 128 + r) * 128;
+    const unsigned char* Bb = cur + G_TILE + (wn * WN + r) * 128;
 #pragma unroll
     for (int ks = 0; ks < GBK / 32; ++ks) {
       const int off = (((4 * ks + g) ^ sw) << 4);
@@ -508,7 +523,7 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[i] = *(const half8*)(Ab + i * 16 * 128 + off);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < NJ; ++j) {
         const half8 bf = *(const half8*)(Bb + j * 16 * 128 + off);
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf, acc[i][j], 0, 0, 0);
@@ -529,16 +544,16 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
       if constexpr (EPI == EPI_SWIGLU) {
         // blocks 2p (gate) and 2p+1 (up) of the packed interleave; output column (n >> 1) + r
 #pragma unroll
-        for (int pr = 0; pr < 4; ++pr) {
-          const int col = ((n0 + wn * 128) >> 1) + pr * 16 + r;
+        for (int pr = 0; pr < NJ / 2; ++pr) {
+          const int col = ((n0 + wn * WN) >> 1) + pr * 16 + r;
           st<f16>((f16*)out, (size_t)tok * ldo + col, silu(acc[i][2 * pr][e]) * acc[i][2 * pr + 1][e]);
         }
       } else {
         // EPI_PART: this split's partial sums at out[sp][tok][n] (ldo = N)
         const size_t rowo = ((size_t)(EPI == EPI_PART ? sp * M : 0) + tok) * ldo;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          float* p = (float*)out + rowo + n0 + wn * 128 + j * 16 + r;
+        for (int j = 0; j < NJ; ++j) {
+          float* p = (float*)out + rowo + n0 + wn * WN + j * 16 + r;
           if constexpr (EPI == EPI_RESID) *p += acc[i][j][e];
           else *p = acc[i][j][e];
         }
@@ -547,12 +562,37 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
   }
 }
 
-template <int EPI>
+template <int EPI, int BN = GBN>
 static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
                              int splits = 1) {
-  hipLaunchKernelGGL((k_gemm_big<EPI>), dim3((N / GBN) * ((M + GBM - 1) / GBM), splits), dim3(512), G_LDS, s, u, W,
-                     M, N, K, out, ldo);
+  hipLaunchKernelGGL((k_gemm_big<EPI, BN>), dim3((N / BN) * ((M + GBM - 1) / GBM), splits), dim3(512), g_lds<BN>(),
+                     s, u, W, M, N, K, out, ldo);
   return hipGetLastError();
+}
+
+// 256 x 192 tiles when N allows them and they need fewer CU-rounds weighted by
+// tile width (rounds of 256 workgroups, one per CU): ceil(T192 / 256) * 192 <
+// ceil(T256 / 256) * 256.  At 1,024 tokens the 7B QKV projection takes one
+// round of 256 narrower tiles instead of 192 wide ones with 64 CUs idle.
+// 256 x 256 tile columns that fill whole rounds of the CUs, when the rest
+// would leave a last round less than half busy and a round is whole tile
+// columns (256 / token tiles an integer); gemm() runs the remaining weight rows
+// as 128 x 128 tiles.  At 1,024 tokens the 7B gate|up projection's 344 big
+// tiles become 256 (64 columns) + 352 small ones for 88 big ones' work.
+static int big_main_cols(int M, int N) {
+  const int tm = (M + GBM - 1) / GBM, tn = N / GBN;
+  if (256 % tm != 0) return tn;
+  const int per_round = 256 / tm;
+  const int full = tn / per_round * per_round, rest = tn - full;
+  if (full == 0 || rest == 0 || 2 * rest * tm > 256) return tn;
+  return full;
+}
+
+static bool big_narrow(int M, int N) {
+  if (N % 192 != 0) return false;
+  const long tm = (M + GBM - 1) / GBM;
+  const long r256 = (tm * (N / 256) + 255) / 256, r192 = (tm * (N / 192) + 255) / 256;
+  return r192 * 192 < r256 * 256;
 }
 
 // ----------------------------------------------------------------------------
@@ -1124,8 +1164,18 @@ static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, i
   // 256 x 256 tiles from 160 of them on (five in eight CUs busy), 128 x 128 below: on the 7B
   // shapes the big tiles won at 172 (gate|up, 288 tokens) and 192 (QKV, 1024 tokens) tiles and
   // lost at 96 and 64
-  if (N % GBN == 0 && (size_t)(N / GBN) * ((M + GBM - 1) / GBM) >= 160)
-    return launch_big<EPI>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+  if (N % GBN == 0 && (size_t)(N / GBN) * ((M + GBM - 1) / GBM) >= 160) {
+    if constexpr (EPI == EPI_STORE)
+      if (big_narrow(M, N)) return launch_big<EPI, 192>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+    const int nb = big_main_cols(M, N) * GBN;
+    hipError_t e = launch_big<EPI>((const f16*)u, (const f16*)W, M, nb, K, out, ldo, s);
+    if (e != hipSuccess || nb == N) return e;
+    // the weight rows past nb in 128 x 128 tiles (output columns nb / 2 on for SwiGLU)
+    void* o2 = EPI == EPI_SWIGLU ? (void*)((f16*)out + nb / 2) : (void*)((float*)out + nb);
+    hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3((N - nb) / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
+                       (const f16*)u, (const f16*)W + (size_t)nb * K, M, K, o2, ldo);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
@@ -1137,9 +1187,14 @@ hipError_t gemm_big_part(const void* u, const void* W, int M, int N, int K, int 
   return launch_big<EPI_PART>((const f16*)u, (const f16*)W, M, N, K, part, N, s, splits);
 }
 
-hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s) {
+hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
+                    int bn) {
   if (M <= 0) return hipSuccess;
-  if (N % GBN != 0 || K % GBK != 0) return hipErrorInvalidValue;
+  if (bn == 192) {
+    if (epi != EPI_STORE || N % 192 != 0 || K % GBK != 0) return hipErrorInvalidValue;
+    return launch_big<EPI_STORE, 192>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+  }
+  if (bn != GBN || N % GBN != 0 || K % GBK != 0) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_STORE: return launch_big<EPI_STORE>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
     case EPI_RESID: return launch_big<EPI_RESID>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);

@@ -37,6 +37,9 @@ struct Segs {
   int n_tok;
   int max_len;  // longest segment
   int max_end;  // largest pos[s] + len(s)
+  // NULL, or the pass's segments longest attention first (pos + len decreasing):
+  // the extension attention dispatches its workgroups in that order
+  const int32_t* order = nullptr;
 };
 
 // Gate/up rows are packed interleaved in blocks of 16: packed row 32i+j is
@@ -111,7 +114,9 @@ hipError_t part_resid(const float* part, int splits, int M, int N, float* h, voi
 
 // The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
 // callable for any M (N a multiple of 256, K of 64); same epilogues.
-hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s);
+// bn: tile width, 256 or (EPI_STORE, N a multiple of 192) 192; gemm() picks it.
+hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
+                    int bn = 256);
 // Split-K form of it (1 <= splits <= K/64): part[s][m][n] = the s-th of `splits`
 // equal ranges of K steps of sum_k u[m][k] W[n][k]; part holds splits * M * N
 // floats.  part_resid adds them to the residual.
@@ -189,9 +194,11 @@ struct QkvParts {
   int nss = 0;
   float eps = 0.f;
 };
+// order: NULL, or a permutation of the B rows (longest first, see len_order)
+// in which their workgroups are dispatched; the results do not depend on it.
 hipError_t attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh,
                        int cap, KvPages kp, int splits, const float2* rope, void* kslab, void* vslab, float* part, void* o,
-                       hipStream_t s, void* olo = nullptr, QkvParts qp = QkvParts{});
+                       hipStream_t s, void* olo = nullptr, QkvParts qp = QkvParts{}, const int32_t* order = nullptr);
 hipError_t attn_merge(int ct, const float* part, int B, int H, int dh, int splits, void* o,
                       hipStream_t s, void* olo = nullptr);
 
@@ -243,6 +250,11 @@ int fused_sync_words(int d, int H);
 // lens[b] += add[b] (device arrays), or, when `set`, lens[b] = add[b] for the
 // rows with add[b] > 0 (a row-level rebuild leaves the other rows' lengths).
 hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStream_t s);
+
+// order[r] = the row of rank r by decreasing lens (ties by row index): a
+// permutation of [0, B) computed on the device, so a captured decode graph
+// follows the lengths of each replay.
+hipError_t len_order(const int32_t* lens, int B, int32_t* order, hipStream_t s);
 
 // Two-phase hashing for the action index (index.hip).  hash_segments: phase 1,
 // seg_out[g] = HashFunc1 of bytes [g s, g s + s) of data (zero-padded past

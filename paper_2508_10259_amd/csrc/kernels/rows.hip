@@ -225,4 +225,23 @@ hipError_t update_lens(int32_t* lens, const int32_t* add, int B, int set, hipStr
   return hipGetLastError();
 }
 
+// rank of row t = rows strictly longer + rows as long with a lower index
+__global__ void k_len_order(const int32_t* __restrict__ lens, int B, int32_t* __restrict__ order) {
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < B; t += gridDim.x * blockDim.x) {
+    const int lt = lens[t];
+    int r = 0;
+    for (int j = 0; j < B; ++j) {
+      const int lj = lens[j];
+      r += (lj > lt) | ((lj == lt) & (j < t));
+    }
+    order[r] = t;
+  }
+}
+
+hipError_t len_order(const int32_t* lens, int B, int32_t* order, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_len_order, dim3((B + 255) / 256), dim3(256), 0, s, lens, B, order);
+  return hipGetLastError();
+}
+
 }  // namespace ams

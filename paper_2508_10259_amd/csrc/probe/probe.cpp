@@ -13,8 +13,9 @@ int ams_probe_gemm(int dtype, int epi, const void* u, const void* ulo, const voi
   return (int)ams::gemm(dtype, epi, u, W, M, N, K, out, ldo, (hipStream_t)stream, ulo, o16, olo);
 }
 
-int ams_probe_gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, void* stream) {
-  return (int)ams::gemm_big(epi, u, W, M, N, K, out, ldo, (hipStream_t)stream);
+int ams_probe_gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, int bn,
+                       void* stream) {
+  return (int)ams::gemm_big(epi, u, W, M, N, K, out, ldo, (hipStream_t)stream, bn);
 }
 
 int ams_probe_gemm_big_part(const void* u, const void* W, int M, int N, int K, int splits, float* part,
@@ -84,14 +85,19 @@ int ams_probe_gemv_rmsnorm(int ct, int epi, const void* hhi, const void* hlo, fl
 
 // decode attention of one pass (jpos) for B rows, merged when splits > 1; K/V in
 // page pools [page][H][64][dh] with row b's page table at pt + b * (cap / 64)
+// (order: NULL or the rows' dispatch order, see len_order)
 int ams_probe_attn_decode(int ct, const float* qkv, const int32_t* lens, int jpos, int B, int H, int dh, int cap,
                           const int32_t* pt, int splits, const void* rope, void* kslab, void* vslab, float* part,
-                          void* o, void* olo, void* stream) {
+                          void* o, void* olo, const int32_t* order, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = ams::attn_decode(ct, qkv, lens, jpos, B, H, dh, cap, ams::KvPages{pt, cap / 64}, splits,
-                                  (const float2*)rope, kslab, vslab, part, o, s, olo);
+                                  (const float2*)rope, kslab, vslab, part, o, s, olo, ams::QkvParts{}, order);
   if (e == hipSuccess && splits > 1) e = ams::attn_merge(ct, part, B, H, dh, splits, o, s, olo);
   return (int)e;
+}
+
+int ams_probe_len_order(const int32_t* lens, int B, int32_t* order, void* stream) {
+  return (int)ams::len_order(lens, B, order, (hipStream_t)stream);
 }
 
 // Causal attention of packed segments (row[s], pos[s], off[s..s+1]) over their rows' K/V pages.

@@ -346,11 +346,17 @@ def test_attn_decode(probe, dtype, dh, cap, lens, jpos, splits):
     part = torch.zeros((B * H * (cap // 64) * (dh + 2),), dtype=torch.float32, device="cuda")
     o = torch.zeros((B, d), dtype=torch.float16 if dtype == "f16" else torch.float32, device="cuda")
     olo = torch.zeros((B, d), dtype=torch.float16, device="cuda") if dtype == "f16" else None  # rounding error of o
+    # the rows dispatched longest first, as the engine orders them (ranks by decreasing length,
+    # ties by row index); the output does not depend on the order
+    order = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    assert probe.ams_probe_len_order(_ptr(lens_d), B, _ptr(order), _stream()) == 0
+    torch.cuda.synchronize()
+    assert order.cpu().numpy().tolist() == sorted(range(B), key=lambda b: (-lens[b], b))
     rc = probe.ams_probe_attn_decode(CT[dtype], C.c_void_p(qkv_d.data_ptr()), C.c_void_p(lens_d.data_ptr()), jpos,
                                      B, H, dh, cap, _ptr(pt_d), splits, C.c_void_p(tab_d.data_ptr()),
                                      C.c_void_p(K_d.data_ptr()),
                                      C.c_void_p(V_d.data_ptr()), C.c_void_p(part.data_ptr()),
-                                     C.c_void_p(o.data_ptr()), _ptr(olo), _stream())
+                                     C.c_void_p(o.data_ptr()), _ptr(olo), _ptr(order), _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = o.float().cpu().numpy().astype(np.float64)
@@ -469,12 +475,16 @@ def test_gemm_big_part(probe, M, N, K, splits):
 
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (100, 256, 384), (256, 512, 1024), (300, 256, 384),
-                                   (513, 768, 1024)])
-def test_gemm_big(probe, epi, M, N, K):
+                                   (513, 768, 1024), (300, 576, 384), (1, 192, 64)])
+@pytest.mark.parametrize("bn", [256, 192])
+def test_gemm_big(probe, epi, M, N, K, bn):
     """The 256 x 256-tile prefill GEMM (direct-to-LDS tiles, swizzled rows) on ragged token
-    counts, against the exact product of its fp16 inputs."""
+    counts, against the exact product of its fp16 inputs; bn = 192: its 256 x 192 tiles (the
+    store epilogue, N a multiple of 192)."""
     import torch
-    log(f"gemm_big epi={epi} M={M} N={N} K={K}")
+    if N % bn or (bn == 192 and epi != EPI_STORE):
+        pytest.skip("256 x 192 tiles serve the store epilogue; N must be a multiple of the tile width")
+    log(f"gemm_big epi={epi} M={M} N={N} K={K} bn={bn}")
     u = _rand((M, K), 41, M, K)
     Wt = _rand((N, K), 42, N, K, std=0.05)
     y = _f(u, "f16") @ _f(Wt, "f16").T
@@ -489,12 +499,47 @@ def test_gemm_big(probe, epi, M, N, K):
         ldo = N
         ref = y + (h0.astype(np.float64) if epi == EPI_RESID else 0.0)
     ud, Wd = _dev(u, "f16"), _dev(Wt, "f16")
-    rc = probe.ams_probe_gemm_big(epi, _ptr(ud), _ptr(Wd), M, N, K, _ptr(out), ldo, _stream())
+    rc = probe.ams_probe_gemm_big(epi, _ptr(ud), _ptr(Wd), M, N, K, _ptr(out), ldo, bn, _stream())
     assert rc == 0
     torch.cuda.synchronize()
     got = out.float().cpu().numpy().astype(np.float64)
     scale = max(1.0, float(np.max(np.abs(ref))))
     tol = 2e-5 * scale * np.sqrt(K / 128)
+    if epi == EPI_SWIGLU:
+        tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
+    err = float(np.max(np.abs(got - ref)))
+    assert err <= tol, f"max abs err {err:.3e} > {tol:.3e}"
+
+
+@pytest.mark.parametrize("M,N,epi", [(2560, 4608, EPI_STORE), (2300, 4608, EPI_STORE), (1024, 22016, EPI_SWIGLU),
+                                     (1000, 22016, EPI_STORE)])
+def test_gemm_tile_plans(probe, M, N, epi):
+    """gemm() where the 256 x 256 tiles would leave a round of the CUs partly idle: at
+    2,560 / 2,300 x 4,608 both tile widths take one round (10 x 18 = 180 tiles of 256 x 256,
+    10 x 24 = 240 of 256 x 192), so it takes the narrower ones; at 1,024 / 1,000 x 22,016 the
+    first 64 tile columns fill one round and the remaining 22 go to 128 x 128 tiles.  Against
+    the exact product (SwiGLU over the interleaved gate / up rows)."""
+    import torch
+    K = 128
+    log(f"gemm tile plan M={M} N={N} K={K} epi={epi}")
+    u = _rand((M, K), 44, M, K)
+    Wt = _rand((N, K), 45, N, K, std=0.05)
+    y = _f(u, "f16") @ _f(Wt, "f16").T
+    if epi == EPI_SWIGLU:
+        g, up = _unpack_gu(y.T, N // 2)
+        ref = (_silu(g) * up).T
+        out = torch.zeros((M, N // 2), dtype=torch.float16, device="cuda")
+        ldo = N // 2
+    else:
+        ref = y
+        out = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+        ldo = N
+    rc = probe.ams_probe_gemm(CT["f16"], epi, _ptr(_dev(u, "f16")), None, _ptr(_dev(Wt, "f16")), M, N, K,
+                              _ptr(out), ldo, None, None, _stream())
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().astype(np.float64)
+    tol = 2e-5 * max(1.0, float(np.max(np.abs(ref))))
     if epi == EPI_SWIGLU:
         tol = max(tol, 2 ** -11 * float(np.max(np.abs(ref))))
     err = float(np.max(np.abs(got - ref)))
@@ -540,6 +585,19 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
         assert torch.equal(olo, (h - h.half().float()).half())
 
 
+@pytest.mark.parametrize("B", [1, 2, 64, 300])
+def test_len_order(probe, B):
+    """The decode attention's dispatch order: the rows by decreasing length, ties by row index
+    (lengths drawn from a narrow range so that ties occur), a permutation of [0, B)."""
+    import torch
+    lens = np.random.default_rng(B).integers(200, 230, B).astype(np.int32)
+    lens_d = torch.from_numpy(lens).cuda()
+    order = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    assert probe.ams_probe_len_order(_ptr(lens_d), B, _ptr(order), _stream()) == 0
+    torch.cuda.synchronize()
+    assert order.cpu().numpy().tolist() == sorted(range(B), key=lambda b: (-int(lens[b]), b))
+
+
 @pytest.mark.parametrize("qsplits,norm", [(1, True), (4, True), (8, False)])
 @pytest.mark.parametrize("splits", [1, 3])
 def test_attn_decode_parts(probe, qsplits, norm, splits):
@@ -581,7 +639,7 @@ def test_attn_decode_parts(probe, qsplits, norm, splits):
         else:
             rc = probe.ams_probe_attn_decode(CT["f16"], _ptr(qkv), _ptr(lens_d), jpos, B, H, dh, cap, _ptr(pt_d),
                                              splits, _ptr(tab_d), _ptr(K_d), _ptr(V_d), _ptr(part), _ptr(o),
-                                             _ptr(olo), _stream())
+                                             _ptr(olo), None, _stream())
         assert rc == 0
         torch.cuda.synchronize()
         res.append((o, olo, K_d, V_d))
