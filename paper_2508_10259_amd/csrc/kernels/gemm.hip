@@ -516,18 +516,45 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
     if (kt + 1 < KT) big_dma<BN>(gsm + ((kt + 1) & 1) * STAGE, A, B, K, (kt + 1) * GBK, alast, wave, lane);
     const unsigned char* Ab = cur + (wm * 64 + r) * 128;
     const unsigned char* Bb = cur + G_TILE + (wn * WN + r) * 128;
+    // every fragment of the K step requested in use order, the MFMA groups (8
+    // MFMAs: two B fragments times four A fragments) interleaved with the
+    // requests of the fragments two groups ahead, so a group does not wait on
+    // the LDS round trip of its own operands (on the 7B builds 1.5-2.5% faster
+    // than the compiler's order, which requested each group's fragments right
+    // before it)
+    half8 af[2][4], bfr[2][NJ];
 #pragma unroll
-    for (int ks = 0; ks < GBK / 32; ++ks) {
+    for (int ks = 0; ks < 2; ++ks) {
       const int off = (((4 * ks + g) ^ sw) << 4);
-      half8 af[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *(const half8*)(Ab + i * 16 * 128 + off);
+      for (int i = 0; i < 4; ++i) af[ks][i] = *(const half8*)(Ab + i * 16 * 128 + off);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const half8 bf = *(const half8*)(Bb + j * 16 * 128 + off);
+      for (int j = 0; j < NJ; ++j) bfr[ks][j] = *(const half8*)(Bb + j * 16 * 128 + off);
+    }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bf, acc[i][j], 0, 0, 0);
-      }
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    if constexpr (NJ == 8) {  // sched_group_barrier masks: 0x100 LDS reads, 0x008 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     }
     __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA into the other stage has landed
     __syncthreads();
@@ -871,44 +898,71 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // one K chunk t: its MFMAs from stage t & 1 and weights w, then staging chunk
+  // t+1, the activation loads of chunk t+2 and the weight loads of chunk t+WP
+  // (into w), each where that chunk exists.  The activation loads go out
+  // before the weight loads: vmcnt retires in issue order, so staging chunk
+  // t+2 next round waits only for loads older than the newest weight chunk.
+  auto step = [&](int t, uint4 (&w)[4], bool st1, bool ld2, bool ldw) __attribute__((always_inline)) {
+    const f16* xb = xs + (size_t)((t & 1) * NX) * MB * 16 * WIDE_LDK;
 #pragma unroll
-  for (int p = 0; p < WP; ++p)
-    if (p < n) wide_wload_fo(wr[p], wstrip, chunk(p));
-  AMS_WIDE_XLOAD(chunk(0));
-  AMS_WIDE_XSTORE(0);
-  if (n > 1) AMS_WIDE_XLOAD(chunk(1));
-  __syncthreads();
-
-  for (int tb = 0; tb < n; tb += WP) {
+    for (int i = 0; i < 4; ++i) {
+      half8 bf[NX][MB];
 #pragma unroll
-    for (int p = 0; p < WP; ++p) {
-      const int t = tb + p;
-      if (t < n) {  // uniform across the workgroup (n is)
-        const f16* xb = xs + (size_t)((t & 1) * NX) * MB * 16 * WIDE_LDK;
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          half8 bf[NX][MB];
+        for (int a = 0; a < NX; ++a)
+          bf[a][mb] = *(const half8*)(xb + (size_t)(a * MB * 16 + mb * 16 + r) * WIDE_LDK + 32 * i + 8 * g);
+      const half8 wf = as_half8(w[i]);
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int a = 0; a < NX; ++a)
-              bf[a][mb] = *(const half8*)(xb + (size_t)(a * MB * 16 + mb * 16 + r) * WIDE_LDK + 32 * i + 8 * g);
-          const half8 wf = as_half8(wr[p][i]);
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int a = 0; a < NX; ++a)
-              acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, bf[a][mb], acc[mb], 0, 0, 0);
-        }
-        // the activation loads go out before the weight loads of this round:
-        // vmcnt retires in issue order, so staging chunk t+2 next round then
-        // waits only for loads older than the newest weight chunk
-        if (t + 1 < n) AMS_WIDE_XSTORE((t + 1) & 1);
-        if (t + 2 < n) AMS_WIDE_XLOAD(chunk(t + 2));
-        if (t + WP < n) wide_wload_fo(wr[p], wstrip, chunk(t + WP));
-        __syncthreads();
-      }
+        for (int a = 0; a < NX; ++a)
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, bf[a][mb], acc[mb], 0, 0, 0);
     }
+    if (st1) AMS_WIDE_XSTORE((t + 1) & 1);
+    if (ld2) AMS_WIDE_XLOAD(chunk(t + 2));
+    __builtin_amdgcn_sched_barrier(0);  // keep the issue order
+    if (ldw) wide_wload_fo(w, wstrip, chunk(t + WP));
+    __syncthreads();
+  };
+  int t = 0;
+  if (n >= 2 * WP) {
+    // Every chunk the prologue and the steps of this loop load exists, so
+    // their loads are unconditional and issued in one order (a step's
+    // activation loads, then its weight loads; the prologue X(c), W(c + WP - 2)
+    // for c = 2 - WP .. 1): the loads in flight at the loop head are the same
+    // from either edge, and the compiler's waits count them exactly instead of
+    // draining them (with conditional loads each step waited for the weights
+    // it had just requested).  Measured on the 7B decoder: 64-row decode 44.4
+    // -> 44.0 ms per step, 16-row 56-token decode 223.0 -> 222.1 ms.
+#pragma unroll
+    for (int c = 2 - WP; c <= 1; ++c) {
+      if (c >= 0) AMS_WIDE_XLOAD(chunk(c));
+      __builtin_amdgcn_sched_barrier(0);
+      wide_wload_fo(wr[c + WP - 2], wstrip, chunk(c + WP - 2));
+      __builtin_amdgcn_sched_barrier(0);
+      if (c == 0) AMS_WIDE_XSTORE(0);  // before the staging registers take chunk 1
+    }
+    __syncthreads();
+    for (; t + 2 * WP <= n; t += WP) {
+#pragma unroll
+      for (int p = 0; p < WP; ++p) step(t + p, wr[p], true, true, true);
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < WP; ++p)
+      if (p < n) wide_wload_fo(wr[p], wstrip, chunk(p));
+    AMS_WIDE_XLOAD(chunk(0));
+    AMS_WIDE_XSTORE(0);
+    if (n > 1) AMS_WIDE_XLOAD(chunk(1));
+    __syncthreads();
+  }
+  // the remaining steps (fewer than 2 WP with the loop above)
+  for (; t < n; t += WP) {
+#pragma unroll
+    for (int p = 0; p < WP; ++p)
+      if (t + p < n) step(t + p, wr[p], t + p + 1 < n, t + p + 2 < n, t + p + WP < n);
   }
 
 #undef AMS_WIDE_XLOAD1
