@@ -144,6 +144,10 @@ hipError_t argmax_feed(int ct, const float* logits, int ld_logits, const void* b
 // ulo (fp16 only, or NULL): the rounding error of u, so that u + ulo is the
 // normalised row to about 22 significant bits.
 hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hipStream_t s, void* ulo = nullptr);
+// h[m] += sum of the split-K partial sums part[s][m] (splits in order), then
+// u[m] = fp16(h[m] / rms(h[m])) (fp16 compute; d <= 16384): part_resid and
+// rmsnorm in one pass, u bitwise what rmsnorm gives.
+hipError_t resid_norm(const float* part, int splits, int M, int d, float* h, float eps, void* u, hipStream_t s);
 
 // out[i] = E[clamp(ids[i])] in the storage type.
 hipError_t embed_rows(int st, const void* E, const int32_t* ids, int n, int d, int vocab, void* out,

@@ -58,6 +58,57 @@ hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hip
   return rmsnorm_t<f16>(h, M, d, eps, (f16*)u, (f16*)ulo, s);
 }
 
+// h[m] += sum_s part[s][m] (splits added in order), then u[m] = fp16 of the
+// new row over its rms: the split-K reduction of a token pass's residual
+// projection with the next RMSNorm in the same pass over the row.  The norm
+// sums the squares in k_rmsnorm's order, so u is bitwise what rmsnorm of the
+// new h gives.
+template <int EPT>
+__global__ __launch_bounds__(1024) void k_resid_norm(const float* __restrict__ part, int splits, int d, float eps,
+                                                     float* __restrict__ h, f16* __restrict__ u) {
+  __shared__ float red[16];
+  const size_t base = (size_t)blockIdx.x * d, MN = (size_t)gridDim.x * d;
+  const int nt = blockDim.x;
+  float x[EPT];
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = threadIdx.x + e * nt;
+    x[e] = 0.f;
+    if (i < d) {
+      float v = 0.f;
+      for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + base + i];
+      x[e] = h[base + i] + v;
+      h[base + i] = x[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) ss = fmaf(x[e], x[e], ss);
+  const float tot = block_sum(ss, red);
+  const float rs = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = threadIdx.x + e * nt;
+    if (i < d) u[base + i] = sat16(x[e] * rs);
+  }
+}
+
+hipError_t resid_norm(const float* part, int splits, int M, int d, float* h, float eps, void* u, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (splits < 1) return hipErrorInvalidValue;
+  const int nt = d <= 4096 ? 256 : 1024;
+  const int ept = (d + nt - 1) / nt;
+#define AMS_RN(E) hipLaunchKernelGGL((k_resid_norm<E>), dim3(M), dim3(nt), 0, s, part, splits, d, eps, h, (f16*)u)
+  if (ept <= 1) AMS_RN(1);
+  else if (ept <= 2) AMS_RN(2);
+  else if (ept <= 4) AMS_RN(4);
+  else if (ept <= 8) AMS_RN(8);
+  else if (ept <= 16) AMS_RN(16);
+  else return hipErrorInvalidValue;
+#undef AMS_RN
+  return hipGetLastError();
+}
+
 // Copies rows as raw elements (8/16-byte chunks); `ids` selects source rows.
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(const T* __restrict__ E, const int32_t* __restrict__ ids, int d,

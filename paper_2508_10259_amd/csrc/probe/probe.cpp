@@ -67,6 +67,10 @@ int ams_probe_part_swiglu(const float* part, int splits, int M, int N, void* out
   return (int)ams::part_swiglu(part, splits, M, N, out, olo, (hipStream_t)stream);
 }
 
+int ams_probe_resid_norm(const float* part, int splits, int M, int d, float* h, float eps, void* u, void* stream) {
+  return (int)ams::resid_norm(part, splits, M, d, h, eps, u, (hipStream_t)stream);
+}
+
 int ams_probe_rmsnorm(int dtype, const float* h, int M, int d, float eps, void* u, void* ulo, void* stream) {
   return (int)ams::rmsnorm(dtype, h, M, d, eps, u, (hipStream_t)stream, ulo);
 }

@@ -585,6 +585,36 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
         assert torch.equal(olo, (h - h.half().float()).half())
 
 
+@pytest.mark.parametrize("M,d,splits", [(1024, 4096, 4), (7, 1024, 8), (300, 5120, 3), (5, 12288, 2)])
+def test_resid_norm(probe, M, d, splits):
+    """The token passes' split-K residual reduction with the next RMSNorm in one pass: h and u
+    bitwise equal to part_resid followed by rmsnorm, and u within fp16 rounding of the fp64
+    definition RMSNorm(h + sum of the partial sums)."""
+    import torch
+    eps = 1e-5
+    log(f"resid_norm M={M} d={d} splits={splits}")
+    part = W.random_gaussian((splits, M, d), 95, M, d, dtype="f32")
+    h0 = W.random_gaussian((M, d), 96, M, d, dtype="f32")
+    pd = torch.from_numpy(part.reshape(-1).copy()).cuda()
+    h1, h2 = torch.from_numpy(h0.copy()).cuda(), torch.from_numpy(h0.copy()).cuda()
+    u1 = torch.zeros((M, d), dtype=torch.float16, device="cuda")
+    u2 = torch.zeros_like(u1)
+    assert probe.ams_probe_resid_norm(_ptr(pd), splits, M, d, _ptr(h1), C.c_float(eps), _ptr(u1), _stream()) == 0
+    assert probe.ams_probe_part_resid(_ptr(pd), splits, M, d, _ptr(h2), None, None, _stream()) == 0
+    assert probe.ams_probe_rmsnorm(CT["f16"], _ptr(h2), M, d, C.c_float(eps), _ptr(u2), None, _stream()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(h1, h2) and torch.equal(u1, u2)
+    hn = h0.astype(np.float64) + part.astype(np.float64).sum(axis=0)
+    rs = 1.0 / np.sqrt(np.mean(hn * hn, axis=1, keepdims=True) + eps)
+    ref = hn * rs
+    err = np.abs(u1.float().cpu().numpy() - ref)
+    # fp16 rounding of the output (half an ulp, subnormals included), the fp32 sums of the
+    # splits and the residual (their terms' magnitudes times n * 2^-24), and the fp32 norm
+    terms = np.abs(h0).astype(np.float64) + np.abs(part).astype(np.float64).sum(axis=0)
+    bound = 2.0 ** -11 * np.abs(ref) + 2.0 ** -25 + (splits + 1) * 2.0 ** -24 * terms * rs + 1e-6 * np.abs(ref)
+    assert bool(np.all(err <= bound)), float(np.max(err - bound))
+
+
 @pytest.mark.parametrize("B", [1, 2, 64, 300])
 def test_len_order(probe, B):
     """The decode attention's dispatch order: the rows by decreasing length, ties by row index
