@@ -276,37 +276,57 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   f16* Pw = Ps + wave * 16 * PPAD;
   constexpr int CH = DH / 8;  // 16-byte chunks per key row
 
-  for (int kt = 0; kt < kv_end; kt += KT) {
-    __syncthreads();  // previous tile's Ks / VT / Ps reads are done
+  // A key tile goes global -> registers -> LDS; the next tile's loads are in
+  // flight while the current one computes.  K: item c (< KT * CH) is key c / CH,
+  // chunk c % CH.  V^T: item c takes keys 4(c & 15) .. +3 of the 16-byte dim
+  // chunk c >> 4 and writes, per dim, those 4 keys as one 8-byte word; the 16
+  // lanes of a group fill one V^T row (64 keys), which keeps the writes free of
+  // bank conflicts.
+  constexpr int KI = KT * CH / 256, NV = KT / 4 * CH, VI = (NV + 255) / 256;
+  uint4 kreg[KI], vreg[VI][4];
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
     const size_t tb = kv_slot(kv_page_u(kp, b, kt), H, h, 0, DH);  // a 64-key tile is one page
     const f16* Kb = kslab + tb;
     const f16* Vb = vslab + tb;
-    for (int c = tid; c < KT * CH; c += 256) {
-      const int kk = c / CH, ch = c % CH;
-      const bool ok = kt + kk < kv_end;
-      *(uint4*)(Ks + kk * KPAD + ch * 8) =
-          ok ? *(const uint4*)(Kb + (size_t)kk * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < KI; ++q) {
+      const int c = tid + 256 * q, kk = c / CH, ch = c % CH;
+      kreg[q] = kt + kk < kv_end ? *(const uint4*)(Kb + (size_t)kk * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
     }
-    // V^T: item c takes keys 4(c & 15) .. +3 of the 16-byte dim chunk c >> 4 and
-    // writes, per dim, those 4 keys as one 8-byte word; the 16 lanes of a group
-    // fill one V^T row (64 keys), which keeps the writes free of bank conflicts
-    for (int c = tid; c < (KT / 4) * CH; c += 256) {
-      const int kq = c & 15, ch = c >> 4;
-      half8 vq[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kt + 4 * kq + i;
-        vq[i] = __builtin_bit_cast(half8, key < kv_end ? *(const uint4*)(Vb + (size_t)(key - kt) * DH + ch * 8)
-                                                       : uint4{0u, 0u, 0u, 0u});
-      }
+    for (int q = 0; q < VI; ++q) {
+      const int c = tid + 256 * q, kq = c & 15, ch = c >> 4;
+      if (c < NV)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        typedef _Float16 half4v __attribute__((ext_vector_type(4)));
-        const half4v w = {vq[0][e], vq[1][e], vq[2][e], vq[3][e]};
-        *(half4v*)(VT + (ch * 8 + e) * VPAD + 4 * kq) = w;
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt + 4 * kq + i;
+          vreg[q][i] = key < kv_end ? *(const uint4*)(Vb + (size_t)(key - kt) * DH + ch * 8) : uint4{0u, 0u, 0u, 0u};
+        }
+    }
+  };
+  load_tile(0);
+  for (int kt = 0; kt < kv_end; kt += KT) {
+    __syncthreads();  // previous tile's Ks / VT / Ps reads are done
+#pragma unroll
+    for (int q = 0; q < KI; ++q) {
+      const int c = tid + 256 * q, kk = c / CH, ch = c % CH;
+      *(uint4*)(Ks + kk * KPAD + ch * 8) = kreg[q];
+    }
+#pragma unroll
+    for (int q = 0; q < VI; ++q) {
+      const int c = tid + 256 * q, kq = c & 15, ch = c >> 4;
+      if (c < NV) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          typedef _Float16 half4v __attribute__((ext_vector_type(4)));
+          const half4v w = {__builtin_bit_cast(half8, vreg[q][0])[e], __builtin_bit_cast(half8, vreg[q][1])[e],
+                            __builtin_bit_cast(half8, vreg[q][2])[e], __builtin_bit_cast(half8, vreg[q][3])[e]};
+          *(half4v*)(VT + (ch * 8 + e) * VPAD + 4 * kq) = w;
+        }
       }
     }
     __syncthreads();
+    if (kt + KT < kv_end) load_tile(kt + KT);
 
     // S for 4 blocks of 16 keys
     f32x4 sc[4];

@@ -468,9 +468,10 @@ __device__ __forceinline__ void big_dma(unsigned char* stage, const f16* A, cons
   }
 }
 
-// BN = 256, or 192 for shapes whose 256-wide tiles leave a round of CUs mostly
-// idle (QKV of the 1,024-token extension: 192 tiles of 256 x 256 on 256 CUs,
-// 256 tiles of 256 x 192); each wave then covers 64 x BN/2.
+// BN = 256, or 192 / 128 for shapes whose 256-wide tiles leave a round of CUs
+// mostly idle (QKV of the 1,024-token extension: 192 tiles of 256 x 256 on 256
+// CUs, 256 tiles of 256 x 192; the columns past whole rounds of gate|up there
+// as 256 x 128 tiles); each wave then covers 64 x BN/2.
 template <int EPI, int BN = GBN>
 __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, const f16* __restrict__ W, int M,
                                                   int N, int K, void* __restrict__ out, int ldo) {
@@ -597,15 +598,11 @@ static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, vo
   return hipGetLastError();
 }
 
-// 256 x 192 tiles when N allows them and they need fewer CU-rounds weighted by
-// tile width (rounds of 256 workgroups, one per CU): ceil(T192 / 256) * 192 <
-// ceil(T256 / 256) * 256.  At 1,024 tokens the 7B QKV projection takes one
-// round of 256 narrower tiles instead of 192 wide ones with 64 CUs idle.
 // 256 x 256 tile columns that fill whole rounds of the CUs, when the rest
 // would leave a last round less than half busy and a round is whole tile
 // columns (256 / token tiles an integer); gemm() runs the remaining weight rows
-// as 128 x 128 tiles.  At 1,024 tokens the 7B gate|up projection's 344 big
-// tiles become 256 (64 columns) + 352 small ones for 88 big ones' work.
+// as 256 x 128 tiles.  At 1,024 tokens the 7B gate|up projection's 344 big
+// tiles become 256 (64 columns) + 176 half-width ones for 88 big ones' work.
 static int big_main_cols(int M, int N) {
   const int tm = (M + GBM - 1) / GBM, tn = N / GBN;
   if (256 % tm != 0) return tn;
@@ -615,6 +612,10 @@ static int big_main_cols(int M, int N) {
   return full;
 }
 
+// 256 x 192 tiles when N allows them and they need fewer CU-rounds weighted by
+// tile width (rounds of 256 workgroups, one per CU): ceil(T192 / 256) * 192 <
+// ceil(T256 / 256) * 256.  At 1,024 tokens the 7B QKV projection takes one
+// round of 256 narrower tiles instead of 192 wide ones with 64 CUs idle.
 static bool big_narrow(int M, int N) {
   if (N % 192 != 0) return false;
   const long tm = (M + GBM - 1) / GBM;
@@ -1224,11 +1225,10 @@ static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, i
     const int nb = big_main_cols(M, N) * GBN;
     hipError_t e = launch_big<EPI>((const f16*)u, (const f16*)W, M, nb, K, out, ldo, s);
     if (e != hipSuccess || nb == N) return e;
-    // the weight rows past nb in 128 x 128 tiles (output columns nb / 2 on for SwiGLU)
+    // the weight rows past nb in 256 x 128 tiles (output columns nb / 2 on for SwiGLU):
+    // the 7B gate|up remainder at 1,024 tokens took 81.9 us as 128 x 128 tiles
     void* o2 = EPI == EPI_SWIGLU ? (void*)((f16*)out + nb / 2) : (void*)((float*)out + nb);
-    hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3((N - nb) / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
-                       (const f16*)u, (const f16*)W + (size_t)nb * K, M, K, o2, ldo);
-    return hipGetLastError();
+    return launch_big<EPI, 128>((const f16*)u, (const f16*)W + (size_t)nb * K, M, N - nb, K, o2, ldo, s);
   }
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
@@ -1247,6 +1247,14 @@ hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, 
   if (bn == 192) {
     if (epi != EPI_STORE || N % 192 != 0 || K % GBK != 0) return hipErrorInvalidValue;
     return launch_big<EPI_STORE, 192>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+  }
+  if (bn == 128) {
+    if (N % 128 != 0 || K % GBK != 0) return hipErrorInvalidValue;
+    switch (epi) {
+      case EPI_STORE: return launch_big<EPI_STORE, 128>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+      case EPI_RESID: return launch_big<EPI_RESID, 128>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+      default: return launch_big<EPI_SWIGLU, 128>((const f16*)u, (const f16*)W, M, N, K, out, ldo, s);
+    }
   }
   if (bn != GBN || N % GBN != 0 || K % GBK != 0) return hipErrorInvalidValue;
   switch (epi) {

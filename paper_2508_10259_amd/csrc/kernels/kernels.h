@@ -114,7 +114,8 @@ hipError_t part_resid(const float* part, int splits, int M, int N, float* h, voi
 
 // The 256 x 256-tile fp16 GEMM that gemm() picks for large prefix builds,
 // callable for any M (N a multiple of 256, K of 64); same epilogues.
-// bn: tile width, 256 or (EPI_STORE, N a multiple of 192) 192; gemm() picks it.
+// bn: tile width, 256, 128 (N a multiple of 128) or (EPI_STORE, N a multiple of
+// 192) 192; gemm() picks it.
 hipError_t gemm_big(int epi, const void* u, const void* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
                     int bn = 256);
 // Split-K form of it (1 <= splits <= K/64): part[s][m][n] = the s-th of `splits`

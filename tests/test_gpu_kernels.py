@@ -476,11 +476,11 @@ def test_gemm_big_part(probe, M, N, K, splits):
 @pytest.mark.parametrize("epi", [EPI_STORE, EPI_RESID, EPI_SWIGLU])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (100, 256, 384), (256, 512, 1024), (300, 256, 384),
                                    (513, 768, 1024), (300, 576, 384), (1, 192, 64)])
-@pytest.mark.parametrize("bn", [256, 192])
+@pytest.mark.parametrize("bn", [256, 192, 128])
 def test_gemm_big(probe, epi, M, N, K, bn):
     """The 256 x 256-tile prefill GEMM (direct-to-LDS tiles, swizzled rows) on ragged token
-    counts, against the exact product of its fp16 inputs; bn = 192: its 256 x 192 tiles (the
-    store epilogue, N a multiple of 192)."""
+    counts, against the exact product of its fp16 inputs; bn = 192 / 128: its 256 x 192 tiles
+    (the store epilogue, N a multiple of 192) and 256 x 128 tiles."""
     import torch
     if N % bn or (bn == 192 and epi != EPI_STORE):
         pytest.skip("256 x 192 tiles serve the store epilogue; N must be a multiple of the tile width")
@@ -517,7 +517,7 @@ def test_gemm_tile_plans(probe, M, N, epi):
     """gemm() where the 256 x 256 tiles would leave a round of the CUs partly idle: at
     2,560 / 2,300 x 4,608 both tile widths take one round (10 x 18 = 180 tiles of 256 x 256,
     10 x 24 = 240 of 256 x 192), so it takes the narrower ones; at 1,024 / 1,000 x 22,016 the
-    first 64 tile columns fill one round and the remaining 22 go to 128 x 128 tiles.  Against
+    first 64 tile columns fill one round and the remaining 22 go to 256 x 128 tiles.  Against
     the exact product (SwiGLU over the interleaved gate / up rows)."""
     import torch
     K = 128
@@ -585,7 +585,8 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
         assert torch.equal(olo, (h - h.half().float()).half())
 
 
-@pytest.mark.parametrize("M,d,splits", [(1024, 4096, 4), (7, 1024, 8), (300, 5120, 3), (5, 12288, 2)])
+@pytest.mark.parametrize("M,d,splits", [(1024, 4096, 4), (7, 1024, 8), (300, 5120, 3), (5, 12288, 2),
+                                         (64, 4096, 8), (33, 1024, 5)])
 def test_resid_norm(probe, M, d, splits):
     """The token passes' split-K residual reduction with the next RMSNorm in one pass: h and u
     bitwise equal to part_resid followed by rmsnorm, and u within fp16 rounding of the fp64
