@@ -277,6 +277,14 @@ int ctx_absorb_status(Ctx& c, std::string& err) {
   return c.book.absorb_async_error(w, err);
 }
 
+// The K/V append rides in the QKV projection's epilogue where that GEMM takes
+// 256 x 256 tiles (7B build: 201 us per layer of k_kv_append and the fp32 k/v
+// columns of qkv saved).
+static bool kv_fusable(const Ctx& c, int M) {
+  const Cfg& m = c.model->cfg;
+  return c.model->ct == DT_F16 && gemm_qkv_fusable(M, 3 * m.d_model, m.head_dim, m.d_model);
+}
+
 // h += x W^T over the M tokens of a token pass (K inputs per token).  At
 // medium token counts in fp16 the 256 x 256-tile GEMM splits K and a reduction
 // adds the partial sums in split order; that reduction also leaves the next
@@ -298,14 +306,22 @@ static hipError_t tokens_resid(Ctx& c, const void* x, const void* W, int M, int 
 
 // One decoder layer over the M tokens of a token pass; u_ready: u already holds
 // RMSNorm(h) (left by the previous residual reduction), and on return whether
-// it holds the norm of this layer's output.
-static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t s, std::string& err, bool& u_ready) {
+// it holds the norm of this layer's output; kv_fused: the QKV projection
+// appends K/V itself (the pass's token tables are in the workspace).
+static hipError_t layer_tokens(Ctx& c, int l, int M, const Segs& sg, hipStream_t s, std::string& err, bool& u_ready,
+                               bool kv_fused) {
   const Model& md = *c.model;
   const Cfg& m = md.cfg;
   const int d = m.d_model, F = m.d_ffn, dt = md.ct;
   if (!u_ready) TRY(rmsnorm(dt, c.h(), M, d, m.rms_eps, c.u(), s));
-  TRY(gemm(dt, EPI_STORE, c.u(), md.wqkv(l), M, 3 * d, d, c.qkv(), 3 * d, s));
-  TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.pages(), c.rope(), c.kslab(l), c.vslab(l), s));
+  if (kv_fused) {  // the QKV GEMM's epilogue appends K/V (the token tables are the pass's)
+    KvEpi kv{(const int64_t*)(c.ws + c.lay.tok_base), (const int32_t*)(c.ws + c.lay.tok_pos), c.kslab(l), c.vslab(l),
+             c.rope(), d, m.head_dim};
+    TRY(gemm_qkv_kv(c.u(), md.wqkv(l), M, d, c.qkv(), kv, s));
+  } else {
+    TRY(gemm(dt, EPI_STORE, c.u(), md.wqkv(l), M, 3 * d, d, c.qkv(), 3 * d, s));
+    TRY(kv_append(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.pages(), c.rope(), c.kslab(l), c.vslab(l), s));
+  }
   TRY(attn_prefill(dt, c.qkv(), sg, m.n_heads, m.head_dim, c.pages(), c.rope(), c.kslab(l), c.vslab(l), c.o(),
                    s));
   TRY(tokens_resid(c, c.o(), md.wo(l), M, d, s, u_ready));
@@ -343,8 +359,12 @@ hipError_t ctx_forward_tokens(Ctx& c, const void* x, const int32_t* counts, cons
     else
       TRY(ingest(c.model->st, (const char*)x + (size_t)ps.tok_src * d * es, ps.n_tok, (int)d, c.h(), s));
     bool u_ready = false;
+    const bool kvf = kv_fusable(c, ps.n_tok);
+    if (kvf)
+      TRY(tok_tables(sg, c.pages(), m.n_heads, m.head_dim, (int64_t*)(c.ws + c.lay.tok_base),
+                     (int32_t*)(c.ws + c.lay.tok_pos), s));
     for (int l = 0; l < m.n_layers; ++l)
-      if (layer_tokens(c, l, ps.n_tok, sg, s, err, u_ready) != hipSuccess) return hipErrorLaunchFailure;
+      if (layer_tokens(c, l, ps.n_tok, sg, s, err, u_ready, kvf) != hipSuccess) return hipErrorLaunchFailure;
     const bool f16 = c.model->ct == DT_F16;  // the fp16 pair of h_last feeds fused-RMSNorm heads
     TRY(gather_last(c.h(), sg, (int)d, c.h_last(), s, f16 ? c.h_last16() : nullptr, f16 ? c.h_last16lo() : nullptr));
   }
@@ -379,7 +399,7 @@ hipError_t ctx_flow(Ctx& c, const FlowHeadView& fh, float* x, float tau0, int n_
       TRY(flow_embed(c.model->st, xp, fh.w_in, fh.w_t, tau, ps.n_tok, a, d, c.h(), s));
       bool u_ready = false;
       for (int l = 0; l < m.n_layers; ++l)
-        if (layer_tokens(c, l, ps.n_tok, sg, s, err, u_ready) != hipSuccess) return hipErrorLaunchFailure;
+        if (layer_tokens(c, l, ps.n_tok, sg, s, err, u_ready, false) != hipSuccess) return hipErrorLaunchFailure;
       TRY(flow_update(c.model->st, c.h(), fh.w_out, m.rms_eps, dt, ps.n_tok, a, d, xp, s));
     }
   }

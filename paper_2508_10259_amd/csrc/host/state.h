@@ -103,6 +103,7 @@ struct CtxLayout {
   size_t slab_layer;  // bytes of K (or V) for one layer: n_pages pages of 64 positions
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
   size_t order;  // the rows by decreasing length [B] int32 (decode attention dispatch order)
+  size_t tok_base, tok_pos;  // a token pass's pool offsets [T] int64 and positions [T] int32 (fused K/V append)
   size_t ss;  // decode rows' sums of squares per 128 residual columns [B][d/128]
   size_t wcnt;  // arrival counters of the wide decode GEMM's weight tiles (zero between launches)
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the
@@ -285,6 +286,8 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
   x.rope = o; o = align256(o + (size_t)capacity * (c.head_dim / 2) * 8);
   x.lens = o; o = align256(o + B * 4);
   x.order = o; o = align256(o + B * 4);
+  x.tok_base = o; o = align256(o + T * 8);
+  x.tok_pos = o; o = align256(o + T * 4);
   // pass metadata of one call: row[B], pos[B], off[2B+1], lens staging[B], src[B],
   // order[B] (each pass's segments by decreasing pos + len, indices local to the pass)
   x.meta_ints = 7 * B + 1;

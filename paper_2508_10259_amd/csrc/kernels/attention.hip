@@ -91,6 +91,27 @@ __global__ __launch_bounds__(256) void k_kv_append(const float* __restrict__ qkv
   }
 }
 
+// tok_base[t] = element offset of (page, head 0, slot) of the pass's token t
+// in a layer's pool, tok_pos[t] = its position (the tables of gemm_qkv_kv)
+__global__ __launch_bounds__(256) void k_tok_tables(const int32_t* __restrict__ row, const int32_t* __restrict__ pos,
+                                                    const int32_t* __restrict__ off, int n_seg, int n_tok, int H,
+                                                    int dh, KvPages kp, int64_t* __restrict__ tok_base,
+                                                    int32_t* __restrict__ tok_pos) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_tok) return;
+  const int s = find_seg(off, n_seg, t);
+  const int b = row[s], p = pos[s] + (t - off[s]);
+  tok_base[t] = (int64_t)kv_slot(kv_page(kp, b, p), H, 0, p & (KV_PAGE - 1), dh);
+  tok_pos[t] = p;
+}
+
+hipError_t tok_tables(Segs sg, KvPages kp, int H, int dh, int64_t* tok_base, int32_t* tok_pos, hipStream_t s) {
+  if (sg.n_tok <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_tok_tables, dim3((sg.n_tok + 255) / 256), dim3(256), 0, s, sg.row, sg.pos, sg.off, sg.n_seg,
+                     sg.n_tok, H, dh, kp, tok_base, tok_pos);
+  return hipGetLastError();
+}
+
 hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;

@@ -15,6 +15,8 @@
 //    LDS double buffering with one barrier per K step, epilogue staged
 //    through LDS so global stores are row-contiguous.
 //  * k_gemm_f32     (fp32 model dtype): 64x64x16 FMA tiles, same epilogue.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -474,7 +476,7 @@ __device__ __forceinline__ void big_dma(unsigned char* stage, const f16* A, cons
 // as 256 x 128 tiles); each wave then covers 64 x BN/2.
 template <int EPI, int BN = GBN>
 __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, const f16* __restrict__ W, int M,
-                                                  int N, int K, void* __restrict__ out, int ldo) {
+                                                  int N, int K, void* __restrict__ out, int ldo, KvEpi kv) {
   constexpr int WN = BN / 2, NJ = WN / 16;  // weight rows per wave, 16-row blocks per wave
   constexpr int STAGE = G_TILE + BN * 128;
   static_assert(EPI != EPI_SWIGLU || NJ % 2 == 0, "gate and up blocks come in pairs");
@@ -576,6 +578,42 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
           const int col = ((n0 + wn * WN) >> 1) + pr * 16 + r;
           st<f16>((f16*)out, (size_t)tok * ldo + col, silu(acc[i][2 * pr][e]) * acc[i][2 * pr + 1][e]);
         }
+      } else if (EPI == EPI_QKV && n0 + wn * WN >= kv.d) {
+        // k or v columns (a wave's 128 columns lie in one of q, k, v: d is a multiple of
+        // 256): heads c / dh .. of this wave, written to the token's pool slot as
+        // k_kv_append writes them (k rotated by the token's position, rotate-half)
+        const int c0 = n0 + wn * WN;
+        const bool isk = c0 < 2 * kv.d;
+        const size_t base = (size_t)kv.tok_base[tok];
+        const int hd0 = (c0 - (isk ? kv.d : 2 * kv.d)) / kv.dh;
+        // rotate-half pairs: dims dd and dd + dh/2 of a head are blocks jj and jj + HB/2
+        // of its HB = dh/16 blocks (the block index a constant: acc stays in registers)
+        auto kstore = [&](auto hbc) __attribute__((always_inline)) {
+          constexpr int HB = decltype(hbc)::value;
+          const int p = kv.tok_pos[tok], half = HB * 8;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int hh = j / HB, jj = j % HB;  // head of this wave, block within the head
+            if (jj < HB / 2) {
+              const int dd = 16 * jj + r;  // < half; its partner is dd + half
+              const float2 cs = kv.rope[(size_t)p * half + dd];
+              const float a = acc[i][j][e], c = acc[i][(j + HB / 2) % NJ][e];
+              f16* dst = (f16*)kv.k + base + (size_t)(hd0 + hh) * KV_PAGE * (2 * half);
+              st<f16>(dst, dd, a * cs.x - c * cs.y);
+              st<f16>(dst, dd + half, a * cs.y + c * cs.x);
+            }
+          }
+        };
+        if (isk) {
+          if (kv.dh == 128) kstore(std::integral_constant<int, 8>{});
+          else kstore(std::integral_constant<int, 4>{});
+        } else {
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int col = 16 * j + r, hh = col / kv.dh, dd = col % kv.dh;
+            st<f16>((f16*)kv.v + base + (size_t)(hd0 + hh) * KV_PAGE * kv.dh, dd, acc[i][j][e]);
+          }
+        }
       } else {
         // EPI_PART: this split's partial sums at out[sp][tok][n] (ldo = N)
         const size_t rowo = ((size_t)(EPI == EPI_PART ? sp * M : 0) + tok) * ldo;
@@ -592,9 +630,9 @@ __global__ __launch_bounds__(512) void k_gemm_big(const f16* __restrict__ u, con
 
 template <int EPI, int BN = GBN>
 static hipError_t launch_big(const f16* u, const f16* W, int M, int N, int K, void* out, int ldo, hipStream_t s,
-                             int splits = 1) {
+                             int splits = 1, const KvEpi& kv = KvEpi{}) {
   hipLaunchKernelGGL((k_gemm_big<EPI, BN>), dim3((N / BN) * ((M + GBM - 1) / GBM), splits), dim3(512), g_lds<BN>(),
-                     s, u, W, M, N, K, out, ldo);
+                     s, u, W, M, N, K, out, ldo, kv);
   return hipGetLastError();
 }
 
@@ -1233,6 +1271,20 @@ static hipError_t gemm_epi(int ct, const void* u, const void* W, int M, int N, i
   hipLaunchKernelGGL((k_gemm_tiled<EPI>), dim3(N / TBN, (M + TBM - 1) / TBM), dim3(256), 0, s,
                      (const f16*)u, (const f16*)W, M, K, out, ldo);
   return hipGetLastError();
+}
+
+bool gemm_qkv_fusable(int M, int N, int dh, int d) {
+  if (M <= 64 || (dh != 64 && dh != 128) || d % 256 != 0 || N != 3 * d) return false;
+  if ((size_t)(N / GBN) * ((M + GBM - 1) / GBM) < 160) return false;  // gemm() takes the tiled kernel
+  return !big_narrow(M, N) && big_main_cols(M, N) == N / GBN;       // ... or other tile widths
+}
+
+hipError_t gemm_qkv_kv(const void* u, const void* W, int M, int K, float* qkv, const KvEpi& kv, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if ((kv.dh != 64 && kv.dh != 128) || kv.d <= 0 || kv.d % 256 != 0 || K % GBK != 0 || !kv.tok_base || !kv.tok_pos ||
+      !kv.k || !kv.v || !kv.rope)
+    return hipErrorInvalidValue;
+  return launch_big<EPI_QKV>((const f16*)u, (const f16*)W, M, 3 * kv.d, K, qkv, 3 * kv.d, s, 1, kv);
 }
 
 hipError_t gemm_big_part(const void* u, const void* W, int M, int N, int K, int splits, float* part, hipStream_t s) {

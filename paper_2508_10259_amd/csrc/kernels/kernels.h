@@ -14,7 +14,8 @@ namespace ams {
 // kernels (GEMM inputs, activations, K/V slab, packed weights): DT_F32 for
 // fp32 models, DT_F16 for bf16 models.
 enum DType { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 /* internal: split-K partial sums */ };
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PART = 3 /* internal: split-K partial sums */,
+           EPI_QKV = 4 /* internal: QKV projection with RoPE + K/V append */ };
 
 // Packed-token pass metadata (device arrays).  Segment s covers tokens
 // off[s]..off[s+1]-1 of the pass, which belong to row `row[s]` at positions
@@ -175,6 +176,24 @@ hipError_t convert(int st, int ct, const void* src, size_t rows, int cols, const
 hipError_t rope_table(float2* tab, int cap, int dh, float theta, hipStream_t s);
 
 // Rotates the new tokens' keys and writes K/V into the slab of one layer.
+// The QKV projection of a token pass with the K/V append in its epilogue: q
+// columns stored fp32 at qkv[m][0..d) (ldo 3d), k rotated (RoPE at the token's
+// position) and v written fp16 into the paged pools.  tok_base[m] = element
+// offset of (page, head 0, slot) of token m in a layer's pool, tok_pos[m] its
+// position (tok_tables).  Any M (head_dim 64 or 128, d a multiple of 256); the
+// engine uses it where gemm_qkv_fusable(M, 3d, dh, d) holds, i.e. where gemm()
+// would take the 256 x 256-tile GEMM for the projection.
+struct KvEpi {
+  const int64_t* tok_base = nullptr;
+  const int32_t* tok_pos = nullptr;
+  void* k = nullptr;  // fp16 pools of the layer
+  void* v = nullptr;
+  const float2* rope = nullptr;
+  int d = 0, dh = 0;
+};
+bool gemm_qkv_fusable(int M, int N, int dh, int d);
+hipError_t gemm_qkv_kv(const void* u, const void* W, int M, int K, float* qkv, const KvEpi& kv, hipStream_t s);
+hipError_t tok_tables(Segs sg, KvPages kp, int H, int dh, int64_t* tok_base, int32_t* tok_pos, hipStream_t s);
 hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s);
 

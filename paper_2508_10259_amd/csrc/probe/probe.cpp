@@ -122,6 +122,28 @@ int ams_probe_attn_decode_parts(int ct, const float* qpart, int qsplits, const f
   return (int)e;
 }
 
+// K/V append of a pass's tokens, and the QKV GEMM with the append in its epilogue
+// (token tables into tok_base / tok_pos first)
+int ams_probe_kv_append(int ct, const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off,
+                        int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const int32_t* pt,
+                        const void* rope, void* kslab, void* vslab, void* stream) {
+  ams::Segs sg{row, pos, off, n_seg, n_tok, max_len, max_end};
+  return (int)ams::kv_append(ct, qkv, sg, H, dh, ams::KvPages{pt, cap / 64}, (const float2*)rope, kslab, vslab,
+                             (hipStream_t)stream);
+}
+int ams_probe_qkv_kv(const void* u, const void* W, int K, float* qkv, const int32_t* row, const int32_t* pos,
+                     const int32_t* off, int n_seg, int n_tok, int H, int dh, int cap, const int32_t* pt,
+                     const void* rope, void* kslab, void* vslab, int64_t* tok_base, int32_t* tok_pos, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  ams::Segs sg{row, pos, off, n_seg, n_tok, 0, 0};
+  ams::KvPages kp{pt, cap / 64};
+  hipError_t e = ams::tok_tables(sg, kp, H, dh, tok_base, tok_pos, s);
+  if (e != hipSuccess) return (int)e;
+  ams::KvEpi kv{tok_base, tok_pos, kslab, vslab, (const float2*)rope, H * dh, dh};
+  return (int)ams::gemm_qkv_kv(u, W, n_tok, K, qkv, kv, s);
+}
+int ams_probe_qkv_fusable(int M, int N, int dh, int d) { return ams::gemm_qkv_fusable(M, N, dh, d) ? 1 : 0; }
+
 int ams_probe_attn_prefill(int ct, const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off,
                            int n_seg, int n_tok, int max_len, int max_end, int H, int dh, int cap, const int32_t* pt,
                            const void* rope, const void* kslab, const void* vslab, void* o, void* stream) {

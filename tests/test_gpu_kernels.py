@@ -452,6 +452,81 @@ def test_attn_prefill(probe, dh, segs):
                 assert err <= tol, (si, i, h, err, tol)
 
 
+@pytest.mark.parametrize("dh,segs", [
+    (128, [(0, 0, 200), (1, 37, 60), (2, 500, 41)]),
+    (64, [(2, 63, 130), (0, 0, 1), (1, 250, 128)]),
+])
+def test_gemm_qkv_kv(probe, dh, segs):
+    """The QKV projection with the K/V append in its epilogue: q columns bitwise those of the
+    256 x 256-tile GEMM, v bitwise and k within one fp16 unit of what k_kv_append writes from
+    that GEMM's output (the same rotation, possibly contracted differently), every other slot
+    of the page pools untouched; sampled k and v against the fp64 product rotated by RoPE."""
+    import torch
+    B, cap, d = 3, 1024, 512
+    H, half = d // dh, dh // 2
+    log(f"gemm_qkv_kv dh={dh} segs={segs}")
+    n_tok = sum(n for _, _, n in segs)
+    off = np.cumsum([0] + [n for _, _, n in segs]).astype(np.int32)
+    u = _rand((n_tok, d), 81, n_tok, dh)
+    Wt = _rand((3 * d, d), 82, d, dh, std=0.05)
+    tab = _rope_tab(cap, dh)
+    perm = np.random.default_rng(83 + dh).permutation(B * (cap // 64)).astype(np.int32)
+    pt_d = torch.from_numpy(perm).cuda()
+    rows = torch.tensor([b for b, _, _ in segs], dtype=torch.int32, device="cuda")
+    pos = torch.tensor([p for _, p, _ in segs], dtype=torch.int32, device="cuda")
+    offd = torch.from_numpy(off).cuda()
+    ud, Wd, tab_d = _dev(u, "f16"), _dev(Wt, "f16"), _dev(tab, "f32")
+    pool = W.random_gaussian((B * (cap // 64) * H * 64 * dh,), 84, dh, dtype="f32").astype(np.float16)
+    KA, VA, KB, VB = (_dev(pool, "f16") for _ in range(4))
+    qa = torch.zeros((n_tok, 3 * d), dtype=torch.float32, device="cuda")
+    qb = torch.zeros_like(qa)
+    tb = torch.zeros((n_tok,), dtype=torch.int64, device="cuda")
+    tp = torch.zeros((n_tok,), dtype=torch.int32, device="cuda")
+    assert probe.ams_probe_qkv_kv(_ptr(ud), _ptr(Wd), d, _ptr(qa), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok,
+                                  H, dh, cap, _ptr(pt_d), _ptr(tab_d), _ptr(KA), _ptr(VA), _ptr(tb), _ptr(tp),
+                                  _stream()) == 0
+    assert probe.ams_probe_gemm_big(EPI_STORE, _ptr(ud), _ptr(Wd), n_tok, 3 * d, d, _ptr(qb), 3 * d, 256,
+                                    _stream()) == 0
+    max_len, max_end = max(n for _, _, n in segs), max(p + n for _, p, n in segs)
+    assert probe.ams_probe_kv_append(CT["f16"], _ptr(qb), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok,
+                                     max_len, max_end, H, dh, cap, _ptr(pt_d), _ptr(tab_d), _ptr(KB), _ptr(VB),
+                                     _stream()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(qa[:, :d], qb[:, :d])
+    assert torch.equal(VA, VB)
+    ka, kb_ = KA.cpu().numpy(), KB.cpu().numpy()
+    diff = np.abs(ka.astype(np.float64) - kb_.astype(np.float64))
+    ulp = np.abs(np.spacing(kb_.astype(np.float16))).astype(np.float64)
+    assert bool(np.all(diff <= ulp)), float(np.max(diff / ulp))
+    # sampled tokens against the definition
+    Kp = _from_pages(ka.reshape(-1, H, 64, dh), perm, B, cap)
+    Vp = _from_pages(VA.cpu().numpy().reshape(-1, H, 64, dh), perm, B, cap)
+    uf, wf = _f(u, "f16"), _f(Wt, "f16")
+    for si, (b, p0, n) in enumerate(segs):
+        for i in sorted({0, n // 2, n - 1}):
+            t, p = off[si] + i, p0 + i
+            y = uf[t] @ wf.T
+            cs = tab[p].astype(np.float64)
+            for h in range(H):
+                k = y[d + h * dh:d + (h + 1) * dh]
+                kr = np.concatenate([k[:half] * cs[:, 0] - k[half:] * cs[:, 1], k[:half] * cs[:, 1] + k[half:] * cs[:, 0]])
+                v = y[2 * d + h * dh:2 * d + (h + 1) * dh]
+                tol = 2.0 ** -10 * np.abs(kr) + 1e-5 * max(1.0, float(np.max(np.abs(y))))
+                assert bool(np.all(np.abs(Kp[b, h, p].astype(np.float64) - kr) <= tol)), (si, i, h)
+                tol = 2.0 ** -10 * np.abs(v) + 1e-5 * max(1.0, float(np.max(np.abs(y))))
+                assert bool(np.all(np.abs(Vp[b, h, p].astype(np.float64) - v) <= tol)), (si, i, h)
+
+
+def test_qkv_fusable(probe):
+    """The fused K/V append rides on the 256 x 256-tile QKV GEMM only: the 7B build's 19,712
+    tokens take it, the 1,024-token extension (256 x 192 tiles) and a one-row build (128 x 128
+    tiles) do not, nor head dims other than 64 and 128."""
+    assert probe.ams_probe_qkv_fusable(19712, 12288, 128, 4096) == 1
+    assert probe.ams_probe_qkv_fusable(1024, 12288, 128, 4096) == 0
+    assert probe.ams_probe_qkv_fusable(288, 12288, 128, 4096) == 0
+    assert probe.ams_probe_qkv_fusable(19712, 12288, 96, 4096) == 0
+
+
 @pytest.mark.parametrize("M,N,K,splits", [(1024, 512, 1024, 4), (300, 256, 704, 3), (65, 768, 384, 6)])
 def test_gemm_big_part(probe, M, N, K, splits):
     """Split-K form of the 256 x 256-tile GEMM: split s holds the product over its own range
