@@ -67,6 +67,10 @@ hipError_t rmsnorm(int ct, const float* h, int M, int d, float eps, void* u, hip
 // values and all their partial sums) is issued before the first add (with the
 // count at run time the loads went out one element at a time: 40.8 us against
 // 24 + 6.4 us for the two separate kernels at 1,024 x 4,096, 4 splits).
+// S == 0 (counts the registers cannot hold at once): the splits go in groups
+// of G, each group's loads for all the thread's elements issued together;
+// a group's last loads past the split count read the last split again and are
+// not added.
 template <int EPT, int S>
 __global__ __launch_bounds__(1024) void k_resid_norm(const float* __restrict__ part, int splits, int d, float eps,
                                                      float* __restrict__ h, f16* __restrict__ u) {
@@ -84,19 +88,39 @@ __global__ __launch_bounds__(1024) void k_resid_norm(const float* __restrict__ p
       for (int sp = 0; sp < S; ++sp) pv[e][sp] = i < d ? part[sp * MN + base + i] : 0.f;
     }
   }
+  float acc[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) acc[e] = 0.f;
+  if constexpr (S > 0) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+#pragma unroll
+      for (int sp = 0; sp < S; ++sp) acc[e] += pv[e][sp];
+  } else {
+    constexpr int G = EPT >= 16 ? 2 : (EPT >= 8 ? 4 : 8);  // 32+ loads in flight, within 128 VGPRs
+    for (int s0 = 0; s0 < splits; s0 += G) {
+      float q[EPT][G];
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int i = threadIdx.x + e * nt, ic = i < d ? i : 0;
+#pragma unroll
+        for (int j = 0; j < G; ++j) q[e][j] = part[(size_t)min(s0 + j, splits - 1) * MN + base + ic];
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+        if (s0 + j < splits)
+#pragma unroll
+          for (int e = 0; e < EPT; ++e) acc[e] += q[e][j];
+    }
+  }
   float ss = 0.f;
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int i = threadIdx.x + e * nt;
-    float v = 0.f;
-    if constexpr (S > 0) {
-#pragma unroll
-      for (int sp = 0; sp < S; ++sp) v += pv[e][sp];
-    } else if (i < d) {
-      for (int sp = 0; sp < splits; ++sp) v += part[sp * MN + base + i];
+    if (i < d) {
+      x[e] += acc[e];
+      h[base + i] = x[e];
     }
-    x[e] += v;
-    if (i < d) h[base + i] = x[e];
   }
 #pragma unroll
   for (int e = 0; e < EPT; ++e) ss = fmaf(x[e], x[e], ss);

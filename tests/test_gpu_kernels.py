@@ -661,7 +661,7 @@ def test_gemm_split_resid(probe, M, K, splits, pair):
 
 
 @pytest.mark.parametrize("M,d,splits", [(1024, 4096, 4), (7, 1024, 8), (300, 5120, 3), (5, 12288, 2),
-                                         (64, 4096, 8), (33, 1024, 5)])
+                                         (64, 4096, 8), (33, 1024, 5), (128, 4096, 16), (96, 5120, 7)])
 def test_resid_norm(probe, M, d, splits):
     """The token passes' split-K residual reduction with the next RMSNorm in one pass: h and u
     bitwise equal to part_resid followed by rmsnorm, and u within fp16 rounding of the fp64
