@@ -508,7 +508,7 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
       const bool ok = key < kv_end;
 #pragma unroll
       for (int i = 0; i < NQI; ++i)
-        kx[c][i] = ok ? *(const uint4*)(Kb + (size_t)(key & (KV_PAGE - 1)) * DH + 32 * i + 8 * g)
+        kx[c][i] = ok ? ld_stream(Kb + (size_t)(key & (KV_PAGE - 1)) * DH + 32 * i + 8 * g)
                       : uint4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
@@ -516,7 +516,7 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kb + 4 * vkq + i;
-        vx[4 * p + i] = key < kv_end ? *(const uint4*)(Vb + (size_t)(key & (KV_PAGE - 1)) * DH + (vq + 8 * p) * 8)
+        vx[4 * p + i] = key < kv_end ? ld_stream(Vb + (size_t)(key & (KV_PAGE - 1)) * DH + (vq + 8 * p) * 8)
                                      : uint4{0u, 0u, 0u, 0u};
       }
   };
@@ -819,7 +819,8 @@ __global__ __launch_bounds__(64 * DECODE_MAX_WAVES, 4) void k_attn_decode(
       asm("" : "+v"(ak), "+v"(av));
       typedef unsigned u32x4g __attribute__((ext_vector_type(4)));
       typedef const u32x4g __attribute__((address_space(1))) gvec;  // global, not flat
-      const u32x4g kx = *(gvec*)ak, vx = *(gvec*)av;
+      // non-temporal, as ld_stream: each pass reads the cache once
+      const u32x4g kx = __builtin_nontemporal_load((gvec*)ak), vx = __builtin_nontemporal_load((gvec*)av);
       kr[it] = uint4{kx[0], kx[1], kx[2], kx[3]};  // what a key that does not exist loaded is never used (see block)
       vr[it] = uint4{vx[0], vx[1], vx[2], vx[3]};
     }

@@ -25,6 +25,16 @@ __device__ __forceinline__ bf16 f2bf(float f) {
   return (bf16)(u >> 16);
 }
 
+// 16 bytes of a stream read once per launch (weights of a decode GEMV, the K/V
+// cache under a decode or extension attention), as a non-temporal load: the
+// stream does not push out what other workgroups re-read from L2 and the
+// Infinity Cache (the activations, the split-K partial sums, the page tables).
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  typedef unsigned u32x4s __attribute__((ext_vector_type(4)));
+  const u32x4s x = __builtin_nontemporal_load((const u32x4s*)p);
+  return uint4{x[0], x[1], x[2], x[3]};
+}
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
   static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }

@@ -166,7 +166,7 @@ __device__ __forceinline__ void load_w(const f16* W, int K, int n0, int cb, int 
       for (int rb = 0; rb < RB; ++rb) {
         const f16* blk = W + (((size_t)((n0 >> 4) + rb) * nch + cb + j) * 4) * 512 + lane * 8;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) w[(j * RB + rb) * 4 + i] = *(const uint4*)(blk + i * 512);
+        for (int i = 0; i < 4; ++i) w[(j * RB + rb) * 4 + i] = ld_stream(blk + i * 512);
       }
     }
   }

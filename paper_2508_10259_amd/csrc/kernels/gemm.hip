@@ -147,7 +147,7 @@ __global__ __launch_bounds__((64 * skinny_max_waves<RB, MB, LO>())) void k_gemm_
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) fw[j][rb][i] = *(const uint4*)(wrow[rb] + kb + 32 * i);
+          for (int i = 0; i < 4; ++i) fw[j][rb][i] = ld_stream(wrow[rb] + kb + 32 * i);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -735,7 +735,7 @@ constexpr int WIDE_ROWS = 128, WIDE_WP = 3, WIDE_LDK = 128 + 16;
 // 38.4 -> 35.2 us, QKV 22.0 -> 20.1 us.
 __device__ __forceinline__ void wide_wload_fo(uint4 (&w)[4], const f16* wstrip, int c) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = *(const uint4*)(wstrip + ((size_t)c * 4 + i) * 512);
+  for (int i = 0; i < 4; ++i) w[i] = ld_stream(wstrip + ((size_t)c * 4 + i) * 512);
 }
 
 // one thread per 16 bytes of the fragment-ordered copy
