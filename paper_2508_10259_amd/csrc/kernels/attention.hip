@@ -234,6 +234,31 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
 // A lane (r, g) = A[r][8g..8g+7], B lane (r, g) = B[8g..8g+7][r],
 // C lane (r, g) = C[4g+i][r], with r = lane & 15, g = lane >> 4.
 
+// Sum (max) over each aligned group of N lanes (N <= 32), every lane of a
+// group receiving the same total: DPP quad permutes for distances 1 and 2,
+// half-row and row mirrors for 4 and 8 (their partner lanes hold equal
+// partial results by then), a lane shuffle for 16.  A group of 16 is one DPP
+// row, so its reductions take no LDS round trip (ds_bpermute).
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int N> __device__ __forceinline__ float group_sum(float v) {
+  if constexpr (N >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+  if constexpr (N >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+  if constexpr (N >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror
+  if constexpr (N >= 16) v += dpp_mov<0x140>(v); // row_mirror
+  if constexpr (N >= 32) v += __shfl_xor(v, 16, 64);
+  return v;
+}
+template <int N> __device__ __forceinline__ float group_max(float v) {
+  if constexpr (N >= 2) v = fmaxf(v, dpp_mov<0xB1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp_mov<0x4E>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp_mov<0x141>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp_mov<0x140>(v));
+  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16, 64));
+  return v;
+}
+
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv,
                                                            const int32_t* __restrict__ row,
@@ -371,8 +396,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
         if (key > qp[i] || key >= kv_end) sc[kb][i] = -INFINITY;
         v = fmaxf(v, sc[kb][i]);
       }
-#pragma unroll
-      for (int o_ = 1; o_ < 16; o_ <<= 1) v = fmaxf(v, __shfl_xor(v, o_, 64));
+      v = group_max<16>(v);
       mx[i] = v;
     }
 #pragma unroll
@@ -386,8 +410,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
         sc[kb][i] = pv;
         rs += pv;
       }
-#pragma unroll
-      for (int o_ = 1; o_ < 16; o_ <<= 1) rs += __shfl_xor(rs, o_, 64);
+      rs = group_sum<16>(rs);
       l[i] = l[i] * alpha + rs;
       m[i] = m_new;
 #pragma unroll
@@ -469,24 +492,9 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
   f16* VT = (f16*)(ext_sm + wave * G::WAVE_LDS);  // [DH][VPAD]: V^T of this wave's block
   f16* Pw = VT + DH * VPAD;                        // [16][PPAD]: P of this wave's block
 
-  // Q fragments (A layout): query r, dims 32i + 8g + e, rotated and scaled
+  // Q fragments (A layout): query r, dims 32i + 8g + e, rotated and scaled;
+  // filled after the first key blocks' loads are issued
   half8 qf[NQI];
-  {
-    const bool ok = r < n;
-    const float* q = qkv + (size_t)(t0 + (ok ? r : 0)) * 3 * d + h * DH;
-    const float2* rp = rope + (size_t)(p0 + (ok ? r : 0)) * HALF;
-#pragma unroll
-    for (int i = 0; i < NQI / 2; ++i) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int dd = 32 * i + 8 * g + e;  // < HALF; its partner is dd + HALF
-        const float a = ok ? q[dd] : 0.f, c = ok ? q[dd + HALF] : 0.f;
-        const float2 cs = rp[dd];
-        qf[i][e] = (f16)((a * cs.x - c * cs.y) * scale);
-        qf[i + NQI / 2][e] = (f16)((a * cs.y + c * cs.x) * scale);
-      }
-    }
-  }
   int qp[4];  // positions of this lane's C rows (queries 4g + e); -1 past the segment
 #pragma unroll
   for (int e = 0; e < 4; ++e) qp[e] = 4 * g + e < n ? p0 + 4 * g + e : -1;
@@ -502,22 +510,24 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
     const size_t pb = kv_slot(kv_page_u(kp, b, kb), H, h, 0, DH);
     const f16* Kb = kslab + pb;
     const f16* Vb = vslab + pb;
+    // every lane loads from its key's slot of the block's page whether or not the
+    // key exists (no branch per load): keys past the segment get score -inf
+    // (block), and their values are zeroed here, since P = 0 times a stale
+    // slot's bits need not be 0
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       const int key = kb + 16 * c + r;
-      const bool ok = key < kv_end;
 #pragma unroll
-      for (int i = 0; i < NQI; ++i)
-        kx[c][i] = ok ? ld_stream(Kb + (size_t)(key & (KV_PAGE - 1)) * DH + 32 * i + 8 * g)
-                      : uint4{0u, 0u, 0u, 0u};
+      for (int i = 0; i < NQI; ++i) kx[c][i] = ld_stream(Kb + (size_t)(key & (KV_PAGE - 1)) * DH + 32 * i + 8 * g);
     }
 #pragma unroll
     for (int p = 0; p < VPASS; ++p)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kb + 4 * vkq + i;
-        vx[4 * p + i] = key < kv_end ? ld_stream(Vb + (size_t)(key & (KV_PAGE - 1)) * DH + (vq + 8 * p) * 8)
-                                     : uint4{0u, 0u, 0u, 0u};
+        const uint4 t = ld_stream(Vb + (size_t)(key & (KV_PAGE - 1)) * DH + (vq + 8 * p) * 8);
+        const bool ok = key < kv_end;
+        vx[4 * p + i] = uint4{ok ? t.x : 0u, ok ? t.y : 0u, ok ? t.z : 0u, ok ? t.w : 0u};
       }
   };
 
@@ -567,8 +577,7 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
         if (key > qp[e] || key >= kv_end) sc[c][e] = -INFINITY;
         mx = fmaxf(mx, sc[c][e]);
       }
-#pragma unroll
-      for (int o_ = 1; o_ < 16; o_ <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o_, 64));
+      mx = group_max<16>(mx);
       const float m_new = fmaxf(m[e], mx);
       const float alpha = (m_new == -INFINITY) ? 1.f : __expf(m[e] - m_new);
       float rs = 0.f;
@@ -578,8 +587,7 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
         sc[c][e] = pv;
         rs += pv;
       }
-#pragma unroll
-      for (int o_ = 1; o_ < 16; o_ <<= 1) rs += __shfl_xor(rs, o_, 64);
+      rs = group_sum<16>(rs);
       l[e] = l[e] * alpha + rs;
       m[e] = m_new;
 #pragma unroll
@@ -610,6 +618,37 @@ __global__ __launch_bounds__(64 * EXT_WAVES, 2) void k_attn_extend(const float* 
   uint4 kn[2][NQI], vn[VLD];
   int kb = wave * EXT_KB;
   if (kb < kv_end) load(kb, kc, vc);
+  {
+    // the query row (rows past the segment read row 0 and are zeroed), 8
+    // consecutive dims and their rotation partners as 16-byte loads
+    const bool ok = r < n;
+    const float* q = qkv + (size_t)(t0 + (ok ? r : 0)) * 3 * d + h * DH;
+    const float2* rp = rope + (size_t)(p0 + (ok ? r : 0)) * HALF;
+#pragma unroll
+    for (int i = 0; i < NQI / 2; ++i) {
+      const int d0 = 32 * i + 8 * g;  // < HALF; its partner is d0 + HALF
+      float a[8], c[8];
+      float2 cs[8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float4 av = *(const float4*)(q + d0 + 4 * u), cv = *(const float4*)(q + d0 + HALF + 4 * u);
+        a[4 * u] = av.x; a[4 * u + 1] = av.y; a[4 * u + 2] = av.z; a[4 * u + 3] = av.w;
+        c[4 * u] = cv.x; c[4 * u + 1] = cv.y; c[4 * u + 2] = cv.z; c[4 * u + 3] = cv.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float4 t = *(const float4*)(rp + d0 + 2 * u);
+        cs[2 * u] = float2{t.x, t.y};
+        cs[2 * u + 1] = float2{t.z, t.w};
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ae = ok ? a[e] : 0.f, ce = ok ? c[e] : 0.f;
+        qf[i][e] = (f16)((ae * cs[e].x - ce * cs[e].y) * scale);
+        qf[i + NQI / 2][e] = (f16)((ae * cs[e].y + ce * cs[e].x) * scale);
+      }
+    }
+  }
   while (kb < kv_end) {
     const int nb = kb + kstep;
     if (nb < kv_end) load(nb, kn, vn);
@@ -743,21 +782,6 @@ template <typename T, int DH> struct DecGeo {
 // at most 8 waves (512 threads) per decode workgroup; a launch may use fewer
 constexpr int DECODE_MAX_WAVES = 8;
 
-// Sum over each aligned group of N lanes (N <= 32), every lane of a group
-// receiving its total: DPP quad permutes for distances 1 and 2, half-row and
-// row mirrors for 4 and 8 (their partner lanes hold equal partial sums by
-// then), a lane shuffle for 16.
-template <int CTRL> __device__ __forceinline__ float dpp_mov(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-template <int N> __device__ __forceinline__ float group_sum(float v) {
-  if constexpr (N >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
-  if constexpr (N >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
-  if constexpr (N >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror
-  if constexpr (N >= 16) v += dpp_mov<0x140>(v); // row_mirror
-  if constexpr (N >= 32) v += __shfl_xor(v, 16, 64);
-  return v;
-}
 
 // Max / sum across the lane groups of size N (values uniform within a group).
 template <int N> __device__ __forceinline__ float cross_max(float v) {
