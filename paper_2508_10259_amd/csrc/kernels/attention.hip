@@ -285,40 +285,6 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   const int d = H * DH;
   const int kv_end = p0 + (n < q_lo + QT ? n : q_lo + QT);  // exclusive
 
-  // Q fragments: this lane's query row r of the wave, dims 32i + 8g + e
-  half8 qf[NQI];
-  {
-    const int qi = q_lo + wave * 16 + r;
-    const bool ok = qi < n;
-    const float* q = qkv + (size_t)(t0 + (ok ? qi : 0)) * 3 * d + h * DH;
-    const float2* rp = rope + (size_t)(p0 + (ok ? qi : 0)) * HALF;
-#pragma unroll
-    for (int i = 0; i < NQI / 2; ++i) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int dd = 32 * i + 8 * g + e;  // < HALF; its partner is dd + HALF
-        const float a = ok ? q[dd] : 0.f, c = ok ? q[dd + HALF] : 0.f;
-        const float2 cs = rp[dd];
-        qf[i][e] = (f16)((a * cs.x - c * cs.y) * scale);
-        qf[i + NQI / 2][e] = (f16)((a * cs.y + c * cs.x) * scale);
-      }
-    }
-  }
-  // query positions of this lane's C rows (4g + i)
-  int qp[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int qi = q_lo + wave * 16 + 4 * g + i;
-    qp[i] = qi < n ? p0 + qi : -1;
-  }
-
-  float m[4], l[4];
-  f32x4 acc[NDJ];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; l[i] = 0.f; }
-#pragma unroll
-  for (int j = 0; j < NDJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   f16* Pw = Ps + wave * 16 * PPAD;
   constexpr int CH = DH / 8;  // 16-byte chunks per key row
 
@@ -351,6 +317,55 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
     }
   };
   load_tile(0);
+  // Q fragments: this lane's query row r of the wave, dims 32i + 8g + e (the
+  // first key tile's loads are already in flight); rows past the segment read
+  // row 0 and are zeroed
+  half8 qf[NQI];
+  {
+    const int qi = q_lo + wave * 16 + r;
+    const bool ok = qi < n;
+    const float* q = qkv + (size_t)(t0 + (ok ? qi : 0)) * 3 * d + h * DH;
+    const float2* rp = rope + (size_t)(p0 + (ok ? qi : 0)) * HALF;
+#pragma unroll
+    for (int i = 0; i < NQI / 2; ++i) {
+      const int d0 = 32 * i + 8 * g;  // < HALF; its partner is d0 + HALF
+      float a[8], c[8];
+      float2 cs[8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float4 av = *(const float4*)(q + d0 + 4 * u), cv = *(const float4*)(q + d0 + HALF + 4 * u);
+        a[4 * u] = av.x; a[4 * u + 1] = av.y; a[4 * u + 2] = av.z; a[4 * u + 3] = av.w;
+        c[4 * u] = cv.x; c[4 * u + 1] = cv.y; c[4 * u + 2] = cv.z; c[4 * u + 3] = cv.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float4 t = *(const float4*)(rp + d0 + 2 * u);
+        cs[2 * u] = float2{t.x, t.y};
+        cs[2 * u + 1] = float2{t.z, t.w};
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ae = ok ? a[e] : 0.f, ce = ok ? c[e] : 0.f;
+        qf[i][e] = (f16)((ae * cs[e].x - ce * cs[e].y) * scale);
+        qf[i + NQI / 2][e] = (f16)((ae * cs[e].y + ce * cs[e].x) * scale);
+      }
+    }
+  }
+  // query positions of this lane's C rows (4g + i)
+  int qp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qi = q_lo + wave * 16 + 4 * g + i;
+    qp[i] = qi < n ? p0 + qi : -1;
+  }
+
+  float m[4], l[4];
+  f32x4 acc[NDJ];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; l[i] = 0.f; }
+#pragma unroll
+  for (int j = 0; j < NDJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
   for (int kt = 0; kt < kv_end; kt += KT) {
     __syncthreads();  // previous tile's Ks / VT / Ps reads are done
 #pragma unroll
