@@ -507,15 +507,6 @@ static hipError_t resid_proj(const Rows& g, const void* x, const void* xlo, cons
     if (wide_fused_reduce(g.n))
       return gemm_wide_reduce(EPI_RESID, x, xlo, Wf, g.n, d, K, splits, c.kpart(), c.wcnt(), nullptr, nullptr, 0,
                               g.h(), o16, olo, ss, nullptr, 0.f, s);
-    // K chunks that the splits cannot share evenly (the 7B down projection's 86
-    // over 8) take the balanced split over the CUs: 24.4 -> 22.6 us at 64 rows.
-    // Even splits stay (balancing them measured slower: O 11.3 -> 16.6 us)
-    if (wide_balanced(d, K)) {
-      const int slots = wide_stream_slots(d, K, WIDE_STREAM_WGS);
-      hipError_t e = gemm_wide_stream(x, xlo, Wf, g.n, d, K, WIDE_STREAM_WGS, c.kpart(), s);
-      if (e == hipSuccess) e = part_resid(c.kpart(), slots, g.n, d, g.h(), o16, olo, s, ss);
-      return e;
-    }
     hipError_t e = gemm_wide(x, xlo, Wf, g.n, d, K, splits, c.kpart(), s);
     if (e == hipSuccess) e = part_resid(c.kpart(), splits, g.n, d, g.h(), o16, olo, s, ss);
     return e;

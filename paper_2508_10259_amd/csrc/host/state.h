@@ -16,7 +16,6 @@
 #include <vector>
 
 #include "fused_limits.h"
-#include "wide_split.h"
 
 namespace ams {
 
@@ -151,9 +150,6 @@ inline int decode_ksplit(int N, int K) {
 // is taken.  On the 7B shapes at 16 and 64 rows this is the measured best of
 // S = 1..8 (QKV 8, gate|up 4, O and down 8); counts that leave the last round
 // of workgroups mostly empty lose to both neighbours.
-// Workgroups of the wide decode GEMM's balanced split (one per CU of an MI355X).
-constexpr int WIDE_STREAM_WGS = 256;
-
 inline int decode_wsplit(int N, int K) {
   const int tiles = std::max(N / 128, 1), smax = std::max(1, std::min(16, (K / 128) / 4));
   auto t = [&](int s) { return (double)((tiles * s + 255) / 256) / s; };
@@ -163,10 +159,6 @@ inline int decode_wsplit(int N, int K) {
   while (t(s) > 1.05 * best) ++s;
   return s;
 }
-
-// The residual projections above 16 rows whose K chunks the uniform split
-// cannot share evenly take the balanced split.
-inline bool wide_balanced(int N, int K) { return (K / 128) % decode_wsplit(N, K) != 0; }
 
 // Persistent decode (one launch per step) applies up to this many rows.
 constexpr int FUSED_MAX_ROWS = 8;
@@ -284,9 +276,7 @@ inline CtxLayout ctx_layout(const Cfg& c, int batch, int capacity, int pass_toke
     const size_t NB = bins_padded(c);
     kp = std::max({kp, decode_wsplit(3 * (int)d, (int)d) * B * 3 * d, decode_wsplit((int)d, (int)d) * B * d,
                    decode_wsplit(2 * (int)F, (int)d) * B * 2 * F, decode_wsplit((int)d, (int)F) * B * d,
-                   decode_wsplit((int)NB, (int)d) * B * NB,
-                   (size_t)wide_stream_slots((int)d, (int)d, WIDE_STREAM_WGS) * B * d,
-                   (size_t)wide_stream_slots((int)d, (int)F, WIDE_STREAM_WGS) * B * d});
+                   decode_wsplit((int)NB, (int)d) * B * NB});
   }
   if (es == 2) kp = std::max(kp, prefill_part_floats(c, (int)x.pass_tokens));
   x.kpart = o; o = align256(o + kp * 4);

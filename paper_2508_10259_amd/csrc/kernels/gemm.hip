@@ -881,11 +881,10 @@ __device__ void wide_reduce(const WideEpi& e, __amdgpu_buffer_rsrc_t pr, int S, 
 // measured 1-2 us faster per projection than GEMM + reduction kernel at 16
 // rows and 1-5 us slower at 64, where the O and down projections' 32 tiles
 // then reduce on 32 CUs; the engine uses it up to 16 rows.
-template <int MB, int LO, int EPI, bool STREAM>
+template <int MB, int LO, int EPI>
 __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, const f16* __restrict__ xlo,
                                                    const f16* __restrict__ W, int M, int K,
-                                                   float* __restrict__ part, int N, WideEpi ep, int slots) {
-  static_assert(!STREAM || EPI == EPI_PART, "the balanced split leaves partial sums to a reduction kernel");
+                                                   float* __restrict__ part, int N, WideEpi ep) {
   constexpr int NX = LO == 2 ? 2 : 1;               // activation arrays (hi, lo)
   constexpr int XCH = NX * MB * 16 * 16;             // 16-byte pieces of one staged chunk
   constexpr int XPT = (XCH + 511) / 512;             // pieces per thread
@@ -894,24 +893,18 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, g = lane >> 4;
-  const int nch = K >> 7;
-  // this workgroup's K chunks s0 .. s0 + n - 1 of the weight tile holding rows n0
-  // (per wave); set per split, or per segment of the balanced split
-  int n0 = 0, s0 = 0, n = 0, rot = 0;
-  const f16* wstrip = W;
+  const int n0 = blockIdx.x * WIDE_ROWS + wave * 16;
+  const int nch = K >> 7, S = gridDim.y, sp = blockIdx.y;
+  const int s0 = sp * nch / S, s1 = (sp + 1) * nch / S, n = s1 - s0;
   // the split's chunks in rotated order, by tile index / 8: the workgroups an XCD
   // runs at once (ids equal mod 8) start at different columns of their rows.
   // Measured on the 7B shapes: 1-5% faster at 16 rows (down 20.7 -> 19.6 us),
   // 0-1.5% at 64; rotating by the tile index itself was slower for gate|up.
+  const int rot = n > 0 ? (int)((blockIdx.x >> 3) % (unsigned)n) : 0;
   auto chunk = [&](int t) { const int u = t + rot; return s0 + (u >= n ? u - n : u); };
+
   // W in fragment order: this wave's strip, lane's 16 bytes of each block
-  auto place = [&](int tile, int c0, int nc, int rk) __attribute__((always_inline)) {
-    n0 = tile * WIDE_ROWS + wave * 16;
-    s0 = c0;
-    n = nc;
-    rot = nc > 0 ? (int)((unsigned)rk % (unsigned)nc) : 0;
-    wstrip = W + (size_t)(n0 / 16) * nch * 2048 + lane * 8;
-  };
+  const f16* wstrip = W + (size_t)(n0 / 16) * (K >> 7) * 2048 + lane * 8;
   uint4 wr[WP][4];
   // activation staging, up to 4 pieces of 16 bytes per thread (named registers:
   // an array here ends up on the stack).  Piece e = tid + 512 q: array
@@ -941,6 +934,8 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   do { AMS_WIDE_XSTORE1(0, x0, stage); AMS_WIDE_XSTORE1(1, x1, stage); AMS_WIDE_XSTORE1(2, x2, stage); AMS_WIDE_XSTORE1(3, x3, stage); } while (0)
 
   f32x4 acc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // one K chunk t: its MFMAs from stage t & 1 and weights w, then staging chunk
   // t+1, the activation loads of chunk t+2 and the weight loads of chunk t+WP
@@ -970,10 +965,6 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
     if (ldw) wide_wload_fo(w, wstrip, chunk(t + WP));
     __syncthreads();
   };
-  // the K loop of one split or segment (acc from zero)
-  auto body = [&]() __attribute__((always_inline)) {
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   int t = 0;
   if (n >= 2 * WP) {
     // Every chunk the prologue and the steps of this loop load exists, so
@@ -1012,59 +1003,23 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
     for (int p = 0; p < WP; ++p)
       if (t + p < n) step(t + p, wr[p], t + p + 1 < n, t + p + 2 < n, t + p + WP < n);
   }
-  };
 
 #undef AMS_WIDE_XLOAD1
 #undef AMS_WIDE_XSTORE1
 #undef AMS_WIDE_XLOAD
 #undef AMS_WIDE_XSTORE
 
-  // lane (r, g) holds rows n0 + 4g + i for token mb*16 + r; slot j of the partial sums
-  auto store_part = [&](int j, bool zero) __attribute__((always_inline)) {
+  // lane (r, g) holds rows n0 + 4g + i for token mb*16 + r
+  if constexpr (EPI == EPI_PART) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const int tok = mb * 16 + r;
       if (tok >= M) continue;
-      float* dst = part + ((size_t)j * M + tok) * N + n0 + 4 * g;
-      *(float4*)dst = zero ? float4{0.f, 0.f, 0.f, 0.f} : float4{acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]};
+      float* dst = part + ((size_t)sp * M + tok) * N + n0 + 4 * g;
+      *(float4*)dst = float4{acc[mb][0], acc[mb][1], acc[mb][2], acc[mb][3]};
     }
-  };
-  if constexpr (STREAM) {
-    // Balanced split: the tiles x K chunks units, tile by tile, in equal shares
-    // over the workgroups (gridDim.x of them, one per CU); a share crossing a
-    // tile boundary is one segment per tile.  A segment writes slot (its
-    // workgroup - the first workgroup of its tile) of that tile, so a tile's
-    // slots hold its K ranges in order, and the workgroup ending a tile zeroes
-    // the tile's slots past its last one: the reduction adds `slots` slots.
-    const int P = gridDim.x;
-    const long long U = (long long)(N / WIDE_ROWS) * nch;
-    long long u = (long long)blockIdx.x * U / P;
-    const long long u_end = (long long)(blockIdx.x + 1) * U / P;
-    while (u < u_end) {
-      const int tile = (int)(u / nch), c0 = (int)(u - (long long)tile * nch);
-      const int nc = (int)min((long long)(nch - c0), u_end - u);
-      place(tile, c0, nc, (int)(blockIdx.x >> 3));
-      body();
-      const int j = (int)blockIdx.x - wide_unit_owner((long long)tile * nch, P, U);
-      store_part(j, false);
-      if (c0 + nc == nch)
-        for (int z = j + 1; z < slots; ++z) store_part(z, true);
-      u += nc;
-    }
-    return;
-  }
-  {
-    const int S = gridDim.y;
-    const int sp = blockIdx.y;
-    const int c0 = sp * nch / S;
-    place((int)blockIdx.x, c0, (sp + 1) * nch / S - c0, (int)(blockIdx.x >> 3));
-    body();
-  }
-  if constexpr (EPI == EPI_PART) {
-    store_part(blockIdx.y, false);
   } else {
     __shared__ int last;
-    const int S = gridDim.y, sp = blockIdx.y;
     const __amdgpu_buffer_rsrc_t pr = wide_rsrc(part, (uint32_t)((size_t)S * M * N * 4));
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -1088,14 +1043,12 @@ __global__ __launch_bounds__(512) void k_gemm_wide(const f16* __restrict__ xhi, 
   }
 }
 
-// STREAM: the balanced split over `splits` workgroups, `slots` partial-sum slots
-template <int MB, int LO, int EPI, bool STREAM = false>
+template <int MB, int LO, int EPI>
 static hipError_t launch_wide(const f16* x, const f16* xlo, const f16* W, int M, int N, int K, int splits,
-                              float* part, const WideEpi& ep, hipStream_t s, int slots = 0) {
+                              float* part, const WideEpi& ep, hipStream_t s) {
   const size_t lds = (size_t)2 * (LO == 2 ? 2 : 1) * MB * 16 * WIDE_LDK * sizeof(f16);
-  const dim3 grid = STREAM ? dim3(splits, 1) : dim3(N / WIDE_ROWS, splits);
-  hipLaunchKernelGGL((k_gemm_wide<MB, LO, EPI, STREAM>), grid, dim3(512), lds, s, x, xlo, W, M, K, part, N, ep,
-                     slots);
+  hipLaunchKernelGGL((k_gemm_wide<MB, LO, EPI>), dim3(N / WIDE_ROWS, splits), dim3(512), lds, s, x, xlo, W, M, K,
+                     part, N, ep);
   return hipGetLastError();
 }
 
@@ -1124,25 +1077,6 @@ hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N
   if (M <= 0) return hipSuccess;
   if (!wide_shape_ok(M, N, K, splits)) return hipErrorInvalidValue;
   return wide_epi<EPI_PART>(u, ulo, W, M, N, K, splits, part, WideEpi{}, s);
-}
-
-hipError_t gemm_wide_stream(const void* u, const void* ulo, const void* W, int M, int N, int K, int wgs, float* part,
-                            hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  if (M > 64 || N % WIDE_ROWS != 0 || K % 128 != 0 || K <= 0 || N <= 0 || wgs < 1) return hipErrorInvalidValue;
-  const int slots = wide_stream_slots(N, K, wgs);
-  wgs = wide_stream_wgs(N, K, wgs);
-  const f16 *x = (const f16*)u, *xl = (const f16*)ulo, *w = (const f16*)W;
-  if (!ulo) {
-    if (M <= 16) return launch_wide<1, 0, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-    if (M <= 32) return launch_wide<2, 0, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-    if (M <= 48) return launch_wide<3, 0, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-    return launch_wide<4, 0, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-  }
-  if (M <= 16) return launch_wide<1, 2, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-  if (M <= 32) return launch_wide<2, 2, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-  if (M <= 48) return launch_wide<3, 2, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
-  return launch_wide<4, 2, EPI_PART, true>(x, xl, w, M, N, K, wgs, part, WideEpi{}, s, slots);
 }
 
 hipError_t gemm_wide_reduce(int epi, const void* u, const void* ulo, const void* W, int M, int N, int K, int splits,

@@ -7,7 +7,6 @@
 #include <stdint.h>
 
 #include "fused_limits.h"
-#include "wide_split.h"
 
 namespace ams {
 
@@ -79,14 +78,6 @@ hipError_t frag_pack(const void* W, int N, int K, void* Wf, hipStream_t s);
 // part_* reductions.
 hipError_t gemm_wide(const void* u, const void* ulo, const void* W, int M, int N, int K, int splits, float* part,
                      hipStream_t s);
-// The same partial sums with the work balanced over `wgs` workgroups: the
-// (128-row tile, 128-wide K chunk) units, tile by tile, in equal contiguous
-// shares, so that no CU round is left partly idle.  Tile t's K ranges land in
-// slots 0, 1, ... of part ([slots][M][N], slots = wide_stream_slots(N, K,
-// wgs)) in K order, and its unused slots are zero, so the part_* reductions
-// over `slots` splits apply unchanged.
-hipError_t gemm_wide_stream(const void* u, const void* ulo, const void* W, int M, int N, int K, int wgs, float* part,
-                            hipStream_t s);
 // The wide decode GEMM (W in fragment order) with its reduction fused: each
 // split stores its partial sums (part, splits * M * N floats) and the last
 // split of every 128-row weight tile to finish (per-tile counters, zero before

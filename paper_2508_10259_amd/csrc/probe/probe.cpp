@@ -40,13 +40,6 @@ int ams_probe_gemm_wide(const void* u, const void* ulo, const void* W, int M, in
   return (int)ams::gemm_wide(u, ulo, W, M, N, K, splits, part, (hipStream_t)stream);
 }
 
-int ams_probe_gemm_wide_stream(const void* u, const void* ulo, const void* W, int M, int N, int K, int wgs,
-                               float* part, void* stream) {
-  return (int)ams::gemm_wide_stream(u, ulo, W, M, N, K, wgs, part, (hipStream_t)stream);
-}
-
-int ams_probe_wide_stream_slots(int N, int K, int wgs) { return ams::wide_stream_slots(N, K, wgs); }
-
 int ams_probe_gemm_wide_reduce(int epi, const void* u, const void* ulo, const void* W, int M, int N, int K,
                                int splits, float* part, unsigned* counters, void* out, void* olo, int ldo, float* h,
                                void* o16, void* olo2, float* ss_out, const float* ss_in, float eps, void* stream) {

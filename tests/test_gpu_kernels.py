@@ -882,61 +882,6 @@ def test_gemm_wide(probe, M, N, K, splits, pair):
     assert float(np.max(np.abs(got - ref))) <= max(tol, 4e-6 * float(np.max(np.abs(ref))))
 
 
-@pytest.mark.parametrize("M", [17, 64])
-@pytest.mark.parametrize("N,K,wgs", [(2048, 4096, 40), (1152, 1408, 99), (1152, 1408, 500), (4096, 11008, 256),
-                                     (384, 1024, 5), (2816, 4096, 256), (256, 4096, 256)])
-@pytest.mark.parametrize("pair", [False, True])
-def test_gemm_wide_stream(probe, M, N, K, wgs, pair):
-    """The wide decode GEMM's balanced split: the (128-row tile, 128-wide K chunk) units in
-    equal contiguous shares over `wgs` workgroups (at most one per unit).  Every slot of
-    every tile is checked against the exact product over the K range it must hold (a tile's
-    ranges in K order, its remaining slots zero), and the slots' sum against the full product.
-    Shapes: shares crossing tile boundaries, one unit per workgroup, more workgroups than
-    units, the 7B down projection's 86 chunks, a share covering a whole tile and more."""
-    import torch
-    log(f"gemm_wide_stream M={M} N={N} K={K} wgs={wgs} pair={pair}")
-    x = W.random_gaussian((M, K), 64, M, K, dtype="f32")
-    if pair:
-        u, ulo = _pair(x)
-        xin = u.astype(np.float64) + ulo.astype(np.float64)
-    else:
-        u, ulo = x.astype(np.float16), None
-        xin = u.astype(np.float64)
-    Wt = _rand((N, K), 65, N, K, std=0.05)
-    Wf = _f(Wt, "f16")
-    y = xin @ Wf.T
-    nch, T = K // 128, N // 128
-    U = T * nch
-    P = min(wgs, U)
-    owner = lambda a: ((a + 1) * P - 1) // U
-    slots = max(owner((t + 1) * nch - 1) - owner(t * nch) + 1 for t in range(T))
-    assert probe.ams_probe_wide_stream_slots(N, K, wgs) == slots
-    ud, Wd = _dev(u, "f16"), _dev(_frag(Wt), "f16")
-    ulod = _dev(ulo, "f16") if pair else None
-    part = torch.full((slots * M * N,), float("nan"), dtype=torch.float32, device="cuda")
-    assert probe.ams_probe_gemm_wide_stream(_ptr(ud), _ptr(ulod), _ptr(Wd), M, N, K, wgs, _ptr(part),
-                                            _stream()) == 0
-    torch.cuda.synchronize()
-    got = part.view(slots, M, N).cpu().numpy().astype(np.float64)
-    tol = 2e-5 * max(1.0, float(np.max(np.abs(y)))) * np.sqrt(K / 128)
-    for t in range(T):
-        w0, w1 = owner(t * nch), owner((t + 1) * nch - 1)
-        rows = slice(128 * t, 128 * (t + 1))
-        for j in range(slots):
-            if w0 + j <= w1:
-                w = w0 + j
-                c0 = max(w * U // P, t * nch) - t * nch
-                c1 = min((w + 1) * U // P, (t + 1) * nch) - t * nch
-                ref = xin[:, 128 * c0:128 * c1] @ Wf[rows, 128 * c0:128 * c1].T
-                assert float(np.max(np.abs(got[j][:, rows] - ref))) <= tol, (t, j, c0, c1)
-            else:
-                assert np.all(got[j][:, rows] == 0.0), (t, j)
-    out = torch.zeros((M, N), dtype=torch.float32, device="cuda")
-    assert probe.ams_probe_part_store(_ptr(part), slots, M, N, _ptr(out), _stream()) == 0
-    torch.cuda.synchronize()
-    assert float(np.max(np.abs(out.cpu().numpy() - y))) <= tol
-
-
 @pytest.mark.parametrize("M", [5, 33, 64])
 @pytest.mark.parametrize("N,K,splits", [(256, 1024, 1), (512, 4096, 8), (1152, 1408, 4), (2048, 1024, 3),
                                         (256, 2048, 16)])
