@@ -103,7 +103,7 @@ struct CtxLayout {
   size_t slab_layer;  // bytes of K (or V) for one layer: n_pages pages of 64 positions
   size_t kv, h, u, qkv, o, a, h_last, h_last16, h_last16lo, hlo, olo, alo, kpart, part, logits, rope, lens, meta, total;
   size_t order;  // the rows by decreasing length [B] int32 (decode attention dispatch order)
-  size_t tok_base, tok_pos;  // a token pass's pool offsets [T] int64 and positions [T] int32 (fused K/V append)
+  size_t tok_base, tok_pos;  // a token pass's pool offsets [T] int64 and positions [T] int32 (K/V append)
   size_t ss;  // decode rows' sums of squares per 128 residual columns [B][d/128]
   size_t wcnt;  // arrival counters of the wide decode GEMM's weight tiles (zero between launches)
   // persistent decode (fp16, up to 8 rows): fp16 pairs [2][B][width] of h, the

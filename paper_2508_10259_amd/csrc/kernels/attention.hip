@@ -112,6 +112,55 @@ hipError_t tok_tables(Segs sg, KvPages kp, int H, int dh, int64_t* tok_base, int
   return hipGetLastError();
 }
 
+// The fp16 append from a pass's token tables (tok_base: element offset of the
+// token's (page, head 0, slot), tok_pos: its position): no per-token search of
+// the segments and the page table in every layer, and four values per 16-byte
+// load; the same arithmetic as k_kv_append, so the same fp16 values.
+__global__ __launch_bounds__(256) void k_kv_append_tab(const float* __restrict__ qkv,
+                                                       const int64_t* __restrict__ tok_base,
+                                                       const int32_t* __restrict__ tok_pos, int H, int dh,
+                                                       const float2* __restrict__ rope, f16* __restrict__ kslab,
+                                                       f16* __restrict__ vslab) {
+  const int i = blockIdx.x;
+  const size_t base = (size_t)tok_base[i];
+  const int p = tok_pos[i];
+  const int d = H * dh, half = dh / 2, hq = half / 4;
+  const float* k = qkv + (size_t)i * 3 * d + d;
+  const float* v = k + d;
+  typedef _Float16 half4v __attribute__((ext_vector_type(4)));
+  for (int e = threadIdx.x; e < H * hq; e += blockDim.x) {  // 4 rotation pairs of head h
+    const int h = e / hq, ii = 4 * (e % hq);
+    const float4 a = *(const float4*)(k + h * dh + ii), c = *(const float4*)(k + h * dh + ii + half);
+    const float4 r0 = *(const float4*)(rope + (size_t)p * half + ii), r1 = *(const float4*)(rope + (size_t)p * half + ii + 2);
+    const float av[4] = {a.x, a.y, a.z, a.w}, cv[4] = {c.x, c.y, c.z, c.w};
+    const float cx[4] = {r0.x, r0.z, r1.x, r1.z}, cy[4] = {r0.y, r0.w, r1.y, r1.w};
+    half4v lo, hi;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      lo[j] = sat16(av[j] * cx[j] - cv[j] * cy[j]);
+      hi[j] = sat16(av[j] * cy[j] + cv[j] * cx[j]);
+    }
+    f16* dst = kslab + base + (size_t)h * KV_PAGE * dh;
+    *(half4v*)(dst + ii) = lo;
+    *(half4v*)(dst + ii + half) = hi;
+  }
+  for (int e = threadIdx.x; e < d / 4; e += blockDim.x) {
+    const int h = 4 * e / dh, dd = 4 * e % dh;
+    const float4 x = *(const float4*)(v + 4 * e);
+    const half4v y = {sat16(x.x), sat16(x.y), sat16(x.z), sat16(x.w)};
+    *(half4v*)(vslab + base + (size_t)h * KV_PAGE * dh + dd) = y;
+  }
+}
+
+hipError_t kv_append_tab(const float* qkv, int n_tok, const int64_t* tok_base, const int32_t* tok_pos, int H, int dh,
+                         const float2* rope, void* kslab, void* vslab, hipStream_t s) {
+  if (n_tok <= 0) return hipSuccess;
+  if (dh % 8 != 0 || !tok_base || !tok_pos) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_kv_append_tab, dim3(n_tok), dim3(256), 0, s, qkv, tok_base, tok_pos, H, dh, rope, (f16*)kslab,
+                     (f16*)vslab);
+  return hipGetLastError();
+}
+
 hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s) {
   if (sg.n_tok <= 0) return hipSuccess;

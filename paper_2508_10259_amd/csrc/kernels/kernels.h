@@ -196,6 +196,9 @@ hipError_t gemm_qkv_kv(const void* u, const void* W, int M, int K, float* qkv, c
 hipError_t tok_tables(Segs sg, KvPages kp, int H, int dh, int64_t* tok_base, int32_t* tok_pos, hipStream_t s);
 hipError_t kv_append(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp, const float2* rope,
                      void* kslab, void* vslab, hipStream_t s);
+// fp16 K/V append of a pass's n_tok tokens from the pass's token tables (tok_tables)
+hipError_t kv_append_tab(const float* qkv, int n_tok, const int64_t* tok_base, const int32_t* tok_pos, int H, int dh,
+                         const float2* rope, void* kslab, void* vslab, hipStream_t s);
 
 // Causal attention of the pass's tokens over each row's slab (cache + new).
 hipError_t attn_prefill(int ct, const float* qkv, Segs sg, int H, int dh, KvPages kp,

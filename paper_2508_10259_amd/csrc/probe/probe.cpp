@@ -131,6 +131,15 @@ int ams_probe_kv_append(int ct, const float* qkv, const int32_t* row, const int3
   return (int)ams::kv_append(ct, qkv, sg, H, dh, ams::KvPages{pt, cap / 64}, (const float2*)rope, kslab, vslab,
                              (hipStream_t)stream);
 }
+int ams_probe_kv_append_tab(const float* qkv, const int32_t* row, const int32_t* pos, const int32_t* off, int n_seg,
+                            int n_tok, int H, int dh, int cap, const int32_t* pt, const void* rope, void* kslab,
+                            void* vslab, int64_t* tok_base, int32_t* tok_pos, void* stream) {
+  ams::Segs sg{row, pos, off, n_seg, n_tok, 0, 0};
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = ams::tok_tables(sg, ams::KvPages{pt, cap / 64}, H, dh, tok_base, tok_pos, s);
+  if (e == hipSuccess) e = ams::kv_append_tab(qkv, n_tok, tok_base, tok_pos, H, dh, (const float2*)rope, kslab, vslab, s);
+  return (int)e;
+}
 int ams_probe_qkv_kv(const void* u, const void* W, int K, float* qkv, const int32_t* row, const int32_t* pos,
                      const int32_t* off, int n_seg, int n_tok, int H, int dh, int cap, const int32_t* pt,
                      const void* rope, void* kslab, void* vslab, int64_t* tok_base, int32_t* tok_pos, void* stream) {

@@ -452,6 +452,52 @@ def test_attn_prefill(probe, dh, segs):
                 assert err <= tol, (si, i, h, err, tol)
 
 
+
+@pytest.mark.parametrize("dh,segs", [
+    (128, [(0, 300, 16), (1, 0, 5), (2, 470, 1), (0, 316, 16)]),
+    (64, [(0, 280, 16), (1, 0, 16), (2, 129, 3)]),
+    (128, [(1, 60, 40), (2, 200, 70), (0, 1000, 24)]),
+])
+def test_kv_append_tab(probe, dh, segs):
+    """The fp16 K/V append from a pass's token tables against k_kv_append on the same inputs:
+    v bitwise, k within one fp16 unit (the same rotation, possibly contracted differently),
+    every other slot of the page pools untouched."""
+    import torch
+    B, cap, d = 3, 1024, 512
+    H = d // dh
+    log(f"kv_append_tab dh={dh} segs={segs}")
+    n_tok = sum(n for _, _, n in segs)
+    off = np.cumsum([0] + [n for _, _, n in segs]).astype(np.int32)
+    qkv = W.random_gaussian((n_tok, 3 * d), 85, n_tok, dh, dtype="f32")
+    tab = _rope_tab(cap, dh)
+    perm = np.random.default_rng(86 + dh).permutation(B * (cap // 64)).astype(np.int32)
+    pt_d = torch.from_numpy(perm).cuda()
+    rows = torch.tensor([b for b, _, _ in segs], dtype=torch.int32, device="cuda")
+    pos = torch.tensor([p for _, p, _ in segs], dtype=torch.int32, device="cuda")
+    offd = torch.from_numpy(off).cuda()
+    qkv_d, tab_d = _dev(qkv, "f32"), _dev(tab, "f32")
+    pool = W.random_gaussian((B * (cap // 64) * H * 64 * dh,), 87, dh, dtype="f32").astype(np.float16)
+    KA, VA, KB, VB = (_dev(pool, "f16") for _ in range(4))
+    tb = torch.zeros((n_tok,), dtype=torch.int64, device="cuda")
+    tp = torch.zeros((n_tok,), dtype=torch.int32, device="cuda")
+    max_len = max(n for _, _, n in segs)
+    max_end = max(p + n for _, p, n in segs)
+    assert probe.ams_probe_kv_append(CT["f16"], _ptr(qkv_d), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok,
+                                     max_len, max_end, H, dh, cap, _ptr(pt_d), _ptr(tab_d), _ptr(KA), _ptr(VA),
+                                     _stream()) == 0
+    assert probe.ams_probe_kv_append_tab(_ptr(qkv_d), _ptr(rows), _ptr(pos), _ptr(offd), len(segs), n_tok, H, dh,
+                                         cap, _ptr(pt_d), _ptr(tab_d), _ptr(KB), _ptr(VB), _ptr(tb), _ptr(tp),
+                                         _stream()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(VA, VB)
+    ka, kb = KA.float().cpu().numpy(), KB.float().cpu().numpy()
+    ulp = np.spacing(np.maximum(np.abs(ka), np.abs(kb)).astype(np.float16)).astype(np.float32)
+    assert bool(np.all(np.abs(ka - kb) <= ulp))
+    # the appended slots changed, the rest of the pools did not
+    assert not torch.equal(KA, _dev(pool, "f16"))
+    changed = (KB.cpu().numpy() != pool) | (VB.cpu().numpy() != pool)
+    assert int(changed.sum()) <= 2 * n_tok * d
+
 @pytest.mark.parametrize("dh,segs", [
     (128, [(0, 0, 200), (1, 37, 60), (2, 500, 41)]),
     (64, [(2, 63, 130), (0, 0, 1), (1, 250, 128)]),
